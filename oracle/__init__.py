@@ -1,0 +1,174 @@
+"""Plain CPU oracle for binarized-GCN inference (test infrastructure).
+
+Only the test suite, ``__graft_entry__.smoke()`` and the benchmark's CPU
+baseline may import this package.  It wraps ``bigcn_oracle.c`` (plain C,
+double precision, sequential reductions) through ctypes and shares no code
+with the HIP library.  See the header of ``bigcn_oracle.c`` for the
+equations followed and the readings of the paper it takes.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "bigcn_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+NORMS = {"sym": 0, "mean": 1}
+ACTS = {"none": 0, "relu": 1}
+
+_p = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_i32 = ctypes.c_int32
+_int = ctypes.c_int
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, no FMA contraction, OpenMP)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+             "-fopenmp", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        lib = ctypes.CDLL(_LIB)
+        lib.oracle_binarize.restype = _int
+        lib.oracle_binarize.argtypes = [_p, _i64, _i32, _i64, _p, _p, _p, _i64,
+                                        _p, _i64, _p]
+        lib.oracle_sign_dot.restype = None
+        lib.oracle_sign_dot.argtypes = [_p, _i64, _i64, _p, _i32, _i64, _i32,
+                                        _p, _i64]
+        lib.oracle_aggregate.restype = None
+        lib.oracle_aggregate.argtypes = [_i64, _p, _p, _int, _p, _p, _p, _i64,
+                                         _i32, _p, _int, _p, _i64, _p, _p, _p]
+        lib.oracle_layer.restype = _int
+        lib.oracle_layer.argtypes = [_i64, _p, _p, _int, _p, _i64, _i32, _p,
+                                     _p, _p, _i32, _p, _int, _p, _i64, _p, _p,
+                                     _p, _p]
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _c(a, dtype):
+    return None if a is None else np.ascontiguousarray(a, dtype=dtype)
+
+
+def words(k: int) -> int:
+    return (k + 63) // 64
+
+
+def binarize(x, mu=None, rstd=None, ids=None, ldw=None):
+    """Sign bits and mean-|y| scale of rows of ``x`` (Eqs. (3)-(4), (7)-(8)).
+
+    Returns ``(bits uint64 [n_out, ldw], scale float64 [n_out])``."""
+    x = _c(x, np.float32)
+    rows, cols = x.shape
+    ldw = words(cols) if ldw is None else ldw
+    ids = _c(ids, np.int64)
+    n_out = rows if ids is None else len(ids)
+    bits = np.zeros((n_out, ldw), dtype=np.uint64)
+    scale = np.zeros(n_out, dtype=np.float64)
+    rc = _load().oracle_binarize(_ptr(x), rows, cols, cols, _ptr(_c(mu, np.float32)),
+                                 _ptr(_c(rstd, np.float32)), _ptr(ids),
+                                 0 if ids is None else len(ids), bits.ctypes.data,
+                                 ldw, scale.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_binarize: non-finite input")
+    return bits, scale
+
+
+def sign_dot(F, B, K: int):
+    """±1 inner products of packed rows, Eq. (11): int64 [m, n_out]."""
+    F = _c(F, np.uint64)
+    B = _c(B, np.uint64)
+    m, ldf = F.shape
+    nout, ldb = B.shape
+    dot = np.zeros((m, nout), dtype=np.int64)
+    _load().oracle_sign_dot(F.ctypes.data, m, ldf, B.ctypes.data, nout, ldb, K,
+                            dot.ctypes.data, nout)
+    return dot
+
+
+def aggregate(rowptr, colidx, norm, beta, alpha, dot, bias=None, act="none",
+              ids=None):
+    """Eq. (13) with ζ of Eq. (11): returns (z fp64, mass fp64, out fp32)."""
+    rowptr = _c(rowptr, np.int64)
+    colidx = _c(colidx, np.int32)
+    beta = _c(beta, np.float64)
+    alpha = _c(alpha, np.float64)
+    dot = _c(dot, np.int64)
+    n = len(rowptr) - 1
+    d = dot.shape[1]
+    ids = _c(ids, np.int64)
+    n_out = n if ids is None else len(ids)
+    z = np.zeros((n_out, d), dtype=np.float64)
+    mass = np.zeros((n_out, d), dtype=np.float64)
+    out = np.zeros((n_out, d), dtype=np.float32)
+    _load().oracle_aggregate(n, rowptr.ctypes.data, colidx.ctypes.data,
+                             NORMS[norm], beta.ctypes.data, alpha.ctypes.data,
+                             dot.ctypes.data, d, d, _ptr(_c(bias, np.float32)),
+                             ACTS[act], _ptr(ids), 0 if ids is None else len(ids),
+                             z.ctypes.data, mass.ctypes.data, out.ctypes.data)
+    return z, mass, out
+
+
+def layer(rowptr, colidx, norm, h, wt, bias=None, act="none", mu=None,
+          rstd=None, ids=None):
+    """One binarised graph-convolution layer (Eqs. (3)-(13)) for the listed
+    output rows.  Returns (z fp64, mass fp64, out fp32, alpha fp64)."""
+    rowptr = _c(rowptr, np.int64)
+    colidx = _c(colidx, np.int32)
+    h = _c(h, np.float32)
+    wt = _c(wt, np.float32)
+    n, d_in = h.shape
+    d_out = wt.shape[0]
+    assert wt.shape[1] == d_in
+    ids = _c(ids, np.int64)
+    n_out = n if ids is None else len(ids)
+    z = np.zeros((n_out, d_out), dtype=np.float64)
+    mass = np.zeros((n_out, d_out), dtype=np.float64)
+    out = np.zeros((n_out, d_out), dtype=np.float32)
+    alpha = np.zeros(d_out, dtype=np.float64)
+    rc = _load().oracle_layer(n, rowptr.ctypes.data, colidx.ctypes.data,
+                              NORMS[norm], h.ctypes.data, d_in, d_in,
+                              _ptr(_c(mu, np.float32)), _ptr(_c(rstd, np.float32)),
+                              wt.ctypes.data, d_out, _ptr(_c(bias, np.float32)),
+                              ACTS[act], _ptr(ids), 0 if ids is None else len(ids),
+                              z.ctypes.data, mass.ctypes.data, out.ctypes.data,
+                              alpha.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_layer failed (%d)" % rc)
+    return z, mass, out, alpha
+
+
+def forward(rowptr, colidx, norm, x, weights_t, biases, acts=None, mu=None,
+            rstd=None):
+    """Free-running multi-layer forward: layer l's input is the fp32 output of
+    layer l-1 (layer 0 reads x, standardised by mu/rstd if given).  Returns a
+    list of (z, mass, out) per layer."""
+    acts = acts or ["none"] * len(weights_t)
+    h = x
+    res = []
+    for l, wt in enumerate(weights_t):
+        z, m, out, _ = layer(rowptr, colidx, norm, h, wt, biases[l], acts[l],
+                             mu if l == 0 else None, rstd if l == 0 else None)
+        res.append((z, m, out))
+        h = out
+    return res
