@@ -1,0 +1,204 @@
+/*
+ * bigcn.h -- C ABI of the MI355X (gfx950) binarized-GCN inference library.
+ *
+ * The library computes the inference path of Bi-GCN ("Bi-GCN: Binary Graph
+ * Convolutional Network", Wang et al., CVPR 2021, Sec. 4.1): each layer
+ * binarises its input node features and its weights by sign with
+ * full-precision per-bucket scales, multiplies the packed signs with an
+ * XNOR / bit-count binary GEMM, and aggregates the rescaled result over the
+ * graph with the normalised adjacency.
+ *
+ * Conventions shared by every entry point
+ *  - All pointers except `layers` (bigcn_forward) are DEVICE pointers owned by
+ *    the caller; the library never allocates, frees or keeps them.  Inputs
+ *    are never written.
+ *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Every
+ *    call only enqueues work on `stream` and returns; results are ready once
+ *    the caller synchronises that stream.  No call synchronises the device.
+ *  - Matrices are row-major with a leading dimension (ld*) counted in
+ *    elements.  Packed sign rows are arrays of uint64_t words: element k of a
+ *    row is bit (k % 64) of word (k / 64), a set bit means +1 (the sign of a
+ *    value y is +1 iff y >= 0, so +0 and -0 give +1), and bits at positions
+ *    k >= cols as well as words beyond ceil(cols / 64) are zero.
+ *  - Arguments are validated on the host before anything is enqueued; an
+ *    invalid call returns an error status and enqueues nothing.  Device-side
+ *    faults (e.g. a column index out of range) are not detected; they surface
+ *    at the caller's next synchronisation.  Inputs must be finite.
+ *  - Calls share no mutable global state: concurrent calls on different
+ *    streams with disjoint outputs and workspaces are safe.
+ */
+#ifndef BIGCN_H
+#define BIGCN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BIGCN_OK = 0,
+  BIGCN_EINVAL = -1,       /* bad pointer, size or enum value              */
+  BIGCN_EALIGN = -2,       /* pointer or leading dimension misaligned      */
+  BIGCN_EWORKSPACE = -3,   /* workspace missing or too small               */
+  BIGCN_EUNSUPPORTED = -4, /* valid request this build does not implement  */
+  BIGCN_EHIP = -5          /* the HIP runtime refused a launch             */
+} bigcn_status;
+
+/* Storage of the binary-GEMM integer result.  All three hold every value
+ * exactly: I32 always, I16 for K <= 32767, F16 (IEEE half) for K <= 2048. */
+typedef enum { BIGCN_I32 = 0, BIGCN_I16 = 1, BIGCN_F16 = 2 } bigcn_itype;
+
+/* Normalised adjacency built from the CSR of Â = A + I (Sec. 3.1):
+ *   SYM:  Ã = D̂^-1/2 Â D̂^-1/2   (Eq. (1))
+ *   MEAN: Ã = D̂^-1 Â            (mean over the closed neighbourhood)
+ * where D̂_ii is the number of entries of row i. */
+typedef enum { BIGCN_NORM_SYM = 0, BIGCN_NORM_MEAN = 1 } bigcn_norm;
+
+/* Output activation.  Bi-GCN uses none (the next layer's binarisation acts
+ * as the non-linearity, Sec. 4.1); ReLU is offered for other uses. */
+typedef enum { BIGCN_ACT_NONE = 0, BIGCN_ACT_RELU = 1 } bigcn_act;
+
+/* Binary-GEMM algorithm.  POPCOUNT: XOR + bit count on the vector ALUs.
+ * MFMA_I8: the signs expanded to +-1 int8 and multiplied on the matrix
+ * cores.  Both give identical results; AUTO picks the faster one. */
+typedef enum {
+  BIGCN_BGEMM_AUTO = 0,
+  BIGCN_BGEMM_POPCOUNT = 1,
+  BIGCN_BGEMM_MFMA_I8 = 2
+} bigcn_bgemm_algo;
+
+/* ---------------------------------------------------------------------------
+ * bigcn_binarize_pack -- sign binarisation with per-row scale.
+ * Eqs. (7)-(8) for node features (one bucket per row of H); Eqs. (3)-(4)
+ * for weights when called on W^T (row j of W^T = column j of W).
+ *
+ *   x      [rows][ldx] fp32; the first `cols` elements of each row are used.
+ *   mu, rstd  both NULL, or both fp32[cols]: the row is first standardised,
+ *          y = (x - mu[c]) * rstd[c], as two separately rounded fp32
+ *          operations (the input batch normalisation of the paper's set-up,
+ *          Sec. 6.2, at inference).  Otherwise y = x.
+ *   rowptr NULL, or int64[rows + 1] row pointers of the CSR of Â (one row per
+ *          node).  With norm == BIGCN_NORM_SYM the scale is multiplied by
+ *          D̂_rr^-1/2 (the source-side factor of Ã); with MEAN it is not.
+ *   bits   [rows][ldw] uint64 output, ldw >= ceil(cols / 64); pad bits and
+ *          pad words are written as zero.  16-byte aligned if ldw is even.
+ *   scale  fp32[rows] output: mean_c |y[r][c]| (times D̂_rr^-1/2, see above).
+ *          This is β of Eq. (7) (α of Eq. (4) for weights) with the bucket
+ *          length cols as divisor.
+ * Errors: EINVAL (NULL x/bits/scale, rows < 0, cols < 1, ldx < cols,
+ *         ldw < ceil(cols/64), only one of mu/rstd, bad norm),
+ *         EALIGN (x not 4-byte aligned, bits not 8-byte aligned).
+ * ------------------------------------------------------------------------- */
+bigcn_status bigcn_binarize_pack(const float* x, int64_t rows, int32_t cols,
+                                 int64_t ldx, const float* mu,
+                                 const float* rstd, const int64_t* rowptr,
+                                 bigcn_norm norm, uint64_t* bits, int64_t ldw,
+                                 float* scale, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * bigcn_bgemm -- binary GEMM of packed sign rows, the ±1 inner products of
+ * Eqs. (11)-(12) computed with XOR and bit count:
+ *     C[i][j] = K - 2 * popcount(F_i XOR B_j) = sum_k s(F_i,k) * s(B_j,k)
+ *
+ *   F   [M][ldf] uint64 packed rows (node features), ldf >= ceil(K/64).
+ *   B   [N][ldb] uint64 packed rows (weights: rows of W^T), ldb >= ceil(K/64).
+ *   K   number of valid sign positions (d_in); pad bits must be zero.
+ *   C   [M][ldc] output of type ctype, ldc >= N.
+ *   algo  see bigcn_bgemm_algo.
+ * Errors: EINVAL (NULL pointers, M < 0, N < 1, K < 1, short leading
+ *         dimensions, ctype that cannot hold K: I16 needs K <= 32767, F16
+ *         needs K <= 2048), EALIGN (F, B not 8-byte aligned; C not aligned to
+ *         its element size), EUNSUPPORTED (K > 8192, or MFMA_I8 for a shape
+ *         that variant does not cover).
+ * ------------------------------------------------------------------------- */
+bigcn_status bigcn_bgemm(const uint64_t* F, int64_t M, int64_t ldf,
+                         const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
+                         void* C, bigcn_itype ctype, int64_t ldc,
+                         bigcn_bgemm_algo algo, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * bigcn_spmm_csr -- aggregation of Eq. (13) with the rescale of Eq. (11):
+ *     out[i][k] = act( rowfac_i * alpha[k] * sum_{e in row i} g[col_e] * C[col_e][k]
+ *                      + bias[k] )
+ * with rowfac_i = D̂_ii^-1/2 (SYM) or D̂_ii^-1 (MEAN), D̂_ii = rowptr[i+1] -
+ * rowptr[i].  With g = β·D̂^-1/2 (SYM) or g = β (MEAN), as written by
+ * bigcn_binarize_pack with rowptr, this is out = act(Ã ζ + b),
+ * ζ_jk = β_j α_k C_jk.  A row with no entries gives act(bias[k]).
+ *
+ *   rowptr  int64[n + 1], non-decreasing, rowptr[0] = 0 (CSR of Â).
+ *   colidx  int32[rowptr[n]], each in [0, n).
+ *   g       fp32[n] per-source-node scale.
+ *   C       [n][ldc] integer products of type ctype, ldc >= d, ldc a
+ *           multiple of 4, C aligned to 4 elements.
+ *   alpha   fp32[d]; bias fp32[d] or NULL.
+ *   out     [n][ldo] fp32, ldo >= d.
+ *   workspace  device memory of at least bigcn_spmm_workspace_bytes(n,
+ *           rowptr_last, d) bytes, 256-byte aligned; contents on entry are
+ *           ignored.  nnz (= rowptr[n]) must be passed on the host.
+ * Sums run in fp32 in a fixed order: results are bitwise reproducible.
+ * Errors: EINVAL, EALIGN (C not aligned to 4 elements, out / g / alpha /
+ *         bias not 4-byte aligned, workspace not 256-byte aligned),
+ *         EWORKSPACE.
+ * ------------------------------------------------------------------------- */
+size_t bigcn_spmm_workspace_bytes(int64_t n, int64_t nnz, int32_t d);
+bigcn_status bigcn_spmm_csr(int64_t n, int64_t nnz, const int64_t* rowptr,
+                            const int32_t* colidx, bigcn_norm norm,
+                            const float* g, const void* C, bigcn_itype ctype,
+                            int32_t d, int64_t ldc, const float* alpha,
+                            const float* bias, bigcn_act act, float* out,
+                            int64_t ldo, void* workspace, size_t ws_bytes,
+                            void* stream);
+
+/* ---------------------------------------------------------------------------
+ * bigcn_forward -- the whole multi-layer forward pass (Sec. 4.1):
+ *     H^(0) = X,  H^(l+1) = act_l( Ã ζ^(l) + b_l ),  l = 0 .. n_layers-1,
+ * every layer binarised (features and weights).  Layer 0 standardises X with
+ * mu / rstd when given (see bigcn_binarize_pack).
+ *
+ * One layer description per layer (HOST array of n_layers entries; the
+ * pointers inside are device pointers):
+ *   d_in, d_out  layer widths; layers[l+1].d_in must equal layers[l].d_out.
+ *   wbits  [d_out][ldw] packed signs of W^T, ldw >= ceil(d_in/64)
+ *   alpha  fp32[d_out]   (both as written by bigcn_binarize_pack on W^T)
+ *   bias   fp32[d_out] or NULL;  act  output activation of the layer.
+ *
+ *   n, nnz, rowptr, colidx, norm   the graph, as for bigcn_spmm_csr.
+ *   x    [n][ldx] fp32 node features, ldx >= layers[0].d_in.
+ *   out  [n][ldo] fp32 result of the last layer, ldo >= last d_out.
+ *   workspace  at least bigcn_forward_workspace_bytes(...) bytes, 256-byte
+ *          aligned; contents on entry are ignored.
+ * Internally each layer's products are kept in the narrowest exact type
+ * (IEEE half for d_in <= 2048, else int16).
+ * Errors: as the per-step calls, plus EINVAL for inconsistent layer widths
+ *         or n_layers < 1, EUNSUPPORTED for d_in > 8192 on a layer.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int32_t d_in;
+  int32_t d_out;
+  const uint64_t* wbits;
+  int64_t ldw;
+  const float* alpha;
+  const float* bias;
+  bigcn_act act;
+} bigcn_layer;
+
+size_t bigcn_forward_workspace_bytes(int64_t n, int64_t nnz,
+                                     const bigcn_layer* layers,
+                                     int32_t n_layers);
+bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
+                           const int32_t* colidx, bigcn_norm norm,
+                           const float* x, int64_t ldx, const float* mu,
+                           const float* rstd, const bigcn_layer* layers,
+                           int32_t n_layers, float* out, int64_t ldo,
+                           void* workspace, size_t ws_bytes, void* stream);
+
+/* Human-readable text of a status code (static storage). */
+const char* bigcn_status_string(bigcn_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BIGCN_H */

@@ -1,0 +1,15 @@
+"""Binarized-GCN (Bi-GCN) inference on AMD MI355X (gfx950).
+
+The compute path is the HIP library ``libbigcn.so`` (C ABI in
+``include/bigcn.h``); this package is its ctypes binding.  PyTorch supplies
+device memory and streams only.
+"""
+from ._lib import (BiGCN, BigcnError, EXPORTS, Layer, LIB_PATH, bigcn_bgemm,
+                   bigcn_binarize_pack, bigcn_forward, bigcn_spmm_csr,
+                   forward_workspace_bytes, load, pack_weights,
+                   spmm_workspace_bytes, words)
+
+__all__ = ["BiGCN", "BigcnError", "EXPORTS", "Layer", "LIB_PATH", "bigcn_bgemm",
+           "bigcn_binarize_pack", "bigcn_forward", "bigcn_spmm_csr",
+           "forward_workspace_bytes", "load", "pack_weights",
+           "spmm_workspace_bytes", "words"]

@@ -1,0 +1,268 @@
+"""ctypes binding of libbigcn.so (include/bigcn.h).
+
+Argument marshalling only: each function checks tensor devices, dtypes and
+shapes, passes raw device pointers and the current HIP stream, and raises
+``BigcnError`` on a non-zero status.  Every step of the computation runs in
+the library's HIP kernels; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbigcn.so")
+
+STATUS = {0: "BIGCN_OK", -1: "BIGCN_EINVAL", -2: "BIGCN_EALIGN",
+          -3: "BIGCN_EWORKSPACE", -4: "BIGCN_EUNSUPPORTED", -5: "BIGCN_EHIP"}
+ITYPES = {"i32": 0, "i16": 1, "f16": 2}
+ITYPE_DTYPES = {"i32": torch.int32, "i16": torch.int16, "f16": torch.float16}
+NORMS = {"sym": 0, "mean": 1}
+ACTS = {"none": 0, "relu": 1}
+ALGOS = {"auto": 0, "popcount": 1, "mfma_i8": 2}
+
+# Every entry point declared in include/bigcn.h.
+EXPORTS = ("bigcn_binarize_pack", "bigcn_bgemm", "bigcn_spmm_workspace_bytes",
+           "bigcn_spmm_csr", "bigcn_forward_workspace_bytes", "bigcn_forward",
+           "bigcn_status_string")
+
+
+class BigcnError(RuntimeError):
+    def __init__(self, fn: str, status: int, text: str):
+        super().__init__("%s failed: %s (%s)" % (fn, STATUS.get(status, status), text))
+        self.status = status
+
+
+class _Layer(ctypes.Structure):
+    _fields_ = [("d_in", ctypes.c_int32), ("d_out", ctypes.c_int32),
+                ("wbits", ctypes.c_void_p), ("ldw", ctypes.c_int64),
+                ("alpha", ctypes.c_void_p), ("bias", ctypes.c_void_p),
+                ("act", ctypes.c_int)]
+
+
+_lib = None
+_p, _i64, _i32, _int, _sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                             ctypes.c_int, ctypes.c_size_t)
+
+
+def load() -> ctypes.CDLL:
+    """Loads libbigcn.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libbigcn.so is not built (run __graft_entry__.build() "
+                           "or python paper_2010_07565_amd/build.py)")
+    lib = ctypes.CDLL(LIB_PATH)
+    lib.bigcn_status_string.restype = ctypes.c_char_p
+    lib.bigcn_status_string.argtypes = [_int]
+    lib.bigcn_binarize_pack.restype = _int
+    lib.bigcn_binarize_pack.argtypes = [_p, _i64, _i32, _i64, _p, _p, _p, _int, _p,
+                                        _i64, _p, _p]
+    lib.bigcn_bgemm.restype = _int
+    lib.bigcn_bgemm.argtypes = [_p, _i64, _i64, _p, _i32, _i64, _i32, _p, _int,
+                                _i64, _int, _p]
+    lib.bigcn_spmm_workspace_bytes.restype = _sz
+    lib.bigcn_spmm_workspace_bytes.argtypes = [_i64, _i64, _i32]
+    lib.bigcn_spmm_csr.restype = _int
+    lib.bigcn_spmm_csr.argtypes = [_i64, _i64, _p, _p, _int, _p, _p, _int, _i32,
+                                   _i64, _p, _p, _int, _p, _i64, _p, _sz, _p]
+    lib.bigcn_forward_workspace_bytes.restype = _sz
+    lib.bigcn_forward_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(_Layer),
+                                                  _i32]
+    lib.bigcn_forward.restype = _int
+    lib.bigcn_forward.argtypes = [_i64, _i64, _p, _p, _int, _p, _i64, _p, _p,
+                                  ctypes.POINTER(_Layer), _i32, _p, _i64, _p, _sz, _p]
+    _lib = lib
+    return lib
+
+
+def _check(fn: str, st: int):
+    if st != 0:
+        raise BigcnError(fn, st, load().bigcn_status_string(st).decode())
+
+
+def _dev(t: Optional[torch.Tensor], dtype, name: str):
+    """Device pointer of an optional tensor after dtype / device checks."""
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    return t.data_ptr()
+
+
+def _ld(t: torch.Tensor, name: str) -> int:
+    """Leading dimension of a row-major 2-D tensor with unit column stride."""
+    if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
+        raise ValueError("%s must be a 2-D row-major tensor" % name)
+    return t.stride(0) if t.shape[0] > 1 else max(t.stride(0), t.shape[1])
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def words(k: int) -> int:
+    return (k + 63) // 64
+
+
+# ------------------------------------------------------------ entry points --
+
+def bigcn_binarize_pack(x: torch.Tensor, bits: torch.Tensor, scale: torch.Tensor,
+                        mu=None, rstd=None, rowptr=None, norm: str = "sym",
+                        cols: Optional[int] = None, stream=None) -> None:
+    """Sign bits (uint64 words stored in an int64 tensor) and per-row scale of
+    the rows of ``x`` (see include/bigcn.h)."""
+    cols = x.shape[1] if cols is None else cols
+    st = load().bigcn_binarize_pack(
+        _dev(x, torch.float32, "x"), x.shape[0], cols, _ld(x, "x"),
+        _dev(mu, torch.float32, "mu"), _dev(rstd, torch.float32, "rstd"),
+        _dev(rowptr, torch.int64, "rowptr"), NORMS[norm],
+        _dev(bits, torch.int64, "bits"), _ld(bits, "bits"),
+        _dev(scale, torch.float32, "scale"), _stream(stream))
+    _check("bigcn_binarize_pack", st)
+
+
+def bigcn_bgemm(F: torch.Tensor, B: torch.Tensor, K: int, C: torch.Tensor,
+                algo: str = "auto", stream=None) -> None:
+    """C[i][j] = K - 2 popcount(F_i ^ B_j); C's dtype selects the storage."""
+    ctype = {v: k for k, v in ITYPE_DTYPES.items()}.get(C.dtype)
+    if ctype is None:
+        raise TypeError("C must be int32, int16 or float16")
+    st = load().bigcn_bgemm(
+        _dev(F, torch.int64, "F"), F.shape[0], _ld(F, "F"),
+        _dev(B, torch.int64, "B"), B.shape[0], _ld(B, "B"), K,
+        _dev(C, C.dtype, "C"), ITYPES[ctype], _ld(C, "C"), ALGOS[algo],
+        _stream(stream))
+    _check("bigcn_bgemm", st)
+
+
+def spmm_workspace_bytes(n: int, nnz: int, d: int) -> int:
+    return load().bigcn_spmm_workspace_bytes(n, nnz, d)
+
+
+def bigcn_spmm_csr(rowptr: torch.Tensor, colidx: torch.Tensor, g: torch.Tensor,
+                   C: torch.Tensor, alpha: torch.Tensor, out: torch.Tensor,
+                   workspace: torch.Tensor, bias=None, norm: str = "sym",
+                   act: str = "none", d: Optional[int] = None, nnz: Optional[int] = None,
+                   stream=None) -> None:
+    """out = act(rowfac * alpha * sum_j g_j C_j + bias) over the CSR rows."""
+    ctype = {v: k for k, v in ITYPE_DTYPES.items()}.get(C.dtype)
+    if ctype is None:
+        raise TypeError("C must be int32, int16 or float16")
+    n = rowptr.shape[0] - 1
+    d = alpha.shape[0] if d is None else d
+    nnz = colidx.shape[0] if nnz is None else nnz
+    st = load().bigcn_spmm_csr(
+        n, nnz, _dev(rowptr, torch.int64, "rowptr"), _dev(colidx, torch.int32, "colidx"),
+        NORMS[norm], _dev(g, torch.float32, "g"), _dev(C, C.dtype, "C"), ITYPES[ctype],
+        d, _ld(C, "C"), _dev(alpha, torch.float32, "alpha"),
+        _dev(bias, torch.float32, "bias"), ACTS[act], _dev(out, torch.float32, "out"),
+        _ld(out, "out"), _dev(workspace, torch.uint8, "workspace"),
+        workspace.numel() if workspace is not None else 0, _stream(stream))
+    _check("bigcn_spmm_csr", st)
+
+
+@dataclass
+class Layer:
+    """A binarised layer: packed signs of W^T, alpha, optional bias."""
+    d_in: int
+    d_out: int
+    wbits: torch.Tensor            # int64 [d_out, ldw] (uint64 words)
+    alpha: torch.Tensor            # fp32 [d_out]
+    bias: Optional[torch.Tensor] = None
+    act: str = "none"
+
+    def _c(self) -> _Layer:
+        return _Layer(self.d_in, self.d_out, _dev(self.wbits, torch.int64, "wbits"),
+                      _ld(self.wbits, "wbits"), _dev(self.alpha, torch.float32, "alpha"),
+                      _dev(self.bias, torch.float32, "bias"), ACTS[self.act])
+
+
+def _layers(layers: Sequence[Layer]):
+    arr = (_Layer * len(layers))()
+    for i, l in enumerate(layers):
+        arr[i] = l._c()
+    return arr
+
+
+def forward_workspace_bytes(n: int, nnz: int, layers: Sequence[Layer]) -> int:
+    return load().bigcn_forward_workspace_bytes(n, nnz, _layers(layers), len(layers))
+
+
+def bigcn_forward(rowptr: torch.Tensor, colidx: torch.Tensor, x: torch.Tensor,
+                  layers: Sequence[Layer], out: torch.Tensor, workspace: torch.Tensor,
+                  mu=None, rstd=None, norm: str = "sym", nnz: Optional[int] = None,
+                  stream=None) -> None:
+    """The whole forward pass into ``out`` [n, last d_out]."""
+    n = rowptr.shape[0] - 1
+    nnz = colidx.shape[0] if nnz is None else nnz
+    arr = _layers(layers)
+    st = load().bigcn_forward(
+        n, nnz, _dev(rowptr, torch.int64, "rowptr"), _dev(colidx, torch.int32, "colidx"),
+        NORMS[norm], _dev(x, torch.float32, "x"), _ld(x, "x"),
+        _dev(mu, torch.float32, "mu"), _dev(rstd, torch.float32, "rstd"),
+        arr, len(layers), _dev(out, torch.float32, "out"), _ld(out, "out"),
+        _dev(workspace, torch.uint8, "workspace"),
+        workspace.numel() if workspace is not None else 0, _stream(stream))
+    _check("bigcn_forward", st)
+
+
+# ----------------------------------------------------------------- helpers --
+
+def pack_weights(wt: torch.Tensor, ldw: Optional[int] = None, stream=None):
+    """Packed signs and alpha of W^T [d_out, d_in] (Eqs. (3)-(4))."""
+    d_out, d_in = wt.shape
+    ldw = words(d_in) if ldw is None else ldw
+    bits = torch.empty((d_out, ldw), dtype=torch.int64, device=wt.device)
+    alpha = torch.empty(d_out, dtype=torch.float32, device=wt.device)
+    bigcn_binarize_pack(wt, bits, alpha, stream=stream)
+    return bits, alpha
+
+
+class BiGCN:
+    """A binarized GCN bound to one graph on one device.
+
+    Weights are packed once at construction; ``forward`` runs the whole pass
+    into a preallocated output with a preallocated workspace."""
+
+    def __init__(self, rowptr, colidx, weights_t, biases=None, acts=None,
+                 norm: str = "sym", mu=None, rstd=None, device="cuda"):
+        self.device = torch.device(device)
+        self.rowptr = torch.as_tensor(rowptr, dtype=torch.int64, device=self.device)
+        self.colidx = torch.as_tensor(colidx, dtype=torch.int32, device=self.device)
+        self.n = self.rowptr.shape[0] - 1
+        self.nnz = self.colidx.shape[0]
+        self.norm = norm
+        self.mu = None if mu is None else torch.as_tensor(mu, dtype=torch.float32,
+                                                          device=self.device)
+        self.rstd = None if rstd is None else torch.as_tensor(rstd, dtype=torch.float32,
+                                                              device=self.device)
+        biases = biases or [None] * len(weights_t)
+        acts = acts or ["none"] * len(weights_t)
+        self.layers = []
+        for wt, b, a in zip(weights_t, biases, acts):
+            wt = torch.as_tensor(wt, dtype=torch.float32, device=self.device).contiguous()
+            wbits, alpha = pack_weights(wt)
+            bt = None if b is None else torch.as_tensor(b, dtype=torch.float32,
+                                                        device=self.device)
+            self.layers.append(Layer(wt.shape[1], wt.shape[0], wbits, alpha, bt, a))
+        self.ws = torch.empty(forward_workspace_bytes(self.n, self.nnz, self.layers),
+                              dtype=torch.uint8, device=self.device)
+        self.out = torch.empty((self.n, self.layers[-1].d_out), dtype=torch.float32,
+                               device=self.device)
+
+    def forward(self, x: torch.Tensor, stream=None) -> torch.Tensor:
+        bigcn_forward(self.rowptr, self.colidx, x, self.layers, self.out, self.ws,
+                      self.mu, self.rstd, self.norm, stream=stream)
+        return self.out

@@ -1,0 +1,282 @@
+// C ABI of the binarized-GCN library: host-side argument validation and the
+// multi-layer forward orchestration.  Every entry point validates on the host
+// and then only enqueues kernels on the caller's stream.
+
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "../../include/bigcn.h"
+#include "bigcn_internal.h"
+
+namespace {
+
+using bigcn::IType;
+
+inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+inline int64_t words(int64_t k) { return (k + 63) / 64; }
+inline size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+inline bool itype_ok(int t) { return t == BIGCN_I32 || t == BIGCN_I16 || t == BIGCN_F16; }
+inline bool itype_holds(int t, int64_t K) {
+  return t == BIGCN_I32 || (t == BIGCN_I16 && K <= 32767) || (t == BIGCN_F16 && K <= 2048);
+}
+// Exact storage used inside the forward pass for a layer of width K.
+inline IType forward_itype(int64_t K) {
+  return K <= 2048 ? IType::F16 : (K <= 32767 ? IType::I16 : IType::I32);
+}
+
+inline bigcn_status hip_status(hipError_t e) { return e == hipSuccess ? BIGCN_OK : BIGCN_EHIP; }
+
+constexpr int32_t kMaxBgemmK = 8192;
+
+bigcn_status check_pack(const float* x, int64_t rows, int32_t cols, int64_t ldx,
+                        const float* mu, const float* rstd, int norm,
+                        const uint64_t* bits, int64_t ldw, const float* scale) {
+  if (rows < 0 || cols < 1 || ldx < cols || ldw < words(cols)) return BIGCN_EINVAL;
+  if ((mu == nullptr) != (rstd == nullptr)) return BIGCN_EINVAL;
+  if (norm != BIGCN_NORM_SYM && norm != BIGCN_NORM_MEAN) return BIGCN_EINVAL;
+  if (rows > 0 && (x == nullptr || bits == nullptr || scale == nullptr)) return BIGCN_EINVAL;
+  if (!aligned(x, 4) || !aligned(bits, 8) || !aligned(scale, 4)) return BIGCN_EALIGN;
+  if (mu != nullptr && (!aligned(mu, 4) || !aligned(rstd, 4))) return BIGCN_EALIGN;
+  return BIGCN_OK;
+}
+
+bigcn_status check_bgemm(const uint64_t* F, int64_t M, int64_t ldf,
+                         const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
+                         const void* C, int ctype, int64_t ldc, int algo) {
+  if (M < 0 || N < 1 || K < 1) return BIGCN_EINVAL;
+  if (ldf < words(K) || ldb < words(K) || ldc < N) return BIGCN_EINVAL;
+  if (!itype_ok(ctype) || !itype_holds(ctype, K)) return BIGCN_EINVAL;
+  if (algo != BIGCN_BGEMM_AUTO && algo != BIGCN_BGEMM_POPCOUNT && algo != BIGCN_BGEMM_MFMA_I8)
+    return BIGCN_EINVAL;
+  if (B == nullptr || (M > 0 && (F == nullptr || C == nullptr))) return BIGCN_EINVAL;
+  if (!aligned(F, 8) || !aligned(B, 8) || !aligned(C, bigcn::itype_size((IType)ctype)))
+    return BIGCN_EALIGN;
+  if (K > kMaxBgemmK) return BIGCN_EUNSUPPORTED;
+  return BIGCN_OK;
+}
+
+bigcn_status check_graph(int64_t n, int64_t nnz, const int64_t* rowptr,
+                         const int32_t* colidx, int norm) {
+  if (n < 0 || nnz < 0 || n > INT32_MAX) return BIGCN_EINVAL;
+  if (norm != BIGCN_NORM_SYM && norm != BIGCN_NORM_MEAN) return BIGCN_EINVAL;
+  if (n > 0 && rowptr == nullptr) return BIGCN_EINVAL;
+  if (nnz > 0 && colidx == nullptr) return BIGCN_EINVAL;
+  if (!aligned(rowptr, 8) || !aligned(colidx, 4)) return BIGCN_EALIGN;
+  return BIGCN_OK;
+}
+
+bigcn_status check_spmm_operands(int64_t n, const float* g, const void* C,
+                                 int ctype, int32_t d, int64_t ldc,
+                                 const float* alpha, const float* bias,
+                                 int act, const float* out, int64_t ldo) {
+  if (d < 1 || ldc < d || ldo < d || (ldc % 4) != 0) return BIGCN_EINVAL;
+  if (!itype_ok(ctype)) return BIGCN_EINVAL;
+  if (act != BIGCN_ACT_NONE && act != BIGCN_ACT_RELU) return BIGCN_EINVAL;
+  if (alpha == nullptr) return BIGCN_EINVAL;
+  if (n > 0 && (g == nullptr || C == nullptr || out == nullptr)) return BIGCN_EINVAL;
+  if (!aligned(g, 4) || !aligned(C, 4 * bigcn::itype_size((IType)ctype)) ||
+      !aligned(out, 4) || !aligned(alpha, 4) || !aligned(bias, 4))
+    return BIGCN_EALIGN;
+  return BIGCN_OK;
+}
+
+hipError_t run_bgemm(const uint64_t* F, int64_t M, int64_t ldf, const uint64_t* B,
+                     int32_t N, int64_t ldb, int32_t K, void* C, IType ct,
+                     int64_t ldc, int algo, hipStream_t s) {
+  if (algo == BIGCN_BGEMM_MFMA_I8 && bigcn::bgemm_mfma_supported(N, K))
+    return bigcn::launch_bgemm_mfma(F, M, ldf, B, N, ldb, K, C, ct, ldc, s);
+  return bigcn::launch_bgemm_popcount(F, M, ldf, B, N, ldb, K, C, ct, ldc, s);
+}
+
+// Workspace layout of bigcn_forward.
+struct ForwardLayout {
+  int64_t ldF, ldc, ldh;
+  size_t off_F, off_g, off_C, off_H0, off_H1, off_spmm, bytes;
+  int32_t dmax;
+};
+
+bool forward_layout(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t nl,
+                    ForwardLayout* L) {
+  int64_t kwmax = 1, dmax = 1, hmax = 1;
+  size_t esmax = 2;
+  for (int32_t l = 0; l < nl; ++l) {
+    kwmax = std::max<int64_t>(kwmax, words(layers[l].d_in));
+    dmax = std::max<int64_t>(dmax, layers[l].d_out);
+    esmax = std::max(esmax, bigcn::itype_size(forward_itype(layers[l].d_in)));
+    if (l + 1 < nl) hmax = std::max<int64_t>(hmax, layers[l].d_out);
+  }
+  L->ldF = (kwmax + 1) / 2 * 2;
+  L->ldc = (dmax + 7) / 8 * 8;
+  L->ldh = (hmax + 3) / 4 * 4;
+  L->dmax = (int32_t)dmax;
+  size_t off = 0;
+  L->off_F = off;
+  off += up256((size_t)n * L->ldF * 8);
+  L->off_g = off;
+  off += up256((size_t)n * 4);
+  L->off_C = off;
+  off += up256((size_t)n * L->ldc * esmax);
+  L->off_H0 = off;
+  if (nl >= 2) off += up256((size_t)n * L->ldh * 4);
+  L->off_H1 = off;
+  if (nl >= 3) off += up256((size_t)n * L->ldh * 4);
+  L->off_spmm = off;
+  off += bigcn::spmm_plan(n, nnz, (int32_t)dmax).bytes;
+  L->bytes = off;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* bigcn_status_string(bigcn_status s) {
+  switch (s) {
+    case BIGCN_OK: return "ok";
+    case BIGCN_EINVAL: return "invalid argument";
+    case BIGCN_EALIGN: return "misaligned pointer or leading dimension";
+    case BIGCN_EWORKSPACE: return "workspace missing or too small";
+    case BIGCN_EUNSUPPORTED: return "unsupported by this build";
+    case BIGCN_EHIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+bigcn_status bigcn_binarize_pack(const float* x, int64_t rows, int32_t cols,
+                                 int64_t ldx, const float* mu, const float* rstd,
+                                 const int64_t* rowptr, bigcn_norm norm,
+                                 uint64_t* bits, int64_t ldw, float* scale,
+                                 void* stream) {
+  bigcn_status st = check_pack(x, rows, cols, ldx, mu, rstd, norm, bits, ldw, scale);
+  if (st != BIGCN_OK) return st;
+  if (!aligned(rowptr, 8)) return BIGCN_EALIGN;
+  return hip_status(bigcn::launch_pack(x, rows, cols, ldx, mu, rstd, rowptr,
+                                       norm == BIGCN_NORM_SYM, bits, ldw, scale,
+                                       (hipStream_t)stream));
+}
+
+bigcn_status bigcn_bgemm(const uint64_t* F, int64_t M, int64_t ldf,
+                         const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
+                         void* C, bigcn_itype ctype, int64_t ldc,
+                         bigcn_bgemm_algo algo, void* stream) {
+  bigcn_status st = check_bgemm(F, M, ldf, B, N, ldb, K, C, ctype, ldc, algo);
+  if (st != BIGCN_OK) return st;
+  if (algo == BIGCN_BGEMM_MFMA_I8 && !bigcn::bgemm_mfma_supported(N, K))
+    return BIGCN_EUNSUPPORTED;
+  return hip_status(run_bgemm(F, M, ldf, B, N, ldb, K, C, (IType)ctype, ldc, algo,
+                              (hipStream_t)stream));
+}
+
+size_t bigcn_spmm_workspace_bytes(int64_t n, int64_t nnz, int32_t d) {
+  if (n < 0 || nnz < 0 || d < 1) return 0;
+  return bigcn::spmm_plan(n, nnz, d).bytes;
+}
+
+bigcn_status bigcn_spmm_csr(int64_t n, int64_t nnz, const int64_t* rowptr,
+                            const int32_t* colidx, bigcn_norm norm,
+                            const float* g, const void* C, bigcn_itype ctype,
+                            int32_t d, int64_t ldc, const float* alpha,
+                            const float* bias, bigcn_act act, float* out,
+                            int64_t ldo, void* workspace, size_t ws_bytes,
+                            void* stream) {
+  bigcn_status st = check_graph(n, nnz, rowptr, colidx, norm);
+  if (st != BIGCN_OK) return st;
+  st = check_spmm_operands(n, g, C, ctype, d, ldc, alpha, bias, act, out, ldo);
+  if (st != BIGCN_OK) return st;
+  const bigcn::SpmmPlan plan = bigcn::spmm_plan(n, nnz, d);
+  if (n > 0 && nnz > 0) {
+    if (workspace == nullptr || ws_bytes < plan.bytes) return BIGCN_EWORKSPACE;
+    if (!aligned(workspace, 256)) return BIGCN_EALIGN;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = bigcn::launch_spmm_rows(n, nnz, rowptr, plan, workspace, s);
+  if (e != hipSuccess) return BIGCN_EHIP;
+  return hip_status(bigcn::launch_spmm(n, nnz, rowptr, colidx,
+                                       norm == BIGCN_NORM_MEAN, g, C, (IType)ctype,
+                                       d, ldc, alpha, bias, act == BIGCN_ACT_RELU,
+                                       out, ldo, plan, workspace, s));
+}
+
+size_t bigcn_forward_workspace_bytes(int64_t n, int64_t nnz,
+                                     const bigcn_layer* layers, int32_t n_layers) {
+  if (n < 0 || nnz < 0 || layers == nullptr || n_layers < 1) return 0;
+  for (int32_t l = 0; l < n_layers; ++l)
+    if (layers[l].d_in < 1 || layers[l].d_out < 1) return 0;
+  ForwardLayout L;
+  forward_layout(n, nnz, layers, n_layers, &L);
+  return L.bytes;
+}
+
+bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
+                           const int32_t* colidx, bigcn_norm norm,
+                           const float* x, int64_t ldx, const float* mu,
+                           const float* rstd, const bigcn_layer* layers,
+                           int32_t n_layers, float* out, int64_t ldo,
+                           void* workspace, size_t ws_bytes, void* stream) {
+  if (layers == nullptr || n_layers < 1) return BIGCN_EINVAL;
+  bigcn_status st = check_graph(n, nnz, rowptr, colidx, norm);
+  if (st != BIGCN_OK) return st;
+  for (int32_t l = 0; l < n_layers; ++l) {
+    const bigcn_layer& ly = layers[l];
+    if (ly.d_in < 1 || ly.d_out < 1 || ly.ldw < words(ly.d_in)) return BIGCN_EINVAL;
+    if (l > 0 && ly.d_in != layers[l - 1].d_out) return BIGCN_EINVAL;
+    if (ly.wbits == nullptr || ly.alpha == nullptr) return BIGCN_EINVAL;
+    if (ly.act != BIGCN_ACT_NONE && ly.act != BIGCN_ACT_RELU) return BIGCN_EINVAL;
+    if (!aligned(ly.wbits, 8) || !aligned(ly.alpha, 4) || !aligned(ly.bias, 4))
+      return BIGCN_EALIGN;
+    if (ly.d_in > kMaxBgemmK) return BIGCN_EUNSUPPORTED;
+  }
+  if (ldx < layers[0].d_in || ldo < layers[n_layers - 1].d_out) return BIGCN_EINVAL;
+  if ((mu == nullptr) != (rstd == nullptr)) return BIGCN_EINVAL;
+  if (n > 0 && (x == nullptr || out == nullptr)) return BIGCN_EINVAL;
+  if (!aligned(x, 4) || !aligned(out, 4) || !aligned(mu, 4) || !aligned(rstd, 4))
+    return BIGCN_EALIGN;
+  ForwardLayout L;
+  forward_layout(n, nnz, layers, n_layers, &L);
+  if (n == 0) return BIGCN_OK;
+  if (workspace == nullptr || ws_bytes < L.bytes) return BIGCN_EWORKSPACE;
+  if (!aligned(workspace, 256)) return BIGCN_EALIGN;
+
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  uint64_t* F = (uint64_t*)(ws + L.off_F);
+  float* g = (float*)(ws + L.off_g);
+  void* C = ws + L.off_C;
+  float* H[2] = {(float*)(ws + L.off_H0), (float*)(ws + L.off_H1)};
+  void* wsp = ws + L.off_spmm;
+
+  // Per-worker start rows depend only on the graph and the chunk size, which
+  // is the same for every layer.
+  const bigcn::SpmmPlan plan0 = bigcn::spmm_plan(n, nnz, L.dmax);
+  hipError_t e = bigcn::launch_spmm_rows(n, nnz, rowptr, plan0, wsp, s);
+  if (e != hipSuccess) return BIGCN_EHIP;
+
+  const float* hin = x;
+  int64_t ldin = ldx;
+  for (int32_t l = 0; l < n_layers; ++l) {
+    const bigcn_layer& ly = layers[l];
+    const bool last = l + 1 == n_layers;
+    float* hout = last ? out : H[l & 1];
+    const int64_t ldout = last ? ldo : L.ldh;
+    const IType ct = forward_itype(ly.d_in);
+    e = bigcn::launch_pack(hin, n, ly.d_in, ldin, l == 0 ? mu : nullptr,
+                           l == 0 ? rstd : nullptr, rowptr, norm == BIGCN_NORM_SYM,
+                           F, L.ldF, g, s);
+    if (e != hipSuccess) return BIGCN_EHIP;
+    e = run_bgemm(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C, ct, L.ldc,
+                  BIGCN_BGEMM_AUTO, s);
+    if (e != hipSuccess) return BIGCN_EHIP;
+    const bigcn::SpmmPlan plan = bigcn::spmm_plan(n, nnz, ly.d_out);
+    e = bigcn::launch_spmm(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN, g, C, ct,
+                           ly.d_out, L.ldc, ly.alpha, ly.bias, ly.act == BIGCN_ACT_RELU,
+                           hout, ldout, plan, wsp, s);
+    if (e != hipSuccess) return BIGCN_EHIP;
+    hin = hout;
+    ldin = ldout;
+  }
+  return BIGCN_OK;
+}
+
+}  // extern "C"

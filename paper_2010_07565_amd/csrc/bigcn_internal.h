@@ -1,0 +1,61 @@
+// Internal launch interface between the C ABI layer (bigcn_api.hip) and the
+// gfx950 kernels (bigcn_kernels.hip).  Arguments are validated by the ABI
+// layer before any of these is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace bigcn {
+
+// Element storage of binary-GEMM products (same values as bigcn_itype).
+enum class IType : int { I32 = 0, I16 = 1, F16 = 2 };
+
+inline size_t itype_size(IType t) { return t == IType::I32 ? 4 : 2; }
+
+// Sign-pack rows of x; see bigcn_binarize_pack.  sym != 0 folds D̂^-1/2 into
+// the scale when rowptr is given.
+hipError_t launch_pack(const float* x, int64_t rows, int32_t cols, int64_t ldx,
+                       const float* mu, const float* rstd,
+                       const int64_t* rowptr, int sym, uint64_t* bits,
+                       int64_t ldw, float* scale, hipStream_t stream);
+
+// C[i][j] = K - 2 popcount(F_i ^ B_j) on the vector ALUs.
+hipError_t launch_bgemm_popcount(const uint64_t* F, int64_t M, int64_t ldf,
+                                 const uint64_t* B, int32_t N, int64_t ldb,
+                                 int32_t K, void* C, IType ct, int64_t ldc,
+                                 hipStream_t stream);
+
+// The same product with +-1 int8 operands on the matrix cores.
+bool bgemm_mfma_supported(int32_t N, int32_t K);
+hipError_t launch_bgemm_mfma(const uint64_t* F, int64_t M, int64_t ldf,
+                             const uint64_t* B, int32_t N, int64_t ldb,
+                             int32_t K, void* C, IType ct, int64_t ldc,
+                             hipStream_t stream);
+
+// Aggregation over the CSR of Â with the fused rescale / bias / activation
+// epilogue.  The edge range [0, nnz) is cut into fixed chunks of `chunk`
+// edges; see bigcn_kernels.hip for the scheme and the workspace layout.
+struct SpmmPlan {
+  int64_t chunk;      // edges per worker
+  int64_t workers;    // ceil(nnz / chunk), at least 1
+  int32_t dpad;       // columns per partial row (multiple of 4)
+  size_t bytes;       // workspace bytes
+  size_t off_rowof, off_tailrow, off_head, off_tail;
+};
+SpmmPlan spmm_plan(int64_t n, int64_t nnz, int32_t d);
+
+// Builds the per-worker start rows (once per graph and chunk size).
+hipError_t launch_spmm_rows(int64_t n, int64_t nnz, const int64_t* rowptr,
+                            const SpmmPlan& plan, void* workspace,
+                            hipStream_t stream);
+// Aggregation proper; requires launch_spmm_rows to have run on `workspace`.
+hipError_t launch_spmm(int64_t n, int64_t nnz, const int64_t* rowptr,
+                       const int32_t* colidx, int mean, const float* g,
+                       const void* C, IType ct, int32_t d, int64_t ldc,
+                       const float* alpha, const float* bias, int relu,
+                       float* out, int64_t ldo, const SpmmPlan& plan,
+                       void* workspace, hipStream_t stream);
+
+}  // namespace bigcn

@@ -1,0 +1,607 @@
+// gfx950 kernels of the binarized-GCN inference path.
+//
+//   k_pack        sign binarisation + per-row mean |y| scale (Eqs. (3)-(4),
+//                 (7)-(8)); one wave per row, one wave ballot per 64 elements
+//                 gives one packed 64-bit word directly.
+//   k_bgemm_pop   binary GEMM C = K - 2 popcount(F ^ B) (Eqs. (11)-(12)); the
+//                 packed weights sit in LDS, each wave owns a tile of RM rows
+//                 whose words arrive through scalar loads, each lane owns CN
+//                 output columns; v_xor_b32 + v_bcnt_u32_b32 per 32 bits.
+//   k_spmm        aggregation out = act(rowfac * alpha * sum g_j C_j + b)
+//                 (Eq. (13) with the rescale of Eq. (11)); the CSR edge range
+//                 is cut into equal chunks, one chunk per worker of L lanes,
+//                 so hub rows of power-law graphs are shared by many workers;
+//                 rows cut by a chunk boundary leave fp32 partial sums that
+//                 k_spmm_fix adds in chunk order (no atomics: bitwise
+//                 reproducible results).
+//
+// Wave size is 64 on gfx950 throughout.
+
+#include "bigcn_internal.h"
+
+#include <hip/hip_fp16.h>
+
+namespace bigcn {
+namespace {
+
+constexpr int kBlock = 256;  // 4 waves
+constexpr int kWavesPerBlock = kBlock / 64;
+
+typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef int int4_t __attribute__((ext_vector_type(4)));
+typedef float float4_t __attribute__((ext_vector_type(4)));
+
+__device__ inline int wave_index_in_block() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+}
+
+__device__ inline float wave_sum(float v) {
+  // Butterfly: every lane ends with the same, order-fixed sum.
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// ---------------------------------------------------------------- pack ----
+
+template <bool STD>
+__global__ __launch_bounds__(kBlock) void k_pack(
+    const float* __restrict__ x, int64_t rows, int32_t cols, int64_t ldx,
+    const float* __restrict__ mu, const float* __restrict__ rstd,
+    const int64_t* __restrict__ rowptr, int sym, uint64_t* __restrict__ bits,
+    int64_t ldw, float* __restrict__ scale) {
+  const int lane = threadIdx.x & 63;
+  const int64_t nwaves = (int64_t)gridDim.x * kWavesPerBlock;
+  const int kw = (cols + 63) >> 6;
+  for (int64_t r = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
+       r < rows; r += nwaves) {
+    const float* xr = x + r * ldx;
+    uint64_t* br = bits + r * ldw;
+    float l1 = 0.f;
+    for (int64_t wb = 0; wb < ldw; wb += 64) {
+      // Lane q keeps word wb + q of this batch of 64 words.
+      uint64_t mine = 0;
+      const int wend = (int)(wb + 64 < kw ? wb + 64 : kw);
+      int w = (int)wb;
+      for (; w + 4 <= wend; w += 4) {
+        float v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int k = (w + u) * 64 + lane;
+          v[u] = k < cols ? xr[k] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int k = (w + u) * 64 + lane;
+          const bool ok = k < cols;
+          float y = v[u];
+          if (STD && ok) {
+            const float t = y - mu[k];  // two separate fp32 roundings
+            y = t * rstd[k];
+          }
+          const uint64_t b = __builtin_amdgcn_ballot_w64(ok && y >= 0.f);
+          l1 += ok ? fabsf(y) : 0.f;
+          if (lane == (int)(w + u - wb)) mine = b;
+        }
+      }
+      for (; w < wend; ++w) {
+        const int k = w * 64 + lane;
+        const bool ok = k < cols;
+        float y = ok ? xr[k] : 0.f;
+        if (STD && ok) {
+          const float t = y - mu[k];
+          y = t * rstd[k];
+        }
+        const uint64_t b = __builtin_amdgcn_ballot_w64(ok && y >= 0.f);
+        l1 += ok ? fabsf(y) : 0.f;
+        if (lane == (int)(w - wb)) mine = b;
+      }
+      if (wb + lane < ldw) br[wb + lane] = mine;  // pad words stay zero
+    }
+    l1 = wave_sum(l1);
+    if (lane == 0) {
+      float s = l1 / (float)cols;
+      if (rowptr != nullptr && sym) {
+        const int64_t dg = rowptr[r + 1] - rowptr[r];
+        s = s * (dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f);
+      }
+      scale[r] = s;
+    }
+  }
+}
+
+// ------------------------------------------------------ bgemm (popcount) ----
+
+template <typename T>
+struct Vec4;
+template <>
+struct Vec4<_Float16> { typedef half4_t type; };
+template <>
+struct Vec4<int16_t> { typedef short4_t type; };
+template <>
+struct Vec4<int32_t> { typedef int4_t type; };
+
+template <typename T>
+__device__ inline T from_int(int v) { return (T)v; }
+
+// Stores CN consecutive results of one row.
+template <typename T, int CN>
+__device__ inline void store_row(T* __restrict__ dst, const int* v, int ncols,
+                                 bool vec) {
+  if (CN == 4 && vec && ncols >= 4) {
+    typename Vec4<T>::type p;
+    p[0] = from_int<T>(v[0]);
+    p[1] = from_int<T>(v[1]);
+    p[2] = from_int<T>(v[2]);
+    p[3] = from_int<T>(v[3]);
+    *reinterpret_cast<typename Vec4<T>::type*>(dst) = p;
+    return;
+  }
+#pragma unroll
+  for (int c = 0; c < CN; ++c)
+    if (c < ncols) dst[c] = from_int<T>(v[c]);
+}
+
+template <int CN, int RM, typename T>
+__global__ __launch_bounds__(kBlock) void k_bgemm_pop(
+    const uint64_t* __restrict__ F, int64_t M, int64_t ldf,
+    const uint64_t* __restrict__ B, int32_t N, int64_t ldb, int32_t K,
+    T* __restrict__ C, int64_t ldc, int vec) {
+  extern __shared__ uint64_t sB[];  // [kw][CN][64]: word w of column j0 + CN*l + c
+  const int lane = threadIdx.x & 63;
+  const int kw = (K + 63) >> 6;
+  const int j0 = blockIdx.y * 64 * CN;
+  for (int idx = threadIdx.x; idx < kw * CN * 64; idx += kBlock) {
+    const int l = idx & 63;
+    const int c = (idx >> 6) % CN;
+    const int w = idx / (64 * CN);
+    const int j = j0 + l * CN + c;
+    sB[idx] = j < N ? B[(int64_t)j * ldb + w] : 0ull;
+  }
+  __syncthreads();
+  const int64_t tiles = (M + RM - 1) / RM;
+  const int64_t nwaves = (int64_t)gridDim.x * kWavesPerBlock;
+  const int jl = j0 + lane * CN;  // first column of this lane
+  const int ncols = N - jl;       // valid columns from jl (may be <= 0)
+  for (int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
+       t < tiles; t += nwaves) {
+    const int64_t i0 = t * RM;
+    uint32_t acc[RM][CN];
+#pragma unroll
+    for (int r = 0; r < RM; ++r)
+#pragma unroll
+      for (int c = 0; c < CN; ++c) acc[r][c] = 0;
+    for (int w = 0; w < kw; ++w) {
+      uint64_t fw[RM];
+#pragma unroll
+      for (int r = 0; r < RM; ++r) {
+        const int64_t i = i0 + r < M ? i0 + r : M - 1;
+        fw[r] = F[i * ldf + w];  // wave-uniform address: scalar load
+      }
+      uint64_t bw[CN];
+#pragma unroll
+      for (int c = 0; c < CN; ++c) bw[c] = sB[(w * CN + c) * 64 + lane];
+#pragma unroll
+      for (int r = 0; r < RM; ++r)
+#pragma unroll
+        for (int c = 0; c < CN; ++c) {
+          const uint64_t z = fw[r] ^ bw[c];
+          acc[r][c] += __builtin_popcount((uint32_t)z);
+          acc[r][c] += __builtin_popcount((uint32_t)(z >> 32));
+        }
+    }
+    if (ncols > 0) {
+#pragma unroll
+      for (int r = 0; r < RM; ++r) {
+        if (i0 + r >= M) break;
+        int v[CN];
+#pragma unroll
+        for (int c = 0; c < CN; ++c) v[c] = K - 2 * (int)acc[r][c];
+        store_row<T, CN>(C + (i0 + r) * ldc + jl, v, ncols, vec != 0);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ spmm ----
+
+template <typename T>
+__device__ inline typename Vec4<T>::type load4(const T* p) {
+  return *reinterpret_cast<const typename Vec4<T>::type*>(p);
+}
+
+// acc[c] += g * v[c], one fused multiply-add per element; for half inputs
+// this is a single v_fma_mix_f32 (the conversion is exact).
+template <typename V>
+__device__ inline void fma4(float4_t& acc, float g, const V& v) {
+  acc[0] = fmaf((float)v[0], g, acc[0]);
+  acc[1] = fmaf((float)v[1], g, acc[1]);
+  acc[2] = fmaf((float)v[2], g, acc[2]);
+  acc[3] = fmaf((float)v[3], g, acc[3]);
+}
+
+struct Epi {
+  float alpha[4];
+  float bias[4];
+  int ncols;  // valid columns of this lane (0..4)
+  int mean;
+  int relu;
+};
+
+__device__ inline float act(float v, int relu) { return relu ? fmaxf(v, 0.f) : v; }
+
+__device__ inline void write_row(float* __restrict__ out, int64_t ldo, int64_t r,
+                                 int c0, const Epi& ep, const float4_t acc,
+                                 float rowfac) {
+  float* o = out + r * ldo + c0;
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    if (c < ep.ncols) o[c] = act(fmaf(acc[c], rowfac * ep.alpha[c], ep.bias[c]), ep.relu);
+}
+
+__device__ inline void write_empty(float* __restrict__ out, int64_t ldo,
+                                   int64_t r, int c0, const Epi& ep) {
+  float* o = out + r * ldo + c0;
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    if (c < ep.ncols) o[c] = act(ep.bias[c], ep.relu);
+}
+
+__device__ inline float row_factor(const int64_t* __restrict__ rowptr, int64_t r,
+                                   int mean) {
+  const float dg = (float)(rowptr[r + 1] - rowptr[r]);
+  return mean ? 1.0f / dg : 1.0f / sqrtf(dg);
+}
+
+// Worker w owns edges [w*chunk, min((w+1)*chunk, nnz)).  It aggregates every
+// row that starts inside its range and ends inside it; the row that reaches
+// past the range end leaves a "tail" partial (plus tail_row[w]); a row that
+// began before the range leaves a "head" partial.  Empty rows are written as
+// act(bias) by the worker whose range holds their position.
+template <int L, typename T, int U>
+__global__ __launch_bounds__(kBlock) void k_spmm(
+    int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
+    const int32_t* __restrict__ colidx, int mean, const float* __restrict__ g,
+    const T* __restrict__ C, int32_t d, int64_t ldc,
+    const float* __restrict__ alpha, const float* __restrict__ bias, int relu,
+    float* __restrict__ out, int64_t ldo, int64_t chunk, int64_t workers,
+    int32_t dpad, const int32_t* __restrict__ row_of,
+    int32_t* __restrict__ tail_row, float* __restrict__ head,
+    float* __restrict__ tail) {
+  constexpr int P = 64 / L;
+  const int lane = threadIdx.x & 63;
+  const int slot = lane / L;
+  if (slot >= P) return;  // idle lanes when L does not divide 64
+  const int sub = lane - slot * L;
+  const int64_t w =
+      ((int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * P + slot;
+  if (w >= workers) return;
+  const int c0 = blockIdx.y * (L * 4) + sub * 4;
+  Epi ep;
+  ep.ncols = d - c0 < 0 ? 0 : (d - c0 > 4 ? 4 : d - c0);
+  ep.mean = mean;
+  ep.relu = relu;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    ep.alpha[c] = c < ep.ncols ? alpha[c0 + c] : 0.f;
+    ep.bias[c] = (c < ep.ncols && bias != nullptr) ? bias[c0 + c] : 0.f;
+  }
+  const bool load_cols = ep.ncols > 0;
+
+  const int64_t s = w * chunk;
+  const int64_t t = s + chunk < nnz ? s + chunk : nnz;
+  int64_t r = row_of[w];
+  int64_t cur_end = rowptr[r + 1];
+  bool before = rowptr[r] < s;
+  if (!before) {
+    for (int64_t q = r - 1; q >= 0 && rowptr[q] == s; --q)
+      write_empty(out, ldo, q, c0, ep);
+  }
+  float4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
+
+  for (int64_t e = s; e < t; e += U) {
+    int32_t jj[U];
+    float gg[U];
+    typename Vec4<T>::type vv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) jj[u] = e + u < t ? colidx[e + u] : -1;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      gg[u] = jj[u] >= 0 ? g[jj[u]] : 0.f;
+      if (jj[u] >= 0 && load_cols)
+        vv[u] = load4<T>(C + (int64_t)jj[u] * ldc + c0);
+      else
+        vv[u] = typename Vec4<T>::type{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t eu = e + u;
+      if (eu >= t) break;
+      if (eu == cur_end) {
+        // Row r is finished inside this range.
+        const float4_t sum = a0 + a1;
+        if (before) {
+          if (load_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
+        } else {
+          write_row(out, ldo, r, c0, ep, sum, row_factor(rowptr, r, mean));
+        }
+        a0 = float4_t{0.f, 0.f, 0.f, 0.f};
+        a1 = float4_t{0.f, 0.f, 0.f, 0.f};
+        before = false;
+        ++r;
+        cur_end = rowptr[r + 1];
+        while (cur_end == eu) {  // empty rows
+          write_empty(out, ldo, r, c0, ep);
+          ++r;
+          cur_end = rowptr[r + 1];
+        }
+      }
+      if (u & 1)
+        fma4(a1, gg[u], vv[u]);
+      else
+        fma4(a0, gg[u], vv[u]);
+    }
+  }
+  const float4_t sum = a0 + a1;
+  if (cur_end == t) {
+    if (before) {
+      if (load_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
+    } else {
+      write_row(out, ldo, r, c0, ep, sum, row_factor(rowptr, r, mean));
+    }
+    if (t == nnz)
+      for (int64_t q = r + 1; q < n; ++q) write_empty(out, ldo, q, c0, ep);
+    if (sub == 0 && blockIdx.y == 0) tail_row[w] = -1;
+  } else if (before) {
+    if (load_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
+    if (sub == 0 && blockIdx.y == 0) tail_row[w] = -1;
+  } else {
+    if (load_cols) *reinterpret_cast<float4_t*>(tail + w * dpad + c0) = sum;
+    if (sub == 0 && blockIdx.y == 0) tail_row[w] = (int32_t)r;
+  }
+}
+
+// Rows cut by chunk boundaries: tail of the owning worker, then the heads of
+// the following workers in order.  One wave per worker.
+__global__ __launch_bounds__(kBlock) void k_spmm_fix(
+    const int64_t* __restrict__ rowptr, int mean, int32_t d,
+    const float* __restrict__ alpha, const float* __restrict__ bias, int relu,
+    float* __restrict__ out, int64_t ldo, int64_t chunk, int64_t workers,
+    int32_t dpad, const int32_t* __restrict__ tail_row,
+    const float* __restrict__ head, const float* __restrict__ tail) {
+  const int lane = threadIdx.x & 63;
+  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
+  if (w >= workers) return;
+  const int32_t r = tail_row[w];
+  if (r < 0) return;
+  const int64_t wend = (rowptr[r + 1] - 1) / chunk;
+  const float rowfac = row_factor(rowptr, r, mean);
+  for (int k = lane; k < d; k += 64) {
+    float s = tail[w * dpad + k];
+    for (int64_t v = w + 1; v <= wend; ++v) s += head[v * dpad + k];
+    const float b = bias != nullptr ? bias[k] : 0.f;
+    out[(int64_t)r * ldo + k] = act(fmaf(s, rowfac * alpha[k], b), relu);
+  }
+}
+
+// row_of[w] = the row holding edge w*chunk.  One thread per row.
+__global__ __launch_bounds__(kBlock) void k_spmm_rows(
+    int64_t n, const int64_t* __restrict__ rowptr, int64_t chunk,
+    int32_t* __restrict__ row_of) {
+  const int64_t r = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (r >= n) return;
+  const int64_t a = rowptr[r], b = rowptr[r + 1];
+  if (b <= a) return;
+  for (int64_t w = (a + chunk - 1) / chunk; w * chunk < b; ++w) row_of[w] = (int32_t)r;
+}
+
+// Graph without edges: every row is act(bias).
+__global__ __launch_bounds__(kBlock) void k_spmm_empty(
+    int64_t n, int32_t d, const float* __restrict__ bias, int relu,
+    float* __restrict__ out, int64_t ldo) {
+  const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (i >= n * (int64_t)d) return;
+  const int64_t r = i / d;
+  const int k = (int)(i - r * d);
+  out[r * ldo + k] = act(bias != nullptr ? bias[k] : 0.f, relu);
+}
+
+inline unsigned grid_cap(int64_t want, int64_t cap) {
+  if (want < 1) want = 1;
+  return (unsigned)(want < cap ? want : cap);
+}
+
+template <int CN, typename T>
+hipError_t bgemm_pop_typed(const uint64_t* F, int64_t M, int64_t ldf,
+                           const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
+                           T* C, int64_t ldc, int vec, hipStream_t stream) {
+  constexpr int RM = 4;
+  const int kw = (K + 63) >> 6;
+  const size_t lds = (size_t)kw * CN * 64 * sizeof(uint64_t);
+  const int64_t tiles = (M + RM - 1) / RM;
+  dim3 grid(grid_cap((tiles + kWavesPerBlock - 1) / kWavesPerBlock, 4096),
+            (unsigned)((N + 64 * CN - 1) / (64 * CN)));
+  hipLaunchKernelGGL((k_bgemm_pop<CN, RM, T>), grid, dim3(kBlock), lds, stream,
+                     F, M, ldf, B, N, ldb, K, C, ldc, vec);
+  return hipGetLastError();
+}
+
+template <int CN>
+hipError_t bgemm_pop_cn(const uint64_t* F, int64_t M, int64_t ldf,
+                        const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
+                        void* C, IType ct, int64_t ldc, hipStream_t stream) {
+  const size_t es = itype_size(ct);
+  const int vec = (ldc % CN == 0) && ((uintptr_t)C % (CN * es) == 0);
+  switch (ct) {
+    case IType::F16:
+      return bgemm_pop_typed<CN>(F, M, ldf, B, N, ldb, K, (_Float16*)C, ldc, vec, stream);
+    case IType::I16:
+      return bgemm_pop_typed<CN>(F, M, ldf, B, N, ldb, K, (int16_t*)C, ldc, vec, stream);
+    default:
+      return bgemm_pop_typed<CN>(F, M, ldf, B, N, ldb, K, (int32_t*)C, ldc, vec, stream);
+  }
+}
+
+template <int L, typename T>
+hipError_t spmm_typed(int64_t n, int64_t nnz, const int64_t* rowptr,
+                      const int32_t* colidx, int mean, const float* g,
+                      const T* C, int32_t d, int64_t ldc, const float* alpha,
+                      const float* bias, int relu, float* out, int64_t ldo,
+                      const SpmmPlan& p, void* ws, hipStream_t stream) {
+  char* base = (char*)ws;
+  const int32_t* row_of = (const int32_t*)(base + p.off_rowof);
+  int32_t* tail_row = (int32_t*)(base + p.off_tailrow);
+  float* head = (float*)(base + p.off_head);
+  float* tail = (float*)(base + p.off_tail);
+  constexpr int P = 64 / L;
+  const int64_t waves = (p.workers + P - 1) / P;
+  dim3 grid((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock),
+            (unsigned)((d + L * 4 - 1) / (L * 4)));
+  hipLaunchKernelGGL((k_spmm<L, T, 4>), grid, dim3(kBlock), 0, stream, n, nnz,
+                     rowptr, colidx, mean, g, C, d, ldc, alpha, bias, relu, out,
+                     ldo, p.chunk, p.workers, p.dpad, row_of, tail_row, head,
+                     tail);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_spmm_fix,
+                     dim3((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock)),
+                     dim3(kBlock), 0, stream, rowptr, mean, d, alpha, bias, relu,
+                     out, ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t spmm_dispatch_l(int64_t n, int64_t nnz, const int64_t* rowptr,
+                           const int32_t* colidx, int mean, const float* g,
+                           const T* C, int32_t d, int64_t ldc,
+                           const float* alpha, const float* bias, int relu,
+                           float* out, int64_t ldo, const SpmmPlan& p, void* ws,
+                           hipStream_t stream) {
+  const int lanes = (d + 3) / 4;  // lanes that cover d columns, 4 per lane
+#define BIGCN_SPMM_L(LV)                                                       \
+  return spmm_typed<LV, T>(n, nnz, rowptr, colidx, mean, g, C, d, ldc, alpha, \
+                           bias, relu, out, ldo, p, ws, stream)
+  if (lanes <= 2) BIGCN_SPMM_L(2);
+  if (lanes <= 4) BIGCN_SPMM_L(4);
+  if (lanes <= 8) BIGCN_SPMM_L(8);
+  if (lanes <= 12) BIGCN_SPMM_L(12);
+  if (lanes <= 16) BIGCN_SPMM_L(16);
+  if (lanes <= 32) BIGCN_SPMM_L(32);
+  BIGCN_SPMM_L(64);
+#undef BIGCN_SPMM_L
+}
+
+}  // namespace
+
+// ------------------------------------------------------------- launchers ----
+
+hipError_t launch_pack(const float* x, int64_t rows, int32_t cols, int64_t ldx,
+                       const float* mu, const float* rstd,
+                       const int64_t* rowptr, int sym, uint64_t* bits,
+                       int64_t ldw, float* scale, hipStream_t stream) {
+  if (rows == 0) return hipSuccess;
+  dim3 grid(grid_cap((rows + kWavesPerBlock - 1) / kWavesPerBlock, 8192));
+  if (mu != nullptr)
+    hipLaunchKernelGGL(k_pack<true>, grid, dim3(kBlock), 0, stream, x, rows, cols,
+                       ldx, mu, rstd, rowptr, sym, bits, ldw, scale);
+  else
+    hipLaunchKernelGGL(k_pack<false>, grid, dim3(kBlock), 0, stream, x, rows,
+                       cols, ldx, mu, rstd, rowptr, sym, bits, ldw, scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_bgemm_popcount(const uint64_t* F, int64_t M, int64_t ldf,
+                                 const uint64_t* B, int32_t N, int64_t ldb,
+                                 int32_t K, void* C, IType ct, int64_t ldc,
+                                 hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  const int kw = (K + 63) >> 6;
+  // Columns per lane: as many as the width needs (up to 4), limited so the
+  // packed weight slab stays within 64 KiB of LDS.
+  int cn = N <= 64 ? 1 : (N <= 128 ? 2 : 4);
+  while (cn > 1 && (size_t)kw * cn * 64 * 8 > 65536) cn >>= 1;
+  if (cn == 4) return bgemm_pop_cn<4>(F, M, ldf, B, N, ldb, K, C, ct, ldc, stream);
+  if (cn == 2) return bgemm_pop_cn<2>(F, M, ldf, B, N, ldb, K, C, ct, ldc, stream);
+  return bgemm_pop_cn<1>(F, M, ldf, B, N, ldb, K, C, ct, ldc, stream);
+}
+
+SpmmPlan spmm_plan(int64_t n, int64_t nnz, int32_t d) {
+  (void)n;
+  SpmmPlan p;
+  // About 16K workers on big graphs; chunks of 16 .. 2048 edges.
+  int64_t chunk = 16;
+  while (chunk < 2048 && chunk * 2 * 16384 <= nnz) chunk *= 2;
+  p.chunk = chunk;
+  p.workers = nnz > 0 ? (nnz + chunk - 1) / chunk : 1;
+  const int lanes = (d + 3) / 4;
+  const int L = lanes <= 2 ? 2 : lanes <= 4 ? 4 : lanes <= 8 ? 8 : lanes <= 12 ? 12
+              : lanes <= 16 ? 16 : lanes <= 32 ? 32 : 64;
+  const int64_t slab = 4 * L;
+  p.dpad = (int32_t)(((d + slab - 1) / slab) * slab);
+  auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
+  size_t off = 0;
+  p.off_rowof = off;
+  off += up((size_t)p.workers * 4);
+  p.off_tailrow = off;
+  off += up((size_t)p.workers * 4);
+  p.off_head = off;
+  off += up((size_t)p.workers * p.dpad * 4);
+  p.off_tail = off;
+  off += up((size_t)p.workers * p.dpad * 4);
+  p.bytes = off;
+  return p;
+}
+
+hipError_t launch_spmm_rows(int64_t n, int64_t nnz, const int64_t* rowptr,
+                            const SpmmPlan& plan, void* workspace,
+                            hipStream_t stream) {
+  if (nnz == 0 || n == 0) return hipSuccess;
+  int32_t* row_of = (int32_t*)((char*)workspace + plan.off_rowof);
+  hipLaunchKernelGGL(k_spmm_rows, dim3((unsigned)((n + kBlock - 1) / kBlock)),
+                     dim3(kBlock), 0, stream, n, rowptr, plan.chunk, row_of);
+  return hipGetLastError();
+}
+
+hipError_t launch_spmm(int64_t n, int64_t nnz, const int64_t* rowptr,
+                       const int32_t* colidx, int mean, const float* g,
+                       const void* C, IType ct, int32_t d, int64_t ldc,
+                       const float* alpha, const float* bias, int relu,
+                       float* out, int64_t ldo, const SpmmPlan& plan,
+                       void* workspace, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  if (nnz == 0) {
+    const int64_t total = n * (int64_t)d;
+    hipLaunchKernelGGL(k_spmm_empty, dim3((unsigned)((total + kBlock - 1) / kBlock)),
+                       dim3(kBlock), 0, stream, n, d, bias, relu, out, ldo);
+    return hipGetLastError();
+  }
+  switch (ct) {
+    case IType::F16:
+      return spmm_dispatch_l<_Float16>(n, nnz, rowptr, colidx, mean, g,
+                                       (const _Float16*)C, d, ldc, alpha, bias,
+                                       relu, out, ldo, plan, workspace, stream);
+    case IType::I16:
+      return spmm_dispatch_l<int16_t>(n, nnz, rowptr, colidx, mean, g,
+                                      (const int16_t*)C, d, ldc, alpha, bias,
+                                      relu, out, ldo, plan, workspace, stream);
+    default:
+      return spmm_dispatch_l<int32_t>(n, nnz, rowptr, colidx, mean, g,
+                                      (const int32_t*)C, d, ldc, alpha, bias,
+                                      relu, out, ldo, plan, workspace, stream);
+  }
+}
+
+bool bgemm_mfma_supported(int32_t N, int32_t K) {
+  (void)N;
+  (void)K;
+  return false;
+}
+
+hipError_t launch_bgemm_mfma(const uint64_t*, int64_t, int64_t, const uint64_t*,
+                             int32_t, int64_t, int32_t, void*, IType, int64_t,
+                             hipStream_t) {
+  return hipErrorNotSupported;
+}
+
+}  // namespace bigcn

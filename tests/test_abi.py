@@ -1,0 +1,147 @@
+"""Host-only checks of the C ABI: the library loads, exports every function
+the header declares, and rejects invalid arguments before touching a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2010_07565_amd as bg
+from paper_2010_07565_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bigcn.h")
+
+EINVAL, EALIGN, EWORKSPACE, EUNSUPPORTED = -1, -2, -3, -4
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bigcn_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_expected_entry_points():
+    assert declared_functions() == sorted(bg.EXPORTS)
+
+
+def test_library_exports_every_declared_function():
+    lib = bg.load()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    lib = bg.load()
+    for st in (0, -1, -2, -3, -4, -5):
+        assert lib.bigcn_status_string(st)
+    assert lib.bigcn_status_string(-99) == b"unknown status"
+
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+def test_pack_validation():
+    lib = bg.load()
+    f = lib.bigcn_binarize_pack
+    assert f(FAKE, -1, 5, 5, None, None, None, 0, FAKE, 1, FAKE, None) == EINVAL
+    assert f(FAKE, 4, 0, 5, None, None, None, 0, FAKE, 1, FAKE, None) == EINVAL
+    assert f(FAKE, 4, 6, 5, None, None, None, 0, FAKE, 1, FAKE, None) == EINVAL   # ldx
+    assert f(FAKE, 4, 65, 65, None, None, None, 0, FAKE, 1, FAKE, None) == EINVAL  # ldw
+    assert f(FAKE, 4, 5, 5, FAKE, None, None, 0, FAKE, 1, FAKE, None) == EINVAL   # mu only
+    assert f(FAKE, 4, 5, 5, None, None, None, 7, FAKE, 1, FAKE, None) == EINVAL   # norm
+    assert f(None, 4, 5, 5, None, None, None, 0, FAKE, 1, FAKE, None) == EINVAL
+    assert f(FAKE + 2, 4, 5, 5, None, None, None, 0, FAKE, 1, FAKE, None) == EALIGN
+    assert f(FAKE, 4, 5, 5, None, None, None, 0, FAKE + 4, 1, FAKE, None) == EALIGN
+
+
+def test_bgemm_validation():
+    lib = bg.load()
+    f = lib.bigcn_bgemm
+    ok = (FAKE, 10, 1, FAKE, 8, 1, 64, FAKE, 0, 8, 0, None)
+    bad = [
+        ((1, -1), EINVAL), ((4, 0), EINVAL), ((6, 0), EINVAL), ((2, 0), EINVAL),
+        ((5, 0), EINVAL), ((9, 7), EINVAL), ((8, 5), EINVAL), ((10, 3), EINVAL),
+        ((0, FAKE + 4), EALIGN), ((7, FAKE + 2), EALIGN),
+    ]
+    for (pos, val), want in bad:
+        args = list(ok)
+        args[pos] = val
+        assert f(*args) == want, (pos, val)
+    # I16 needs K <= 32767, F16 needs K <= 2048; K > 8192 is unsupported.
+    assert f(FAKE, 10, 64, FAKE, 8, 64, 4000, FAKE, 2, 8, 0, None) == EINVAL
+    assert f(FAKE, 10, 200, FAKE, 8, 200, 9000, FAKE, 0, 8, 0, None) == EUNSUPPORTED
+
+
+def test_spmm_validation():
+    lib = bg.load()
+    f = lib.bigcn_spmm_csr
+    base = [10, 40, FAKE, FAKE, 0, FAKE, FAKE, 2, 7, 8, FAKE, None, 0, FAKE, 7,
+            FAKE, 1 << 20, None]
+    assert f(*base[:15], None, 0, None) == EWORKSPACE
+    assert f(*base[:15], FAKE, 16, None) == EWORKSPACE
+    assert f(*base[:15], FAKE + 64, 1 << 20, None) == EALIGN
+    for pos, val, want in [(0, -1, EINVAL), (1, -5, EINVAL), (4, 3, EINVAL),
+                           (7, 9, EINVAL), (8, 0, EINVAL), (9, 6, EINVAL),
+                           (9, 10, EINVAL), (12, 2, EINVAL), (14, 6, EINVAL),
+                           (10, None, EINVAL), (2, FAKE + 4, EALIGN),
+                           (6, FAKE + 2, EALIGN)]:
+        args = list(base)
+        args[pos] = val
+        assert f(*args) == want, (pos, val)
+
+
+def test_forward_validation():
+    lib = bg.load()
+    L = _lib._Layer
+    layers = (L * 2)(L(100, 16, FAKE, 2, FAKE, None, 0), L(16, 4, FAKE, 1, FAKE, None, 0))
+    n, nnz = 50, 200
+    need = lib.bigcn_forward_workspace_bytes(n, nnz, layers, 2)
+    assert need > 0
+    args = [n, nnz, FAKE, FAKE, 0, FAKE, 100, None, None, layers, 2, FAKE, 4, FAKE,
+            need, None]
+    a = list(args)
+    a[14] = need - 1
+    assert lib.bigcn_forward(*a) == EWORKSPACE
+    a = list(args)
+    a[10] = 0
+    assert lib.bigcn_forward(*a) == EINVAL
+    bad = (L * 2)(L(100, 16, FAKE, 2, FAKE, None, 0), L(15, 4, FAKE, 1, FAKE, None, 0))
+    a = list(args)
+    a[9] = bad
+    assert lib.bigcn_forward(*a) == EINVAL        # widths do not chain
+    short = (L * 2)(L(100, 16, FAKE, 1, FAKE, None, 0), L(16, 4, FAKE, 1, FAKE, None, 0))
+    a = list(args)
+    a[9] = short
+    assert lib.bigcn_forward(*a) == EINVAL        # ldw < ceil(100/64)
+    a = list(args)
+    a[6] = 99
+    assert lib.bigcn_forward(*a) == EINVAL        # ldx < d_in
+    a = list(args)
+    a[13] = FAKE + 128
+    assert lib.bigcn_forward(*a) == EALIGN        # workspace alignment
+
+
+def test_workspace_queries_grow_with_size():
+    s1 = bg.spmm_workspace_bytes(1000, 10_000, 64)
+    s2 = bg.spmm_workspace_bytes(1000, 1_000_000, 64)
+    s3 = bg.spmm_workspace_bytes(1000, 1_000_000, 256)
+    assert 0 < s1 < s2 < s3
+    assert bg.spmm_workspace_bytes(-1, 10, 4) == 0
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_forward_workspace_fits_the_workloads(cfg):
+    """The workspace needed by each workload stays a small multiple of the
+    node data (well inside 288 GB)."""
+    import workloads
+    c = workloads.CONFIGS[cfg]
+    n, nnz = c["n"], 2 * c["undirected"] + c["n"]
+    dims = c["dims"]
+    L = _lib._Layer
+    arr = (L * (len(dims) - 1))(*[L(dims[i], dims[i + 1], FAKE, (dims[i] + 63) // 64,
+                                    FAKE, None, 0) for i in range(len(dims) - 1)])
+    ws = bg.load().bigcn_forward_workspace_bytes(n, nnz, arr, len(dims) - 1)
+    hidden = max(dims[1:-1]) if len(dims) > 2 else 0
+    assert ws >= n * 2 * max(dims[1:])           # the product matrix alone
+    assert ws <= n * (8 * 64 + 2 * 4 * hidden + 4 * 256 + 64) + 8 * nnz + (64 << 20)

@@ -1,0 +1,264 @@
+"""GPU path (through the C ABI) against the CPU oracle, stage by stage.
+
+Bits and binary-GEMM integers must match bit for bit; scales within 1e-5
+relative; layer outputs within 1e-5 of the summed-term mass (helpers.TOL).
+Every input comes from the seeded generators or from the oracle; nothing the
+GPU computes is fed to the oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+import paper_2010_07565_amd as bg
+from helpers import TOL, mass_error, plain_rel_error, u64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    bg.load()
+    return torch.device("cuda:0")
+
+
+def _t(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+def _colnorm(rowptr):
+    return 1.0 / np.sqrt(np.diff(rowptr).astype(np.float64))
+
+
+# ------------------------------------------------------------------- pack --
+
+PACK_SHAPES = [(1, 1), (3, 63), (5, 64), (7, 65), (130, 127), (257, 128),
+               (100, 500), (33, 1433), (20, 4200)]
+
+
+@pytest.mark.parametrize("rows,cols", PACK_SHAPES)
+@pytest.mark.parametrize("mode", ["plain", "std_sym", "std_mean"])
+def test_pack_matches_oracle(dev, rows, cols, mode):
+    rng = np.random.default_rng(rows * 7919 + cols)
+    x = rng.standard_normal((rows, cols)).astype(np.float32)
+    x[:, ::7] = 0.0
+    x[::3, 1::11] = -0.0
+    mu = rstd = None
+    if mode != "plain":
+        mu, rstd = workloads.bn_stats(x)
+        x[::2, ::5] = mu[::5]           # exact zeros after standardisation
+    g = workloads.random_small_graph(rows, 3 * rows, rng) if rows > 1 else \
+        workloads.graph_from_edges(1, [])
+    kw = (cols + 63) // 64
+    ldw = kw + 2
+    ref_bits, ref_beta = oracle.binarize(x, mu, rstd, ldw=ldw)
+    bits = torch.full((rows, ldw), -1, dtype=torch.int64, device=dev)   # poison
+    scale = torch.full((rows,), float("nan"), dtype=torch.float32, device=dev)
+    norm = "mean" if mode == "std_mean" else "sym"
+    rowptr = None if mode == "plain" else _t(g.rowptr, dev)
+    bg.bigcn_binarize_pack(_t(x, dev), bits, scale,
+                           None if mu is None else _t(mu, dev),
+                           None if rstd is None else _t(rstd, dev), rowptr, norm)
+    torch.cuda.synchronize()
+    assert np.array_equal(u64(bits), ref_bits)
+    want = ref_beta * (_colnorm(g.rowptr) if mode == "std_sym" else 1.0)
+    got = scale.cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(got - want) <= 1e-5 * np.abs(want) + 1e-30)
+
+
+def test_pack_strided_input(dev):
+    rng = np.random.default_rng(5)
+    big = rng.standard_normal((50, 300)).astype(np.float32)
+    x = big[:, 17:17 + 200]
+    ref_bits, ref_beta = oracle.binarize(x)
+    xt = _t(big, dev)[:, 17:17 + 200]
+    bits = torch.empty((50, 4), dtype=torch.int64, device=dev)
+    scale = torch.empty(50, dtype=torch.float32, device=dev)
+    bg.bigcn_binarize_pack(xt, bits, scale)
+    torch.cuda.synchronize()
+    assert np.array_equal(u64(bits), ref_bits)
+    assert np.allclose(scale.cpu().numpy(), ref_beta, rtol=1e-5, atol=0)
+
+
+# ------------------------------------------------------------------ bgemm --
+
+BGEMM_SHAPES = [(1, 1, 1), (5, 3, 63), (130, 7, 64), (257, 40, 65), (100, 41, 100),
+                (64, 47, 128), (1000, 64, 256), (333, 65, 500), (77, 128, 602),
+                (999, 200, 1433), (513, 256, 256), (70, 300, 4100), (9, 256, 8192),
+                (4099, 256, 128)]
+
+
+@pytest.mark.parametrize("M,N,K", BGEMM_SHAPES)
+def test_bgemm_matches_oracle(dev, M, N, K):
+    rng = np.random.default_rng(M * 131 + N * 17 + K)
+    F, _ = oracle.binarize(rng.standard_normal((M, K)).astype(np.float32))
+    B, _ = oracle.binarize(rng.standard_normal((N, K)).astype(np.float32))
+    F[M // 2] = B[N // 2]                      # an exact +K entry
+    ref = oracle.sign_dot(F, B, K)
+    Ft, Bt = _t(F.view(np.int64), dev), _t(B.view(np.int64), dev)
+    for ctype, dt in (("i32", torch.int32), ("i16", torch.int16), ("f16", torch.float16)):
+        if ctype == "f16" and K > 2048:
+            continue
+        ldc = N + 5
+        C = torch.full((M, ldc), 77, dtype=dt, device=dev)             # poison
+        bg.bigcn_bgemm(Ft, Bt, K, C[:, :N], algo="popcount")
+        torch.cuda.synchronize()
+        got = C.cpu().numpy()
+        assert np.array_equal(got[:, :N].astype(np.int64), ref), ctype
+        assert np.all(got[:, N:] == 77), ctype                          # pads untouched
+
+
+# ------------------------------------------------------------------- spmm --
+
+def _star_plus_random(n, rng):
+    g = workloads.random_small_graph(n, 3 * n, rng, isolated=5)
+    edges = set()
+    for i in range(n - 5):
+        for j in g.colidx[g.rowptr[i]:g.rowptr[i + 1]]:
+            if i < j:
+                edges.add((i, int(j)))
+    for j in range(1, n - 5, 2):               # hub: node 0 reaches half the graph
+        edges.add((0, j))
+    return workloads.graph_from_edges(n, sorted(edges))
+
+
+def _with_empty_rows(rng):
+    """CSR (no self-loops) with empty rows at the start, the end, in runs and
+    around chunk boundaries."""
+    n = 400
+    deg = rng.integers(0, 40, size=n)
+    deg[:3] = 0
+    deg[-4:] = 0
+    deg[100:110] = 0
+    deg[200] = 900
+    rowptr = np.concatenate([[0], np.cumsum(deg)]).astype(np.int64)
+    live = np.flatnonzero(deg > 0)          # sources must have D̂_jj > 0
+    colidx = np.concatenate([np.sort(rng.choice(live, size=k, replace=k > len(live)))
+                             for k in deg]).astype(np.int32)
+    return workloads.Graph(n, rowptr, colidx)
+
+
+SPMM_D = [1, 3, 7, 8, 40, 41, 47, 64, 256, 300]
+
+
+@pytest.mark.parametrize("graph_kind", ["star", "empty_rows"])
+@pytest.mark.parametrize("d", SPMM_D)
+def test_spmm_matches_oracle(dev, graph_kind, d):
+    rng = np.random.default_rng(d * 13 + (graph_kind == "star"))
+    g = _star_plus_random(600, rng) if graph_kind == "star" else _with_empty_rows(rng)
+    K = 1433
+    dot = (2 * rng.integers(-40, 41, size=(g.n, d)) + 1).astype(np.int64)
+    dot[::17] = K                               # extreme values
+    beta = rng.uniform(0.1, 2.0, g.n).astype(np.float32).astype(np.float64)
+    alpha = rng.uniform(0.1, 2.0, d).astype(np.float32)
+    bias = rng.uniform(-0.1, 0.1, d).astype(np.float32)
+    combos = [("f16", "sym", None, "none"), ("i16", "mean", bias, "relu"),
+              ("i32", "sym", bias, "none"), ("f16", "mean", bias, "relu")]
+    for ctype, norm, b, act in combos:
+        z, m, _ = oracle.aggregate(g.rowptr, g.colidx, norm, beta, alpha.astype(np.float64),
+                                   dot, b, act)
+        deg = np.diff(g.rowptr).astype(np.float64)
+        if norm == "sym":
+            cn = np.where(deg > 0, 1.0 / np.sqrt(np.maximum(deg, 1)), 0.0)
+            gg = (beta * cn).astype(np.float32)
+        else:
+            gg = beta.astype(np.float32)
+        dt = bg._lib.ITYPE_DTYPES[ctype]
+        ldc = (d + 3) // 4 * 4 + 4
+        C = torch.zeros((g.n, ldc), dtype=dt, device=dev)
+        C[:, :d] = _t(dot, dev).to(dt)
+        ldo = d + 3
+        out = torch.full((g.n, ldo), float("nan"), dtype=torch.float32, device=dev)
+        ws = torch.empty(bg.spmm_workspace_bytes(g.n, g.nnz, d), dtype=torch.uint8,
+                         device=dev)
+        bg.bigcn_spmm_csr(_t(g.rowptr, dev), _t(g.colidx, dev), _t(gg, dev), C,
+                          _t(alpha, dev), out[:, :d], ws,
+                          None if b is None else _t(b, dev), norm, act)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        assert np.all(np.isnan(got[:, d:])), "pad columns written"
+        err = mass_error(got[:, :d], z, m, relu=act == "relu")
+        assert err <= TOL, (ctype, norm, act, err)
+
+
+def test_spmm_no_edges(dev):
+    n, d = 10, 5
+    rowptr = torch.zeros(n + 1, dtype=torch.int64, device=dev)
+    colidx = torch.zeros(1, dtype=torch.int32, device=dev)
+    bias = torch.tensor([-1.0, 0.5, 0.0, 2.0, -0.25], device=dev)
+    out = torch.full((n, d), float("nan"), device=dev)
+    C = torch.zeros((n, 8), dtype=torch.float16, device=dev)
+    g = torch.ones(n, device=dev)
+    alpha = torch.ones(d, device=dev)
+    bg.bigcn_spmm_csr(rowptr, colidx, g, C, alpha, out, None, bias, "sym", "relu",
+                      nnz=0)
+    torch.cuda.synchronize()
+    assert torch.equal(out.cpu(), torch.relu(bias.cpu()).expand(n, d))
+
+
+def test_spmm_is_bitwise_reproducible(dev):
+    rng = np.random.default_rng(99)
+    g = _star_plus_random(3000, rng)
+    d = 256
+    C = _t(rng.integers(-255, 256, size=(g.n, d)).astype(np.float16), dev)
+    gg = _t(rng.uniform(0.1, 1, g.n).astype(np.float32), dev)
+    alpha = _t(rng.uniform(0.1, 1, d).astype(np.float32), dev)
+    ws = torch.empty(bg.spmm_workspace_bytes(g.n, g.nnz, d), dtype=torch.uint8, device=dev)
+    outs = []
+    for _ in range(3):
+        out = torch.empty((g.n, d), device=dev)
+        bg.bigcn_spmm_csr(_t(g.rowptr, dev), _t(g.colidx, dev), gg, C, alpha, out, ws)
+        outs.append(out.cpu())
+    assert torch.equal(outs[0], outs[1]) and torch.equal(outs[0], outs[2])
+
+
+# ----------------------------------------------------- a layer, end to end --
+
+def gpu_layer(dev, g, norm, h, wt, bias, act="none", mu=None, rstd=None,
+              rowptr_t=None, colidx_t=None, ht=None):
+    """pack -> bgemm -> spmm through the three entry points."""
+    n, K = h.shape if ht is None else ht.shape
+    d = wt.shape[0]
+    rowptr_t = _t(g.rowptr, dev) if rowptr_t is None else rowptr_t
+    colidx_t = _t(g.colidx, dev) if colidx_t is None else colidx_t
+    ht = _t(h, dev) if ht is None else ht
+    wbits, alpha = bg.pack_weights(_t(wt, dev))
+    kw = (K + 63) // 64
+    F = torch.empty((n, kw), dtype=torch.int64, device=dev)
+    gs = torch.empty(n, dtype=torch.float32, device=dev)
+    bg.bigcn_binarize_pack(ht, F, gs, None if mu is None else _t(mu, dev),
+                           None if rstd is None else _t(rstd, dev), rowptr_t, norm)
+    ldc = (d + 7) // 8 * 8
+    C = torch.empty((n, ldc), dtype=torch.float16 if K <= 2048 else torch.int16, device=dev)
+    bg.bigcn_bgemm(F, wbits, K, C[:, :d])
+    out = torch.empty((n, d), dtype=torch.float32, device=dev)
+    ws = torch.empty(bg.spmm_workspace_bytes(n, g.nnz, d), dtype=torch.uint8, device=dev)
+    bg.bigcn_spmm_csr(rowptr_t, colidx_t, gs, C, alpha, out, ws,
+                      None if bias is None else _t(bias, dev), norm, act, d=d)
+    return out, F, C[:, :d], alpha
+
+
+@pytest.mark.parametrize("K,d,norm", [(130, 7, "sym"), (1433, 64, "sym"),
+                                      (64, 256, "mean"), (602, 41, "mean"),
+                                      (256, 47, "sym")])
+def test_layer_matches_oracle(dev, K, d, norm):
+    rng = np.random.default_rng(K + d)
+    g = _star_plus_random(700, rng)
+    x = rng.standard_normal((g.n, K)).astype(np.float32)
+    mu, rstd = workloads.bn_stats(x)
+    wt = workloads.glorot_t(K, d, rng)
+    b = rng.uniform(-0.1, 0.1, d).astype(np.float32)
+    out, F, C, alpha = gpu_layer(dev, g, norm, x, wt, b, mu=mu, rstd=rstd)
+    torch.cuda.synchronize()
+    z, m, _, a_ref = oracle.layer(g.rowptr, g.colidx, norm, x, wt, b, mu=mu, rstd=rstd)
+    fb, _ = oracle.binarize(x, mu, rstd)
+    assert np.array_equal(u64(F), fb)
+    wb, _ = oracle.binarize(wt)
+    assert np.array_equal(C.cpu().numpy().astype(np.int64), oracle.sign_dot(fb, wb, K))
+    assert np.allclose(alpha.cpu().numpy(), a_ref, rtol=1e-5, atol=0)
+    err = mass_error(out.cpu().numpy(), z, m)
+    print("K=%d d=%d %s mass err %.2e plain rel %.2e" % (K, d, norm, err,
+          plain_rel_error(out.cpu().numpy(), z, m)))
+    assert err <= TOL

@@ -1,0 +1,157 @@
+"""The five synthetic workloads at full size, on the GPU, against the oracle.
+
+Per layer, the GPU layer (pack -> bgemm -> spmm through the C ABI, all rows,
+the launch shapes the forward pass uses) is compared with the oracle on
+every row for the two small workloads and on sampled rows (random rows, the
+first and last rows and the highest-degree hubs) for the large ones.  Layer 0
+reads the workload's features; hidden layers read a seeded N(0,1) stand-in
+input of the right width.  The forward pass is then checked to equal the
+chain of entry points bit for bit, and, on the small workloads, against a
+free-running oracle forward pass.
+"""
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+import paper_2010_07565_amd as bg
+from helpers import TOL, mass_error, plain_rel_error, sample_rows, u64
+from test_gpu_parity import _t, gpu_layer
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+_CACHE = {}
+
+
+def log(msg):
+    print("[%s] %s" % (time.strftime("%H:%M:%S"), msg), flush=True)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    bg.load()
+    return torch.device("cuda:0")
+
+
+def workload(cfg):
+    if cfg not in _CACHE:
+        t = time.time()
+        _CACHE[cfg] = workloads.make_workload(cfg)
+        log("workload %d (%s) generated in %.1f s: %s" % (
+            cfg, _CACHE[cfg].name, time.time() - t, workloads.degree_summary(_CACHE[cfg].graph)))
+    return _CACHE[cfg]
+
+
+@pytest.mark.timeout(1200)
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_workload_layers_match_oracle(dev, cfg):
+    w = workload(cfg)
+    g = w.graph
+    rowptr_t, colidx_t = _t(g.rowptr, dev), _t(g.colidx, dev)
+    ids = None if cfg <= 2 else sample_rows(g, 256, seed=cfg)
+    for l, wt in enumerate(w.weights_t):
+        K, d = wt.shape[1], wt.shape[0]
+        if l == 0:
+            h, mu, rstd = w.x, w.mu, w.rstd
+        else:
+            h, mu, rstd = workloads.layer_input(g.n, K, seed=1000 * cfg + l), None, None
+        log("cfg %d layer %d: %d -> %d, n=%d nnz=%d" % (cfg, l, K, d, g.n, g.nnz))
+        out, F, C, alpha = gpu_layer(dev, g, w.norm, h, wt, w.biases[l], mu=mu, rstd=rstd,
+                                     rowptr_t=rowptr_t, colidx_t=colidx_t)
+        torch.cuda.synchronize()
+        # bits of every row, bit for bit
+        fb, _ = oracle.binarize(h, mu, rstd)
+        assert np.array_equal(u64(F), fb), "packed bits differ"
+        # integer products of the sampled rows (or all), exactly
+        wb, _ = oracle.binarize(wt)
+        rows = np.arange(g.n) if ids is None else ids
+        ref_dot = oracle.sign_dot(fb[rows], wb, K)
+        assert np.array_equal(C[torch.from_numpy(rows).to(dev)].cpu().numpy().astype(np.int64),
+                              ref_dot), "binary GEMM differs"
+        t = time.time()
+        z, m, _, a_ref = oracle.layer(g.rowptr, g.colidx, w.norm, h, wt, w.biases[l],
+                                      mu=mu, rstd=rstd, ids=ids)
+        got = out.cpu().numpy() if ids is None else out[torch.from_numpy(ids).to(dev)].cpu().numpy()
+        assert bool(torch.isfinite(out).all())
+        err = mass_error(got, z, m)
+        log("  oracle %.1f s; mass-normalised err %.2e, plain rel err %.2e, rows %d" % (
+            time.time() - t, err, plain_rel_error(got, z, m), len(got)))
+        assert np.allclose(alpha.cpu().numpy(), a_ref, rtol=1e-5, atol=0)
+        assert err <= TOL
+        del out, F, C
+
+
+def chained(dev, w, rowptr_t, colidx_t, xt):
+    h = xt
+    for l, wt in enumerate(w.weights_t):
+        out, _, _, _ = gpu_layer(dev, w.graph, w.norm, None, wt, w.biases[l],
+                                 mu=w.mu if l == 0 else None, rstd=w.rstd if l == 0 else None,
+                                 rowptr_t=rowptr_t, colidx_t=colidx_t, ht=h)
+        h = out
+    return h
+
+
+@pytest.mark.timeout(1200)
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_forward_equals_chained_layers(dev, cfg):
+    w = workload(cfg)
+    g = w.graph
+    rowptr_t, colidx_t = _t(g.rowptr, dev), _t(g.colidx, dev)
+    xt = _t(w.x, dev)
+    model = bg.BiGCN(rowptr_t, colidx_t, w.weights_t, w.biases, norm=w.norm,
+                     mu=w.mu, rstd=w.rstd, device=dev)
+    out = model.forward(xt).clone()
+    out2 = model.forward(xt).clone()
+    ref = chained(dev, w, rowptr_t, colidx_t, xt)
+    torch.cuda.synchronize()
+    log("cfg %d forward vs chained: max |diff| %.3g" % (cfg, (out - ref).abs().max().item()))
+    assert torch.equal(out, out2), "forward pass not reproducible"
+    assert torch.equal(out, ref), "forward pass differs from the chained entry points"
+    assert bool(torch.isfinite(out).all())
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_forward_free_running_matches_oracle(dev, cfg):
+    """GPU forward vs the oracle's own free-running forward.  Hidden values
+    within rounding of zero may take either sign; every sign flip must be such
+    a legitimate near-zero, and rows whose neighbourhood holds no flipped node
+    must meet the bar."""
+    w = workload(cfg)
+    g = w.graph
+    rowptr_t, colidx_t = _t(g.rowptr, dev), _t(g.colidx, dev)
+    xt = _t(w.x, dev)
+    ref = oracle.forward(g.rowptr, g.colidx, w.norm, w.x, w.weights_t, w.biases,
+                         mu=w.mu, rstd=w.rstd)
+    h = xt
+    flipped_nodes = np.zeros(g.n, dtype=bool)
+    for l, wt in enumerate(w.weights_t):
+        out, _, _, _ = gpu_layer(dev, g, w.norm, None, wt, w.biases[l],
+                                 mu=w.mu if l == 0 else None, rstd=w.rstd if l == 0 else None,
+                                 rowptr_t=rowptr_t, colidx_t=colidx_t, ht=h)
+        got = out.cpu().numpy()
+        z, m, o = ref[l]
+        # rows that depend on a node whose earlier-layer bits differ
+        tainted = np.zeros(g.n, dtype=bool)
+        if flipped_nodes.any():
+            src = np.repeat(np.arange(g.n), np.diff(g.rowptr))
+            hit = flipped_nodes[g.colidx]
+            tainted[np.unique(src[hit])] = True
+        clean = ~tainted
+        err = mass_error(got[clean], z[clean], m[clean])
+        flips = (got >= 0) != (o >= 0)
+        log("cfg %d layer %d: clean rows %d/%d, mass err %.2e, sign flips %d" % (
+            cfg, l, clean.sum(), g.n, err, int(flips.sum())))
+        assert err <= TOL
+        if l + 1 < len(w.weights_t):
+            assert np.all(np.abs(z[flips & clean[:, None]]) <= TOL * m[flips & clean[:, None]])
+            flipped_nodes = flips.any(axis=1) | tainted
+        h = out
+    # the model object gives the same result as the chain
+    model = bg.BiGCN(rowptr_t, colidx_t, w.weights_t, w.biases, norm=w.norm,
+                     mu=w.mu, rstd=w.rstd, device=dev)
+    assert torch.equal(model.forward(xt), h)
