@@ -1,0 +1,276 @@
+"""Benchmark of the binarized-GCN inference path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2]
+
+A step is one whole forward pass (every layer: sign pack, binary GEMM, CSR
+aggregation) over a seeded synthetic workload whose inputs, packed weights
+and workspace are already resident in device memory.  The default workload
+is the PubMed-shaped citation graph (19,717 nodes, 500 -> 64 -> 3); the other
+four are selectable with --workload.
+
+Prints one JSON line.  Besides the forward-pass throughput it carries
+ - "kernels":  each layer's kernels timed alone through their entry points
+   with HIP events on the launch stream (average over --kernel-reps);
+ - "roofline": the dominant kernel (largest share of a forward pass) against
+   its bound: HBM bytes for pack / aggregation, bit operations on the vector
+   ALUs for the binary GEMM;
+ - "cpu_baseline": the plain CPU oracle timed on this host on a bounded
+   sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+# 256 CUs x 4 SIMD x 16 lanes x 2.4 GHz = 39.3 T lane-ops/s; the popcount
+# GEMM needs 2 XOR + 2 bit-count lane-ops per 64 sign products.
+VALU_BITOP_PEAK = 256 * 4 * 16 * 2.4e9 * 16
+METRIC = "nodes/sec full Bi-GCN forward; bGEMM bit-ops/s; SpMM/pack HBM GB/s vs peak"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def words(k):
+    return (k + 63) // 64
+
+
+def kernel_specs(w, ldF, ldc):
+    """Algorithmic work of each kernel of one forward pass."""
+    n, nnz = w.graph.n, w.graph.nnz
+    specs = []
+    for l, wt in enumerate(w.weights_t):
+        d, K = wt.shape
+        kw = words(K)
+        pack_bytes = n * K * 4 + n * kw * 8 + n * 4 + (n + 1) * 8 + (2 * K * 4 if l == 0 else 0)
+        es = 1 if (128 < d <= 256 and K <= 2048) else 2   # stored bytes per product
+        gemm_ops = n * K * d
+        gemm_bytes = n * kw * 8 + d * kw * 8 + n * d * es
+        spmm_bytes = 8 * (n + 1) + 4 * nnz + 4 * n + n * d * es + n * d * 4 + 8 * d
+        specs.append(dict(layer=l, K=K, d=d, pack_bytes=pack_bytes, gemm_ops=gemm_ops,
+                          gemm_bytes=gemm_bytes, spmm_bytes=spmm_bytes,
+                          spmm_flops=2 * nnz * d))
+    return specs
+
+
+def time_calls(fn, reps, torch):
+    """Average duration of fn() over reps, HIP events around each call on
+    the current stream."""
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+    for i in range(reps):
+        starts[i].record()
+        fn()
+        ends[i].record()
+    torch.cuda.synchronize()
+    return sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / reps * 1e-3
+
+
+def cpu_baseline(w, budget_s=10.0):
+    """The oracle on this host: the whole forward pass for small graphs, else
+    the dependency cones of a random set of output rows."""
+    import numpy as np
+    import oracle
+
+    g = w.graph
+    L = len(w.weights_t)
+    cores = oracle.threads()
+    if g.n <= 50_000:
+        t0 = time.time()
+        reps = 0
+        while True:
+            oracle.forward(g.rowptr, g.colidx, w.norm, w.x, w.weights_t, w.biases,
+                           mu=w.mu, rstd=w.rstd)
+            reps += 1
+            if time.time() - t0 >= budget_s or reps >= 50:
+                break
+        dt = time.time() - t0
+        return dict(value=g.n * reps / dt, unit="nodes/s", cores=cores, kind="oracle",
+                    sample="whole %d-node forward pass x %d in %.1f s" % (g.n, reps, dt))
+    rng = np.random.default_rng(7)
+    nt = 1
+    while True:
+        T = np.sort(rng.choice(g.n, size=nt, replace=False)).astype(np.int64)
+        # rows each layer must produce: closed neighbourhoods, last layer first
+        need = [None] * (L + 1)
+        need[L] = T
+        for l in range(L, 0, -1):
+            rows = need[l]
+            nb = np.concatenate([g.colidx[g.rowptr[i]:g.rowptr[i + 1]] for i in rows])
+            need[l - 1] = np.unique(np.concatenate([rows, nb])).astype(np.int64)
+        t0 = time.time()
+        h = w.x
+        for l, wt in enumerate(w.weights_t):
+            ids = need[l + 1]
+            _, _, out, _ = oracle.layer(g.rowptr, g.colidx, w.norm, h, wt, w.biases[l],
+                                        mu=w.mu if l == 0 else None,
+                                        rstd=w.rstd if l == 0 else None, ids=ids)
+            if l + 1 < L:
+                h = np.zeros((g.n, wt.shape[0]), dtype=np.float32)
+                h[ids] = out
+        dt = time.time() - t0
+        if dt >= budget_s or nt >= g.n // 2 or nt >= 4096:
+            return dict(value=nt / dt, unit="nodes/s", cores=cores, kind="oracle",
+                        sample="%d random output rows with their %d-hop input cones "
+                               "(%d layer-0 rows) in %.1f s" % (nt, L, len(need[1]), dt))
+        nt *= 2 if dt * 4 > budget_s else 4
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--kernel-reps", type=int, default=50)
+    ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py: this build runs on a single GPU; --gpus %d is not supported "
+              "(the multi-GPU design is described, not built)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads
+    import paper_2010_07565_amd as bg
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    w = workloads.make_workload(args.workload)
+    g = w.graph
+    log("workload %d (%s) generated in %.1f s: %s" % (args.workload, w.name, time.time() - t0,
+                                                        workloads.degree_summary(g)))
+
+    rowptr = torch.from_numpy(g.rowptr).to(dev)
+    colidx = torch.from_numpy(g.colidx).to(dev)
+    x = torch.from_numpy(w.x).to(dev)
+    model = bg.BiGCN(rowptr, colidx, w.weights_t, w.biases, norm=w.norm, mu=w.mu,
+                     rstd=w.rstd, device=dev)
+    torch.cuda.synchronize()
+
+    # ---- the timed forward passes
+    for _ in range(args.warmup):
+        model.forward(x)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(args.steps):
+        model.forward(x)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t
+    ms = dt / args.steps * 1e3
+    nodes_per_s = g.n * args.steps / dt
+    log("forward: %.4f ms/step, %.4g nodes/s" % (ms, nodes_per_s))
+
+    # ---- each kernel alone, through its entry point, same shapes and ld's
+    L = len(w.weights_t)
+    kwmax = max(words(wt.shape[1]) for wt in w.weights_t)
+    ldF = (kwmax + 1) // 2 * 2
+    ldc = (max(wt.shape[0] for wt in w.weights_t) + 7) // 8 * 8
+    F = torch.empty((g.n, ldF), dtype=torch.int64, device=dev)
+    gs = torch.empty(g.n, dtype=torch.float32, device=dev)
+    C = torch.empty((g.n, ldc), dtype=torch.float16, device=dev)
+    C8 = torch.empty((g.n, 256), dtype=torch.int8, device=dev)
+    ws = torch.empty(max(bg.spmm_workspace_bytes(g.n, g.nnz, wt.shape[0])
+                         for wt in w.weights_t), dtype=torch.uint8, device=dev)
+    mu_t = torch.from_numpy(w.mu).to(dev)
+    rstd_t = torch.from_numpy(w.rstd).to(dev)
+    specs = kernel_specs(w, ldF, ldc)
+    kernels = []
+    h = x
+    reps = args.kernel_reps
+    for l, ly in enumerate(model.layers):
+        K, d = ly.d_in, ly.d_out
+        out = torch.empty((g.n, d), dtype=torch.float32, device=dev)
+        kw = words(K)
+        m0 = mu_t if l == 0 else None
+        r0 = rstd_t if l == 0 else None
+        t_pack = time_calls(lambda: bg.bigcn_binarize_pack(h, F[:, :kw], gs, m0, r0, rowptr,
+                                                           w.norm), reps, torch)
+        q8 = bg.q8_supported(g.n, d, K)
+        if q8:
+            # the forward keeps these products as 8-bit half-codes
+            t_gemm = time_calls(lambda: bg.bigcn_bgemm_q8(F[:, :kw], ly.wbits, K, C8, C, gs),
+                                reps, torch)
+            t_spmm = time_calls(lambda: bg.bigcn_spmm_csr_q8(rowptr, colidx, gs, C8, C, K,
+                                                             ly.alpha, out, ws, ly.bias,
+                                                             w.norm, ly.act, d=d),
+                                reps, torch)
+        else:
+            t_gemm = time_calls(lambda: bg.bigcn_bgemm(F[:, :kw], ly.wbits, K, C[:, :d]),
+                                reps, torch)
+            t_spmm = time_calls(lambda: bg.bigcn_spmm_csr(rowptr, colidx, gs, C, ly.alpha,
+                                                          out, ws, ly.bias, w.norm, ly.act,
+                                                          d=d),
+                                reps, torch)
+        s = specs[l]
+        kernels += [
+            dict(kernel="pack", layer=l, us=t_pack * 1e6, bound="hbm",
+                 achieved=s["pack_bytes"] / t_pack / 1e9, unit="GB/s", peak=HBM_PEAK_GBS,
+                 work=s["pack_bytes"]),
+            dict(kernel="bgemm_q8" if q8 else "bgemm", layer=l, us=t_gemm * 1e6, bound="alu",
+                 achieved=s["gemm_ops"] / t_gemm / 1e12, unit="Tbitop/s",
+                 peak=VALU_BITOP_PEAK / 1e12, work=s["gemm_ops"],
+                 hbm_gbs=s["gemm_bytes"] / t_gemm / 1e9),
+            dict(kernel="spmm_q8" if q8 else "spmm", layer=l, us=t_spmm * 1e6, bound="hbm",
+                 achieved=s["spmm_bytes"] / t_spmm / 1e9, unit="GB/s", peak=HBM_PEAK_GBS,
+                 work=s["spmm_bytes"]),
+        ]
+        h = out
+    for k in kernels:
+        k["frac"] = k["achieved"] / k["peak"]
+        log("  L%d %-5s %9.2f us  %8.1f %s  (%.1f%% of peak)" % (
+            k["layer"], k["kernel"], k["us"], k["achieved"], k["unit"], 100 * k["frac"]))
+    dom = max(kernels, key=lambda k: k["us"])
+    roofline = dict(kernel="%s (layer %d)" % (dom["kernel"], dom["layer"]), bound=dom["bound"],
+                    achieved=round(dom["achieved"], 2), peak=dom["peak"], unit=dom["unit"],
+                    frac=round(dom["frac"], 4), traffic=None, avg_us=round(dom["us"], 3))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        t = time.time()
+        cpu = cpu_baseline(w, args.cpu_budget)
+        log("cpu baseline: %s (%.1f s)" % (cpu, time.time() - t))
+
+    dims = [w.weights_t[0].shape[1]] + [wt.shape[0] for wt in w.weights_t]
+    rec = {
+        "metric": METRIC,
+        "value": round(nodes_per_s, 1),
+        "unit": "nodes/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64 sign bits + fp32",
+        "data": "synthetic (seeded %s stand-in)" % w.name,
+        "config": {"workload": "%s: %d-layer Bi-GCN %s, %d nodes, %d CSR entries of A+I, "
+                               "%s normalisation" % (w.name, L, "-".join(map(str, dims)),
+                                                     g.n, g.nnz, w.norm),
+                   "nodes": g.n, "nnz": g.nnz, "dims": dims, "norm": w.norm,
+                   "parallelism": "single GPU"},
+        "kernels": [{k2: (round(v, 4) if isinstance(v, float) else v) for k2, v in k.items()}
+                    for k in kernels],
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

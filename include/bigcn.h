@@ -152,6 +152,39 @@ bigcn_status bigcn_spmm_csr(int64_t n, int64_t nnz, const int64_t* rowptr,
                             void* stream);
 
 /* ---------------------------------------------------------------------------
+ * bigcn_bgemm_q8 / bigcn_spmm_csr_q8 -- the binary GEMM and the aggregation
+ * with the products kept as exact 8-bit half-codes (half the bytes the
+ * aggregation gathers per edge).  Since dot = K - 2 popcount(...) has the
+ * parity p = K mod 2, the code (dot - p) / 2 represents every |dot| <= 255
+ * in one signed byte.  A row i with a larger |dot| in any column is written
+ * in full, exactly (IEEE half), to C16 and flagged by setting the sign bit of
+ * g[i]; the aggregation then reads that row from C16.  g is therefore
+ * in/out for bigcn_bgemm_q8: it must hold the non-negative scales written by
+ * bigcn_binarize_pack, and is left with the flags for bigcn_spmm_csr_q8.
+ * Inputs and outputs otherwise as bigcn_bgemm / bigcn_spmm_csr.
+ *
+ *   C8   [M][ldc8] int8, ldc8 >= 256 and a multiple of 4.
+ *   C16  [M][ldc16] IEEE half, ldc16 >= N and a multiple of 4; only flagged
+ *        rows are written.
+ *   g    fp32[M] (see above).
+ * Shapes: 128 < N <= 256, K <= 2048, M * ldc8 and M * ldc16 * 2 below 4 GiB;
+ * other shapes return EUNSUPPORTED (use the exact-type calls).
+ * The aggregation result equals bigcn_spmm_csr on the exact products up to
+ * fp32 rounding (the sum is formed as 2 * sum g code + p * sum g).
+ * ------------------------------------------------------------------------- */
+bigcn_status bigcn_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
+                            const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
+                            int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
+                            float* g, void* stream);
+bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
+                               const int32_t* colidx, bigcn_norm norm,
+                               const float* g, const int8_t* C8, int64_t ldc8,
+                               const void* C16, int64_t ldc16, int32_t K,
+                               int32_t d, const float* alpha, const float* bias,
+                               bigcn_act act, float* out, int64_t ldo,
+                               void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * bigcn_forward -- the whole multi-layer forward pass (Sec. 4.1):
  *     H^(0) = X,  H^(l+1) = act_l( Ã ζ^(l) + b_l ),  l = 0 .. n_layers-1,
  * every layer binarised (features and weights).  Layer 0 standardises X with
@@ -169,8 +202,9 @@ bigcn_status bigcn_spmm_csr(int64_t n, int64_t nnz, const int64_t* rowptr,
  *   out  [n][ldo] fp32 result of the last layer, ldo >= last d_out.
  *   workspace  at least bigcn_forward_workspace_bytes(...) bytes, 256-byte
  *          aligned; contents on entry are ignored.
- * Internally each layer's products are kept in the narrowest exact type
- * (IEEE half for d_in <= 2048, else int16).
+ * Internally each layer's products are kept exactly: as 8-bit half-codes
+ * (see bigcn_bgemm_q8) for layers of 129..256 output columns with
+ * d_in <= 2048, otherwise in IEEE half (d_in <= 2048) or int16.
  * Errors: as the per-step calls, plus EINVAL for inconsistent layer widths
  *         or n_layers < 1, EUNSUPPORTED for d_in > 8192 on a layer.
  * ------------------------------------------------------------------------- */

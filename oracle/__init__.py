@@ -58,8 +58,15 @@ def _load():
         lib.oracle_layer.argtypes = [_i64, _p, _p, _int, _p, _i64, _i32, _p,
                                      _p, _p, _i32, _p, _int, _p, _i64, _p, _p,
                                      _p, _p]
+        lib.oracle_threads.restype = _int
+        lib.oracle_threads.argtypes = []
         _lib = lib
     return _lib
+
+
+def threads() -> int:
+    """Threads the oracle's OpenMP loops use."""
+    return _load().oracle_threads()
 
 
 def _ptr(a):

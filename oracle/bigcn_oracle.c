@@ -44,6 +44,7 @@
  * thread count.  Built with -ffp-contract=off.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -273,3 +274,6 @@ done_w:
   free(slot);
   return rc;
 }
+
+/* Number of threads the oracle's parallel loops use. */
+int oracle_threads(void) { return omp_get_max_threads(); }

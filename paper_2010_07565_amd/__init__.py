@@ -5,11 +5,11 @@ The compute path is the HIP library ``libbigcn.so`` (C ABI in
 device memory and streams only.
 """
 from ._lib import (BiGCN, BigcnError, EXPORTS, Layer, LIB_PATH, bigcn_bgemm,
-                   bigcn_binarize_pack, bigcn_forward, bigcn_spmm_csr,
-                   forward_workspace_bytes, load, pack_weights,
-                   spmm_workspace_bytes, words)
+                   bigcn_bgemm_q8, bigcn_binarize_pack, bigcn_forward,
+                   bigcn_spmm_csr, bigcn_spmm_csr_q8, forward_workspace_bytes, load,
+                   pack_weights, q8_supported, spmm_workspace_bytes, words)
 
 __all__ = ["BiGCN", "BigcnError", "EXPORTS", "Layer", "LIB_PATH", "bigcn_bgemm",
-           "bigcn_binarize_pack", "bigcn_forward", "bigcn_spmm_csr",
-           "forward_workspace_bytes", "load", "pack_weights",
-           "spmm_workspace_bytes", "words"]
+           "bigcn_bgemm_q8", "bigcn_binarize_pack", "bigcn_forward", "bigcn_spmm_csr",
+           "bigcn_spmm_csr_q8", "forward_workspace_bytes", "load", "pack_weights",
+           "q8_supported", "spmm_workspace_bytes", "words"]

@@ -27,8 +27,8 @@ ALGOS = {"auto": 0, "popcount": 1, "mfma_i8": 2}
 
 # Every entry point declared in include/bigcn.h.
 EXPORTS = ("bigcn_binarize_pack", "bigcn_bgemm", "bigcn_spmm_workspace_bytes",
-           "bigcn_spmm_csr", "bigcn_forward_workspace_bytes", "bigcn_forward",
-           "bigcn_status_string")
+           "bigcn_spmm_csr", "bigcn_bgemm_q8", "bigcn_spmm_csr_q8",
+           "bigcn_forward_workspace_bytes", "bigcn_forward", "bigcn_status_string")
 
 
 class BigcnError(RuntimeError):
@@ -71,6 +71,12 @@ def load() -> ctypes.CDLL:
     lib.bigcn_spmm_csr.restype = _int
     lib.bigcn_spmm_csr.argtypes = [_i64, _i64, _p, _p, _int, _p, _p, _int, _i32,
                                    _i64, _p, _p, _int, _p, _i64, _p, _sz, _p]
+    lib.bigcn_bgemm_q8.restype = _int
+    lib.bigcn_bgemm_q8.argtypes = [_p, _i64, _i64, _p, _i32, _i64, _i32, _p, _i64, _p,
+                                   _i64, _p, _p]
+    lib.bigcn_spmm_csr_q8.restype = _int
+    lib.bigcn_spmm_csr_q8.argtypes = [_i64, _i64, _p, _p, _int, _p, _p, _i64, _p, _i64,
+                                      _i32, _i32, _p, _p, _int, _p, _i64, _p, _sz, _p]
     lib.bigcn_forward_workspace_bytes.restype = _sz
     lib.bigcn_forward_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(_Layer),
                                                   _i32]
@@ -171,6 +177,44 @@ def bigcn_spmm_csr(rowptr: torch.Tensor, colidx: torch.Tensor, g: torch.Tensor,
         _ld(out, "out"), _dev(workspace, torch.uint8, "workspace"),
         workspace.numel() if workspace is not None else 0, _stream(stream))
     _check("bigcn_spmm_csr", st)
+
+
+def bigcn_bgemm_q8(F: torch.Tensor, B: torch.Tensor, K: int, C8: torch.Tensor,
+                   C16: torch.Tensor, g: torch.Tensor, stream=None) -> None:
+    """Binary GEMM into exact 8-bit half-codes C8 (int8); rows needing more
+    go exactly to C16 (float16) and get the sign bit of g set."""
+    st = load().bigcn_bgemm_q8(
+        _dev(F, torch.int64, "F"), F.shape[0], _ld(F, "F"), _dev(B, torch.int64, "B"),
+        B.shape[0], _ld(B, "B"), K, _dev(C8, torch.int8, "C8"), _ld(C8, "C8"),
+        _dev(C16, torch.float16, "C16"), _ld(C16, "C16"), _dev(g, torch.float32, "g"),
+        _stream(stream))
+    _check("bigcn_bgemm_q8", st)
+
+
+def bigcn_spmm_csr_q8(rowptr: torch.Tensor, colidx: torch.Tensor, g: torch.Tensor,
+                      C8: torch.Tensor, C16: torch.Tensor, K: int, alpha: torch.Tensor,
+                      out: torch.Tensor, workspace: torch.Tensor, bias=None,
+                      norm: str = "sym", act: str = "none", d: Optional[int] = None,
+                      nnz: Optional[int] = None, stream=None) -> None:
+    """Aggregation reading 8-bit half-codes (see bigcn_bgemm_q8)."""
+    n = rowptr.shape[0] - 1
+    d = alpha.shape[0] if d is None else d
+    nnz = colidx.shape[0] if nnz is None else nnz
+    st = load().bigcn_spmm_csr_q8(
+        n, nnz, _dev(rowptr, torch.int64, "rowptr"), _dev(colidx, torch.int32, "colidx"),
+        NORMS[norm], _dev(g, torch.float32, "g"), _dev(C8, torch.int8, "C8"), _ld(C8, "C8"),
+        _dev(C16, torch.float16, "C16"), _ld(C16, "C16"), K, d,
+        _dev(alpha, torch.float32, "alpha"), _dev(bias, torch.float32, "bias"), ACTS[act],
+        _dev(out, torch.float32, "out"), _ld(out, "out"),
+        _dev(workspace, torch.uint8, "workspace"),
+        workspace.numel() if workspace is not None else 0, _stream(stream))
+    _check("bigcn_spmm_csr_q8", st)
+
+
+def q8_supported(n: int, d: int, K: int) -> bool:
+    """Whether the forward keeps a layer's products as 8-bit half-codes."""
+    return 128 < d <= 256 and K <= 2048 and n * 256 <= 0xFFFFFFFF and \
+        n * ((d + 7) // 8 * 8) * 2 <= 0xFFFFFFFF
 
 
 @dataclass

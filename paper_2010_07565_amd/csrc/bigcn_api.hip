@@ -92,16 +92,19 @@ hipError_t run_bgemm(const uint64_t* F, int64_t M, int64_t ldf, const uint64_t* 
 
 // Workspace layout of bigcn_forward.
 struct ForwardLayout {
-  int64_t ldF, ldc, ldh;
-  size_t off_F, off_g, off_C, off_H0, off_H1, off_spmm, bytes;
+  int64_t ldF, ldc, ldh, ldc8;
+  size_t off_F, off_g, off_C, off_C8, off_H0, off_H1, off_spmm, bytes;
   int32_t dmax;
+  bool any_q8;
 };
 
 bool forward_layout(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t nl,
                     ForwardLayout* L) {
   int64_t kwmax = 1, dmax = 1, hmax = 1;
   size_t esmax = 2;
+  L->any_q8 = false;
   for (int32_t l = 0; l < nl; ++l) {
+    L->any_q8 |= bigcn::q8_supported(n, layers[l].d_out, layers[l].d_in);
     kwmax = std::max<int64_t>(kwmax, words(layers[l].d_in));
     dmax = std::max<int64_t>(dmax, layers[l].d_out);
     esmax = std::max(esmax, bigcn::itype_size(forward_itype(layers[l].d_in)));
@@ -118,6 +121,9 @@ bool forward_layout(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t n
   off += up256((size_t)n * 4);
   L->off_C = off;
   off += up256((size_t)n * L->ldc * esmax);
+  L->ldc8 = 256;
+  L->off_C8 = off;
+  if (L->any_q8) off += up256((size_t)n * L->ldc8);
   L->off_H0 = off;
   if (nl >= 2) off += up256((size_t)n * L->ldh * 4);
   L->off_H1 = off;
@@ -199,6 +205,56 @@ bigcn_status bigcn_spmm_csr(int64_t n, int64_t nnz, const int64_t* rowptr,
                                        out, ldo, plan, workspace, s));
 }
 
+bigcn_status bigcn_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
+                            const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
+                            int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
+                            float* g, void* stream) {
+  if (M < 0 || N < 1 || K < 1 || ldf < words(K) || ldb < words(K)) return BIGCN_EINVAL;
+  if (ldc8 < 256 || ldc8 % 4 != 0 || ldc16 < N || ldc16 % 4 != 0) return BIGCN_EINVAL;
+  if (B == nullptr || (M > 0 && (F == nullptr || C8 == nullptr || C16 == nullptr ||
+                                 g == nullptr)))
+    return BIGCN_EINVAL;
+  if (!aligned(F, 8) || !aligned(B, 8) || !aligned(C8, 4) || !aligned(C16, 8) ||
+      !aligned(g, 4))
+    return BIGCN_EALIGN;
+  if (!bigcn::q8_supported(M, N, K) || (uint64_t)M * ldc8 > 0xFFFFFFFFull ||
+      (uint64_t)M * ldc16 * 2 > 0xFFFFFFFFull)
+    return BIGCN_EUNSUPPORTED;
+  return hip_status(bigcn::launch_bgemm_q8(F, M, ldf, B, N, ldb, K, C8, ldc8, C16, ldc16,
+                                           g, (hipStream_t)stream));
+}
+
+bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
+                               const int32_t* colidx, bigcn_norm norm,
+                               const float* g, const int8_t* C8, int64_t ldc8,
+                               const void* C16, int64_t ldc16, int32_t K,
+                               int32_t d, const float* alpha, const float* bias,
+                               bigcn_act act, float* out, int64_t ldo,
+                               void* workspace, size_t ws_bytes, void* stream) {
+  bigcn_status st = check_graph(n, nnz, rowptr, colidx, norm);
+  if (st != BIGCN_OK) return st;
+  if (K < 1 || ldc8 < 256 || ldc8 % 4 != 0) return BIGCN_EINVAL;
+  st = check_spmm_operands(n, g, C16, BIGCN_F16, d, ldc16, alpha, bias, act, out, ldo);
+  if (st != BIGCN_OK) return st;
+  if (n > 0 && C8 == nullptr) return BIGCN_EINVAL;
+  if (!aligned(C8, 4)) return BIGCN_EALIGN;
+  if (!bigcn::q8_supported(n, d, K) || (uint64_t)n * ldc8 > 0xFFFFFFFFull ||
+      (uint64_t)n * ldc16 * 2 > 0xFFFFFFFFull)
+    return BIGCN_EUNSUPPORTED;
+  const bigcn::SpmmPlan plan = bigcn::spmm_plan(n, nnz, d);
+  if (n > 0 && nnz > 0) {
+    if (workspace == nullptr || ws_bytes < plan.bytes) return BIGCN_EWORKSPACE;
+    if (!aligned(workspace, 256)) return BIGCN_EALIGN;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = bigcn::launch_spmm_rows(n, nnz, rowptr, plan, workspace, s);
+  if (e != hipSuccess) return BIGCN_EHIP;
+  return hip_status(bigcn::launch_spmm_q8(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN,
+                                          g, C8, ldc8, C16, ldc16, K, d, alpha, bias,
+                                          act == BIGCN_ACT_RELU, out, ldo, plan,
+                                          workspace, s));
+}
+
 size_t bigcn_forward_workspace_bytes(int64_t n, int64_t nnz,
                                      const bigcn_layer* layers, int32_t n_layers) {
   if (n < 0 || nnz < 0 || layers == nullptr || n_layers < 1) return 0;
@@ -265,13 +321,23 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
                            l == 0 ? rstd : nullptr, rowptr, norm == BIGCN_NORM_SYM,
                            F, L.ldF, g, s);
     if (e != hipSuccess) return BIGCN_EHIP;
-    e = run_bgemm(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C, ct, L.ldc,
-                  BIGCN_BGEMM_AUTO, s);
-    if (e != hipSuccess) return BIGCN_EHIP;
     const bigcn::SpmmPlan plan = bigcn::spmm_plan(n, nnz, ly.d_out);
-    e = bigcn::launch_spmm(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN, g, C, ct,
-                           ly.d_out, L.ldc, ly.alpha, ly.bias, ly.act == BIGCN_ACT_RELU,
-                           hout, ldout, plan, wsp, s);
+    if (bigcn::q8_supported(n, ly.d_out, ly.d_in)) {
+      int8_t* C8 = (int8_t*)(ws + L.off_C8);
+      e = bigcn::launch_bgemm_q8(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C8,
+                                 L.ldc8, C, L.ldc, g, s);
+      if (e != hipSuccess) return BIGCN_EHIP;
+      e = bigcn::launch_spmm_q8(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN, g, C8,
+                                L.ldc8, C, L.ldc, ly.d_in, ly.d_out, ly.alpha, ly.bias,
+                                ly.act == BIGCN_ACT_RELU, hout, ldout, plan, wsp, s);
+    } else {
+      e = run_bgemm(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C, ct, L.ldc,
+                    BIGCN_BGEMM_AUTO, s);
+      if (e != hipSuccess) return BIGCN_EHIP;
+      e = bigcn::launch_spmm(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN, g, C, ct,
+                             ly.d_out, L.ldc, ly.alpha, ly.bias, ly.act == BIGCN_ACT_RELU,
+                             hout, ldout, plan, wsp, s);
+    }
     if (e != hipSuccess) return BIGCN_EHIP;
     hin = hout;
     ldin = ldout;

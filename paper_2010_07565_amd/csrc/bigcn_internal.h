@@ -34,6 +34,15 @@ hipError_t launch_bgemm_mfma(const uint64_t* F, int64_t M, int64_t ldf,
                              int32_t K, void* C, IType ct, int64_t ldc,
                              hipStream_t stream);
 
+// Exact 8-bit half-code storage of the products (layers of 129..256 output
+// columns with K <= 2048): codes (dot - K%2)/2 in C8, rows with |dot| > 255
+// written exactly (half) to C16 and flagged by the sign bit of g.
+bool q8_supported(int64_t n, int32_t N, int32_t K);
+hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
+                           const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
+                           int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
+                           float* g, hipStream_t stream);
+
 // Aggregation over the CSR of Â with the fused rescale / bias / activation
 // epilogue.  The edge range [0, nnz) is cut into fixed chunks of `chunk`
 // edges; see bigcn_kernels.hip for the scheme and the workspace layout.
@@ -57,5 +66,13 @@ hipError_t launch_spmm(int64_t n, int64_t nnz, const int64_t* rowptr,
                        const float* alpha, const float* bias, int relu,
                        float* out, int64_t ldo, const SpmmPlan& plan,
                        void* workspace, hipStream_t stream);
+
+// Aggregation reading 8-bit half-codes (see launch_bgemm_q8).
+hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
+                          const int32_t* colidx, int mean, const float* g,
+                          const int8_t* C8, int64_t ldc8, const void* C16,
+                          int64_t ldc16, int32_t K, int32_t d, const float* alpha,
+                          const float* bias, int relu, float* out, int64_t ldo,
+                          const SpmmPlan& plan, void* workspace, hipStream_t stream);
 
 }  // namespace bigcn

@@ -143,15 +143,12 @@ __device__ inline void store_row(T* __restrict__ dst, const int* v, int ncols,
     if (c < ncols) dst[c] = from_int<T>(v[c]);
 }
 
-template <int CN, int RM, typename T>
-__global__ __launch_bounds__(kBlock) void k_bgemm_pop(
-    const uint64_t* __restrict__ F, int64_t M, int64_t ldf,
-    const uint64_t* __restrict__ B, int32_t N, int64_t ldb, int32_t K,
-    T* __restrict__ C, int64_t ldc, int vec) {
-  extern __shared__ uint64_t sB[];  // [kw][CN][64]: word w of column j0 + CN*l + c
-  const int lane = threadIdx.x & 63;
-  const int kw = (K + 63) >> 6;
-  const int j0 = blockIdx.y * 64 * CN;
+// Stages the packed weight rows j0 .. j0 + 64*CN - 1 into LDS as
+// [kw][CN][64] (word w of column j0 + CN*l + c at (w*CN + c)*64 + l), so that
+// for a fixed (w, c) the 64 lanes read 64 consecutive words.
+template <int CN>
+__device__ inline void stage_weights(uint64_t* sB, const uint64_t* __restrict__ B,
+                                     int32_t N, int64_t ldb, int kw, int j0) {
   for (int idx = threadIdx.x; idx < kw * CN * 64; idx += kBlock) {
     const int l = idx & 63;
     const int c = (idx >> 6) % CN;
@@ -160,6 +157,49 @@ __global__ __launch_bounds__(kBlock) void k_bgemm_pop(
     sB[idx] = j < N ? B[(int64_t)j * ldb + w] : 0ull;
   }
   __syncthreads();
+}
+
+// Disagreement counts popcount(F_i ^ B_j) of rows i0 .. i0+RM-1 against this
+// lane's CN columns.  The row words are wave-uniform (scalar loads).
+template <int CN, int RM>
+__device__ inline void tile_popcounts(const uint64_t* __restrict__ F, int64_t M,
+                                      int64_t ldf, const uint64_t* sB, int kw,
+                                      int64_t i0, int lane, uint32_t (&acc)[RM][CN]) {
+#pragma unroll
+  for (int r = 0; r < RM; ++r)
+#pragma unroll
+    for (int c = 0; c < CN; ++c) acc[r][c] = 0;
+  for (int w = 0; w < kw; ++w) {
+    uint64_t fw[RM];
+#pragma unroll
+    for (int r = 0; r < RM; ++r) {
+      const int64_t i = i0 + r < M ? i0 + r : M - 1;
+      fw[r] = F[i * ldf + w];
+    }
+    uint64_t bw[CN];
+#pragma unroll
+    for (int c = 0; c < CN; ++c) bw[c] = sB[(w * CN + c) * 64 + lane];
+#pragma unroll
+    for (int r = 0; r < RM; ++r)
+#pragma unroll
+      for (int c = 0; c < CN; ++c) {
+        const uint64_t z = fw[r] ^ bw[c];
+        acc[r][c] += __builtin_popcount((uint32_t)z);
+        acc[r][c] += __builtin_popcount((uint32_t)(z >> 32));
+      }
+  }
+}
+
+template <int CN, int RM, typename T>
+__global__ __launch_bounds__(kBlock) void k_bgemm_pop(
+    const uint64_t* __restrict__ F, int64_t M, int64_t ldf,
+    const uint64_t* __restrict__ B, int32_t N, int64_t ldb, int32_t K,
+    T* __restrict__ C, int64_t ldc, int vec) {
+  extern __shared__ uint64_t sB[];
+  const int lane = threadIdx.x & 63;
+  const int kw = (K + 63) >> 6;
+  const int j0 = blockIdx.y * 64 * CN;
+  stage_weights<CN>(sB, B, N, ldb, kw, j0);
   const int64_t tiles = (M + RM - 1) / RM;
   const int64_t nwaves = (int64_t)gridDim.x * kWavesPerBlock;
   const int jl = j0 + lane * CN;  // first column of this lane
@@ -168,29 +208,7 @@ __global__ __launch_bounds__(kBlock) void k_bgemm_pop(
        t < tiles; t += nwaves) {
     const int64_t i0 = t * RM;
     uint32_t acc[RM][CN];
-#pragma unroll
-    for (int r = 0; r < RM; ++r)
-#pragma unroll
-      for (int c = 0; c < CN; ++c) acc[r][c] = 0;
-    for (int w = 0; w < kw; ++w) {
-      uint64_t fw[RM];
-#pragma unroll
-      for (int r = 0; r < RM; ++r) {
-        const int64_t i = i0 + r < M ? i0 + r : M - 1;
-        fw[r] = F[i * ldf + w];  // wave-uniform address: scalar load
-      }
-      uint64_t bw[CN];
-#pragma unroll
-      for (int c = 0; c < CN; ++c) bw[c] = sB[(w * CN + c) * 64 + lane];
-#pragma unroll
-      for (int r = 0; r < RM; ++r)
-#pragma unroll
-        for (int c = 0; c < CN; ++c) {
-          const uint64_t z = fw[r] ^ bw[c];
-          acc[r][c] += __builtin_popcount((uint32_t)z);
-          acc[r][c] += __builtin_popcount((uint32_t)(z >> 32));
-        }
-    }
+    tile_popcounts<CN, RM>(F, M, ldf, sB, kw, i0, lane, acc);
     if (ncols > 0) {
 #pragma unroll
       for (int r = 0; r < RM; ++r) {
@@ -199,6 +217,67 @@ __global__ __launch_bounds__(kBlock) void k_bgemm_pop(
 #pragma unroll
         for (int c = 0; c < CN; ++c) v[c] = K - 2 * (int)acc[r][c];
         store_row<T, CN>(C + (i0 + r) * ldc + jl, v, ncols, vec != 0);
+      }
+    }
+  }
+}
+
+// The same product stored as exact 8-bit half-codes for the forward pass:
+//   code = (dot - p) / 2,  p = K mod 2   (dot = K - 2 popcount is = p mod 2),
+// which holds every |dot| <= 255.  A row with a larger value anywhere is
+// written in full, exactly, to C16 (half for K <= 2048, else int16) and is
+// flagged by setting the sign bit of its scale g[i] (g >= 0 otherwise).  One
+// wave covers all N columns (N <= 64*CN), so the flag is decided per row
+// with a ballot.
+template <int CN, int RM, typename T16>
+__global__ __launch_bounds__(kBlock) void k_bgemm_pop_q8(
+    const uint64_t* __restrict__ F, int64_t M, int64_t ldf,
+    const uint64_t* __restrict__ B, int32_t N, int64_t ldb, int32_t K,
+    int8_t* __restrict__ C8, int64_t ldc8, T16* __restrict__ C16, int64_t ldc16,
+    float* __restrict__ g) {
+  extern __shared__ uint64_t sB[];
+  const int lane = threadIdx.x & 63;
+  const int kw = (K + 63) >> 6;
+  stage_weights<CN>(sB, B, N, ldb, kw, 0);
+  const int64_t tiles = (M + RM - 1) / RM;
+  const int64_t nwaves = (int64_t)gridDim.x * kWavesPerBlock;
+  const int jl = lane * CN;
+  const int ncols = N - jl;
+  const int par = K & 1;
+  for (int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
+       t < tiles; t += nwaves) {
+    const int64_t i0 = t * RM;
+    uint32_t acc[RM][CN];
+    tile_popcounts<CN, RM>(F, M, ldf, sB, kw, i0, lane, acc);
+#pragma unroll
+    for (int r = 0; r < RM; ++r) {
+      if (i0 + r >= M) break;  // wave-uniform
+      const int64_t i = i0 + r;
+      int v[CN];
+      bool big = false;
+#pragma unroll
+      for (int c = 0; c < CN; ++c) {
+        v[c] = K - 2 * (int)acc[r][c];
+        const int code = (v[c] - par) >> 1;
+        big |= (c < ncols) && (code < -128 || code > 127);
+      }
+      if (ncols > 0) {
+        int8_t* dst = C8 + i * ldc8 + jl;
+        if (CN == 4 && ncols >= 4) {
+          uint32_t packed = 0;
+#pragma unroll
+          for (int c = 0; c < CN; ++c)
+            packed |= (uint32_t)(uint8_t)(int8_t)((v[c] - par) >> 1) << (8 * c);
+          *reinterpret_cast<uint32_t*>(dst) = packed;
+        } else {
+#pragma unroll
+          for (int c = 0; c < CN; ++c)
+            if (c < ncols) dst[c] = (int8_t)((v[c] - par) >> 1);
+        }
+      }
+      if (__builtin_amdgcn_ballot_w64(big) != 0) {
+        if (ncols > 0) store_row<T16, CN>(C16 + i * ldc16 + jl, v, ncols, false);
+        if (lane == 0) g[i] = -fabsf(g[i]);
       }
     }
   }
@@ -225,33 +304,48 @@ struct Epi {
   float alpha[4];
   float bias[4];
   int ncols;  // valid columns of this lane (0..4)
-  int mean;
   int relu;
+  bool vec;   // 16-byte output stores allowed
 };
 
 __device__ inline float act(float v, int relu) { return relu ? fmaxf(v, 0.f) : v; }
 
+__device__ inline void store_out(float* __restrict__ o, const Epi& ep,
+                                 const float4_t v) {
+  if (ep.vec && ep.ncols == 4) {
+    *reinterpret_cast<float4_t*>(o) = v;
+    return;
+  }
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    if (c < ep.ncols) o[c] = v[c];
+}
+
 __device__ inline void write_row(float* __restrict__ out, int64_t ldo, int64_t r,
                                  int c0, const Epi& ep, const float4_t acc,
                                  float rowfac) {
-  float* o = out + r * ldo + c0;
+  float4_t v;
 #pragma unroll
-  for (int c = 0; c < 4; ++c)
-    if (c < ep.ncols) o[c] = act(fmaf(acc[c], rowfac * ep.alpha[c], ep.bias[c]), ep.relu);
+  for (int c = 0; c < 4; ++c) v[c] = act(fmaf(acc[c], rowfac * ep.alpha[c], ep.bias[c]), ep.relu);
+  store_out(out + r * ldo + c0, ep, v);
 }
 
 __device__ inline void write_empty(float* __restrict__ out, int64_t ldo,
                                    int64_t r, int c0, const Epi& ep) {
-  float* o = out + r * ldo + c0;
+  float4_t v;
 #pragma unroll
-  for (int c = 0; c < 4; ++c)
-    if (c < ep.ncols) o[c] = act(ep.bias[c], ep.relu);
+  for (int c = 0; c < 4; ++c) v[c] = act(ep.bias[c], ep.relu);
+  store_out(out + r * ldo + c0, ep, v);
+}
+
+__device__ inline float row_factor_deg(int64_t deg, int mean) {
+  const float dg = (float)deg;
+  return mean ? 1.0f / dg : 1.0f / sqrtf(dg);
 }
 
 __device__ inline float row_factor(const int64_t* __restrict__ rowptr, int64_t r,
                                    int mean) {
-  const float dg = (float)(rowptr[r + 1] - rowptr[r]);
-  return mean ? 1.0f / dg : 1.0f / sqrtf(dg);
+  return row_factor_deg(rowptr[r + 1] - rowptr[r], mean);
 }
 
 // Worker w owns edges [w*chunk, min((w+1)*chunk, nnz)).  It aggregates every
@@ -259,61 +353,79 @@ __device__ inline float row_factor(const int64_t* __restrict__ rowptr, int64_t r
 // past the range end leaves a "tail" partial (plus tail_row[w]); a row that
 // began before the range leaves a "head" partial.  Empty rows are written as
 // act(bias) by the worker whose range holds their position.
+//
+// Latency hiding: column indices are fetched one group of U edges ahead of
+// the group whose g / C rows are being gathered, and the ends of the next
+// four rows are kept in a small queue that is refilled as rows finish.  With
+// L == 64 the worker is the whole wave, so edge and row bookkeeping is
+// wave-uniform and lives in scalar registers.
 template <int L, typename T, int U>
 __global__ __launch_bounds__(kBlock) void k_spmm(
     int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, int mean, const float* __restrict__ g,
     const T* __restrict__ C, int32_t d, int64_t ldc,
     const float* __restrict__ alpha, const float* __restrict__ bias, int relu,
-    float* __restrict__ out, int64_t ldo, int64_t chunk, int64_t workers,
-    int32_t dpad, const int32_t* __restrict__ row_of,
+    float* __restrict__ out, int64_t ldo, int vec_out, int64_t chunk,
+    int64_t workers, int32_t dpad, const int32_t* __restrict__ row_of,
     int32_t* __restrict__ tail_row, float* __restrict__ head,
     float* __restrict__ tail) {
+  typedef typename Vec4<T>::type V;
   constexpr int P = 64 / L;
   const int lane = threadIdx.x & 63;
-  const int slot = lane / L;
+  const int slot = L == 64 ? 0 : lane / L;
   if (slot >= P) return;  // idle lanes when L does not divide 64
   const int sub = lane - slot * L;
   const int64_t w =
-      ((int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * P + slot;
+      ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * P + slot;
   if (w >= workers) return;
   const int c0 = blockIdx.y * (L * 4) + sub * 4;
   Epi ep;
   ep.ncols = d - c0 < 0 ? 0 : (d - c0 > 4 ? 4 : d - c0);
-  ep.mean = mean;
   ep.relu = relu;
+  ep.vec = vec_out != 0;
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     ep.alpha[c] = c < ep.ncols ? alpha[c0 + c] : 0.f;
     ep.bias[c] = (c < ep.ncols && bias != nullptr) ? bias[c0 + c] : 0.f;
   }
   const bool load_cols = ep.ncols > 0;
+  const int64_t kEnd = INT64_MAX;
 
   const int64_t s = w * chunk;
   const int64_t t = s + chunk < nnz ? s + chunk : nnz;
   int64_t r = row_of[w];
+  int64_t cur_beg = rowptr[r];
+  int64_t q1 = r + 2 <= n ? rowptr[r + 2] : kEnd;
+  int64_t q2 = r + 3 <= n ? rowptr[r + 3] : kEnd;
+  int64_t q3 = r + 4 <= n ? rowptr[r + 4] : kEnd;
   int64_t cur_end = rowptr[r + 1];
-  bool before = rowptr[r] < s;
+  bool before = cur_beg < s;
   if (!before) {
     for (int64_t q = r - 1; q >= 0 && rowptr[q] == s; --q)
       write_empty(out, ldo, q, c0, ep);
   }
   float4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
 
+  int32_t jn[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) jn[u] = s + u < t ? colidx[s + u] : -1;
+
   for (int64_t e = s; e < t; e += U) {
     int32_t jj[U];
     float gg[U];
-    typename Vec4<T>::type vv[U];
+    V vv[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) jj[u] = e + u < t ? colidx[e + u] : -1;
+    for (int u = 0; u < U; ++u) jj[u] = jn[u];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       gg[u] = jj[u] >= 0 ? g[jj[u]] : 0.f;
       if (jj[u] >= 0 && load_cols)
         vv[u] = load4<T>(C + (int64_t)jj[u] * ldc + c0);
       else
-        vv[u] = typename Vec4<T>::type{0, 0, 0, 0};
+        vv[u] = V{0, 0, 0, 0};
     }
+#pragma unroll
+    for (int u = 0; u < U; ++u) jn[u] = e + U + u < t ? colidx[e + U + u] : -1;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t eu = e + u;
@@ -324,18 +436,20 @@ __global__ __launch_bounds__(kBlock) void k_spmm(
         if (before) {
           if (load_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
         } else {
-          write_row(out, ldo, r, c0, ep, sum, row_factor(rowptr, r, mean));
+          write_row(out, ldo, r, c0, ep, sum, row_factor_deg(cur_end - cur_beg, mean));
         }
         a0 = float4_t{0.f, 0.f, 0.f, 0.f};
         a1 = float4_t{0.f, 0.f, 0.f, 0.f};
         before = false;
-        ++r;
-        cur_end = rowptr[r + 1];
-        while (cur_end == eu) {  // empty rows
-          write_empty(out, ldo, r, c0, ep);
+        do {  // next row; rows without entries are written on the way
+          cur_beg = cur_end;
           ++r;
-          cur_end = rowptr[r + 1];
-        }
+          cur_end = q1;
+          q1 = q2;
+          q2 = q3;
+          q3 = r + 4 <= n ? rowptr[r + 4] : kEnd;
+          if (cur_end == eu) write_empty(out, ldo, r, c0, ep);
+        } while (cur_end == eu);
       }
       if (u & 1)
         fma4(a1, gg[u], vv[u]);
@@ -348,7 +462,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm(
     if (before) {
       if (load_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
     } else {
-      write_row(out, ldo, r, c0, ep, sum, row_factor(rowptr, r, mean));
+      write_row(out, ldo, r, c0, ep, sum, row_factor_deg(cur_end - cur_beg, mean));
     }
     if (t == nnz)
       for (int64_t q = r + 1; q < n; ++q) write_empty(out, ldo, q, c0, ep);
@@ -362,8 +476,383 @@ __global__ __launch_bounds__(kBlock) void k_spmm(
   }
 }
 
+// Buffer resource for raw (unformatted) loads: base, stride 0, byte range,
+// and the gfx9 default of the fourth descriptor word.  Loads past the range
+// return zero.
+template <typename T>
+__device__ inline __amdgpu_buffer_rsrc_t raw_rsrc(const T* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(p), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+template <typename T>
+struct Gather;
+template <>
+struct Gather<_Float16> {
+  __device__ static half4_t load(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
+    return __builtin_bit_cast(half4_t, __builtin_amdgcn_raw_buffer_load_b64(rs, voff, soff, 0));
+  }
+};
+template <>
+struct Gather<int16_t> {
+  __device__ static short4_t load(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
+    return __builtin_bit_cast(short4_t, __builtin_amdgcn_raw_buffer_load_b64(rs, voff, soff, 0));
+  }
+};
+template <>
+struct Gather<int32_t> {
+  __device__ static int4_t load(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
+    return __builtin_bit_cast(int4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0));
+  }
+};
+
+// The same aggregation with one worker per wave (layers wider than 128
+// columns; each block row of the grid covers 256 columns).  All bookkeeping
+// is wave-uniform and kept in 32-bit offsets from the chunk start:
+//  - column indices and node scales arrive 64 edges at a time, one per lane,
+//    two batches ahead (indices) and one batch ahead (scales), and are
+//    broadcast with v_readlane;
+//  - each gathered row is one buffer load whose row offset is a scalar
+//    (one s_mul per edge) and whose column offset is a per-lane constant;
+//  - the ends of the next 64 rows sit one per lane, double-buffered;
+//  - U gathers are issued before the first is consumed.
+// The byte size of C must fit in 32 bits (checked by the launcher).
+template <typename T, int U>
+__global__ __launch_bounds__(kBlock) void k_spmm_wave(
+    int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
+    const int32_t* __restrict__ colidx, int mean, const float* __restrict__ g,
+    const T* __restrict__ C, int32_t d, int64_t ldc,
+    const float* __restrict__ alpha, const float* __restrict__ bias, int relu,
+    float* __restrict__ out, int64_t ldo, int vec_out, int64_t chunk,
+    int64_t workers, int32_t dpad, const int32_t* __restrict__ row_of,
+    int32_t* __restrict__ tail_row, float* __restrict__ head,
+    float* __restrict__ tail) {
+  typedef typename Vec4<T>::type V;
+  static_assert(64 % U == 0, "group size");
+  const int lane = threadIdx.x & 63;
+  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
+  if (w >= workers) return;
+  const int c0 = blockIdx.y * 256 + lane * 4;
+  const int64_t cl = c0 + 4 <= ldc ? c0 : ldc - 4;  // in-bounds load column
+  Epi ep;
+  ep.ncols = d - c0 < 0 ? 0 : (d - c0 > 4 ? 4 : d - c0);
+  ep.relu = relu;
+  ep.vec = vec_out != 0;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    ep.alpha[c] = c < ep.ncols ? alpha[c0 + c] : 0.f;
+    ep.bias[c] = (c < ep.ncols && bias != nullptr) ? bias[c0 + c] : 0.f;
+  }
+  const bool own_cols = ep.ncols > 0;
+  const int row_bytes = (int)(ldc * (int64_t)sizeof(T));
+  const __amdgpu_buffer_rsrc_t rsC = raw_rsrc(C, (uint32_t)(n * row_bytes));
+  const int voff = (int)(cl * (int64_t)sizeof(T));
+
+  const int64_t s = w * chunk;
+  const int nE = (int)((s + chunk < nnz ? s + chunk : nnz) - s);  // edges here
+  const int64_t t = s + nE;
+  // Row ends as offsets from s, clamped to [-1, chunk + 1].
+  auto rel = [&](int64_t v) -> int {
+    const int64_t x = v - s;
+    return (int)(x < -1 ? -1 : (x > chunk + 1 ? chunk + 1 : x));
+  };
+  int64_t r = row_of[w];
+  int64_t rbase = r;
+  int win = rel(rowptr[rbase + 1 + lane < n ? rbase + 1 + lane : n]);
+  int win_nx = rel(rowptr[rbase + 65 + lane < n ? rbase + 65 + lane : n]);
+  const int64_t beg0 = rowptr[r];
+  bool before = beg0 < s;
+  int cur_beg = rel(beg0);
+  int cur_end = __builtin_amdgcn_readlane(win, 0);
+  if (!before) {
+    for (int64_t q = r - 1; q >= 0 && rowptr[q] == s; --q)
+      write_empty(out, ldo, q, c0, ep);
+  }
+  float4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
+
+  // Batches of 64 edges: A = current (indices + scales), B = next (indices
+  // + scales), Cn = the one after (indices only).
+  auto ld_idx = [&](int eb) -> int32_t {
+    const int x = eb + lane;
+    return colidx[s + (x < nE ? x : nE - 1)];
+  };
+  int32_t jA = ld_idx(0);
+  int32_t jB = ld_idx(64);
+  float gA = g[jA];
+  float gB = g[jB];
+  int32_t jCn = ld_idx(128);
+
+  for (int eb = 0; eb < nE; eb += 64) {
+    for (int m = 0; m < 64; m += U) {
+      const int e0 = eb + m;
+      if (e0 >= nE) break;
+      V vv[U];
+      float gg[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = __builtin_amdgcn_readlane(jA, m + u);
+        gg[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                              __builtin_bit_cast(int, gA), m + u));
+        vv[u] = Gather<T>::load(rsC, voff, (int)((uint32_t)j * (uint32_t)row_bytes));
+      }
+      if (e0 + U <= nE && cur_end >= e0 + U) {
+        // No row ends inside this group: accumulate straight through.
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (u & 1)
+            fma4(a1, gg[u], vv[u]);
+          else
+            fma4(a0, gg[u], vv[u]);
+        }
+        continue;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int eu = e0 + u;
+        if (eu >= nE) break;
+        if (eu == cur_end) {
+          const float4_t sum = a0 + a1;
+          if (before) {
+            if (own_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
+          } else if (own_cols) {
+            write_row(out, ldo, r, c0, ep, sum, row_factor_deg(cur_end - cur_beg, mean));
+          }
+          a0 = float4_t{0.f, 0.f, 0.f, 0.f};
+          a1 = float4_t{0.f, 0.f, 0.f, 0.f};
+          before = false;
+          do {  // next row; rows without entries are written on the way
+            cur_beg = cur_end;
+            ++r;
+            if (r - rbase == 64) {
+              rbase = r;
+              win = win_nx;
+              win_nx = rel(rowptr[rbase + 65 + lane < n ? rbase + 65 + lane : n]);
+            }
+            cur_end = __builtin_amdgcn_readlane(win, (int)(r - rbase));
+            if (cur_end == eu && own_cols) write_empty(out, ldo, r, c0, ep);
+          } while (cur_end == eu);
+        }
+        if (u & 1)
+          fma4(a1, gg[u], vv[u]);
+        else
+          fma4(a0, gg[u], vv[u]);
+      }
+    }
+    // Rotate the batches: A <- B, B <- (C, its scales), C <- next indices.
+    jA = jB;
+    gA = gB;
+    jB = jCn;
+    gB = g[jB];
+    jCn = ld_idx(eb + 192);
+  }
+  const float4_t sum = a0 + a1;
+  if (cur_end == nE) {
+    if (before) {
+      if (own_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
+    } else if (own_cols) {
+      write_row(out, ldo, r, c0, ep, sum, row_factor_deg(cur_end - cur_beg, mean));
+    }
+    if (t == nnz && own_cols)
+      for (int64_t q = r + 1; q < n; ++q) write_empty(out, ldo, q, c0, ep);
+    if (lane == 0 && blockIdx.y == 0) tail_row[w] = -1;
+  } else if (before) {
+    if (own_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
+    if (lane == 0 && blockIdx.y == 0) tail_row[w] = -1;
+  } else {
+    if (own_cols) *reinterpret_cast<float4_t*>(tail + w * dpad + c0) = sum;
+    if (lane == 0 && blockIdx.y == 0) tail_row[w] = (int32_t)r;
+  }
+}
+
+__device__ inline float4_t codes_to_float(uint32_t x) {
+  float4_t f;
+  f[0] = (float)(int)(int8_t)(x & 0xff);
+  f[1] = (float)(int)(int8_t)((x >> 8) & 0xff);
+  f[2] = (float)(int)(int8_t)((x >> 16) & 0xff);
+  f[3] = (float)(int)(int8_t)(x >> 24);
+  return f;
+}
+
+__device__ inline void fma4f(float4_t& acc, float g, const float4_t& v) {
+  acc[0] = fmaf(v[0], g, acc[0]);
+  acc[1] = fmaf(v[1], g, acc[1]);
+  acc[2] = fmaf(v[2], g, acc[2]);
+  acc[3] = fmaf(v[3], g, acc[3]);
+}
+
+// Whole-wave aggregation over 8-bit half-codes (see k_bgemm_pop_q8):
+//   sum_j g_j dot_jk = 2 * sum_j g_j code_jk + p * sum_j g_j.
+// An edge whose source row is flagged (sign bit of g_j) reads that row's
+// exact products from C16 instead and adds g_j (dot - p) / 2 to the same
+// accumulator, so partial sums and the fix-up are the same as for exact
+// storage.  Structure otherwise as k_spmm_wave.
+template <typename T16, int U>
+__global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
+    int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
+    const int32_t* __restrict__ colidx, int mean, const float* __restrict__ g,
+    const int8_t* __restrict__ C8, int64_t ldc8, const T16* __restrict__ C16,
+    int64_t ldc16, int par, int32_t d, const float* __restrict__ alpha,
+    const float* __restrict__ bias, int relu, float* __restrict__ out,
+    int64_t ldo, int vec_out, int64_t chunk, int64_t workers, int32_t dpad,
+    const int32_t* __restrict__ row_of, int32_t* __restrict__ tail_row,
+    float* __restrict__ head, float* __restrict__ tail) {
+  static_assert(64 % U == 0, "group size");
+  const int lane = threadIdx.x & 63;
+  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
+  if (w >= workers) return;
+  const int c0 = lane * 4;  // d <= 256: one block row
+  Epi ep;
+  ep.ncols = d - c0 < 0 ? 0 : (d - c0 > 4 ? 4 : d - c0);
+  ep.relu = relu;
+  ep.vec = vec_out != 0;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    ep.alpha[c] = c < ep.ncols ? alpha[c0 + c] : 0.f;
+    ep.bias[c] = (c < ep.ncols && bias != nullptr) ? bias[c0 + c] : 0.f;
+  }
+  const bool own_cols = ep.ncols > 0;
+  const int rb8 = (int)ldc8;
+  const int rb16 = (int)(ldc16 * (int64_t)sizeof(T16));
+  const __amdgpu_buffer_rsrc_t rs8 = raw_rsrc(C8, (uint32_t)(n * rb8));
+  const __amdgpu_buffer_rsrc_t rs16 = raw_rsrc(C16, (uint32_t)(n * rb16));
+  const int voff8 = c0 + 4 <= ldc8 ? c0 : (int)ldc8 - 4;
+  const int voff16 = (int)((c0 + 4 <= ldc16 ? c0 : ldc16 - 4) * (int64_t)sizeof(T16));
+  const float fpar = (float)par;
+
+  const int64_t s = w * chunk;
+  const int nE = (int)((s + chunk < nnz ? s + chunk : nnz) - s);
+  const int64_t t = s + nE;
+  auto rel = [&](int64_t v) -> int {
+    const int64_t x = v - s;
+    return (int)(x < -1 ? -1 : (x > chunk + 1 ? chunk + 1 : x));
+  };
+  int64_t r = row_of[w];
+  int64_t rbase = r;
+  int win = rel(rowptr[rbase + 1 + lane < n ? rbase + 1 + lane : n]);
+  int win_nx = rel(rowptr[rbase + 65 + lane < n ? rbase + 65 + lane : n]);
+  const int64_t beg0 = rowptr[r];
+  bool before = beg0 < s;
+  int cur_beg = rel(beg0);
+  int cur_end = __builtin_amdgcn_readlane(win, 0);
+  if (!before) {
+    for (int64_t q = r - 1; q >= 0 && rowptr[q] == s; --q)
+      write_empty(out, ldo, q, c0, ep);
+  }
+  float4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
+  float gsum = 0.f;  // sum of g_j over the current row (for the parity term)
+
+  auto ld_idx = [&](int eb) -> int32_t {
+    const int x = eb + lane;
+    return colidx[s + (x < nE ? x : nE - 1)];
+  };
+  int32_t jA = ld_idx(0);
+  int32_t jB = ld_idx(64);
+  float gA = g[jA];
+  float gB = g[jB];
+  int32_t jCn = ld_idx(128);
+
+  for (int eb = 0; eb < nE; eb += 64) {
+    const uint64_t flagged = __builtin_amdgcn_ballot_w64(__builtin_bit_cast(int, gA) < 0);
+    for (int m = 0; m < 64; m += U) {
+      const int e0 = eb + m;
+      if (e0 >= nE) break;
+      uint32_t vv[U];
+      float gg[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = __builtin_amdgcn_readlane(jA, m + u);
+        gg[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                              __builtin_bit_cast(int, gA), m + u));
+        vv[u] = __builtin_amdgcn_raw_buffer_load_b32(rs8, voff8,
+                                                     (int)((uint32_t)j * (uint32_t)rb8), 0);
+      }
+      const bool any_flag = ((flagged >> m) & ((1ull << U) - 1)) != 0;
+      if (e0 + U <= nE && cur_end >= e0 + U && !any_flag) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (u & 1)
+            fma4f(a1, gg[u], codes_to_float(vv[u]));
+          else
+            fma4f(a0, gg[u], codes_to_float(vv[u]));
+          gsum += gg[u];
+        }
+        continue;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int eu = e0 + u;
+        if (eu >= nE) break;
+        if (eu == cur_end) {
+          const float4_t sum = 2.f * (a0 + a1) + fpar * gsum;
+          if (before) {
+            if (own_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
+          } else if (own_cols) {
+            write_row(out, ldo, r, c0, ep, sum, row_factor_deg(cur_end - cur_beg, mean));
+          }
+          a0 = float4_t{0.f, 0.f, 0.f, 0.f};
+          a1 = float4_t{0.f, 0.f, 0.f, 0.f};
+          gsum = 0.f;
+          before = false;
+          do {  // next row; rows without entries are written on the way
+            cur_beg = cur_end;
+            ++r;
+            if (r - rbase == 64) {
+              rbase = r;
+              win = win_nx;
+              win_nx = rel(rowptr[rbase + 65 + lane < n ? rbase + 65 + lane : n]);
+            }
+            cur_end = __builtin_amdgcn_readlane(win, (int)(r - rbase));
+            if (cur_end == eu && own_cols) write_empty(out, ldo, r, c0, ep);
+          } while (cur_end == eu);
+        }
+        float gj = gg[u];
+        float4_t v;
+        if (__builtin_bit_cast(int, gj) < 0) {
+          // Flagged source row: its exact products, as (dot - p) / 2.
+          gj = fabsf(gj);
+          const int j = __builtin_amdgcn_readlane(jA, m + u);
+          const typename Vec4<T16>::type x = Gather<T16>::load(
+              rs16, voff16, (int)((uint32_t)j * (uint32_t)rb16));
+#pragma unroll
+          for (int c = 0; c < 4; ++c) v[c] = ((float)x[c] - fpar) * 0.5f;
+        } else {
+          v = codes_to_float(vv[u]);
+        }
+        if (u & 1)
+          fma4f(a1, gj, v);
+        else
+          fma4f(a0, gj, v);
+        gsum += gj;
+      }
+    }
+    jA = jB;
+    gA = gB;
+    jB = jCn;
+    gB = g[jB];
+    jCn = ld_idx(eb + 192);
+  }
+  const float4_t sum = 2.f * (a0 + a1) + fpar * gsum;
+  if (cur_end == nE) {
+    if (before) {
+      if (own_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
+    } else if (own_cols) {
+      write_row(out, ldo, r, c0, ep, sum, row_factor_deg(cur_end - cur_beg, mean));
+    }
+    if (t == nnz && own_cols)
+      for (int64_t q = r + 1; q < n; ++q) write_empty(out, ldo, q, c0, ep);
+    if (lane == 0) tail_row[w] = -1;
+  } else if (before) {
+    if (own_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
+    if (lane == 0) tail_row[w] = -1;
+  } else {
+    if (own_cols) *reinterpret_cast<float4_t*>(tail + w * dpad + c0) = sum;
+    if (lane == 0) tail_row[w] = (int32_t)r;
+  }
+}
+
 // Rows cut by chunk boundaries: tail of the owning worker, then the heads of
-// the following workers in order.  One wave per worker.
+// the following workers in order.  Each wave scans 64 workers and combines
+// the rows whose owner is among them, lanes over columns.
 __global__ __launch_bounds__(kBlock) void k_spmm_fix(
     const int64_t* __restrict__ rowptr, int mean, int32_t d,
     const float* __restrict__ alpha, const float* __restrict__ bias, int relu,
@@ -371,17 +860,23 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix(
     int32_t dpad, const int32_t* __restrict__ tail_row,
     const float* __restrict__ head, const float* __restrict__ tail) {
   const int lane = threadIdx.x & 63;
-  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
-  if (w >= workers) return;
-  const int32_t r = tail_row[w];
-  if (r < 0) return;
-  const int64_t wend = (rowptr[r + 1] - 1) / chunk;
-  const float rowfac = row_factor(rowptr, r, mean);
-  for (int k = lane; k < d; k += 64) {
-    float s = tail[w * dpad + k];
-    for (int64_t v = w + 1; v <= wend; ++v) s += head[v * dpad + k];
-    const float b = bias != nullptr ? bias[k] : 0.f;
-    out[(int64_t)r * ldo + k] = act(fmaf(s, rowfac * alpha[k], b), relu);
+  const int64_t w0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * 64;
+  if (w0 >= workers) return;
+  const int32_t tr = w0 + lane < workers ? tail_row[w0 + lane] : -1;
+  uint64_t mask = __builtin_amdgcn_ballot_w64(tr >= 0);
+  while (mask != 0) {
+    const int q = __builtin_ctzll(mask);
+    mask &= mask - 1;
+    const int64_t w = w0 + q;
+    const int32_t r = __builtin_amdgcn_readlane(tr, q);
+    const int64_t wend = (rowptr[r + 1] - 1) / chunk;
+    const float rowfac = row_factor(rowptr, r, mean);
+    for (int k = lane; k < d; k += 64) {
+      float sacc = tail[w * dpad + k];
+      for (int64_t v = w + 1; v <= wend; ++v) sacc += head[v * dpad + k];
+      const float b = bias != nullptr ? bias[k] : 0.f;
+      out[(int64_t)r * ldo + k] = act(fmaf(sacc, rowfac * alpha[k], b), relu);
+    }
   }
 }
 
@@ -455,20 +950,60 @@ hipError_t spmm_typed(int64_t n, int64_t nnz, const int64_t* rowptr,
   float* head = (float*)(base + p.off_head);
   float* tail = (float*)(base + p.off_tail);
   constexpr int P = 64 / L;
+  constexpr int U = 8;  // edges per group; one group in flight ahead
+  const int vec_out = (ldo % 4 == 0) && ((uintptr_t)out % 16 == 0);
   const int64_t waves = (p.workers + P - 1) / P;
   dim3 grid((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock),
             (unsigned)((d + L * 4 - 1) / (L * 4)));
-  hipLaunchKernelGGL((k_spmm<L, T, 4>), grid, dim3(kBlock), 0, stream, n, nnz,
+  hipLaunchKernelGGL((k_spmm<L, T, U>), grid, dim3(kBlock), 0, stream, n, nnz,
                      rowptr, colidx, mean, g, C, d, ldc, alpha, bias, relu, out,
-                     ldo, p.chunk, p.workers, p.dpad, row_of, tail_row, head,
-                     tail);
+                     ldo, vec_out, p.chunk, p.workers, p.dpad, row_of, tail_row,
+                     head, tail);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const int64_t fix_waves = (p.workers + 63) / 64;
   hipLaunchKernelGGL(k_spmm_fix,
-                     dim3((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock)),
+                     dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
                      dim3(kBlock), 0, stream, rowptr, mean, d, alpha, bias, relu,
                      out, ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail);
   return hipGetLastError();
+}
+
+template <typename T>
+hipError_t spmm_wave_typed(int64_t n, int64_t nnz, const int64_t* rowptr,
+                           const int32_t* colidx, int mean, const float* g,
+                           const T* C, int32_t d, int64_t ldc, const float* alpha,
+                           const float* bias, int relu, float* out, int64_t ldo,
+                           const SpmmPlan& p, void* ws, hipStream_t stream) {
+  char* base = (char*)ws;
+  const int32_t* row_of = (const int32_t*)(base + p.off_rowof);
+  int32_t* tail_row = (int32_t*)(base + p.off_tailrow);
+  float* head = (float*)(base + p.off_head);
+  float* tail = (float*)(base + p.off_tail);
+  const int vec_out = (ldo % 4 == 0) && ((uintptr_t)out % 16 == 0);
+  dim3 grid((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock),
+            (unsigned)((d + 255) / 256));
+  constexpr int U = 8;
+  hipLaunchKernelGGL((k_spmm_wave<T, U>), grid, dim3(kBlock), 0, stream, n, nnz,
+                     rowptr, colidx, mean, g, C, d, ldc, alpha, bias, relu, out,
+                     ldo, vec_out, p.chunk, p.workers, p.dpad, row_of, tail_row,
+                     head, tail);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t fix_waves = (p.workers + 63) / 64;
+  hipLaunchKernelGGL(k_spmm_fix,
+                     dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
+                     dim3(kBlock), 0, stream, rowptr, mean, d, alpha, bias, relu,
+                     out, ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail);
+  return hipGetLastError();
+}
+
+// Lanes per worker for a layer width: 4 columns per lane; wider than 128
+// columns takes whole-wave workers (L = 64).
+inline int spmm_lanes(int32_t d) {
+  const int lanes = (d + 3) / 4;
+  return lanes <= 2 ? 2 : lanes <= 4 ? 4 : lanes <= 8 ? 8 : lanes <= 12 ? 12
+       : lanes <= 16 ? 16 : lanes <= 32 ? 32 : 64;
 }
 
 template <typename T>
@@ -478,17 +1013,22 @@ hipError_t spmm_dispatch_l(int64_t n, int64_t nnz, const int64_t* rowptr,
                            const float* alpha, const float* bias, int relu,
                            float* out, int64_t ldo, const SpmmPlan& p, void* ws,
                            hipStream_t stream) {
-  const int lanes = (d + 3) / 4;  // lanes that cover d columns, 4 per lane
 #define BIGCN_SPMM_L(LV)                                                       \
   return spmm_typed<LV, T>(n, nnz, rowptr, colidx, mean, g, C, d, ldc, alpha, \
                            bias, relu, out, ldo, p, ws, stream)
-  if (lanes <= 2) BIGCN_SPMM_L(2);
-  if (lanes <= 4) BIGCN_SPMM_L(4);
-  if (lanes <= 8) BIGCN_SPMM_L(8);
-  if (lanes <= 12) BIGCN_SPMM_L(12);
-  if (lanes <= 16) BIGCN_SPMM_L(16);
-  if (lanes <= 32) BIGCN_SPMM_L(32);
-  BIGCN_SPMM_L(64);
+  switch (spmm_lanes(d)) {
+    case 2: BIGCN_SPMM_L(2);
+    case 4: BIGCN_SPMM_L(4);
+    case 8: BIGCN_SPMM_L(8);
+    case 12: BIGCN_SPMM_L(12);
+    case 16: BIGCN_SPMM_L(16);
+    case 32: BIGCN_SPMM_L(32);
+    default:
+      // Whole-wave workers address C with 32-bit buffer offsets.
+      if ((uint64_t)n * (uint64_t)ldc * sizeof(T) > 0xFFFFFFFFull) BIGCN_SPMM_L(32);
+      return spmm_wave_typed<T>(n, nnz, rowptr, colidx, mean, g, C, d, ldc, alpha,
+                                bias, relu, out, ldo, p, ws, stream);
+  }
 #undef BIGCN_SPMM_L
 }
 
@@ -534,10 +1074,7 @@ SpmmPlan spmm_plan(int64_t n, int64_t nnz, int32_t d) {
   while (chunk < 2048 && chunk * 2 * 16384 <= nnz) chunk *= 2;
   p.chunk = chunk;
   p.workers = nnz > 0 ? (nnz + chunk - 1) / chunk : 1;
-  const int lanes = (d + 3) / 4;
-  const int L = lanes <= 2 ? 2 : lanes <= 4 ? 4 : lanes <= 8 ? 8 : lanes <= 12 ? 12
-              : lanes <= 16 ? 16 : lanes <= 32 ? 32 : 64;
-  const int64_t slab = 4 * L;
+  const int64_t slab = 4 * spmm_lanes(d);
   p.dpad = (int32_t)(((d + slab - 1) / slab) * slab);
   auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
   size_t off = 0;
@@ -590,6 +1127,64 @@ hipError_t launch_spmm(int64_t n, int64_t nnz, const int64_t* rowptr,
                                       (const int32_t*)C, d, ldc, alpha, bias,
                                       relu, out, ldo, plan, workspace, stream);
   }
+}
+
+bool q8_supported(int64_t n, int32_t N, int32_t K) {
+  const int kw = (K + 63) >> 6;
+  if (N <= 128 || N > 256 || K > 2048) return false;
+  if ((size_t)kw * 4 * 64 * 8 > 65536) return false;
+  return (uint64_t)n * 256u <= 0xFFFFFFFFull &&
+         (uint64_t)n * (uint64_t)((N + 7) / 8 * 8) * 2u <= 0xFFFFFFFFull;
+}
+
+hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
+                           const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
+                           int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
+                           float* g, hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  constexpr int RM = 4;
+  constexpr int CN = 4;
+  const int kw = (K + 63) >> 6;
+  const size_t lds = (size_t)kw * CN * 64 * sizeof(uint64_t);
+  const int64_t tiles = (M + RM - 1) / RM;
+  dim3 grid(grid_cap((tiles + kWavesPerBlock - 1) / kWavesPerBlock, 4096));
+  hipLaunchKernelGGL((k_bgemm_pop_q8<CN, RM, _Float16>), grid, dim3(kBlock), lds,
+                     stream, F, M, ldf, B, N, ldb, K, C8, ldc8, (_Float16*)C16, ldc16, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
+                          const int32_t* colidx, int mean, const float* g,
+                          const int8_t* C8, int64_t ldc8, const void* C16,
+                          int64_t ldc16, int32_t K, int32_t d, const float* alpha,
+                          const float* bias, int relu, float* out, int64_t ldo,
+                          const SpmmPlan& p, void* ws, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  if (nnz == 0) {
+    const int64_t total = n * (int64_t)d;
+    hipLaunchKernelGGL(k_spmm_empty, dim3((unsigned)((total + kBlock - 1) / kBlock)),
+                       dim3(kBlock), 0, stream, n, d, bias, relu, out, ldo);
+    return hipGetLastError();
+  }
+  char* base = (char*)ws;
+  const int32_t* row_of = (const int32_t*)(base + p.off_rowof);
+  int32_t* tail_row = (int32_t*)(base + p.off_tailrow);
+  float* head = (float*)(base + p.off_head);
+  float* tail = (float*)(base + p.off_tail);
+  const int vec_out = (ldo % 4 == 0) && ((uintptr_t)out % 16 == 0);
+  dim3 grid((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock));
+  hipLaunchKernelGGL((k_spmm_wave_q8<_Float16, 8>), grid, dim3(kBlock), 0, stream,
+                     n, nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16,
+                     ldc16, K & 1, d, alpha, bias, relu, out, ldo, vec_out, p.chunk,
+                     p.workers, p.dpad, row_of, tail_row, head, tail);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t fix_waves = (p.workers + 63) / 64;
+  hipLaunchKernelGGL(k_spmm_fix,
+                     dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
+                     dim3(kBlock), 0, stream, rowptr, mean, d, alpha, bias, relu,
+                     out, ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail);
+  return hipGetLastError();
 }
 
 bool bgemm_mfma_supported(int32_t N, int32_t K) {

@@ -18,7 +18,7 @@ EINVAL, EALIGN, EWORKSPACE, EUNSUPPORTED = -1, -2, -3, -4
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(bigcn_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(bigcn_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_header_declares_the_expected_entry_points():

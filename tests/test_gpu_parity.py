@@ -218,7 +218,9 @@ def test_spmm_is_bitwise_reproducible(dev):
 
 def gpu_layer(dev, g, norm, h, wt, bias, act="none", mu=None, rstd=None,
               rowptr_t=None, colidx_t=None, ht=None):
-    """pack -> bgemm -> spmm through the three entry points."""
+    """pack -> bgemm -> spmm through the entry points, with the product
+    storage the forward pass picks for this shape (8-bit half-codes for
+    129..256 output columns, else exact 16-bit)."""
     n, K = h.shape if ht is None else ht.shape
     d = wt.shape[0]
     rowptr_t = _t(g.rowptr, dev) if rowptr_t is None else rowptr_t
@@ -232,17 +234,37 @@ def gpu_layer(dev, g, norm, h, wt, bias, act="none", mu=None, rstd=None,
                            None if rstd is None else _t(rstd, dev), rowptr_t, norm)
     ldc = (d + 7) // 8 * 8
     C = torch.empty((n, ldc), dtype=torch.float16 if K <= 2048 else torch.int16, device=dev)
-    bg.bigcn_bgemm(F, wbits, K, C[:, :d])
     out = torch.empty((n, d), dtype=torch.float32, device=dev)
     ws = torch.empty(bg.spmm_workspace_bytes(n, g.nnz, d), dtype=torch.uint8, device=dev)
-    bg.bigcn_spmm_csr(rowptr_t, colidx_t, gs, C, alpha, out, ws,
-                      None if bias is None else _t(bias, dev), norm, act, d=d)
+    b = None if bias is None else _t(bias, dev)
+    if bg.q8_supported(n, d, K):
+        C8 = torch.empty((n, 256), dtype=torch.int8, device=dev)
+        bg.bigcn_bgemm_q8(F, wbits, K, C8, C, gs)
+        bg.bigcn_spmm_csr_q8(rowptr_t, colidx_t, gs, C8, C, K, alpha, out, ws, b, norm,
+                             act, d=d)
+        return out, F, (C8, C, gs), alpha
+    bg.bigcn_bgemm(F, wbits, K, C[:, :d])
+    bg.bigcn_spmm_csr(rowptr_t, colidx_t, gs, C, alpha, out, ws, b, norm, act, d=d)
     return out, F, C[:, :d], alpha
+
+
+def decode_products(prod, K, d):
+    """Integer products from either storage: an exact tensor, or the 8-bit
+    half-codes with their flagged exact rows (sign bit of g)."""
+    if isinstance(prod, torch.Tensor):
+        return prod.cpu().numpy().astype(np.int64)
+    C8, C16, gs = prod
+    codes = C8[:, :d].cpu().numpy().astype(np.int64)
+    dot = 2 * codes + (K & 1)
+    flagged = np.signbit(gs.cpu().numpy())
+    dot[flagged] = C16[:, :d].cpu().numpy()[flagged].astype(np.int64)
+    return dot
 
 
 @pytest.mark.parametrize("K,d,norm", [(130, 7, "sym"), (1433, 64, "sym"),
                                       (64, 256, "mean"), (602, 41, "mean"),
-                                      (256, 47, "sym")])
+                                      (256, 47, "sym"), (1433, 200, "sym"),
+                                      (255, 256, "mean"), (602, 256, "sym")])
 def test_layer_matches_oracle(dev, K, d, norm):
     rng = np.random.default_rng(K + d)
     g = _star_plus_random(700, rng)
@@ -256,9 +278,79 @@ def test_layer_matches_oracle(dev, K, d, norm):
     fb, _ = oracle.binarize(x, mu, rstd)
     assert np.array_equal(u64(F), fb)
     wb, _ = oracle.binarize(wt)
-    assert np.array_equal(C.cpu().numpy().astype(np.int64), oracle.sign_dot(fb, wb, K))
+    assert np.array_equal(decode_products(C, K, d), oracle.sign_dot(fb, wb, K))
     assert np.allclose(alpha.cpu().numpy(), a_ref, rtol=1e-5, atol=0)
     err = mass_error(out.cpu().numpy(), z, m)
     print("K=%d d=%d %s mass err %.2e plain rel %.2e" % (K, d, norm, err,
           plain_rel_error(out.cpu().numpy(), z, m)))
     assert err <= TOL
+
+
+# ------------------------------------------------------ 8-bit half-codes --
+
+Q8_SHAPES = [(1, 129, 64), (77, 200, 100), (1000, 256, 127), (513, 256, 128),
+             (333, 256, 255), (400, 256, 256), (257, 130, 300), (300, 256, 602),
+             (64, 256, 1433), (65, 256, 2048)]
+
+
+@pytest.mark.parametrize("M,N,K", Q8_SHAPES)
+def test_bgemm_q8_matches_oracle(dev, M, N, K):
+    rng = np.random.default_rng(M + N + K)
+    F, _ = oracle.binarize(rng.standard_normal((M, K)).astype(np.float32))
+    B, _ = oracle.binarize(rng.standard_normal((N, K)).astype(np.float32))
+    F[M // 2] = B[N // 3]                      # |dot| = K in one column
+    if M > 3:
+        F[1] = B[0]
+        F[2] = ~B[1] & F[2]                     # partial complement
+    ref = oracle.sign_dot(F, B, K)
+    gsc = rng.uniform(0.0, 2.0, M).astype(np.float32)
+    gsc[::5] = 0.0
+    Ft, Bt = _t(F.view(np.int64), dev), _t(B.view(np.int64), dev)
+    C8 = torch.full((M, 256 + 4), 99, dtype=torch.int8, device=dev)
+    C16 = torch.zeros((M, (N + 7) // 8 * 8), dtype=torch.float16, device=dev)
+    gt = _t(gsc, dev)
+    bg.bigcn_bgemm_q8(Ft, Bt, K, C8, C16, gt)
+    torch.cuda.synchronize()
+    got_g = gt.cpu().numpy()
+    flagged = np.signbit(got_g)
+    assert np.array_equal(np.abs(got_g), gsc)                 # only the sign may change
+    assert np.array_equal(flagged, (np.abs(ref) > 255).any(axis=1))
+    assert np.array_equal(decode_products((C8, C16, gt), K, N), ref)
+    if K <= 255:
+        assert not flagged.any()
+
+
+@pytest.mark.parametrize("d,K,norm,act", [(129, 64, "sym", "none"), (200, 255, "mean", "relu"),
+                                          (256, 256, "sym", "none"), (256, 602, "mean", "none"),
+                                          (256, 1433, "sym", "relu")])
+def test_spmm_q8_matches_oracle(dev, d, K, norm, act):
+    rng = np.random.default_rng(d + K)
+    g = _star_plus_random(900, rng)
+    par = K & 1
+    dot = 2 * rng.integers(-60, 61, size=(g.n, d)) + par
+    big_rows = rng.choice(g.n, size=30, replace=False)
+    if K > 255:
+        dot[big_rows, 0] = K                   # needs the exact fallback
+    beta = rng.uniform(0.1, 2.0, g.n).astype(np.float32).astype(np.float64)
+    beta[big_rows[:3]] = 0.0
+    alpha = rng.uniform(0.1, 2.0, d).astype(np.float32)
+    bias = rng.uniform(-0.1, 0.1, d).astype(np.float32)
+    z, m, _ = oracle.aggregate(g.rowptr, g.colidx, norm, beta, alpha.astype(np.float64),
+                               dot, bias, act)
+    deg = np.diff(g.rowptr).astype(np.float64)
+    gg = (beta / np.sqrt(deg) if norm == "sym" else beta).astype(np.float32)
+    flag = (np.abs(dot) > 255).any(axis=1)
+    gg[flag] = -np.abs(gg[flag])               # sign bit marks the exact rows
+    codes = np.clip((dot - par) // 2, -128, 127).astype(np.int8)
+    C8 = torch.zeros((g.n, 256), dtype=torch.int8, device=dev)
+    C8[:, :d] = _t(codes, dev)
+    ldc16 = (d + 7) // 8 * 8
+    C16 = torch.zeros((g.n, ldc16), dtype=torch.float16, device=dev)
+    C16[:, :d] = _t(np.where(flag[:, None], dot, 0).astype(np.float16), dev)
+    out = torch.full((g.n, d), float("nan"), dtype=torch.float32, device=dev)
+    ws = torch.empty(bg.spmm_workspace_bytes(g.n, g.nnz, d), dtype=torch.uint8, device=dev)
+    bg.bigcn_spmm_csr_q8(_t(g.rowptr, dev), _t(g.colidx, dev), _t(gg, dev), C8, C16, K,
+                         _t(alpha, dev), out, ws, _t(bias, dev), norm, act)
+    torch.cuda.synchronize()
+    err = mass_error(out.cpu().numpy(), z, m, relu=act == "relu")
+    assert err <= TOL, err

@@ -19,7 +19,7 @@ import oracle
 import workloads
 import paper_2010_07565_amd as bg
 from helpers import TOL, mass_error, plain_rel_error, sample_rows, u64
-from test_gpu_parity import _t, gpu_layer
+from test_gpu_parity import _t, decode_products, gpu_layer
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -70,8 +70,8 @@ def test_workload_layers_match_oracle(dev, cfg):
         wb, _ = oracle.binarize(wt)
         rows = np.arange(g.n) if ids is None else ids
         ref_dot = oracle.sign_dot(fb[rows], wb, K)
-        assert np.array_equal(C[torch.from_numpy(rows).to(dev)].cpu().numpy().astype(np.int64),
-                              ref_dot), "binary GEMM differs"
+        got_dot = decode_products(C, K, d)[rows]
+        assert np.array_equal(got_dot, ref_dot), "binary GEMM differs"
         t = time.time()
         z, m, _, a_ref = oracle.layer(g.rowptr, g.colidx, w.norm, h, wt, w.biases[l],
                                       mu=mu, rstd=rstd, ids=ids)
