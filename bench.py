@@ -9,8 +9,10 @@ is the PubMed-shaped citation graph (19,717 nodes, 500 -> 64 -> 3); the other
 four are selectable with --workload.
 
 Prints one JSON line.  Besides the forward-pass throughput it carries
- - "kernels":  each layer's kernels timed alone through their entry points
-   with HIP events on the launch stream (average over --kernel-reps);
+ - "kernels":  each layer's steps timed alone through their entry points
+   (HIP events around a graph replay of --kernel-reps back-to-back calls on
+   the launch stream); the aggregation step is its three kernels (row plan,
+   aggregation, fix-up of rows cut by chunk boundaries);
  - "roofline": the dominant kernel (largest share of a forward pass) against
    its bound: HBM bytes for pack / aggregation, bit operations on the vector
    ALUs for the binary GEMM;
@@ -63,16 +65,24 @@ def kernel_specs(w, ldF, ldc):
 
 
 def time_calls(fn, reps, torch):
-    """Average duration of fn() over reps, HIP events around each call on
-    the current stream."""
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
-    for i in range(reps):
-        starts[i].record()
-        fn()
-        ends[i].record()
+    """Average GPU duration of one fn() call: `reps` calls are captured into a
+    HIP graph and replayed between two HIP events on the launch stream, so no
+    host launch gap falls inside the measured interval."""
+    fn()                                   # warm up (first-touch, code load)
     torch.cuda.synchronize()
-    return sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / reps * 1e-3
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(reps):
+            fn()
+    graph.replay()                         # warm replay
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    graph.replay()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / reps * 1e-3
 
 
 def cpu_baseline(w, budget_s=10.0):
@@ -131,9 +141,11 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
-    ap.add_argument("--kernel-reps", type=int, default=50)
+    ap.add_argument("--kernel-reps", type=int, default=20)
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true",
+                    help="report eager calls instead of the HIP-graph replay")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -162,18 +174,31 @@ def main():
                      rstd=w.rstd, device=dev)
     torch.cuda.synchronize()
 
-    # ---- the timed forward passes
-    for _ in range(args.warmup):
-        model.forward(x)
+    # ---- the timed forward passes: eager calls, then the same pass replayed
+    # from a HIP graph (the serving loop); the graph's output is checked
+    # against the eager one bit for bit before it is timed.
+    def timed(fn, steps, warmup):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t) / steps
+
+    eager_s = timed(lambda: model.forward(x), args.steps, args.warmup)
+    eager_out = model.out.clone()
+    replay = model.capture(x)
+    replay()
     torch.cuda.synchronize()
-    t = time.perf_counter()
-    for _ in range(args.steps):
-        model.forward(x)
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t
-    ms = dt / args.steps * 1e3
-    nodes_per_s = g.n * args.steps / dt
-    log("forward: %.4f ms/step, %.4g nodes/s" % (ms, nodes_per_s))
+    assert torch.equal(model.out, eager_out), "graph replay differs from the eager pass"
+    graph_s = timed(replay, args.steps, args.warmup)
+    step_s = graph_s if not args.eager else eager_s
+    ms = step_s * 1e3
+    nodes_per_s = g.n / step_s
+    log("forward: eager %.4f ms/step, graph replay %.4f ms/step -> %.4g nodes/s" % (
+        eager_s * 1e3, graph_s * 1e3, nodes_per_s))
 
     # ---- each kernel alone, through its entry point, same shapes and ld's
     L = len(w.weights_t)
@@ -254,6 +279,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 5),
+        "mode": "eager" if args.eager else "hip_graph_replay",
+        "eager_ms_per_step": round(eager_s * 1e3, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

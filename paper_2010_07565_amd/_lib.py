@@ -310,3 +310,22 @@ class BiGCN:
         bigcn_forward(self.rowptr, self.colidx, x, self.layers, self.out, self.ws,
                       self.mu, self.rstd, self.norm, stream=stream)
         return self.out
+
+    def capture(self, x: torch.Tensor):
+        """Records one forward pass on ``x`` into a HIP graph and returns a
+        function that replays it (into ``self.out``).  The graph keeps the
+        device addresses of ``x``, the weights and the workspace: refill
+        ``x`` in place to run on new features.  Nothing is allocated or
+        cleared inside the captured region."""
+        graph = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            bigcn_forward(self.rowptr, self.colidx, x, self.layers, self.out, self.ws,
+                          self.mu, self.rstd, self.norm)
+        torch.cuda.synchronize()
+        self._graph = graph                     # keep the graph alive
+
+        def replay():
+            graph.replay()
+            return self.out
+        return replay

@@ -111,6 +111,82 @@ __global__ __launch_bounds__(kBlock) void k_pack(
   }
 }
 
+// Same computation with RW rows per wave in flight: all RW*kw loads of a
+// row group are issued before the first ballot, the per-column mean / rstd
+// sit in LDS, and the RW row sums are reduced together.  kw <= KWT <= 32.
+template <bool STD, int RW, int KWT>
+__global__ __launch_bounds__(kBlock) void k_pack_rows(
+    const float* __restrict__ x, int64_t rows, int32_t cols, int64_t ldx,
+    const float* __restrict__ mu, const float* __restrict__ rstd,
+    const int64_t* __restrict__ rowptr, int sym, uint64_t* __restrict__ bits,
+    int64_t ldw, float* __restrict__ scale) {
+  extern __shared__ float s_norm[];  // mu[0..cols), rstd[cols..2 cols)
+  if (STD) {
+    for (int i = threadIdx.x; i < cols; i += kBlock) {
+      s_norm[i] = mu[i];
+      s_norm[cols + i] = rstd[i];
+    }
+    __syncthreads();
+  }
+  const int lane = threadIdx.x & 63;
+  const int kw = (cols + 63) >> 6;
+  const int64_t step = (int64_t)gridDim.x * kWavesPerBlock * RW;
+  for (int64_t r0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * RW;
+       r0 < rows; r0 += step) {
+    float v[RW][KWT];
+#pragma unroll
+    for (int q = 0; q < RW; ++q) {
+      const int64_t r = r0 + q < rows ? r0 + q : rows - 1;
+#pragma unroll
+      for (int w = 0; w < KWT; ++w) {
+        const int k = w * 64 + lane;
+        v[q][w] = (w < kw && k < cols) ? x[r * ldx + k] : 0.f;
+      }
+    }
+    float l1[RW];
+    uint64_t mine[RW];
+#pragma unroll
+    for (int q = 0; q < RW; ++q) {
+      l1[q] = 0.f;
+      mine[q] = 0;
+#pragma unroll
+      for (int w = 0; w < KWT; ++w) {
+        if (w >= kw) break;  // wave-uniform
+        const int k = w * 64 + lane;
+        const bool ok = k < cols;
+        float y = v[q][w];
+        if (STD && ok) {
+          const float t = y - s_norm[k];  // two separate fp32 roundings
+          y = t * s_norm[cols + k];
+        }
+        const uint64_t b = __builtin_amdgcn_ballot_w64(ok && y >= 0.f);
+        l1[q] += ok ? fabsf(y) : 0.f;
+        if (lane == w) mine[q] = b;
+      }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+#pragma unroll
+      for (int q = 0; q < RW; ++q) l1[q] += __shfl_xor(l1[q], off, 64);
+#pragma unroll
+    for (int q = 0; q < RW; ++q) {
+      const int64_t r = r0 + q;
+      if (r >= rows) break;  // wave-uniform
+      uint64_t* br = bits + r * ldw;
+      for (int64_t wb = 0; wb < ldw; wb += 64)
+        if (wb + lane < ldw) br[wb + lane] = wb == 0 ? mine[q] : 0ull;
+      if (lane == q) {
+        float sc = l1[q] / (float)cols;
+        if (rowptr != nullptr && sym) {
+          const int64_t dg = rowptr[r + 1] - rowptr[r];
+          sc = sc * (dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f);
+        }
+        scale[r] = sc;
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------ bgemm (popcount) ----
 
 template <typename T>
@@ -393,6 +469,9 @@ __global__ __launch_bounds__(kBlock) void k_spmm(
 
   const int64_t s = w * chunk;
   const int64_t t = s + chunk < nnz ? s + chunk : nnz;
+  int32_t jn[U];  // first group's column indices: independent of the row lookup
+#pragma unroll
+  for (int u = 0; u < U; ++u) jn[u] = s + u < t ? colidx[s + u] : -1;
   int64_t r = row_of[w];
   int64_t cur_beg = rowptr[r];
   int64_t q1 = r + 2 <= n ? rowptr[r + 2] : kEnd;
@@ -405,10 +484,6 @@ __global__ __launch_bounds__(kBlock) void k_spmm(
       write_empty(out, ldo, q, c0, ep);
   }
   float4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
-
-  int32_t jn[U];
-#pragma unroll
-  for (int u = 0; u < U; ++u) jn[u] = s + u < t ? colidx[s + u] : -1;
 
   for (int64_t e = s; e < t; e += U) {
     int32_t jj[U];
@@ -851,8 +926,10 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
 }
 
 // Rows cut by chunk boundaries: tail of the owning worker, then the heads of
-// the following workers in order.  Each wave scans 64 workers and combines
-// the rows whose owner is among them, lanes over columns.
+// the following workers, added in order.  A group of LC lanes (LC a power of
+// two covering the layer width, at most 64) serves one worker, so every cut
+// row is combined in parallel.
+template <int LC>
 __global__ __launch_bounds__(kBlock) void k_spmm_fix(
     const int64_t* __restrict__ rowptr, int mean, int32_t d,
     const float* __restrict__ alpha, const float* __restrict__ bias, int relu,
@@ -860,24 +937,49 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix(
     int32_t dpad, const int32_t* __restrict__ tail_row,
     const float* __restrict__ head, const float* __restrict__ tail) {
   const int lane = threadIdx.x & 63;
-  const int64_t w0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * 64;
-  if (w0 >= workers) return;
-  const int32_t tr = w0 + lane < workers ? tail_row[w0 + lane] : -1;
-  uint64_t mask = __builtin_amdgcn_ballot_w64(tr >= 0);
-  while (mask != 0) {
-    const int q = __builtin_ctzll(mask);
-    mask &= mask - 1;
-    const int64_t w = w0 + q;
-    const int32_t r = __builtin_amdgcn_readlane(tr, q);
-    const int64_t wend = (rowptr[r + 1] - 1) / chunk;
-    const float rowfac = row_factor(rowptr, r, mean);
-    for (int k = lane; k < d; k += 64) {
-      float sacc = tail[w * dpad + k];
-      for (int64_t v = w + 1; v <= wend; ++v) sacc += head[v * dpad + k];
-      const float b = bias != nullptr ? bias[k] : 0.f;
-      out[(int64_t)r * ldo + k] = act(fmaf(sacc, rowfac * alpha[k], b), relu);
+  const int64_t w = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / LC;
+  if (w >= workers) return;
+  const int sub = lane % LC;
+  const int32_t r = tail_row[w];
+  if (r < 0) return;
+  const int64_t wend = (rowptr[r + 1] - 1) / chunk;
+  const float rowfac = row_factor(rowptr, r, mean);
+  for (int k = sub; k < d; k += LC) {
+    float sacc = tail[w * dpad + k];
+    int64_t v = w + 1;
+    for (; v + 8 <= wend + 1; v += 8) {  // eight loads in flight, added in order
+      float h[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) h[u] = head[(v + u) * dpad + k];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sacc += h[u];
     }
+    for (; v <= wend; ++v) sacc += head[v * dpad + k];
+    const float b = bias != nullptr ? bias[k] : 0.f;
+    out[(int64_t)r * ldo + k] = act(fmaf(sacc, rowfac * alpha[k], b), relu);
   }
+}
+
+hipError_t launch_fix(const int64_t* rowptr, int mean, int32_t d, const float* alpha,
+                      const float* bias, int relu, float* out, int64_t ldo,
+                      const SpmmPlan& p, const int32_t* tail_row, const float* head,
+                      const float* tail, hipStream_t stream) {
+  const int lc = d <= 4 ? 4 : d <= 8 ? 8 : d <= 16 ? 16 : d <= 32 ? 32 : 64;
+  const int64_t threads = p.workers * lc;
+  const dim3 grid((unsigned)((threads + kBlock - 1) / kBlock));
+#define BIGCN_FIX(LCV)                                                          \
+  hipLaunchKernelGGL(k_spmm_fix<LCV>, grid, dim3(kBlock), 0, stream, rowptr, mean, d, \
+                     alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,      \
+                     tail_row, head, tail)
+  switch (lc) {
+    case 4: BIGCN_FIX(4); break;
+    case 8: BIGCN_FIX(8); break;
+    case 16: BIGCN_FIX(16); break;
+    case 32: BIGCN_FIX(32); break;
+    default: BIGCN_FIX(64); break;
+  }
+#undef BIGCN_FIX
+  return hipGetLastError();
 }
 
 // row_of[w] = the row holding edge w*chunk.  One thread per row.
@@ -961,12 +1063,8 @@ hipError_t spmm_typed(int64_t n, int64_t nnz, const int64_t* rowptr,
                      head, tail);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t fix_waves = (p.workers + 63) / 64;
-  hipLaunchKernelGGL(k_spmm_fix,
-                     dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
-                     dim3(kBlock), 0, stream, rowptr, mean, d, alpha, bias, relu,
-                     out, ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail);
-  return hipGetLastError();
+  return launch_fix(rowptr, mean, d, alpha, bias, relu, out, ldo, p, tail_row, head,
+                    tail, stream);
 }
 
 template <typename T>
@@ -990,12 +1088,8 @@ hipError_t spmm_wave_typed(int64_t n, int64_t nnz, const int64_t* rowptr,
                      head, tail);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t fix_waves = (p.workers + 63) / 64;
-  hipLaunchKernelGGL(k_spmm_fix,
-                     dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
-                     dim3(kBlock), 0, stream, rowptr, mean, d, alpha, bias, relu,
-                     out, ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail);
-  return hipGetLastError();
+  return launch_fix(rowptr, mean, d, alpha, bias, relu, out, ldo, p, tail_row, head,
+                    tail, stream);
 }
 
 // Lanes per worker for a layer width: 4 columns per lane; wider than 128
@@ -1032,6 +1126,37 @@ hipError_t spmm_dispatch_l(int64_t n, int64_t nnz, const int64_t* rowptr,
 #undef BIGCN_SPMM_L
 }
 
+template <bool STD, int RW, int KWT>
+hipError_t pack_rows_launch(const float* x, int64_t rows, int32_t cols, int64_t ldx,
+                            const float* mu, const float* rstd, const int64_t* rowptr,
+                            int sym, uint64_t* bits, int64_t ldw, float* scale,
+                            hipStream_t stream) {
+  const int64_t groups = (rows + RW - 1) / RW;
+  dim3 grid(grid_cap((groups + kWavesPerBlock - 1) / kWavesPerBlock, 8192));
+  const size_t lds = STD ? (size_t)2 * cols * sizeof(float) : 0;
+  hipLaunchKernelGGL((k_pack_rows<STD, RW, KWT>), grid, dim3(kBlock), lds, stream, x,
+                     rows, cols, ldx, mu, rstd, rowptr, sym, bits, ldw, scale);
+  return hipGetLastError();
+}
+
+template <bool STD>
+hipError_t pack_rows_dispatch(const float* x, int64_t rows, int32_t cols, int64_t ldx,
+                              const float* mu, const float* rstd, const int64_t* rowptr,
+                              int sym, uint64_t* bits, int64_t ldw, float* scale,
+                              hipStream_t stream) {
+  const int kw = (cols + 63) >> 6;
+#define BIGCN_PACK(RWV, KWV)                                                          \
+  return pack_rows_launch<STD, RWV, KWV>(x, rows, cols, ldx, mu, rstd, rowptr, sym, \
+                                         bits, ldw, scale, stream)
+  if (kw <= 1) BIGCN_PACK(8, 1);
+  if (kw <= 2) BIGCN_PACK(8, 2);
+  if (kw <= 4) BIGCN_PACK(4, 4);
+  if (kw <= 8) BIGCN_PACK(2, 8);
+  if (kw <= 16) BIGCN_PACK(1, 16);
+  BIGCN_PACK(1, 32);
+#undef BIGCN_PACK
+}
+
 }  // namespace
 
 // ------------------------------------------------------------- launchers ----
@@ -1041,6 +1166,14 @@ hipError_t launch_pack(const float* x, int64_t rows, int32_t cols, int64_t ldx,
                        const int64_t* rowptr, int sym, uint64_t* bits,
                        int64_t ldw, float* scale, hipStream_t stream) {
   if (rows == 0) return hipSuccess;
+  const int kw = (cols + 63) >> 6;
+  if (kw <= 32) {
+    if (mu != nullptr)
+      return pack_rows_dispatch<true>(x, rows, cols, ldx, mu, rstd, rowptr, sym, bits,
+                                      ldw, scale, stream);
+    return pack_rows_dispatch<false>(x, rows, cols, ldx, mu, rstd, rowptr, sym, bits,
+                                     ldw, scale, stream);
+  }
   dim3 grid(grid_cap((rows + kWavesPerBlock - 1) / kWavesPerBlock, 8192));
   if (mu != nullptr)
     hipLaunchKernelGGL(k_pack<true>, grid, dim3(kBlock), 0, stream, x, rows, cols,
@@ -1179,12 +1312,8 @@ hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                      p.workers, p.dpad, row_of, tail_row, head, tail);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t fix_waves = (p.workers + 63) / 64;
-  hipLaunchKernelGGL(k_spmm_fix,
-                     dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
-                     dim3(kBlock), 0, stream, rowptr, mean, d, alpha, bias, relu,
-                     out, ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail);
-  return hipGetLastError();
+  return launch_fix(rowptr, mean, d, alpha, bias, relu, out, ldo, p, tail_row, head,
+                    tail, stream);
 }
 
 bool bgemm_mfma_supported(int32_t N, int32_t K) {

@@ -354,3 +354,40 @@ def test_spmm_q8_matches_oracle(dev, d, K, norm, act):
     torch.cuda.synchronize()
     err = mass_error(out.cpu().numpy(), z, m, relu=act == "relu")
     assert err <= TOL, err
+
+
+# ------------------------------------------------------------ graph replay --
+
+def test_captured_forward_replays_match_eager(dev):
+    """A HIP-graph capture of bigcn_forward replays to the eager result, bit
+    for bit, replay after replay, with eager work in between and the input
+    refilled in place."""
+    rng = np.random.default_rng(321)
+    g = _star_plus_random(800, rng)
+    dims = [300, 200, 64, 7]
+    xs = [rng.standard_normal((g.n, dims[0])).astype(np.float32) for _ in range(3)]
+    mu, rstd = workloads.bn_stats(xs[0])
+    wts = [workloads.glorot_t(dims[i], dims[i + 1], rng) for i in range(3)]
+    bs = [rng.uniform(-0.1, 0.1, dims[i + 1]).astype(np.float32) for i in range(3)]
+    model = bg.BiGCN(g.rowptr, g.colidx, wts, bs, norm="sym", mu=mu, rstd=rstd, device=dev)
+    x = _t(xs[0], dev)
+    replay = model.capture(x)
+    for it in range(6):
+        xi = xs[it % 3]
+        x.copy_(_t(xi, dev))
+        got = replay().clone()
+        torch.cuda.synchronize()
+        # eager work between replays: a different layer call and a sync
+        junk = torch.empty((g.n, 8), device=dev)
+        bg.bigcn_spmm_csr(_t(g.rowptr, dev), _t(g.colidx, dev),
+                          torch.ones(g.n, device=dev),
+                          torch.zeros((g.n, 8), dtype=torch.float16, device=dev),
+                          torch.ones(8, device=dev), junk,
+                          torch.empty(bg.spmm_workspace_bytes(g.n, g.nnz, 8),
+                                      dtype=torch.uint8, device=dev))
+        torch.cuda.synchronize()
+        ref_model = bg.BiGCN(g.rowptr, g.colidx, wts, bs, norm="sym", mu=mu, rstd=rstd,
+                             device=dev)
+        ref = ref_model.forward(_t(xi, dev)).clone()
+        torch.cuda.synchronize()
+        assert torch.equal(got, ref), "replay %d differs from eager" % it
