@@ -207,7 +207,7 @@ def main():
     ldc = (max(wt.shape[0] for wt in w.weights_t) + 7) // 8 * 8
     F = torch.empty((g.n, ldF), dtype=torch.int64, device=dev)
     gs = torch.empty(g.n, dtype=torch.float32, device=dev)
-    C = torch.empty((g.n, ldc), dtype=torch.float16, device=dev)
+    C = torch.empty((g.n, max(256, ldc)), dtype=torch.float16, device=dev)
     C8 = torch.empty((g.n, 256), dtype=torch.int8, device=dev)
     ws = torch.empty(max(bg.spmm_workspace_bytes(g.n, g.nnz, wt.shape[0])
                          for wt in w.weights_t), dtype=torch.uint8, device=dev)

@@ -90,40 +90,51 @@ hipError_t run_bgemm(const uint64_t* F, int64_t M, int64_t ldf, const uint64_t* 
   return bigcn::launch_bgemm_popcount(F, M, ldf, B, N, ldb, K, C, ct, ldc, s);
 }
 
-// Workspace layout of bigcn_forward.
+// Workspace layout of bigcn_forward.  Two sets of (scale g, 8-bit codes C8,
+// 16-bit products C16) alternate between layers, so a layer can write the
+// next layer's products while its own are being read.
 struct ForwardLayout {
-  int64_t ldF, ldc, ldh, ldc8;
-  size_t off_F, off_g, off_C, off_C8, off_H0, off_H1, off_spmm, bytes;
+  int64_t ldF, ldh, ldc8, ldc16;
+  size_t off_F, off_g[2], off_C8[2], off_C16[2], off_H0, off_H1, off_spmm, bytes;
   int32_t dmax;
-  bool any_q8;
 };
+
+// Whether layer l's aggregation can produce layer l+1's products in its
+// epilogue, and in which storage (see bigcn::FusedNext).
+int fuse_kind(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t nl, int32_t l) {
+  if (l + 1 >= nl || nnz == 0) return 0;
+  const bigcn_layer& a = layers[l];
+  const bigcn_layer& b = layers[l + 1];
+  if (!bigcn::q8_supported(n, a.d_out, a.d_in)) return 0;  // producer: 8-bit wave kernel
+  if (b.d_in > 256) return 0;
+  if (bigcn::q8_supported(n, b.d_out, b.d_in)) return 1;
+  return b.d_out <= 128 ? 2 : 0;
+}
 
 bool forward_layout(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t nl,
                     ForwardLayout* L) {
   int64_t kwmax = 1, dmax = 1, hmax = 1;
-  size_t esmax = 2;
-  L->any_q8 = false;
   for (int32_t l = 0; l < nl; ++l) {
-    L->any_q8 |= bigcn::q8_supported(n, layers[l].d_out, layers[l].d_in);
     kwmax = std::max<int64_t>(kwmax, words(layers[l].d_in));
     dmax = std::max<int64_t>(dmax, layers[l].d_out);
-    esmax = std::max(esmax, bigcn::itype_size(forward_itype(layers[l].d_in)));
     if (l + 1 < nl) hmax = std::max<int64_t>(hmax, layers[l].d_out);
   }
   L->ldF = (kwmax + 1) / 2 * 2;
-  L->ldc = (dmax + 7) / 8 * 8;
   L->ldh = (hmax + 3) / 4 * 4;
+  L->ldc8 = 256;
+  L->ldc16 = std::max<int64_t>(256, (dmax + 7) / 8 * 8);
   L->dmax = (int32_t)dmax;
   size_t off = 0;
   L->off_F = off;
   off += up256((size_t)n * L->ldF * 8);
-  L->off_g = off;
-  off += up256((size_t)n * 4);
-  L->off_C = off;
-  off += up256((size_t)n * L->ldc * esmax);
-  L->ldc8 = 256;
-  L->off_C8 = off;
-  if (L->any_q8) off += up256((size_t)n * L->ldc8);
+  for (int s = 0; s < 2; ++s) {
+    L->off_g[s] = off;
+    off += up256((size_t)n * 4);
+    L->off_C8[s] = off;
+    off += up256((size_t)n * L->ldc8);
+    L->off_C16[s] = off;
+    off += up256((size_t)n * L->ldc16 * 2);
+  }
   L->off_H0 = off;
   if (nl >= 2) off += up256((size_t)n * L->ldh * 4);
   L->off_H1 = off;
@@ -210,7 +221,7 @@ bigcn_status bigcn_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
                             int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
                             float* g, void* stream) {
   if (M < 0 || N < 1 || K < 1 || ldf < words(K) || ldb < words(K)) return BIGCN_EINVAL;
-  if (ldc8 < 256 || ldc8 % 4 != 0 || ldc16 < N || ldc16 % 4 != 0) return BIGCN_EINVAL;
+  if (ldc8 < 256 || ldc8 % 4 != 0 || ldc16 < 256 || ldc16 % 4 != 0) return BIGCN_EINVAL;
   if (B == nullptr || (M > 0 && (F == nullptr || C8 == nullptr || C16 == nullptr ||
                                  g == nullptr)))
     return BIGCN_EINVAL;
@@ -233,7 +244,7 @@ bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                                void* workspace, size_t ws_bytes, void* stream) {
   bigcn_status st = check_graph(n, nnz, rowptr, colidx, norm);
   if (st != BIGCN_OK) return st;
-  if (K < 1 || ldc8 < 256 || ldc8 % 4 != 0) return BIGCN_EINVAL;
+  if (K < 1 || ldc8 < 256 || ldc8 % 4 != 0 || ldc16 < 256) return BIGCN_EINVAL;
   st = check_spmm_operands(n, g, C16, BIGCN_F16, d, ldc16, alpha, bias, act, out, ldo);
   if (st != BIGCN_OK) return st;
   if (n > 0 && C8 == nullptr) return BIGCN_EINVAL;
@@ -252,7 +263,7 @@ bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
   return hip_status(bigcn::launch_spmm_q8(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN,
                                           g, C8, ldc8, C16, ldc16, K, d, alpha, bias,
                                           act == BIGCN_ACT_RELU, out, ldo, plan,
-                                          workspace, s));
+                                          workspace, nullptr, s));
 }
 
 size_t bigcn_forward_workspace_bytes(int64_t n, int64_t nnz,
@@ -298,8 +309,6 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
   uint64_t* F = (uint64_t*)(ws + L.off_F);
-  float* g = (float*)(ws + L.off_g);
-  void* C = ws + L.off_C;
   float* H[2] = {(float*)(ws + L.off_H0), (float*)(ws + L.off_H1)};
   void* wsp = ws + L.off_spmm;
 
@@ -311,34 +320,58 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
 
   const float* hin = x;
   int64_t ldin = ldx;
+  bool have_products = false;  // layer l's products already written by layer l-1
   for (int32_t l = 0; l < n_layers; ++l) {
     const bigcn_layer& ly = layers[l];
     const bool last = l + 1 == n_layers;
-    float* hout = last ? out : H[l & 1];
-    const int64_t ldout = last ? ldo : L.ldh;
+    const int set = l & 1;
+    float* g = (float*)(ws + L.off_g[set]);
+    int8_t* C8 = (int8_t*)(ws + L.off_C8[set]);
+    void* C16 = ws + L.off_C16[set];
+    const bool q8 = bigcn::q8_supported(n, ly.d_out, ly.d_in);
     const IType ct = forward_itype(ly.d_in);
-    e = bigcn::launch_pack(hin, n, ly.d_in, ldin, l == 0 ? mu : nullptr,
-                           l == 0 ? rstd : nullptr, rowptr, norm == BIGCN_NORM_SYM,
-                           F, L.ldF, g, s);
-    if (e != hipSuccess) return BIGCN_EHIP;
+    if (!have_products) {
+      e = bigcn::launch_pack(hin, n, ly.d_in, ldin, l == 0 ? mu : nullptr,
+                             l == 0 ? rstd : nullptr, rowptr, norm == BIGCN_NORM_SYM,
+                             F, L.ldF, g, s);
+      if (e != hipSuccess) return BIGCN_EHIP;
+      if (q8)
+        e = bigcn::launch_bgemm_q8(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C8,
+                                   L.ldc8, C16, L.ldc16, g, s);
+      else
+        e = run_bgemm(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C16, ct, L.ldc16,
+                      BIGCN_BGEMM_AUTO, s);
+      if (e != hipSuccess) return BIGCN_EHIP;
+    }
+    const int kind = fuse_kind(n, nnz, layers, n_layers, l);
+    float* hout = last ? out : (kind != 0 ? nullptr : H[l & 1]);
+    const int64_t ldout = last ? ldo : L.ldh;
     const bigcn::SpmmPlan plan = bigcn::spmm_plan(n, nnz, ly.d_out);
-    if (bigcn::q8_supported(n, ly.d_out, ly.d_in)) {
-      int8_t* C8 = (int8_t*)(ws + L.off_C8);
-      e = bigcn::launch_bgemm_q8(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C8,
-                                 L.ldc8, C, L.ldc, g, s);
-      if (e != hipSuccess) return BIGCN_EHIP;
+    if (q8) {
+      bigcn::FusedNext fn = {};
+      fn.kind = kind;
+      if (kind != 0) {
+        const bigcn_layer& nxt = layers[l + 1];
+        const int nset = (l + 1) & 1;
+        fn.wbits = nxt.wbits;
+        fn.ldw = nxt.ldw;
+        fn.d_out = nxt.d_out;
+        fn.C8 = (int8_t*)(ws + L.off_C8[nset]);
+        fn.ldc8 = L.ldc8;
+        fn.C16 = ws + L.off_C16[nset];
+        fn.ldc16 = L.ldc16;
+        fn.g = (float*)(ws + L.off_g[nset]);
+      }
       e = bigcn::launch_spmm_q8(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN, g, C8,
-                                L.ldc8, C, L.ldc, ly.d_in, ly.d_out, ly.alpha, ly.bias,
-                                ly.act == BIGCN_ACT_RELU, hout, ldout, plan, wsp, s);
+                                L.ldc8, C16, L.ldc16, ly.d_in, ly.d_out, ly.alpha, ly.bias,
+                                ly.act == BIGCN_ACT_RELU, hout, ldout, plan, wsp, &fn, s);
     } else {
-      e = run_bgemm(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C, ct, L.ldc,
-                    BIGCN_BGEMM_AUTO, s);
-      if (e != hipSuccess) return BIGCN_EHIP;
-      e = bigcn::launch_spmm(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN, g, C, ct,
-                             ly.d_out, L.ldc, ly.alpha, ly.bias, ly.act == BIGCN_ACT_RELU,
+      e = bigcn::launch_spmm(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN, g, C16, ct,
+                             ly.d_out, L.ldc16, ly.alpha, ly.bias, ly.act == BIGCN_ACT_RELU,
                              hout, ldout, plan, wsp, s);
     }
     if (e != hipSuccess) return BIGCN_EHIP;
+    have_products = kind != 0;
     hin = hout;
     ldin = ldout;
   }

@@ -35,13 +35,33 @@ hipError_t launch_bgemm_mfma(const uint64_t* F, int64_t M, int64_t ldf,
                              hipStream_t stream);
 
 // Exact 8-bit half-code storage of the products (layers of 129..256 output
-// columns with K <= 2048): codes (dot - K%2)/2 in C8, rows with |dot| > 255
-// written exactly (half) to C16 and flagged by the sign bit of g.
+// columns with K <= 2048): codes (dot - K%2)/2 in C8 rows of 256 bytes in
+// lane-interleaved order (column k at byte 4*(k%64) + k/64); rows with
+// |dot| > 255 written exactly (half, same order, 256 per row) to C16 and
+// flagged by the sign bit of g.
 bool q8_supported(int64_t n, int32_t N, int32_t K);
 hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
                            const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
                            int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
                            float* g, hipStream_t stream);
+
+// A next layer fused into the 8-bit aggregation's epilogue: the finished
+// output rows are binarised and multiplied with the next weights in place.
+//   kind 0: none (the output rows are written);
+//   kind 1: next products as 8-bit half-codes (C8, C16 fallback, flags in g);
+//   kind 2: next products exact in half, natural column order (C16, ldc16).
+// g receives the next layer's per-node scale.
+struct FusedNext {
+  int kind;
+  const uint64_t* wbits;  // next layer's packed W^T [d_out][ldw]
+  int64_t ldw;
+  int32_t d_out;
+  int8_t* C8;
+  int64_t ldc8;
+  void* C16;
+  int64_t ldc16;
+  float* g;
+};
 
 // Aggregation over the CSR of Â with the fused rescale / bias / activation
 // epilogue.  The edge range [0, nnz) is cut into fixed chunks of `chunk`
@@ -67,12 +87,15 @@ hipError_t launch_spmm(int64_t n, int64_t nnz, const int64_t* rowptr,
                        float* out, int64_t ldo, const SpmmPlan& plan,
                        void* workspace, hipStream_t stream);
 
-// Aggregation reading 8-bit half-codes (see launch_bgemm_q8).
+// Aggregation reading 8-bit half-codes (see launch_bgemm_q8); with a
+// FusedNext of kind > 0 the output rows feed the next layer instead of (or,
+// if out != nullptr, besides) being written.
 hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                           const int32_t* colidx, int mean, const float* g,
                           const int8_t* C8, int64_t ldc8, const void* C16,
                           int64_t ldc16, int32_t K, int32_t d, const float* alpha,
                           const float* bias, int relu, float* out, int64_t ldo,
-                          const SpmmPlan& plan, void* workspace, hipStream_t stream);
+                          const SpmmPlan& plan, void* workspace,
+                          const FusedNext* next, hipStream_t stream);
 
 }  // namespace bigcn

@@ -219,17 +219,18 @@ __device__ inline void store_row(T* __restrict__ dst, const int* v, int ncols,
     if (c < ncols) dst[c] = from_int<T>(v[c]);
 }
 
-// Stages the packed weight rows j0 .. j0 + 64*CN - 1 into LDS as
-// [kw][CN][64] (word w of column j0 + CN*l + c at (w*CN + c)*64 + l), so that
-// for a fixed (w, c) the 64 lanes read 64 consecutive words.
-template <int CN>
+// Stages packed weight rows into LDS as [kw][CN][64]: entry (w*CN + c)*64 + l
+// holds word w of the column lane l owns in slot c, so that for a fixed
+// (w, c) the 64 lanes read 64 consecutive words.  Lane l owns columns
+// j0 + CN*l + c (consecutive) or, with IL, l + 64*c (lane-interleaved).
+template <int CN, bool IL = false>
 __device__ inline void stage_weights(uint64_t* sB, const uint64_t* __restrict__ B,
                                      int32_t N, int64_t ldb, int kw, int j0) {
   for (int idx = threadIdx.x; idx < kw * CN * 64; idx += kBlock) {
     const int l = idx & 63;
     const int c = (idx >> 6) % CN;
     const int w = idx / (64 * CN);
-    const int j = j0 + l * CN + c;
+    const int j = IL ? l + 64 * c : j0 + l * CN + c;
     sB[idx] = j < N ? B[(int64_t)j * ldb + w] : 0ull;
   }
   __syncthreads();
@@ -300,59 +301,51 @@ __global__ __launch_bounds__(kBlock) void k_bgemm_pop(
 
 // The same product stored as exact 8-bit half-codes for the forward pass:
 //   code = (dot - p) / 2,  p = K mod 2   (dot = K - 2 popcount is = p mod 2),
-// which holds every |dot| <= 255.  A row with a larger value anywhere is
-// written in full, exactly, to C16 (half for K <= 2048, else int16) and is
-// flagged by setting the sign bit of its scale g[i] (g >= 0 otherwise).  One
-// wave covers all N columns (N <= 64*CN), so the flag is decided per row
-// with a ballot.
-template <int CN, int RM, typename T16>
+// which holds every |dot| <= 255.  Rows are 256 bytes in lane-interleaved
+// order: column k sits at byte 4*(k % 64) + k / 64, so that lane l finds its
+// columns l, l+64, l+128, l+192 in one 32-bit word.  A row with a larger
+// |dot| anywhere is written in full, exactly, to C16 (IEEE half, the same
+// interleaved order, 256 halves per row) and flagged by setting the sign bit
+// of its scale g[i] (g >= 0 otherwise).  One wave covers all N <= 256
+// columns, so the flag is decided per row with a ballot.
+template <int RM>
 __global__ __launch_bounds__(kBlock) void k_bgemm_pop_q8(
     const uint64_t* __restrict__ F, int64_t M, int64_t ldf,
     const uint64_t* __restrict__ B, int32_t N, int64_t ldb, int32_t K,
-    int8_t* __restrict__ C8, int64_t ldc8, T16* __restrict__ C16, int64_t ldc16,
-    float* __restrict__ g) {
+    int8_t* __restrict__ C8, int64_t ldc8, _Float16* __restrict__ C16,
+    int64_t ldc16, float* __restrict__ g) {
   extern __shared__ uint64_t sB[];
   const int lane = threadIdx.x & 63;
   const int kw = (K + 63) >> 6;
-  stage_weights<CN>(sB, B, N, ldb, kw, 0);
+  stage_weights<4, true>(sB, B, N, ldb, kw, 0);
   const int64_t tiles = (M + RM - 1) / RM;
   const int64_t nwaves = (int64_t)gridDim.x * kWavesPerBlock;
-  const int jl = lane * CN;
-  const int ncols = N - jl;
   const int par = K & 1;
   for (int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
        t < tiles; t += nwaves) {
     const int64_t i0 = t * RM;
-    uint32_t acc[RM][CN];
-    tile_popcounts<CN, RM>(F, M, ldf, sB, kw, i0, lane, acc);
+    uint32_t acc[RM][4];
+    tile_popcounts<4, RM>(F, M, ldf, sB, kw, i0, lane, acc);
 #pragma unroll
     for (int r = 0; r < RM; ++r) {
       if (i0 + r >= M) break;  // wave-uniform
       const int64_t i = i0 + r;
-      int v[CN];
+      int v[4];
       bool big = false;
+      uint32_t packed = 0;
 #pragma unroll
-      for (int c = 0; c < CN; ++c) {
+      for (int c = 0; c < 4; ++c) {
         v[c] = K - 2 * (int)acc[r][c];
         const int code = (v[c] - par) >> 1;
-        big |= (c < ncols) && (code < -128 || code > 127);
+        big |= (lane + 64 * c < N) && (code < -128 || code > 127);
+        packed |= (uint32_t)(uint8_t)(int8_t)code << (8 * c);
       }
-      if (ncols > 0) {
-        int8_t* dst = C8 + i * ldc8 + jl;
-        if (CN == 4 && ncols >= 4) {
-          uint32_t packed = 0;
-#pragma unroll
-          for (int c = 0; c < CN; ++c)
-            packed |= (uint32_t)(uint8_t)(int8_t)((v[c] - par) >> 1) << (8 * c);
-          *reinterpret_cast<uint32_t*>(dst) = packed;
-        } else {
-#pragma unroll
-          for (int c = 0; c < CN; ++c)
-            if (c < ncols) dst[c] = (int8_t)((v[c] - par) >> 1);
-        }
-      }
+      *reinterpret_cast<uint32_t*>(C8 + i * ldc8 + 4 * lane) = packed;
       if (__builtin_amdgcn_ballot_w64(big) != 0) {
-        if (ncols > 0) store_row<T16, CN>(C16 + i * ldc16 + jl, v, ncols, false);
+        half4_t h;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) h[c] = (_Float16)v[c];
+        *reinterpret_cast<half4_t*>(C16 + i * ldc16 + 4 * lane) = h;
         if (lane == 0) g[i] = -fabsf(g[i]);
       }
     }
@@ -755,43 +748,167 @@ __device__ inline void fma4f(float4_t& acc, float g, const float4_t& v) {
   acc[3] = fmaf(v[3], g, acc[3]);
 }
 
+// What the aggregation does with a finished output row in the 8-bit path.
+// Lane l holds columns l + 64c of the row (c = 0..3, interleaved).
+//   NX == 0: write act(rowfac*alpha*acc + b) to out (columns l + 64c).
+//   NX == 1: the next layer (K' = d inputs, 128 < d' <= 256 outputs) is fused:
+//            its sign bits are the four ballots of the output values (word c
+//            = ballot of slot c, because lane l holds element l + 64c), its
+//            scale is their mean magnitude (summed per lane over c, then a
+//            butterfly: the order of the pack kernel), and its products
+//            against the next weights (in LDS) are written as 8-bit
+//            half-codes with the exact fallback, as k_bgemm_pop_q8 does.
+//   NX == 2: as 1, but the next layer has d' <= 128 outputs; its products are
+//            written exactly (half, natural column order) for the narrow
+//            aggregation kernel.
+// With NX > 0 the output row is also written to out if out != nullptr.
+struct NextLayer {
+  const uint64_t* sB;  // LDS: next weights, [kw'][4][64] interleaved columns
+  int32_t dn;          // next layer's output width d'
+  int8_t* C8;          // NX == 1: codes [n][ldc8]
+  int64_t ldc8;
+  _Float16* C16;       // NX == 1: exact fallback rows; NX == 2: products
+  int64_t ldc16;
+  float* g;            // next layer's per-node scale
+  int sym;             // fold D̂^-1/2 into the next scale
+};
+
+struct EpiIL {
+  float alpha[4], bias[4];
+  bool valid[4];       // column lane + 64c < d
+  int relu;
+  int32_t d;
+};
+
+template <int NX>
+__device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4_t acc,
+                                  const EpiIL& ep, float* __restrict__ out, int64_t ldo,
+                                  const NextLayer& nx, int lane) {
+  const float rowfac = deg > 0 ? row_factor_deg(deg, mean) : 0.f;
+  float v[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const float t = deg > 0 ? fmaf(acc[c], rowfac * ep.alpha[c], ep.bias[c]) : ep.bias[c];
+    v[c] = act(t, ep.relu);
+  }
+  if (NX == 0 || out != nullptr) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (ep.valid[c]) out[r * ldo + lane + 64 * c] = v[c];
+  }
+  if (NX == 0) return;
+  // Next layer: signs (one ballot per 64 elements = one packed word) and
+  // mean magnitude, exactly as the pack kernel forms them.
+  uint64_t word[4];
+  float l1 = 0.f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    word[c] = __builtin_amdgcn_ballot_w64(ep.valid[c] && v[c] >= 0.f);
+    l1 += ep.valid[c] ? fabsf(v[c]) : 0.f;
+  }
+  l1 = wave_sum(l1);
+  float sc = l1 / (float)ep.d;
+  if (nx.sym) sc = sc * (deg > 0 ? 1.0f / sqrtf((float)deg) : 0.f);
+  const int kwn = (ep.d + 63) >> 6;
+  const int Kn = ep.d;
+  if (NX == 1) {
+    const int par = Kn & 1;
+    bool big = false;
+    uint32_t packed = 0;
+    int dot[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      uint32_t pc = 0;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        if (w >= kwn) break;
+        const uint64_t z = word[w] ^ nx.sB[(w * 4 + c) * 64 + lane];
+        pc += __builtin_popcount((uint32_t)z);
+        pc += __builtin_popcount((uint32_t)(z >> 32));
+      }
+      dot[c] = Kn - 2 * (int)pc;
+      const int code = (dot[c] - par) >> 1;
+      big |= (lane + 64 * c < nx.dn) && (code < -128 || code > 127);
+      packed |= (uint32_t)(uint8_t)(int8_t)code << (8 * c);
+    }
+    *reinterpret_cast<uint32_t*>(nx.C8 + r * nx.ldc8 + 4 * lane) = packed;
+    const bool flag = __builtin_amdgcn_ballot_w64(big) != 0;
+    if (flag) {
+      half4_t h;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) h[c] = (_Float16)dot[c];
+      *reinterpret_cast<half4_t*>(nx.C16 + r * nx.ldc16 + 4 * lane) = h;
+    }
+    if (lane == 0) nx.g[r] = flag ? -sc : sc;
+  } else {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int k = lane + 64 * c;
+      if (k >= nx.dn) break;
+      uint32_t pc = 0;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        if (w >= kwn) break;
+        const uint64_t z = word[w] ^ nx.sB[(w * 4 + c) * 64 + lane];
+        pc += __builtin_popcount((uint32_t)z);
+        pc += __builtin_popcount((uint32_t)(z >> 32));
+      }
+      nx.C16[r * nx.ldc16 + k] = (_Float16)(Kn - 2 * (int)pc);
+    }
+    if (lane == 0) nx.g[r] = sc;
+  }
+}
+
+__device__ inline void make_epi_il(EpiIL& ep, int lane, int32_t d,
+                                   const float* __restrict__ alpha,
+                                   const float* __restrict__ bias, int relu) {
+  ep.relu = relu;
+  ep.d = d;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int k = lane + 64 * c;
+    ep.valid[c] = k < d;
+    ep.alpha[c] = k < d ? alpha[k] : 0.f;
+    ep.bias[c] = (k < d && bias != nullptr) ? bias[k] : 0.f;
+  }
+}
+
 // Whole-wave aggregation over 8-bit half-codes (see k_bgemm_pop_q8):
 //   sum_j g_j dot_jk = 2 * sum_j g_j code_jk + p * sum_j g_j.
 // An edge whose source row is flagged (sign bit of g_j) reads that row's
 // exact products from C16 instead and adds g_j (dot - p) / 2 to the same
 // accumulator, so partial sums and the fix-up are the same as for exact
-// storage.  Structure otherwise as k_spmm_wave.
-template <typename T16, int U>
+// storage.  Lane l accumulates columns l + 64c; partial rows are stored in
+// the same interleaved order.  Structure otherwise as k_spmm_wave; finished
+// rows go through finish_row<NX>.
+template <int U, int NX>
 __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
     int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, int mean, const float* __restrict__ g,
-    const int8_t* __restrict__ C8, int64_t ldc8, const T16* __restrict__ C16,
+    const int8_t* __restrict__ C8, int64_t ldc8, const _Float16* __restrict__ C16,
     int64_t ldc16, int par, int32_t d, const float* __restrict__ alpha,
     const float* __restrict__ bias, int relu, float* __restrict__ out,
-    int64_t ldo, int vec_out, int64_t chunk, int64_t workers, int32_t dpad,
+    int64_t ldo, int64_t chunk, int64_t workers, int32_t dpad,
     const int32_t* __restrict__ row_of, int32_t* __restrict__ tail_row,
-    float* __restrict__ head, float* __restrict__ tail) {
+    float* __restrict__ head, float* __restrict__ tail, NextLayer nx,
+    const uint64_t* __restrict__ Bn, int64_t ldbn) {
   static_assert(64 % U == 0, "group size");
+  extern __shared__ uint64_t sBn[];
+  if (NX > 0) {
+    stage_weights<4, true>(sBn, Bn, nx.dn, ldbn, (d + 63) >> 6, 0);
+    nx.sB = sBn;
+  }
   const int lane = threadIdx.x & 63;
   const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
   if (w >= workers) return;
-  const int c0 = lane * 4;  // d <= 256: one block row
-  Epi ep;
-  ep.ncols = d - c0 < 0 ? 0 : (d - c0 > 4 ? 4 : d - c0);
-  ep.relu = relu;
-  ep.vec = vec_out != 0;
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    ep.alpha[c] = c < ep.ncols ? alpha[c0 + c] : 0.f;
-    ep.bias[c] = (c < ep.ncols && bias != nullptr) ? bias[c0 + c] : 0.f;
-  }
-  const bool own_cols = ep.ncols > 0;
+  EpiIL ep;
+  make_epi_il(ep, lane, d, alpha, bias, relu);
   const int rb8 = (int)ldc8;
-  const int rb16 = (int)(ldc16 * (int64_t)sizeof(T16));
+  const int rb16 = (int)(ldc16 * 2);
   const __amdgpu_buffer_rsrc_t rs8 = raw_rsrc(C8, (uint32_t)(n * rb8));
   const __amdgpu_buffer_rsrc_t rs16 = raw_rsrc(C16, (uint32_t)(n * rb16));
-  const int voff8 = c0 + 4 <= ldc8 ? c0 : (int)ldc8 - 4;
-  const int voff16 = (int)((c0 + 4 <= ldc16 ? c0 : ldc16 - 4) * (int64_t)sizeof(T16));
+  const int voff8 = 4 * lane;
+  const int voff16 = 8 * lane;
   const float fpar = (float)par;
 
   const int64_t s = w * chunk;
@@ -801,6 +918,12 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
     const int64_t x = v - s;
     return (int)(x < -1 ? -1 : (x > chunk + 1 ? chunk + 1 : x));
   };
+  auto ld_idx = [&](int eb) -> int32_t {
+    const int x = eb + lane;
+    return colidx[s + (x < nE ? x : nE - 1)];
+  };
+  int32_t jA = ld_idx(0);  // issued before the row lookups
+  int32_t jB = ld_idx(64);
   int64_t r = row_of[w];
   int64_t rbase = r;
   int win = rel(rowptr[rbase + 1 + lane < n ? rbase + 1 + lane : n]);
@@ -809,19 +932,13 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
   bool before = beg0 < s;
   int cur_beg = rel(beg0);
   int cur_end = __builtin_amdgcn_readlane(win, 0);
+  const float4_t zero4 = {0.f, 0.f, 0.f, 0.f};
   if (!before) {
     for (int64_t q = r - 1; q >= 0 && rowptr[q] == s; --q)
-      write_empty(out, ldo, q, c0, ep);
+      finish_row<NX>(q, 0, mean, zero4, ep, out, ldo, nx, lane);
   }
-  float4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
+  float4_t a0 = zero4, a1 = zero4;
   float gsum = 0.f;  // sum of g_j over the current row (for the parity term)
-
-  auto ld_idx = [&](int eb) -> int32_t {
-    const int x = eb + lane;
-    return colidx[s + (x < nE ? x : nE - 1)];
-  };
-  int32_t jA = ld_idx(0);
-  int32_t jB = ld_idx(64);
   float gA = g[jA];
   float gB = g[jB];
   int32_t jCn = ld_idx(128);
@@ -860,15 +977,15 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
         if (eu == cur_end) {
           const float4_t sum = 2.f * (a0 + a1) + fpar * gsum;
           if (before) {
-            if (own_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
-          } else if (own_cols) {
-            write_row(out, ldo, r, c0, ep, sum, row_factor_deg(cur_end - cur_beg, mean));
+            *reinterpret_cast<float4_t*>(head + w * dpad + 4 * lane) = sum;
+          } else {
+            finish_row<NX>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nx, lane);
           }
-          a0 = float4_t{0.f, 0.f, 0.f, 0.f};
-          a1 = float4_t{0.f, 0.f, 0.f, 0.f};
+          a0 = zero4;
+          a1 = zero4;
           gsum = 0.f;
           before = false;
-          do {  // next row; rows without entries are written on the way
+          do {  // next row; rows without entries are finished on the way
             cur_beg = cur_end;
             ++r;
             if (r - rbase == 64) {
@@ -877,7 +994,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
               win_nx = rel(rowptr[rbase + 65 + lane < n ? rbase + 65 + lane : n]);
             }
             cur_end = __builtin_amdgcn_readlane(win, (int)(r - rbase));
-            if (cur_end == eu && own_cols) write_empty(out, ldo, r, c0, ep);
+            if (cur_end == eu) finish_row<NX>(r, 0, mean, zero4, ep, out, ldo, nx, lane);
           } while (cur_end == eu);
         }
         float gj = gg[u];
@@ -886,7 +1003,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
           // Flagged source row: its exact products, as (dot - p) / 2.
           gj = fabsf(gj);
           const int j = __builtin_amdgcn_readlane(jA, m + u);
-          const typename Vec4<T16>::type x = Gather<T16>::load(
+          const half4_t x = Gather<_Float16>::load(
               rs16, voff16, (int)((uint32_t)j * (uint32_t)rb16));
 #pragma unroll
           for (int c = 0; c < 4; ++c) v[c] = ((float)x[c] - fpar) * 0.5f;
@@ -909,19 +1026,61 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
   const float4_t sum = 2.f * (a0 + a1) + fpar * gsum;
   if (cur_end == nE) {
     if (before) {
-      if (own_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
-    } else if (own_cols) {
-      write_row(out, ldo, r, c0, ep, sum, row_factor_deg(cur_end - cur_beg, mean));
+      *reinterpret_cast<float4_t*>(head + w * dpad + 4 * lane) = sum;
+    } else {
+      finish_row<NX>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nx, lane);
     }
-    if (t == nnz && own_cols)
-      for (int64_t q = r + 1; q < n; ++q) write_empty(out, ldo, q, c0, ep);
+    if (t == nnz)
+      for (int64_t q = r + 1; q < n; ++q)
+        finish_row<NX>(q, 0, mean, zero4, ep, out, ldo, nx, lane);
     if (lane == 0) tail_row[w] = -1;
   } else if (before) {
-    if (own_cols) *reinterpret_cast<float4_t*>(head + w * dpad + c0) = sum;
+    *reinterpret_cast<float4_t*>(head + w * dpad + 4 * lane) = sum;
     if (lane == 0) tail_row[w] = -1;
   } else {
-    if (own_cols) *reinterpret_cast<float4_t*>(tail + w * dpad + c0) = sum;
+    *reinterpret_cast<float4_t*>(tail + w * dpad + 4 * lane) = sum;
     if (lane == 0) tail_row[w] = (int32_t)r;
+  }
+}
+
+// Fix-up of the 8-bit path: rows cut by chunk boundaries, partial rows in
+// interleaved order, finished with the same finish_row<NX>.  One wave scans
+// four workers and finishes their cut rows in turn.
+template <int NX>
+__global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
+    const int64_t* __restrict__ rowptr, int mean, int32_t d,
+    const float* __restrict__ alpha, const float* __restrict__ bias, int relu,
+    float* __restrict__ out, int64_t ldo, int64_t chunk, int64_t workers,
+    int32_t dpad, const int32_t* __restrict__ tail_row,
+    const float* __restrict__ head, const float* __restrict__ tail, NextLayer nx,
+    const uint64_t* __restrict__ Bn, int64_t ldbn) {
+  extern __shared__ uint64_t sBn[];
+  if (NX > 0) {
+    stage_weights<4, true>(sBn, Bn, nx.dn, ldbn, (d + 63) >> 6, 0);
+    nx.sB = sBn;
+  }
+  const int lane = threadIdx.x & 63;
+  const int64_t w0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * 4;
+  EpiIL ep;
+  make_epi_il(ep, lane, d, alpha, bias, relu);
+  for (int q = 0; q < 4; ++q) {
+    const int64_t w = w0 + q;
+    if (w >= workers) break;
+    const int32_t r = tail_row[w];
+    if (r < 0) continue;
+    const int64_t wend = (rowptr[r + 1] - 1) / chunk;
+    float4_t acc = *reinterpret_cast<const float4_t*>(tail + w * dpad + 4 * lane);
+    int64_t v = w + 1;
+    for (; v + 8 <= wend + 1; v += 8) {  // eight loads in flight, added in order
+      float4_t h[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        h[u] = *reinterpret_cast<const float4_t*>(head + (v + u) * dpad + 4 * lane);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc += h[u];
+    }
+    for (; v <= wend; ++v) acc += *reinterpret_cast<const float4_t*>(head + v * dpad + 4 * lane);
+    finish_row<NX>(r, rowptr[r + 1] - rowptr[r], mean, acc, ep, out, ldo, nx, lane);
   }
 }
 
@@ -1276,13 +1435,50 @@ hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
                            float* g, hipStream_t stream) {
   if (M == 0) return hipSuccess;
   constexpr int RM = 4;
-  constexpr int CN = 4;
   const int kw = (K + 63) >> 6;
-  const size_t lds = (size_t)kw * CN * 64 * sizeof(uint64_t);
+  const size_t lds = (size_t)kw * 4 * 64 * sizeof(uint64_t);
   const int64_t tiles = (M + RM - 1) / RM;
   dim3 grid(grid_cap((tiles + kWavesPerBlock - 1) / kWavesPerBlock, 4096));
-  hipLaunchKernelGGL((k_bgemm_pop_q8<CN, RM, _Float16>), grid, dim3(kBlock), lds,
-                     stream, F, M, ldf, B, N, ldb, K, C8, ldc8, (_Float16*)C16, ldc16, g);
+  hipLaunchKernelGGL((k_bgemm_pop_q8<RM>), grid, dim3(kBlock), lds, stream, F, M, ldf,
+                     B, N, ldb, K, C8, ldc8, (_Float16*)C16, ldc16, g);
+  return hipGetLastError();
+}
+
+template <int NX>
+hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
+                      const int32_t* colidx, int mean, const float* g,
+                      const int8_t* C8, int64_t ldc8, const void* C16, int64_t ldc16,
+                      int32_t K, int32_t d, const float* alpha, const float* bias,
+                      int relu, float* out, int64_t ldo, const SpmmPlan& p, void* ws,
+                      const FusedNext& fn, hipStream_t stream) {
+  char* base = (char*)ws;
+  const int32_t* row_of = (const int32_t*)(base + p.off_rowof);
+  int32_t* tail_row = (int32_t*)(base + p.off_tailrow);
+  float* head = (float*)(base + p.off_head);
+  float* tail = (float*)(base + p.off_tail);
+  NextLayer nx;
+  nx.sB = nullptr;
+  nx.dn = fn.d_out;
+  nx.C8 = fn.C8;
+  nx.ldc8 = fn.ldc8;
+  nx.C16 = (_Float16*)fn.C16;
+  nx.ldc16 = fn.ldc16;
+  nx.g = fn.g;
+  nx.sym = !mean;
+  const size_t lds = NX > 0 ? (size_t)((d + 63) >> 6) * 4 * 64 * sizeof(uint64_t) : 0;
+  dim3 grid((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock));
+  hipLaunchKernelGGL((k_spmm_wave_q8<8, NX>), grid, dim3(kBlock), lds, stream, n, nnz,
+                     rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16, ldc16,
+                     K & 1, d, alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,
+                     row_of, tail_row, head, tail, nx, fn.wbits, fn.ldw);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t fix_waves = (p.workers + 3) / 4;
+  hipLaunchKernelGGL((k_spmm_fix_q8<NX>),
+                     dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
+                     dim3(kBlock), lds, stream, rowptr, mean, d, alpha, bias, relu, out,
+                     ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail, nx, fn.wbits,
+                     fn.ldw);
   return hipGetLastError();
 }
 
@@ -1291,29 +1487,28 @@ hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                           const int8_t* C8, int64_t ldc8, const void* C16,
                           int64_t ldc16, int32_t K, int32_t d, const float* alpha,
                           const float* bias, int relu, float* out, int64_t ldo,
-                          const SpmmPlan& p, void* ws, hipStream_t stream) {
+                          const SpmmPlan& p, void* ws, const FusedNext* next,
+                          hipStream_t stream) {
   if (n == 0) return hipSuccess;
-  if (nnz == 0) {
+  FusedNext none = {};
+  const FusedNext& fn = next != nullptr ? *next : none;
+  if (nnz == 0 && fn.kind == 0) {
     const int64_t total = n * (int64_t)d;
     hipLaunchKernelGGL(k_spmm_empty, dim3((unsigned)((total + kBlock - 1) / kBlock)),
                        dim3(kBlock), 0, stream, n, d, bias, relu, out, ldo);
     return hipGetLastError();
   }
-  char* base = (char*)ws;
-  const int32_t* row_of = (const int32_t*)(base + p.off_rowof);
-  int32_t* tail_row = (int32_t*)(base + p.off_tailrow);
-  float* head = (float*)(base + p.off_head);
-  float* tail = (float*)(base + p.off_tail);
-  const int vec_out = (ldo % 4 == 0) && ((uintptr_t)out % 16 == 0);
-  dim3 grid((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock));
-  hipLaunchKernelGGL((k_spmm_wave_q8<_Float16, 8>), grid, dim3(kBlock), 0, stream,
-                     n, nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16,
-                     ldc16, K & 1, d, alpha, bias, relu, out, ldo, vec_out, p.chunk,
-                     p.workers, p.dpad, row_of, tail_row, head, tail);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return launch_fix(rowptr, mean, d, alpha, bias, relu, out, ldo, p, tail_row, head,
-                    tail, stream);
+  switch (fn.kind) {
+    case 1:
+      return spmm_q8_nx<1>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
+                           alpha, bias, relu, out, ldo, p, ws, fn, stream);
+    case 2:
+      return spmm_q8_nx<2>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
+                           alpha, bias, relu, out, ldo, p, ws, fn, stream);
+    default:
+      return spmm_q8_nx<0>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
+                           alpha, bias, relu, out, ldo, p, ws, fn, stream);
+  }
 }
 
 bool bgemm_mfma_supported(int32_t N, int32_t K) {

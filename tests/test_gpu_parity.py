@@ -232,7 +232,7 @@ def gpu_layer(dev, g, norm, h, wt, bias, act="none", mu=None, rstd=None,
     gs = torch.empty(n, dtype=torch.float32, device=dev)
     bg.bigcn_binarize_pack(ht, F, gs, None if mu is None else _t(mu, dev),
                            None if rstd is None else _t(rstd, dev), rowptr_t, norm)
-    ldc = (d + 7) // 8 * 8
+    ldc = max(256, (d + 7) // 8 * 8)
     C = torch.empty((n, ldc), dtype=torch.float16 if K <= 2048 else torch.int16, device=dev)
     out = torch.empty((n, d), dtype=torch.float32, device=dev)
     ws = torch.empty(bg.spmm_workspace_bytes(n, g.nnz, d), dtype=torch.uint8, device=dev)
@@ -248,16 +248,24 @@ def gpu_layer(dev, g, norm, h, wt, bias, act="none", mu=None, rstd=None,
     return out, F, C[:, :d], alpha
 
 
+def il_pos(d):
+    """Position of column k in a lane-interleaved 256-wide row."""
+    k = np.arange(d)
+    return 4 * (k % 64) + k // 64
+
+
 def decode_products(prod, K, d):
     """Integer products from either storage: an exact tensor, or the 8-bit
-    half-codes with their flagged exact rows (sign bit of g)."""
+    half-codes (lane-interleaved rows) with their flagged exact rows (sign
+    bit of g)."""
     if isinstance(prod, torch.Tensor):
         return prod.cpu().numpy().astype(np.int64)
     C8, C16, gs = prod
-    codes = C8[:, :d].cpu().numpy().astype(np.int64)
+    pos = il_pos(d)
+    codes = C8.cpu().numpy()[:, pos].astype(np.int64)
     dot = 2 * codes + (K & 1)
     flagged = np.signbit(gs.cpu().numpy())
-    dot[flagged] = C16[:, :d].cpu().numpy()[flagged].astype(np.int64)
+    dot[flagged] = C16.cpu().numpy()[flagged][:, pos].astype(np.int64)
     return dot
 
 
@@ -307,7 +315,7 @@ def test_bgemm_q8_matches_oracle(dev, M, N, K):
     gsc[::5] = 0.0
     Ft, Bt = _t(F.view(np.int64), dev), _t(B.view(np.int64), dev)
     C8 = torch.full((M, 256 + 4), 99, dtype=torch.int8, device=dev)
-    C16 = torch.zeros((M, (N + 7) // 8 * 8), dtype=torch.float16, device=dev)
+    C16 = torch.zeros((M, 256), dtype=torch.float16, device=dev)
     gt = _t(gsc, dev)
     bg.bigcn_bgemm_q8(Ft, Bt, K, C8, C16, gt)
     torch.cuda.synchronize()
@@ -342,11 +350,13 @@ def test_spmm_q8_matches_oracle(dev, d, K, norm, act):
     flag = (np.abs(dot) > 255).any(axis=1)
     gg[flag] = -np.abs(gg[flag])               # sign bit marks the exact rows
     codes = np.clip((dot - par) // 2, -128, 127).astype(np.int8)
-    C8 = torch.zeros((g.n, 256), dtype=torch.int8, device=dev)
-    C8[:, :d] = _t(codes, dev)
-    ldc16 = (d + 7) // 8 * 8
-    C16 = torch.zeros((g.n, ldc16), dtype=torch.float16, device=dev)
-    C16[:, :d] = _t(np.where(flag[:, None], dot, 0).astype(np.float16), dev)
+    pos = il_pos(d)
+    c8 = np.zeros((g.n, 256), dtype=np.int8)
+    c8[:, pos] = codes
+    C8 = _t(c8, dev)
+    c16 = np.zeros((g.n, 256), dtype=np.float16)
+    c16[:, pos] = np.where(flag[:, None], dot, 0).astype(np.float16)
+    C16 = _t(c16, dev)
     out = torch.full((g.n, d), float("nan"), dtype=torch.float32, device=dev)
     ws = torch.empty(bg.spmm_workspace_bytes(g.n, g.nnz, d), dtype=torch.uint8, device=dev)
     bg.bigcn_spmm_csr_q8(_t(g.rowptr, dev), _t(g.colidx, dev), _t(gg, dev), C8, C16, K,
