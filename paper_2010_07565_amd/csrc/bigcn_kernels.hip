@@ -352,6 +352,113 @@ __global__ __launch_bounds__(kBlock) void k_bgemm_pop_q8(
   }
 }
 
+// ------------------------------------------------------------ bgemm (MFMA) --
+//
+// The same product on the matrix cores.  With a, b in {0,1} the sign bits
+// (pad bits are 0) and s = 2a - 1, for k < K:
+//     sum s_a s_b = 4 sum a b - 2 sum a - 2 sum b + K,
+// so the signs are expanded to {0,1} bytes and v_mfma_i32_16x16x64_i8 forms
+// sum a b exactly over one 64-bit word per instruction.  Operand layout
+// (gfx950): lane l of A holds row l % 16, bytes 16*(l/16) .. +15 of the word;
+// lane l of B holds column l % 16 with the same bytes; lane L, register R of
+// the result holds row 4*(L/16) + R, column L % 16.
+// A block stages up to KC words of the weights, already expanded, in LDS in
+// B-operand order ([word][column tile][lane] x 16 bytes, so each operand
+// load is one conflict-free 16-byte read); each wave owns two 16-row tiles
+// that share every weight operand.  N <= 256; at most 32 KB of LDS.
+
+typedef int int4v_t __attribute__((ext_vector_type(4)));
+
+// 16 sign bits -> 16 bytes of {0,1} (bit q of each nibble to byte q).
+__device__ inline int4v_t expand16(uint32_t bits) {
+  int4v_t r;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t nib = (bits >> (4 * q)) & 0xFu;
+    r[q] = (int)((nib * 0x00204081u) & 0x01010101u);
+  }
+  return r;
+}
+
+template <int NT, typename T>
+__global__ __launch_bounds__(kBlock) void k_bgemm_mfma(
+    const uint64_t* __restrict__ F, int64_t M, int64_t ldf,
+    const uint64_t* __restrict__ B, int32_t N, int64_t ldb, int32_t K,
+    T* __restrict__ C, int64_t ldc) {
+  constexpr int KC = NT >= 16 ? 2 : 4;  // words staged per pass (<= 32 KB)
+  extern __shared__ int4v_t sW[];                       // [KC][NT][64]
+  __shared__ int sPb[256];                              // sum b per column
+  const int lane = threadIdx.x & 63;
+  const int wv = wave_index_in_block();
+  const int kw = (K + 63) >> 6;
+  for (int j = threadIdx.x; j < 256; j += kBlock) {
+    int pc = 0;
+    if (j < N)
+      for (int w = 0; w < kw; ++w) pc += __builtin_popcountll(B[(int64_t)j * ldb + w]);
+    sPb[j] = pc;
+  }
+  const int m = lane & 15, grp = lane >> 4;
+  const int64_t rows_per_block = kWavesPerBlock * 32;
+  for (int64_t base = (int64_t)blockIdx.x * rows_per_block; base < M;
+       base += (int64_t)gridDim.x * rows_per_block) {
+    const int64_t r0 = base + wv * 32;  // this wave: rows r0 .. r0+31
+    int4v_t acc[2][NT];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int jt = 0; jt < NT; ++jt) acc[t][jt] = int4v_t{0, 0, 0, 0};
+    int pa[2] = {0, 0};
+    for (int w0 = 0; w0 < kw; w0 += KC) {
+      const int kc = kw - w0 < KC ? kw - w0 : KC;
+      __syncthreads();  // previous chunk fully consumed
+      for (int idx = threadIdx.x; idx < kc * NT * 64; idx += kBlock) {
+        const int l = idx & 63;
+        const int jt = (idx >> 6) % NT;
+        const int w = idx / (64 * NT);
+        const int col = jt * 16 + (l & 15);
+        const uint64_t word = col < N ? B[(int64_t)col * ldb + w0 + w] : 0ull;
+        sW[(w * NT + jt) * 64 + l] = expand16((uint32_t)(word >> (16 * (l >> 4))) & 0xFFFFu);
+      }
+      __syncthreads();
+      for (int w = 0; w < kc; ++w) {
+        int4v_t a[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const int64_t row = r0 + t * 16 + m;
+          const uint64_t f = row < M ? F[row * ldf + w0 + w] : 0ull;
+          pa[t] += __builtin_popcountll(f);
+          a[t] = expand16((uint32_t)(f >> (16 * grp)) & 0xFFFFu);
+        }
+#pragma unroll
+        for (int jt = 0; jt < NT; ++jt) {
+          const int4v_t b = sW[(w * NT + jt) * 64 + lane];
+          acc[0][jt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[0], b, acc[0][jt], 0, 0, 0);
+          acc[1][jt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[1], b, acc[1][jt], 0, 0, 0);
+        }
+      }
+    }
+    // Each lane counted 4x the bits of its row (one per lane group); every
+    // lane of a row's group sees the whole word, so pa is per row already.
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+      for (int R = 0; R < 4; ++R) {
+        const int mr = 4 * grp + R;                     // output row in the tile
+        const int pa_r = __shfl(pa[t], mr, 64);          // lanes 0..15 hold rows 0..15
+        const int64_t row = r0 + t * 16 + mr;
+#pragma unroll
+        for (int jt = 0; jt < NT; ++jt) {
+          const int col = jt * 16 + m;
+          if (row < M && col < N) {
+            const int dot = K - 2 * (pa_r + sPb[col]) + 4 * acc[t][jt][R];
+            C[row * ldc + col] = (T)dot;
+          }
+        }
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ spmm ----
 
 template <typename T>
@@ -1511,16 +1618,46 @@ hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
   }
 }
 
-bool bgemm_mfma_supported(int32_t N, int32_t K) {
-  (void)N;
-  (void)K;
-  return false;
+bool bgemm_mfma_supported(int32_t N, int32_t K) { return N >= 1 && N <= 256 && K >= 1; }
+
+template <int NT>
+static void launch_mfma_nt(dim3 grid, size_t lds, hipStream_t stream, const uint64_t* F,
+                           int64_t M, int64_t ldf, const uint64_t* B, int32_t N,
+                           int64_t ldb, int32_t K, void* C, IType ct, int64_t ldc) {
+  switch (ct) {
+    case IType::F16:
+      hipLaunchKernelGGL((k_bgemm_mfma<NT, _Float16>), grid, dim3(kBlock), lds, stream, F,
+                         M, ldf, B, N, ldb, K, (_Float16*)C, ldc);
+      break;
+    case IType::I16:
+      hipLaunchKernelGGL((k_bgemm_mfma<NT, int16_t>), grid, dim3(kBlock), lds, stream, F,
+                         M, ldf, B, N, ldb, K, (int16_t*)C, ldc);
+      break;
+    default:
+      hipLaunchKernelGGL((k_bgemm_mfma<NT, int32_t>), grid, dim3(kBlock), lds, stream, F,
+                         M, ldf, B, N, ldb, K, (int32_t*)C, ldc);
+      break;
+  }
 }
 
-hipError_t launch_bgemm_mfma(const uint64_t*, int64_t, int64_t, const uint64_t*,
-                             int32_t, int64_t, int32_t, void*, IType, int64_t,
-                             hipStream_t) {
-  return hipErrorNotSupported;
+hipError_t launch_bgemm_mfma(const uint64_t* F, int64_t M, int64_t ldf, const uint64_t* B,
+                             int32_t N, int64_t ldb, int32_t K, void* C, IType ct,
+                             int64_t ldc, hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  const int NT = N <= 16 ? 1 : N <= 32 ? 2 : N <= 64 ? 4 : N <= 128 ? 8 : 16;
+  const int kw = (K + 63) / 64;
+  const int kc = NT >= 16 ? 2 : 4;
+  const size_t lds = (size_t)(kw < kc ? kw : kc) * NT * 64 * 16;
+  const int64_t blocks = (M + kWavesPerBlock * 32 - 1) / (kWavesPerBlock * 32);
+  const dim3 grid(grid_cap(blocks, 2048));
+  switch (NT) {
+    case 1: launch_mfma_nt<1>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc); break;
+    case 2: launch_mfma_nt<2>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc); break;
+    case 4: launch_mfma_nt<4>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc); break;
+    case 8: launch_mfma_nt<8>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc); break;
+    default: launch_mfma_nt<16>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc); break;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace bigcn

@@ -90,20 +90,30 @@ BGEMM_SHAPES = [(1, 1, 1), (5, 3, 63), (130, 7, 64), (257, 40, 65), (100, 41, 10
                 (4099, 256, 128)]
 
 
+@pytest.mark.parametrize("algo", ["popcount", "mfma_i8"])
 @pytest.mark.parametrize("M,N,K", BGEMM_SHAPES)
-def test_bgemm_matches_oracle(dev, M, N, K):
+def test_bgemm_matches_oracle(dev, M, N, K, algo):
     rng = np.random.default_rng(M * 131 + N * 17 + K)
     F, _ = oracle.binarize(rng.standard_normal((M, K)).astype(np.float32))
     B, _ = oracle.binarize(rng.standard_normal((N, K)).astype(np.float32))
     F[M // 2] = B[N // 2]                      # an exact +K entry
+    if M > 2:                                  # an exact -K entry (pad bits kept 0)
+        F[M - 1] = ~B[0]
+        if K % 64:
+            F[M - 1, -1] &= np.uint64((1 << (K % 64)) - 1)
     ref = oracle.sign_dot(F, B, K)
     Ft, Bt = _t(F.view(np.int64), dev), _t(B.view(np.int64), dev)
+    if algo == "mfma_i8" and N > 256:
+        C = torch.zeros((M, N), dtype=torch.int32, device=dev)
+        with pytest.raises(bg.BigcnError):
+            bg.bigcn_bgemm(Ft, Bt, K, C, algo=algo)
+        return
     for ctype, dt in (("i32", torch.int32), ("i16", torch.int16), ("f16", torch.float16)):
         if ctype == "f16" and K > 2048:
             continue
         ldc = N + 5
         C = torch.full((M, ldc), 77, dtype=dt, device=dev)             # poison
-        bg.bigcn_bgemm(Ft, Bt, K, C[:, :N], algo="popcount")
+        bg.bigcn_bgemm(Ft, Bt, K, C[:, :N], algo=algo)
         torch.cuda.synchronize()
         got = C.cpu().numpy()
         assert np.array_equal(got[:, :N].astype(np.int64), ref), ctype
