@@ -16,8 +16,17 @@ Prints one JSON line.  Besides the forward-pass throughput it carries
  - "roofline": the dominant kernel (largest share of a forward pass) against
    its bound: HBM bytes for pack / aggregation, bit operations on the vector
    ALUs for the binary GEMM;
+ - "bgemm_ab": the binary GEMM of every layer shape run with both
+   algorithms (XOR + bit count on the vector ALUs, +-1 int8 on the matrix
+   cores) on the same random sign bits, checked equal, each against its
+   own peak in sign products per second;
  - "cpu_baseline": the plain CPU oracle timed on this host on a bounded
    sample of the same workload.
+
+    python bench.py --bgemm-ab
+
+runs only the two-algorithm comparison, over the layer shapes of all five
+workloads, and prints it as one JSON line.
 """
 from __future__ import annotations
 
@@ -35,6 +44,8 @@ HBM_PEAK_GBS = 8000.0
 # 256 CUs x 4 SIMD x 16 lanes x 2.4 GHz = 39.3 T lane-ops/s; the popcount
 # GEMM needs 2 XOR + 2 bit-count lane-ops per 64 sign products.
 VALU_BITOP_PEAK = 256 * 4 * 16 * 2.4e9 * 16
+# Dense int8 MFMA: 5.0 P ops/s = 2.5 P multiply-adds/s, one sign product each.
+MFMA_I8_BITOP_PEAK = 2.5e15
 METRIC = "nodes/sec full Bi-GCN forward; bGEMM bit-ops/s; SpMM/pack HBM GB/s vs peak"
 
 
@@ -83,6 +94,38 @@ def time_calls(fn, reps, torch):
     end.record()
     torch.cuda.synchronize()
     return start.elapsed_time(end) / reps * 1e-3
+
+
+def bgemm_ab(shapes, reps, torch, bg, dev):
+    """Both binary-GEMM algorithms on each (M, N, K): seeded random sign bits
+    (pad bits zero), results compared bit for bit, durations from time_calls."""
+    out = []
+    for M, N, K in shapes:
+        kw = words(K)
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(M * 7919 + N * 31 + K)
+        F = torch.randint(-2 ** 62, 2 ** 62, (M, kw), dtype=torch.int64, device=dev,
+                          generator=gen)
+        B = torch.randint(-2 ** 62, 2 ** 62, (N, kw), dtype=torch.int64, device=dev,
+                          generator=gen)
+        if K % 64:
+            F[:, -1] &= (1 << (K % 64)) - 1
+            B[:, -1] &= (1 << (K % 64)) - 1
+        dt = torch.float16 if K <= 2048 else torch.int16
+        res, rec = {}, dict(M=M, N=N, K=K, sign_products=M * N * K)
+        for algo, peak in (("popcount", VALU_BITOP_PEAK), ("mfma_i8", MFMA_I8_BITOP_PEAK)):
+            C = torch.empty((M, N), dtype=dt, device=dev)
+            t = time_calls(lambda: bg.bigcn_bgemm(F, B, K, C, algo=algo), reps, torch)
+            res[algo] = C
+            rec[algo] = dict(us=round(t * 1e6, 3), tbitops=round(M * N * K / t / 1e12, 2),
+                             frac=round(M * N * K / t / peak, 4))
+        rec["equal"] = bool(torch.equal(res["popcount"], res["mfma_i8"]))
+        rec["faster"] = min(("popcount", "mfma_i8"), key=lambda a: rec[a]["us"])
+        out.append(rec)
+        log("  bgemm %8d x %3d x %4d: popcount %9.2f us  mfma_i8 %9.2f us  equal=%s" % (
+            M, N, K, rec["popcount"]["us"], rec["mfma_i8"]["us"], rec["equal"]))
+        del F, B, res
+    return out
 
 
 def cpu_baseline(w, budget_s=10.0):
@@ -146,6 +189,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true",
                     help="report eager calls instead of the HIP-graph replay")
+    ap.add_argument("--bgemm-ab", action="store_true",
+                    help="only compare the two binary-GEMM algorithms on every "
+                         "workload's layer shapes")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -161,6 +207,17 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    if args.bgemm_ab:
+        shapes = []
+        for c in workloads.CONFIGS.values():
+            for K, d in zip(c["dims"][:-1], c["dims"][1:]):
+                shapes.append((c["n"], d, K))
+        ab = bgemm_ab(shapes, args.kernel_reps, torch, bg, dev)
+        assert all(r["equal"] for r in ab), "binary-GEMM algorithms disagree"
+        print(json.dumps({"bgemm_ab": ab, "peaks_tbitops": {
+            "popcount": VALU_BITOP_PEAK / 1e12, "mfma_i8": MFMA_I8_BITOP_PEAK / 1e12}}),
+              flush=True)
+        return
     t0 = time.time()
     w = workloads.make_workload(args.workload)
     g = w.graph
@@ -264,6 +321,9 @@ def main():
                     achieved=round(dom["achieved"], 2), peak=dom["peak"], unit=dom["unit"],
                     frac=round(dom["frac"], 4), traffic=None, avg_us=round(dom["us"], 3))
 
+    ab = bgemm_ab([(g.n, ly.d_out, ly.d_in) for ly in model.layers], reps, torch, bg, dev)
+    assert all(r["equal"] for r in ab), "binary-GEMM algorithms disagree"
+
     cpu = None
     if not args.no_cpu_baseline:
         t = time.time()
@@ -294,6 +354,7 @@ def main():
         "kernels": [{k2: (round(v, 4) if isinstance(v, float) else v) for k2, v in k.items()}
                     for k in kernels],
         "roofline": roofline,
+        "bgemm_ab": ab,
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)

@@ -61,8 +61,11 @@ typedef enum { BIGCN_NORM_SYM = 0, BIGCN_NORM_MEAN = 1 } bigcn_norm;
 typedef enum { BIGCN_ACT_NONE = 0, BIGCN_ACT_RELU = 1 } bigcn_act;
 
 /* Binary-GEMM algorithm.  POPCOUNT: XOR + bit count on the vector ALUs.
- * MFMA_I8: the signs expanded to +-1 int8 and multiplied on the matrix
- * cores.  Both give identical results; AUTO picks the faster one. */
+ * MFMA_I8: the signs expanded to {0,1} bytes and multiplied on the matrix
+ * cores (int8 in, int32 accumulate), the +-1 product recovered exactly as
+ * 4*sum(ab) - 2*sum(a) - 2*sum(b) + K; N <= 256.  Both give identical
+ * results.  AUTO takes MFMA_I8 for M >= 65536 rows with K >= 256 (where it
+ * measured faster on MI355X) and POPCOUNT otherwise. */
 typedef enum {
   BIGCN_BGEMM_AUTO = 0,
   BIGCN_BGEMM_POPCOUNT = 1,

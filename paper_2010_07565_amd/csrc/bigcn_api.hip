@@ -82,10 +82,20 @@ bigcn_status check_spmm_operands(int64_t n, const float* g, const void* C,
   return BIGCN_OK;
 }
 
+// AUTO takes the matrix cores where they measured faster on MI355X: at
+// least 64K rows and K >= 256 (a contraction long enough to pay for the
+// sign expansion).  With K <= 128 the product write dominates and the
+// popcount kernel's wider stores win; below 64K rows both are launch bound.
+bool auto_picks_mfma(int64_t M, int32_t N, int32_t K) {
+  return bigcn::bgemm_mfma_supported(N, K) && M >= 65536 && K >= 256;
+}
+
 hipError_t run_bgemm(const uint64_t* F, int64_t M, int64_t ldf, const uint64_t* B,
                      int32_t N, int64_t ldb, int32_t K, void* C, IType ct,
                      int64_t ldc, int algo, hipStream_t s) {
-  if (algo == BIGCN_BGEMM_MFMA_I8 && bigcn::bgemm_mfma_supported(N, K))
+  const bool mfma = algo == BIGCN_BGEMM_MFMA_I8 ||
+                    (algo == BIGCN_BGEMM_AUTO && auto_picks_mfma(M, N, K));
+  if (mfma && bigcn::bgemm_mfma_supported(N, K))
     return bigcn::launch_bgemm_mfma(F, M, ldf, B, N, ldb, K, C, ct, ldc, s);
   return bigcn::launch_bgemm_popcount(F, M, ldf, B, N, ldb, K, C, ct, ldc, s);
 }

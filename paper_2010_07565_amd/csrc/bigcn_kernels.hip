@@ -362,10 +362,15 @@ __global__ __launch_bounds__(kBlock) void k_bgemm_pop_q8(
 // (gfx950): lane l of A holds row l % 16, bytes 16*(l/16) .. +15 of the word;
 // lane l of B holds column l % 16 with the same bytes; lane L, register R of
 // the result holds row 4*(L/16) + R, column L % 16.
-// A block stages up to KC words of the weights, already expanded, in LDS in
-// B-operand order ([word][column tile][lane] x 16 bytes, so each operand
-// load is one conflict-free 16-byte read); each wave owns two 16-row tiles
-// that share every weight operand.  N <= 256; at most 32 KB of LDS.
+// Work split: a block owns one group of NT column tiles (NT*16 <= 128
+// columns) and walks row tiles of 4 waves x 32 rows; each wave's two 16-row
+// tiles share every weight operand.  The block stages kc words of its
+// columns' weights, already expanded, in LDS in B-operand order
+// ([word][tile][lane] x 16 bytes: each operand load is one conflict-free
+// 16-byte read).  When kc covers all of K the staged weights are kept for
+// every row tile of the block (grid is a multiple of the group count, so a
+// block's group never changes).  The next feature word is loaded before the
+// current word's MFMAs are issued.
 
 typedef int int4v_t __attribute__((ext_vector_type(4)));
 
@@ -380,77 +385,93 @@ __device__ inline int4v_t expand16(uint32_t bits) {
   return r;
 }
 
+constexpr int kMfmaLdsBytes = 48 * 1024;  // staged weights per block
+
 template <int NT, typename T>
 __global__ __launch_bounds__(kBlock) void k_bgemm_mfma(
     const uint64_t* __restrict__ F, int64_t M, int64_t ldf,
     const uint64_t* __restrict__ B, int32_t N, int64_t ldb, int32_t K,
-    T* __restrict__ C, int64_t ldc) {
-  constexpr int KC = NT >= 16 ? 2 : 4;  // words staged per pass (<= 32 KB)
-  extern __shared__ int4v_t sW[];                       // [KC][NT][64]
-  __shared__ int sPb[256];                              // sum b per column
+    T* __restrict__ C, int64_t ldc, int32_t groups, int32_t kc_max) {
+  extern __shared__ int4v_t sW[];                       // [kc][NT][64]
+  __shared__ int sPb[NT * 16];                          // sum b per column
   const int lane = threadIdx.x & 63;
   const int wv = wave_index_in_block();
   const int kw = (K + 63) >> 6;
-  for (int j = threadIdx.x; j < 256; j += kBlock) {
+  const int m = lane & 15, grp = lane >> 4;
+  const int cg = blockIdx.x % groups;
+  const int c0 = cg * NT * 16;
+  for (int j = threadIdx.x; j < NT * 16; j += kBlock) {
     int pc = 0;
-    if (j < N)
-      for (int w = 0; w < kw; ++w) pc += __builtin_popcountll(B[(int64_t)j * ldb + w]);
+    if (c0 + j < N)
+      for (int w = 0; w < kw; ++w) pc += __builtin_popcountll(B[(int64_t)(c0 + j) * ldb + w]);
     sPb[j] = pc;
   }
-  const int m = lane & 15, grp = lane >> 4;
+  const bool resident = kc_max >= kw;
+  bool staged = false;
   const int64_t rows_per_block = kWavesPerBlock * 32;
-  for (int64_t base = (int64_t)blockIdx.x * rows_per_block; base < M;
-       base += (int64_t)gridDim.x * rows_per_block) {
+  const int64_t row_step = (int64_t)(gridDim.x / groups) * rows_per_block;
+  for (int64_t base = (int64_t)(blockIdx.x / groups) * rows_per_block; base < M;
+       base += row_step) {
     const int64_t r0 = base + wv * 32;  // this wave: rows r0 .. r0+31
+    const int64_t rowA = r0 + m, rowB = r0 + 16 + m;
+    const uint64_t* fa = F + (rowA < M ? rowA : 0) * ldf;
+    const uint64_t* fb = F + (rowB < M ? rowB : 0) * ldf;
     int4v_t acc[2][NT];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int jt = 0; jt < NT; ++jt) acc[t][jt] = int4v_t{0, 0, 0, 0};
-    int pa[2] = {0, 0};
-    for (int w0 = 0; w0 < kw; w0 += KC) {
-      const int kc = kw - w0 < KC ? kw - w0 : KC;
-      __syncthreads();  // previous chunk fully consumed
-      for (int idx = threadIdx.x; idx < kc * NT * 64; idx += kBlock) {
-        const int l = idx & 63;
-        const int jt = (idx >> 6) % NT;
-        const int w = idx / (64 * NT);
-        const int col = jt * 16 + (l & 15);
-        const uint64_t word = col < N ? B[(int64_t)col * ldb + w0 + w] : 0ull;
-        sW[(w * NT + jt) * 64 + l] = expand16((uint32_t)(word >> (16 * (l >> 4))) & 0xFFFFu);
-      }
-      __syncthreads();
-      for (int w = 0; w < kc; ++w) {
-        int4v_t a[2];
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const int64_t row = r0 + t * 16 + m;
-          const uint64_t f = row < M ? F[row * ldf + w0 + w] : 0ull;
-          pa[t] += __builtin_popcountll(f);
-          a[t] = expand16((uint32_t)(f >> (16 * grp)) & 0xFFFFu);
+    int pa0 = 0, pa1 = 0;
+    for (int w0 = 0; w0 < kw; w0 += kc_max) {
+      const int kc = kw - w0 < kc_max ? kw - w0 : kc_max;
+      if (!(resident && staged)) {
+        __syncthreads();  // previous chunk fully consumed
+        for (int idx = threadIdx.x; idx < kc * NT * 64; idx += kBlock) {
+          const int l = idx & 63;
+          const int jt = (idx >> 6) % NT;
+          const int w = idx / (64 * NT);
+          const int col = c0 + jt * 16 + (l & 15);
+          const uint64_t word = col < N ? B[(int64_t)col * ldb + w0 + w] : 0ull;
+          sW[(w * NT + jt) * 64 + l] =
+              expand16((uint32_t)(word >> (16 * (l >> 4))) & 0xFFFFu);
         }
+        __syncthreads();
+        staged = true;
+      }
+      uint64_t na = rowA < M ? fa[w0] : 0ull;
+      uint64_t nb = rowB < M ? fb[w0] : 0ull;
+      for (int w = 0; w < kc; ++w) {
+        const uint64_t f0 = na, f1 = nb;
+        if (w + 1 < kc) {
+          na = rowA < M ? fa[w0 + w + 1] : 0ull;
+          nb = rowB < M ? fb[w0 + w + 1] : 0ull;
+        }
+        pa0 += __builtin_popcountll(f0);
+        pa1 += __builtin_popcountll(f1);
+        const int4v_t a0 = expand16((uint32_t)(f0 >> (16 * grp)) & 0xFFFFu);
+        const int4v_t a1 = expand16((uint32_t)(f1 >> (16 * grp)) & 0xFFFFu);
 #pragma unroll
         for (int jt = 0; jt < NT; ++jt) {
-          const int4v_t b = sW[(w * NT + jt) * 64 + lane];
-          acc[0][jt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[0], b, acc[0][jt], 0, 0, 0);
-          acc[1][jt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[1], b, acc[1][jt], 0, 0, 0);
+          const int4v_t bop = sW[(w * NT + jt) * 64 + lane];
+          acc[0][jt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0, bop, acc[0][jt], 0, 0, 0);
+          acc[1][jt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1, bop, acc[1][jt], 0, 0, 0);
         }
       }
     }
-    // Each lane counted 4x the bits of its row (one per lane group); every
-    // lane of a row's group sees the whole word, so pa is per row already.
+    // Lanes m, m+16, m+32, m+48 all hold row m's full popcount.
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
+      const int pa = t == 0 ? pa0 : pa1;
 #pragma unroll
       for (int R = 0; R < 4; ++R) {
         const int mr = 4 * grp + R;                     // output row in the tile
-        const int pa_r = __shfl(pa[t], mr, 64);          // lanes 0..15 hold rows 0..15
+        const int pa_r = __shfl(pa, mr, 64);
         const int64_t row = r0 + t * 16 + mr;
 #pragma unroll
         for (int jt = 0; jt < NT; ++jt) {
-          const int col = jt * 16 + m;
+          const int col = c0 + jt * 16 + m;
           if (row < M && col < N) {
-            const int dot = K - 2 * (pa_r + sPb[col]) + 4 * acc[t][jt][R];
+            const int dot = K - 2 * (pa_r + sPb[jt * 16 + m]) + 4 * acc[t][jt][R];
             C[row * ldc + col] = (T)dot;
           }
         }
@@ -1623,19 +1644,20 @@ bool bgemm_mfma_supported(int32_t N, int32_t K) { return N >= 1 && N <= 256 && K
 template <int NT>
 static void launch_mfma_nt(dim3 grid, size_t lds, hipStream_t stream, const uint64_t* F,
                            int64_t M, int64_t ldf, const uint64_t* B, int32_t N,
-                           int64_t ldb, int32_t K, void* C, IType ct, int64_t ldc) {
+                           int64_t ldb, int32_t K, void* C, IType ct, int64_t ldc,
+                           int32_t groups, int32_t kc_max) {
   switch (ct) {
     case IType::F16:
       hipLaunchKernelGGL((k_bgemm_mfma<NT, _Float16>), grid, dim3(kBlock), lds, stream, F,
-                         M, ldf, B, N, ldb, K, (_Float16*)C, ldc);
+                         M, ldf, B, N, ldb, K, (_Float16*)C, ldc, groups, kc_max);
       break;
     case IType::I16:
       hipLaunchKernelGGL((k_bgemm_mfma<NT, int16_t>), grid, dim3(kBlock), lds, stream, F,
-                         M, ldf, B, N, ldb, K, (int16_t*)C, ldc);
+                         M, ldf, B, N, ldb, K, (int16_t*)C, ldc, groups, kc_max);
       break;
     default:
       hipLaunchKernelGGL((k_bgemm_mfma<NT, int32_t>), grid, dim3(kBlock), lds, stream, F,
-                         M, ldf, B, N, ldb, K, (int32_t*)C, ldc);
+                         M, ldf, B, N, ldb, K, (int32_t*)C, ldc, groups, kc_max);
       break;
   }
 }
@@ -1644,18 +1666,24 @@ hipError_t launch_bgemm_mfma(const uint64_t* F, int64_t M, int64_t ldf, const ui
                              int32_t N, int64_t ldb, int32_t K, void* C, IType ct,
                              int64_t ldc, hipStream_t stream) {
   if (M == 0) return hipSuccess;
-  const int NT = N <= 16 ? 1 : N <= 32 ? 2 : N <= 64 ? 4 : N <= 128 ? 8 : 16;
   const int kw = (K + 63) / 64;
-  const int kc = NT >= 16 ? 2 : 4;
-  const size_t lds = (size_t)(kw < kc ? kw : kc) * NT * 64 * 16;
-  const int64_t blocks = (M + kWavesPerBlock * 32 - 1) / (kWavesPerBlock * 32);
-  const dim3 grid(grid_cap(blocks, 2048));
+  const int tiles = (N + 15) / 16;
+  // Column tiles per block: a power of two <= 8, halved while the block's
+  // expanded weights (1 KB per tile and word) would not stay resident.
+  int NT = 1;
+  while (NT < tiles && NT < 8) NT *= 2;
+  while (NT > 1 && (size_t)kw * NT * 1024 > (size_t)kMfmaLdsBytes) NT /= 2;
+  const int groups = (tiles + NT - 1) / NT;
+  const int kc_max = std::min(kw, kMfmaLdsBytes / (NT * 1024));
+  const size_t lds = (size_t)kc_max * NT * 1024;
+  const int64_t row_blocks = (M + kWavesPerBlock * 32 - 1) / (kWavesPerBlock * 32);
+  const int64_t cap = 4096 - 4096 % groups;
+  const dim3 grid((unsigned)std::min<int64_t>(row_blocks * groups, cap));
   switch (NT) {
-    case 1: launch_mfma_nt<1>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc); break;
-    case 2: launch_mfma_nt<2>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc); break;
-    case 4: launch_mfma_nt<4>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc); break;
-    case 8: launch_mfma_nt<8>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc); break;
-    default: launch_mfma_nt<16>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc); break;
+    case 1: launch_mfma_nt<1>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc, groups, kc_max); break;
+    case 2: launch_mfma_nt<2>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc, groups, kc_max); break;
+    case 4: launch_mfma_nt<4>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc, groups, kc_max); break;
+    default: launch_mfma_nt<8>(grid, lds, stream, F, M, ldf, B, N, ldb, K, C, ct, ldc, groups, kc_max); break;
   }
   return hipGetLastError();
 }
