@@ -20,6 +20,9 @@ Prints one JSON line.  Besides the forward-pass throughput it carries
    algorithms (XOR + bit count on the vector ALUs, +-1 int8 on the matrix
    cores) on the same random sign bits, checked equal, each against its
    own peak in sign products per second;
+ - "paper_theoretical": the paper's analytic cycle-operation and size
+   ratios for this workload (theory, quoted as such), beside the ratio of
+   the fp32 features to the packed sign words this library stores;
  - "cpu_baseline": the plain CPU oracle timed on this host on a bounded
    sample of the same workload.
 
@@ -331,6 +334,22 @@ def main():
         log("cpu baseline: %s (%.1f s)" % (cpu, time.time() - t))
 
     dims = [w.weights_t[0].shape[1]] + [wt.shape[0] for wt in w.weights_t]
+    from paper_2010_07565_amd import costmodel
+    undirected = (g.nnz - g.n) // 2
+    theory = costmodel.theoretical_ratios(g.n, undirected, dims)
+    paper = {
+        "kind": "the paper's analytic counts (Sec. 5: cycle operations, model and "
+                "feature sizes, full precision over binarized) for this workload; "
+                "not measurements",
+        "cycle_op_speedup": round(theory["cycle_ops"], 2),
+        "model_size_ratio": round(theory["model_size"], 2),
+        "data_size_ratio": round(theory["data_size"], 2),
+        "co_shares": {k: round(v, 3) for k, v in
+                      costmodel.co_breakdown(g.n, undirected, dims).items()},
+        "quoted": "about 47x fewer cycle operations and about 30x less memory on "
+                  "the citation graphs (Sec. 6.3)",
+        "stored_feature_ratio": round((g.n * dims[0] * 4) / (g.n * ldF * 8 + g.n * 4), 2),
+    }
     rec = {
         "metric": METRIC,
         "value": round(nodes_per_s, 1),
@@ -355,6 +374,7 @@ def main():
                     for k in kernels],
         "roofline": roofline,
         "bgemm_ab": ab,
+        "paper_theoretical": paper,
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
