@@ -68,7 +68,7 @@ def kernel_specs(w, ldF, ldc):
         d, K = wt.shape
         kw = words(K)
         pack_bytes = n * K * 4 + n * kw * 8 + n * 4 + (n + 1) * 8 + (2 * K * 4 if l == 0 else 0)
-        es = 1 if (128 < d <= 256 and K <= 2048) else 2   # stored bytes per product
+        es = 1 if (d <= 256 and K <= 2048) else 2   # stored bytes per product
         gemm_ops = n * K * d
         gemm_bytes = n * kw * 8 + d * kw * 8 + n * d * es
         spmm_bytes = 8 * (n + 1) + 4 * nnz + 4 * n + n * d * es + n * d * 4 + 8 * d
@@ -192,6 +192,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true",
                     help="report eager calls instead of the HIP-graph replay")
+    ap.add_argument("--forward-only", action="store_true",
+                    help="time the forward pass only (no per-kernel table, no "
+                         "algorithm comparison, no CPU baseline): for profiling")
     ap.add_argument("--bgemm-ab", action="store_true",
                     help="only compare the two binary-GEMM algorithms on every "
                          "workload's layer shapes")
@@ -260,6 +263,12 @@ def main():
     log("forward: eager %.4f ms/step, graph replay %.4f ms/step -> %.4g nodes/s" % (
         eager_s * 1e3, graph_s * 1e3, nodes_per_s))
 
+    if args.forward_only:
+        print(json.dumps({"metric": METRIC, "value": round(nodes_per_s, 1), "unit": "nodes/s",
+                          "ms_per_step": round(ms, 5), "workload": w.name,
+                          "mode": "eager" if args.eager else "hip_graph_replay"}), flush=True)
+        return
+
     # ---- each kernel alone, through its entry point, same shapes and ld's
     L = len(w.weights_t)
     kwmax = max(words(wt.shape[1]) for wt in w.weights_t)
@@ -287,10 +296,14 @@ def main():
                                                            w.norm), reps, torch)
         q8 = bg.q8_supported(g.n, d, K)
         if q8:
-            # the forward keeps these products as 8-bit half-codes
-            t_gemm = time_calls(lambda: bg.bigcn_bgemm_q8(F[:, :kw], ly.wbits, K, C8, C, gs),
+            # the forward keeps these products as 8-bit half-codes, in rows
+            # of q8_row(d) entries
+            W = bg.q8_row(d)
+            c8 = C8.view(-1)[:g.n * W].view(g.n, W)
+            c16 = C.view(-1)[:g.n * W].view(g.n, W)
+            t_gemm = time_calls(lambda: bg.bigcn_bgemm_q8(F[:, :kw], ly.wbits, K, c8, c16, gs),
                                 reps, torch)
-            t_spmm = time_calls(lambda: bg.bigcn_spmm_csr_q8(rowptr, colidx, gs, C8, C, K,
+            t_spmm = time_calls(lambda: bg.bigcn_spmm_csr_q8(rowptr, colidx, gs, c8, c16, K,
                                                              ly.alpha, out, ws, ly.bias,
                                                              w.norm, ly.act, d=d),
                                 reps, torch)

@@ -166,15 +166,17 @@ bigcn_status bigcn_spmm_csr(int64_t n, int64_t nnz, const int64_t* rowptr,
  * bigcn_binarize_pack, and is left with the flags for bigcn_spmm_csr_q8.
  * Inputs and outputs otherwise as bigcn_bgemm / bigcn_spmm_csr.
  *
- *   C8   [M][ldc8] int8, ldc8 >= 256 and a multiple of 4.  Row order is
- *        lane-interleaved: column k sits at position 4*(k % 64) + k / 64
- *        (the 64 lanes of a wave each find their columns l, l+64, l+128,
- *        l+192 in one 32-bit word).
- *   C16  [M][ldc16] IEEE half, ldc16 >= 256 and a multiple of 4, the same
+ * Row width: NB = 1, 2 or 4 bytes per lane for N (d for the aggregation)
+ * of at most 64, 128 or 256 columns; a row spans W = 64 * NB entries.
+ *   C8   [M][ldc8] int8, ldc8 >= W and a multiple of 4.  Row order is
+ *        lane-interleaved: column k sits at position NB*(k % 64) + k / 64
+ *        (the 64 lanes of a wave each find their columns l, l+64, ... in
+ *        one NB-byte word); for N <= 64 that is the natural order.
+ *   C16  [M][ldc16] IEEE half, ldc16 >= W and a multiple of 4, the same
  *        interleaved order; only flagged rows are written.
  *   g    fp32[M] (see above).
- * Shapes: 128 < N <= 256, K <= 2048, M * ldc8 and M * ldc16 * 2 below 4 GiB;
- * other shapes return EUNSUPPORTED (use the exact-type calls).
+ * Shapes: 1 <= N <= 256, K <= 2048, M * W and M * W * 2 below 4 GiB; other
+ * shapes return EUNSUPPORTED (use the exact-type calls).
  * The aggregation result equals bigcn_spmm_csr on the exact products up to
  * fp32 rounding (the sum is formed as 2 * sum g code + p * sum g).
  * ------------------------------------------------------------------------- */
@@ -209,12 +211,13 @@ bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
  *   workspace  at least bigcn_forward_workspace_bytes(...) bytes, 256-byte
  *          aligned; contents on entry are ignored.
  * Internally each layer's products are kept exactly: as 8-bit half-codes
- * (see bigcn_bgemm_q8) for layers of 129..256 output columns with
- * d_in <= 2048, otherwise in IEEE half (d_in <= 2048) or int16.  When such
- * a layer is followed by one with d_in <= 256 and d_out <= 256, the next
- * layer's sign pack and binary GEMM run inside the aggregation that produces
- * its input: the hidden activations are never written to memory.  The result
- * is bit-identical to chaining the per-step entry points.
+ * (see bigcn_bgemm_q8) for layers of up to 256 output columns with
+ * d_in <= 2048, otherwise in IEEE half (d_in <= 2048) or int16.  When two
+ * consecutive layers both use 8-bit codes, the second layer's sign pack and
+ * binary GEMM run inside the aggregation that produces its input: the
+ * hidden activations are never written to memory.  The result is
+ * bit-identical to chaining the per-step entry points (bigcn_binarize_pack,
+ * bigcn_bgemm_q8, bigcn_spmm_csr_q8 for 8-bit layers).
  * Errors: as the per-step calls, plus EINVAL for inconsistent layer widths
  *         or n_layers < 1, EUNSUPPORTED for d_in > 8192 on a layer.
  * ------------------------------------------------------------------------- */

@@ -211,10 +211,25 @@ def bigcn_spmm_csr_q8(rowptr: torch.Tensor, colidx: torch.Tensor, g: torch.Tenso
     _check("bigcn_spmm_csr_q8", st)
 
 
+def q8_lane_bytes(d: int) -> int:
+    """Bytes per lane of the 8-bit layout for d output columns."""
+    return 1 if d <= 64 else 2 if d <= 128 else 4
+
+
+def q8_row(d: int) -> int:
+    """Entries per row of the 8-bit layout (codes in C8, halves in C16)."""
+    return 64 * q8_lane_bytes(d)
+
+
+def q8_position(k: int, d: int) -> int:
+    """Position of column k in a row of the 8-bit layout."""
+    nb = q8_lane_bytes(d)
+    return nb * (k % 64) + k // 64
+
+
 def q8_supported(n: int, d: int, K: int) -> bool:
     """Whether the forward keeps a layer's products as 8-bit half-codes."""
-    return 128 < d <= 256 and K <= 2048 and n * 256 <= 0xFFFFFFFF and \
-        n * ((d + 7) // 8 * 8) * 2 <= 0xFFFFFFFF
+    return 1 <= d <= 256 and 1 <= K <= 2048 and n * q8_row(d) * 2 <= 0xFFFFFFFF
 
 
 @dataclass

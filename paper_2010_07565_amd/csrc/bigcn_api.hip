@@ -102,24 +102,27 @@ hipError_t run_bgemm(const uint64_t* F, int64_t M, int64_t ldf, const uint64_t* 
 
 // Workspace layout of bigcn_forward.  Two sets of (scale g, 8-bit codes C8,
 // 16-bit products C16) alternate between layers, so a layer can write the
-// next layer's products while its own are being read.
+// next layer's products while its own are being read.  ldc8 / ldc16 are the
+// capacities per node; an 8-bit layer uses rows of q8_row(d_out).
 struct ForwardLayout {
   int64_t ldF, ldh, ldc8, ldc16;
   size_t off_F, off_g[2], off_C8[2], off_C16[2], off_H0, off_H1, off_spmm, bytes;
   int32_t dmax;
 };
 
-// Whether layer l's aggregation can produce layer l+1's products in its
-// epilogue, and in which storage (see bigcn::FusedNext).
+// Whether layer l's aggregation produces layer l+1's products in its
+// epilogue (see bigcn::FusedNext): both layers on the 8-bit path.
 int fuse_kind(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t nl, int32_t l) {
   if (l + 1 >= nl || nnz == 0) return 0;
   const bigcn_layer& a = layers[l];
   const bigcn_layer& b = layers[l + 1];
   if (!bigcn::q8_supported(n, a.d_out, a.d_in)) return 0;  // producer: 8-bit wave kernel
-  if (b.d_in > 256) return 0;
-  if (bigcn::q8_supported(n, b.d_out, b.d_in)) return 1;
-  return b.d_out <= 128 ? 2 : 0;
+  return bigcn::q8_supported(n, b.d_out, b.d_in) ? 1 : 0;
 }
+
+// Row stride (bytes of codes, or halves of exact products) of the 8-bit
+// layout for a layer of d outputs.
+inline int64_t q8_row(int32_t d) { return 64 * bigcn::q8_lane_bytes(d); }
 
 bool forward_layout(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t nl,
                     ForwardLayout* L) {
@@ -231,7 +234,8 @@ bigcn_status bigcn_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
                             int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
                             float* g, void* stream) {
   if (M < 0 || N < 1 || K < 1 || ldf < words(K) || ldb < words(K)) return BIGCN_EINVAL;
-  if (ldc8 < 256 || ldc8 % 4 != 0 || ldc16 < 256 || ldc16 % 4 != 0) return BIGCN_EINVAL;
+  if (ldc8 < q8_row(N) || ldc8 % 4 != 0 || ldc16 < q8_row(N) || ldc16 % 4 != 0)
+    return BIGCN_EINVAL;
   if (B == nullptr || (M > 0 && (F == nullptr || C8 == nullptr || C16 == nullptr ||
                                  g == nullptr)))
     return BIGCN_EINVAL;
@@ -254,7 +258,8 @@ bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                                void* workspace, size_t ws_bytes, void* stream) {
   bigcn_status st = check_graph(n, nnz, rowptr, colidx, norm);
   if (st != BIGCN_OK) return st;
-  if (K < 1 || ldc8 < 256 || ldc8 % 4 != 0 || ldc16 < 256) return BIGCN_EINVAL;
+  if (K < 1 || d < 1 || ldc8 < q8_row(d) || ldc8 % 4 != 0 || ldc16 < q8_row(d))
+    return BIGCN_EINVAL;
   st = check_spmm_operands(n, g, C16, BIGCN_F16, d, ldc16, alpha, bias, act, out, ldo);
   if (st != BIGCN_OK) return st;
   if (n > 0 && C8 == nullptr) return BIGCN_EINVAL;
@@ -347,7 +352,7 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
       if (e != hipSuccess) return BIGCN_EHIP;
       if (q8)
         e = bigcn::launch_bgemm_q8(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C8,
-                                   L.ldc8, C16, L.ldc16, g, s);
+                                   q8_row(ly.d_out), C16, q8_row(ly.d_out), g, s);
       else
         e = run_bgemm(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C16, ct, L.ldc16,
                       BIGCN_BGEMM_AUTO, s);
@@ -367,13 +372,14 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
         fn.ldw = nxt.ldw;
         fn.d_out = nxt.d_out;
         fn.C8 = (int8_t*)(ws + L.off_C8[nset]);
-        fn.ldc8 = L.ldc8;
+        fn.ldc8 = q8_row(nxt.d_out);
         fn.C16 = ws + L.off_C16[nset];
-        fn.ldc16 = L.ldc16;
+        fn.ldc16 = q8_row(nxt.d_out);
         fn.g = (float*)(ws + L.off_g[nset]);
       }
       e = bigcn::launch_spmm_q8(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN, g, C8,
-                                L.ldc8, C16, L.ldc16, ly.d_in, ly.d_out, ly.alpha, ly.bias,
+                                q8_row(ly.d_out), C16, q8_row(ly.d_out), ly.d_in, ly.d_out,
+                                ly.alpha, ly.bias,
                                 ly.act == BIGCN_ACT_RELU, hout, ldout, plan, wsp, &fn, s);
     } else {
       e = bigcn::launch_spmm(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN, g, C16, ct,

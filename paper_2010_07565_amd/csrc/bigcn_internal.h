@@ -34,11 +34,12 @@ hipError_t launch_bgemm_mfma(const uint64_t* F, int64_t M, int64_t ldf,
                              int32_t K, void* C, IType ct, int64_t ldc,
                              hipStream_t stream);
 
-// Exact 8-bit half-code storage of the products (layers of 129..256 output
-// columns with K <= 2048): codes (dot - K%2)/2 in C8 rows of 256 bytes in
-// lane-interleaved order (column k at byte 4*(k%64) + k/64); rows with
-// |dot| > 255 written exactly (half, same order, 256 per row) to C16 and
-// flagged by the sign bit of g.
+// Exact 8-bit half-code storage of the products (layers of up to 256 output
+// columns with K <= 2048): codes (dot - K%2)/2 in C8 rows of 64*NB bytes,
+// NB = q8_lane_bytes(N), in lane-interleaved order (column k at byte
+// NB*(k%64) + k/64); rows with |dot| > 255 written exactly (half, same
+// order, 64*NB per row) to C16 and flagged by the sign bit of g.
+constexpr int q8_lane_bytes(int32_t N) { return N <= 64 ? 1 : N <= 128 ? 2 : 4; }
 bool q8_supported(int64_t n, int32_t N, int32_t K);
 hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
                            const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
@@ -48,8 +49,8 @@ hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
 // A next layer fused into the 8-bit aggregation's epilogue: the finished
 // output rows are binarised and multiplied with the next weights in place.
 //   kind 0: none (the output rows are written);
-//   kind 1: next products as 8-bit half-codes (C8, C16 fallback, flags in g);
-//   kind 2: next products exact in half, natural column order (C16, ldc16).
+//   kind 1: next products as 8-bit half-codes (C8, C16 fallback, flags in g),
+//           rows of 64*q8_lane_bytes(d_out) codes / halves.
 // g receives the next layer's per-node scale.
 struct FusedNext {
   int kind;

@@ -301,14 +301,46 @@ __global__ __launch_bounds__(kBlock) void k_bgemm_pop(
 
 // The same product stored as exact 8-bit half-codes for the forward pass:
 //   code = (dot - p) / 2,  p = K mod 2   (dot = K - 2 popcount is = p mod 2),
-// which holds every |dot| <= 255.  Rows are 256 bytes in lane-interleaved
-// order: column k sits at byte 4*(k % 64) + k / 64, so that lane l finds its
-// columns l, l+64, l+128, l+192 in one 32-bit word.  A row with a larger
-// |dot| anywhere is written in full, exactly, to C16 (IEEE half, the same
-// interleaved order, 256 halves per row) and flagged by setting the sign bit
-// of its scale g[i] (g >= 0 otherwise).  One wave covers all N <= 256
-// columns, so the flag is decided per row with a ballot.
-template <int RM>
+// which holds every |dot| <= 255.  A row holds 64*NB bytes (NB = 1, 2, 4 for
+// up to 64, 128, 256 outputs) in lane-interleaved order: column k sits at
+// byte NB*(k % 64) + k / 64, so that lane l finds its columns l + 64c
+// (c < NB) in one NB-byte word.  A row with a larger |dot| anywhere is
+// written in full, exactly, to C16 (IEEE half, the same interleaved order,
+// 64*NB halves per row) and flagged by setting the sign bit of its scale
+// g[i] (g >= 0 otherwise).  One wave covers all N columns, so the flag is
+// decided per row with a ballot.
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef float float2_t __attribute__((ext_vector_type(2)));
+
+template <int NB>
+__device__ inline void store_codes(int8_t* p, uint32_t packed) {
+  if constexpr (NB == 4)
+    *reinterpret_cast<uint32_t*>(p) = packed;
+  else if constexpr (NB == 2)
+    *reinterpret_cast<uint16_t*>(p) = (uint16_t)packed;
+  else
+    *reinterpret_cast<uint8_t*>(p) = (uint8_t)packed;
+}
+
+template <int NB>
+__device__ inline void store_exact(_Float16* p, const int* v) {
+  if constexpr (NB == 4) {
+    half4_t h;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) h[c] = (_Float16)v[c];
+    *reinterpret_cast<half4_t*>(p) = h;
+  } else if constexpr (NB == 2) {
+    half2_t h;
+    h[0] = (_Float16)v[0];
+    h[1] = (_Float16)v[1];
+    *reinterpret_cast<half2_t*>(p) = h;
+  } else {
+    *p = (_Float16)v[0];
+  }
+}
+
+template <int RM, int NB>
 __global__ __launch_bounds__(kBlock) void k_bgemm_pop_q8(
     const uint64_t* __restrict__ F, int64_t M, int64_t ldf,
     const uint64_t* __restrict__ B, int32_t N, int64_t ldb, int32_t K,
@@ -317,35 +349,32 @@ __global__ __launch_bounds__(kBlock) void k_bgemm_pop_q8(
   extern __shared__ uint64_t sB[];
   const int lane = threadIdx.x & 63;
   const int kw = (K + 63) >> 6;
-  stage_weights<4, true>(sB, B, N, ldb, kw, 0);
+  stage_weights<NB, true>(sB, B, N, ldb, kw, 0);
   const int64_t tiles = (M + RM - 1) / RM;
   const int64_t nwaves = (int64_t)gridDim.x * kWavesPerBlock;
   const int par = K & 1;
   for (int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
        t < tiles; t += nwaves) {
     const int64_t i0 = t * RM;
-    uint32_t acc[RM][4];
-    tile_popcounts<4, RM>(F, M, ldf, sB, kw, i0, lane, acc);
+    uint32_t acc[RM][NB];
+    tile_popcounts<NB, RM>(F, M, ldf, sB, kw, i0, lane, acc);
 #pragma unroll
     for (int r = 0; r < RM; ++r) {
       if (i0 + r >= M) break;  // wave-uniform
       const int64_t i = i0 + r;
-      int v[4];
+      int v[NB];
       bool big = false;
       uint32_t packed = 0;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
+      for (int c = 0; c < NB; ++c) {
         v[c] = K - 2 * (int)acc[r][c];
         const int code = (v[c] - par) >> 1;
         big |= (lane + 64 * c < N) && (code < -128 || code > 127);
         packed |= (uint32_t)(uint8_t)(int8_t)code << (8 * c);
       }
-      *reinterpret_cast<uint32_t*>(C8 + i * ldc8 + 4 * lane) = packed;
+      store_codes<NB>(C8 + i * ldc8 + NB * lane, packed);
       if (__builtin_amdgcn_ballot_w64(big) != 0) {
-        half4_t h;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) h[c] = (_Float16)v[c];
-        *reinterpret_cast<half4_t*>(C16 + i * ldc16 + 4 * lane) = h;
+        store_exact<NB>(C16 + i * ldc16 + NB * lane, v);
         if (lane == 0) g[i] = -fabsf(g[i]);
       }
     }
@@ -860,42 +889,95 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave(
   }
 }
 
+// Lane views of the 8-bit layout (see k_bgemm_pop_q8): NB codes or NB exact
+// halves per lane, widened to float4 with the unused components zero.
+template <int NB>
+__device__ inline uint32_t gather_codes(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
+  if constexpr (NB == 4)
+    return __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, 0);
+  else if constexpr (NB == 2)
+    return __builtin_amdgcn_raw_buffer_load_b16(rs, voff, soff, 0);
+  else
+    return __builtin_amdgcn_raw_buffer_load_b8(rs, voff, soff, 0);
+}
+
+template <int NB>
 __device__ inline float4_t codes_to_float(uint32_t x) {
-  float4_t f;
-  f[0] = (float)(int)(int8_t)(x & 0xff);
-  f[1] = (float)(int)(int8_t)((x >> 8) & 0xff);
-  f[2] = (float)(int)(int8_t)((x >> 16) & 0xff);
-  f[3] = (float)(int)(int8_t)(x >> 24);
+  float4_t f = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < NB; ++c) f[c] = (float)(int)(int8_t)((x >> (8 * c)) & 0xff);
   return f;
 }
 
-__device__ inline void fma4f(float4_t& acc, float g, const float4_t& v) {
-  acc[0] = fmaf(v[0], g, acc[0]);
-  acc[1] = fmaf(v[1], g, acc[1]);
-  acc[2] = fmaf(v[2], g, acc[2]);
-  acc[3] = fmaf(v[3], g, acc[3]);
+// (dot - p) / 2 from a flagged row's exact products.
+template <int NB>
+__device__ inline float4_t gather_exact(__amdgpu_buffer_rsrc_t rs, int voff, int soff,
+                                        float fpar) {
+  float4_t v = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (NB == 4) {
+    const half4_t x = __builtin_bit_cast(half4_t, __builtin_amdgcn_raw_buffer_load_b64(rs, voff, soff, 0));
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] = ((float)x[c] - fpar) * 0.5f;
+  } else if constexpr (NB == 2) {
+    const half2_t x = __builtin_bit_cast(half2_t, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, 0));
+    v[0] = ((float)x[0] - fpar) * 0.5f;
+    v[1] = ((float)x[1] - fpar) * 0.5f;
+  } else {
+    const _Float16 x = __builtin_bit_cast(_Float16, (uint16_t)__builtin_amdgcn_raw_buffer_load_b16(rs, voff, soff, 0));
+    v[0] = ((float)x - fpar) * 0.5f;
+  }
+  return v;
+}
+
+template <int NB>
+__device__ inline void fma_n(float4_t& acc, float g, const float4_t& v) {
+#pragma unroll
+  for (int c = 0; c < NB; ++c) acc[c] = fmaf(v[c], g, acc[c]);
+}
+
+// Partial rows of the 8-bit path: NB floats per lane at p = base + NB*lane.
+template <int NB>
+__device__ inline void store_partial(float* p, const float4_t v) {
+  if constexpr (NB == 4)
+    *reinterpret_cast<float4_t*>(p) = v;
+  else if constexpr (NB == 2)
+    *reinterpret_cast<float2_t*>(p) = float2_t{v[0], v[1]};
+  else
+    *p = v[0];
+}
+
+template <int NB>
+__device__ inline float4_t load_partial(const float* p) {
+  float4_t v = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (NB == 4) {
+    v = *reinterpret_cast<const float4_t*>(p);
+  } else if constexpr (NB == 2) {
+    const float2_t x = *reinterpret_cast<const float2_t*>(p);
+    v[0] = x[0];
+    v[1] = x[1];
+  } else {
+    v[0] = *p;
+  }
+  return v;
 }
 
 // What the aggregation does with a finished output row in the 8-bit path.
-// Lane l holds columns l + 64c of the row (c = 0..3, interleaved).
+// Lane l holds columns l + 64c of the row (c < NB, interleaved).
 //   NX == 0: write act(rowfac*alpha*acc + b) to out (columns l + 64c).
-//   NX == 1: the next layer (K' = d inputs, 128 < d' <= 256 outputs) is fused:
-//            its sign bits are the four ballots of the output values (word c
-//            = ballot of slot c, because lane l holds element l + 64c), its
-//            scale is their mean magnitude (summed per lane over c, then a
-//            butterfly: the order of the pack kernel), and its products
-//            against the next weights (in LDS) are written as 8-bit
+//   NX == 1: the next layer (K' = d inputs, d' <= 256 outputs, NBN bytes per
+//            lane) is fused: its sign bits are the ballots of the output
+//            values (word c = ballot of slot c, because lane l holds element
+//            l + 64c), its scale is their mean magnitude (summed per lane
+//            over c, then a butterfly: the order of the pack kernel), and its
+//            products against the next weights (in LDS) are written as 8-bit
 //            half-codes with the exact fallback, as k_bgemm_pop_q8 does.
-//   NX == 2: as 1, but the next layer has d' <= 128 outputs; its products are
-//            written exactly (half, natural column order) for the narrow
-//            aggregation kernel.
-// With NX > 0 the output row is also written to out if out != nullptr.
+// With NX == 1 the output row is also written to out if out != nullptr.
 struct NextLayer {
-  const uint64_t* sB;  // LDS: next weights, [kw'][4][64] interleaved columns
+  const uint64_t* sB;  // LDS: next weights, [kw'][NBN][64] interleaved columns
   int32_t dn;          // next layer's output width d'
-  int8_t* C8;          // NX == 1: codes [n][ldc8]
+  int8_t* C8;          // codes [n][ldc8]
   int64_t ldc8;
-  _Float16* C16;       // NX == 1: exact fallback rows; NX == 2: products
+  _Float16* C16;       // exact fallback rows [n][ldc16]
   int64_t ldc16;
   float* g;            // next layer's per-node scale
   int sym;             // fold D̂^-1/2 into the next scale
@@ -908,85 +990,63 @@ struct EpiIL {
   int32_t d;
 };
 
-template <int NX>
+template <int NX, int NB, int NBN>
 __device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4_t acc,
                                   const EpiIL& ep, float* __restrict__ out, int64_t ldo,
                                   const NextLayer& nx, int lane) {
   const float rowfac = deg > 0 ? row_factor_deg(deg, mean) : 0.f;
-  float v[4];
+  float v[NB];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
+  for (int c = 0; c < NB; ++c) {
     const float t = deg > 0 ? fmaf(acc[c], rowfac * ep.alpha[c], ep.bias[c]) : ep.bias[c];
     v[c] = act(t, ep.relu);
   }
   if (NX == 0 || out != nullptr) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c)
+    for (int c = 0; c < NB; ++c)
       if (ep.valid[c]) out[r * ldo + lane + 64 * c] = v[c];
   }
   if (NX == 0) return;
   // Next layer: signs (one ballot per 64 elements = one packed word) and
   // mean magnitude, exactly as the pack kernel forms them.
-  uint64_t word[4];
+  uint64_t word[NB];
   float l1 = 0.f;
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
+  for (int c = 0; c < NB; ++c) {
     word[c] = __builtin_amdgcn_ballot_w64(ep.valid[c] && v[c] >= 0.f);
     l1 += ep.valid[c] ? fabsf(v[c]) : 0.f;
   }
   l1 = wave_sum(l1);
   float sc = l1 / (float)ep.d;
   if (nx.sym) sc = sc * (deg > 0 ? 1.0f / sqrtf((float)deg) : 0.f);
-  const int kwn = (ep.d + 63) >> 6;
+  const int kwn = (ep.d + 63) >> 6;  // <= NB
   const int Kn = ep.d;
-  if (NX == 1) {
-    const int par = Kn & 1;
-    bool big = false;
-    uint32_t packed = 0;
-    int dot[4];
+  const int par = Kn & 1;
+  bool big = false;
+  uint32_t packed = 0;
+  int dot[NBN];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      uint32_t pc = 0;
+  for (int c = 0; c < NBN; ++c) {
+    uint32_t pc = 0;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        if (w >= kwn) break;
-        const uint64_t z = word[w] ^ nx.sB[(w * 4 + c) * 64 + lane];
-        pc += __builtin_popcount((uint32_t)z);
-        pc += __builtin_popcount((uint32_t)(z >> 32));
-      }
-      dot[c] = Kn - 2 * (int)pc;
-      const int code = (dot[c] - par) >> 1;
-      big |= (lane + 64 * c < nx.dn) && (code < -128 || code > 127);
-      packed |= (uint32_t)(uint8_t)(int8_t)code << (8 * c);
+    for (int w = 0; w < NB; ++w) {
+      if (w >= kwn) break;
+      const uint64_t z = word[w] ^ nx.sB[(w * NBN + c) * 64 + lane];
+      pc += __builtin_popcount((uint32_t)z);
+      pc += __builtin_popcount((uint32_t)(z >> 32));
     }
-    *reinterpret_cast<uint32_t*>(nx.C8 + r * nx.ldc8 + 4 * lane) = packed;
-    const bool flag = __builtin_amdgcn_ballot_w64(big) != 0;
-    if (flag) {
-      half4_t h;
-#pragma unroll
-      for (int c = 0; c < 4; ++c) h[c] = (_Float16)dot[c];
-      *reinterpret_cast<half4_t*>(nx.C16 + r * nx.ldc16 + 4 * lane) = h;
-    }
-    if (lane == 0) nx.g[r] = flag ? -sc : sc;
-  } else {
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int k = lane + 64 * c;
-      if (k >= nx.dn) break;
-      uint32_t pc = 0;
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        if (w >= kwn) break;
-        const uint64_t z = word[w] ^ nx.sB[(w * 4 + c) * 64 + lane];
-        pc += __builtin_popcount((uint32_t)z);
-        pc += __builtin_popcount((uint32_t)(z >> 32));
-      }
-      nx.C16[r * nx.ldc16 + k] = (_Float16)(Kn - 2 * (int)pc);
-    }
-    if (lane == 0) nx.g[r] = sc;
+    dot[c] = Kn - 2 * (int)pc;
+    const int code = (dot[c] - par) >> 1;
+    big |= (lane + 64 * c < nx.dn) && (code < -128 || code > 127);
+    packed |= (uint32_t)(uint8_t)(int8_t)code << (8 * c);
   }
+  store_codes<NBN>(nx.C8 + r * nx.ldc8 + NBN * lane, packed);
+  const bool flag = __builtin_amdgcn_ballot_w64(big) != 0;
+  if (flag) store_exact<NBN>(nx.C16 + r * nx.ldc16 + NBN * lane, dot);
+  if (lane == 0) nx.g[r] = flag ? -sc : sc;
 }
 
+template <int NB>
 __device__ inline void make_epi_il(EpiIL& ep, int lane, int32_t d,
                                    const float* __restrict__ alpha,
                                    const float* __restrict__ bias, int relu) {
@@ -995,9 +1055,9 @@ __device__ inline void make_epi_il(EpiIL& ep, int lane, int32_t d,
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     const int k = lane + 64 * c;
-    ep.valid[c] = k < d;
-    ep.alpha[c] = k < d ? alpha[k] : 0.f;
-    ep.bias[c] = (k < d && bias != nullptr) ? bias[k] : 0.f;
+    ep.valid[c] = c < NB && k < d;
+    ep.alpha[c] = ep.valid[c] ? alpha[k] : 0.f;
+    ep.bias[c] = (ep.valid[c] && bias != nullptr) ? bias[k] : 0.f;
   }
 }
 
@@ -1006,10 +1066,10 @@ __device__ inline void make_epi_il(EpiIL& ep, int lane, int32_t d,
 // An edge whose source row is flagged (sign bit of g_j) reads that row's
 // exact products from C16 instead and adds g_j (dot - p) / 2 to the same
 // accumulator, so partial sums and the fix-up are the same as for exact
-// storage.  Lane l accumulates columns l + 64c; partial rows are stored in
-// the same interleaved order.  Structure otherwise as k_spmm_wave; finished
-// rows go through finish_row<NX>.
-template <int U, int NX>
+// storage.  Lane l accumulates columns l + 64c (c < NB); partial rows are
+// stored in the same interleaved order.  Structure otherwise as
+// k_spmm_wave; finished rows go through finish_row<NX, NB, NBN>.
+template <int U, int NX, int NB, int NBN>
 __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
     int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, int mean, const float* __restrict__ g,
@@ -1023,20 +1083,20 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
   static_assert(64 % U == 0, "group size");
   extern __shared__ uint64_t sBn[];
   if (NX > 0) {
-    stage_weights<4, true>(sBn, Bn, nx.dn, ldbn, (d + 63) >> 6, 0);
+    stage_weights<NBN, true>(sBn, Bn, nx.dn, ldbn, (d + 63) >> 6, 0);
     nx.sB = sBn;
   }
   const int lane = threadIdx.x & 63;
   const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
   if (w >= workers) return;
   EpiIL ep;
-  make_epi_il(ep, lane, d, alpha, bias, relu);
+  make_epi_il<NB>(ep, lane, d, alpha, bias, relu);
   const int rb8 = (int)ldc8;
   const int rb16 = (int)(ldc16 * 2);
   const __amdgpu_buffer_rsrc_t rs8 = raw_rsrc(C8, (uint32_t)(n * rb8));
   const __amdgpu_buffer_rsrc_t rs16 = raw_rsrc(C16, (uint32_t)(n * rb16));
-  const int voff8 = 4 * lane;
-  const int voff16 = 8 * lane;
+  const int voff8 = NB * lane;
+  const int voff16 = 2 * NB * lane;
   const float fpar = (float)par;
 
   const int64_t s = w * chunk;
@@ -1063,7 +1123,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
   const float4_t zero4 = {0.f, 0.f, 0.f, 0.f};
   if (!before) {
     for (int64_t q = r - 1; q >= 0 && rowptr[q] == s; --q)
-      finish_row<NX>(q, 0, mean, zero4, ep, out, ldo, nx, lane);
+      finish_row<NX, NB, NBN>(q, 0, mean, zero4, ep, out, ldo, nx, lane);
   }
   float4_t a0 = zero4, a1 = zero4;
   float gsum = 0.f;  // sum of g_j over the current row (for the parity term)
@@ -1083,17 +1143,16 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
         const int j = __builtin_amdgcn_readlane(jA, m + u);
         gg[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
                                               __builtin_bit_cast(int, gA), m + u));
-        vv[u] = __builtin_amdgcn_raw_buffer_load_b32(rs8, voff8,
-                                                     (int)((uint32_t)j * (uint32_t)rb8), 0);
+        vv[u] = gather_codes<NB>(rs8, voff8, (int)((uint32_t)j * (uint32_t)rb8));
       }
       const bool any_flag = ((flagged >> m) & ((1ull << U) - 1)) != 0;
       if (e0 + U <= nE && cur_end >= e0 + U && !any_flag) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           if (u & 1)
-            fma4f(a1, gg[u], codes_to_float(vv[u]));
+            fma_n<NB>(a1, gg[u], codes_to_float<NB>(vv[u]));
           else
-            fma4f(a0, gg[u], codes_to_float(vv[u]));
+            fma_n<NB>(a0, gg[u], codes_to_float<NB>(vv[u]));
           gsum += gg[u];
         }
         continue;
@@ -1105,9 +1164,9 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
         if (eu == cur_end) {
           const float4_t sum = 2.f * (a0 + a1) + fpar * gsum;
           if (before) {
-            *reinterpret_cast<float4_t*>(head + w * dpad + 4 * lane) = sum;
+            store_partial<NB>(head + w * dpad + NB * lane, sum);
           } else {
-            finish_row<NX>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nx, lane);
+            finish_row<NX, NB, NBN>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nx, lane);
           }
           a0 = zero4;
           a1 = zero4;
@@ -1122,7 +1181,8 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
               win_nx = rel(rowptr[rbase + 65 + lane < n ? rbase + 65 + lane : n]);
             }
             cur_end = __builtin_amdgcn_readlane(win, (int)(r - rbase));
-            if (cur_end == eu) finish_row<NX>(r, 0, mean, zero4, ep, out, ldo, nx, lane);
+            if (cur_end == eu)
+              finish_row<NX, NB, NBN>(r, 0, mean, zero4, ep, out, ldo, nx, lane);
           } while (cur_end == eu);
         }
         float gj = gg[u];
@@ -1131,17 +1191,14 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
           // Flagged source row: its exact products, as (dot - p) / 2.
           gj = fabsf(gj);
           const int j = __builtin_amdgcn_readlane(jA, m + u);
-          const half4_t x = Gather<_Float16>::load(
-              rs16, voff16, (int)((uint32_t)j * (uint32_t)rb16));
-#pragma unroll
-          for (int c = 0; c < 4; ++c) v[c] = ((float)x[c] - fpar) * 0.5f;
+          v = gather_exact<NB>(rs16, voff16, (int)((uint32_t)j * (uint32_t)rb16), fpar);
         } else {
-          v = codes_to_float(vv[u]);
+          v = codes_to_float<NB>(vv[u]);
         }
         if (u & 1)
-          fma4f(a1, gj, v);
+          fma_n<NB>(a1, gj, v);
         else
-          fma4f(a0, gj, v);
+          fma_n<NB>(a0, gj, v);
         gsum += gj;
       }
     }
@@ -1154,27 +1211,27 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
   const float4_t sum = 2.f * (a0 + a1) + fpar * gsum;
   if (cur_end == nE) {
     if (before) {
-      *reinterpret_cast<float4_t*>(head + w * dpad + 4 * lane) = sum;
+      store_partial<NB>(head + w * dpad + NB * lane, sum);
     } else {
-      finish_row<NX>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nx, lane);
+      finish_row<NX, NB, NBN>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nx, lane);
     }
     if (t == nnz)
       for (int64_t q = r + 1; q < n; ++q)
-        finish_row<NX>(q, 0, mean, zero4, ep, out, ldo, nx, lane);
+        finish_row<NX, NB, NBN>(q, 0, mean, zero4, ep, out, ldo, nx, lane);
     if (lane == 0) tail_row[w] = -1;
   } else if (before) {
-    *reinterpret_cast<float4_t*>(head + w * dpad + 4 * lane) = sum;
+    store_partial<NB>(head + w * dpad + NB * lane, sum);
     if (lane == 0) tail_row[w] = -1;
   } else {
-    *reinterpret_cast<float4_t*>(tail + w * dpad + 4 * lane) = sum;
+    store_partial<NB>(tail + w * dpad + NB * lane, sum);
     if (lane == 0) tail_row[w] = (int32_t)r;
   }
 }
 
 // Fix-up of the 8-bit path: rows cut by chunk boundaries, partial rows in
-// interleaved order, finished with the same finish_row<NX>.  One wave scans
-// four workers and finishes their cut rows in turn.
-template <int NX>
+// interleaved order, finished with the same finish_row.  One wave scans four
+// workers and finishes their cut rows in turn.
+template <int NX, int NB, int NBN>
 __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
     const int64_t* __restrict__ rowptr, int mean, int32_t d,
     const float* __restrict__ alpha, const float* __restrict__ bias, int relu,
@@ -1184,31 +1241,31 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
     const uint64_t* __restrict__ Bn, int64_t ldbn) {
   extern __shared__ uint64_t sBn[];
   if (NX > 0) {
-    stage_weights<4, true>(sBn, Bn, nx.dn, ldbn, (d + 63) >> 6, 0);
+    stage_weights<NBN, true>(sBn, Bn, nx.dn, ldbn, (d + 63) >> 6, 0);
     nx.sB = sBn;
   }
   const int lane = threadIdx.x & 63;
   const int64_t w0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * 4;
   EpiIL ep;
-  make_epi_il(ep, lane, d, alpha, bias, relu);
+  make_epi_il<NB>(ep, lane, d, alpha, bias, relu);
   for (int q = 0; q < 4; ++q) {
     const int64_t w = w0 + q;
     if (w >= workers) break;
     const int32_t r = tail_row[w];
     if (r < 0) continue;
     const int64_t wend = (rowptr[r + 1] - 1) / chunk;
-    float4_t acc = *reinterpret_cast<const float4_t*>(tail + w * dpad + 4 * lane);
+    float4_t acc = load_partial<NB>(tail + w * dpad + NB * lane);
     int64_t v = w + 1;
     for (; v + 8 <= wend + 1; v += 8) {  // eight loads in flight, added in order
       float4_t h[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        h[u] = *reinterpret_cast<const float4_t*>(head + (v + u) * dpad + 4 * lane);
+      for (int u = 0; u < 8; ++u) h[u] = load_partial<NB>(head + (v + u) * dpad + NB * lane);
 #pragma unroll
       for (int u = 0; u < 8; ++u) acc += h[u];
     }
-    for (; v <= wend; ++v) acc += *reinterpret_cast<const float4_t*>(head + v * dpad + 4 * lane);
-    finish_row<NX>(r, rowptr[r + 1] - rowptr[r], mean, acc, ep, out, ldo, nx, lane);
+    for (; v <= wend; ++v) acc += load_partial<NB>(head + v * dpad + NB * lane);
+    finish_row<NX, NB, NBN>(r, rowptr[r + 1] - rowptr[r], mean, acc, ep, out, ldo, nx,
+                            lane);
   }
 }
 
@@ -1495,7 +1552,10 @@ SpmmPlan spmm_plan(int64_t n, int64_t nnz, int32_t d) {
   p.chunk = chunk;
   p.workers = nnz > 0 ? (nnz + chunk - 1) / chunk : 1;
   const int64_t slab = 4 * spmm_lanes(d);
-  p.dpad = (int32_t)(((d + slab - 1) / slab) * slab);
+  // Wide enough for both partial-row layouts: L lanes x 4 columns (exact
+  // products) and 64 lanes x NB columns (8-bit path).
+  p.dpad = (int32_t)std::max<int64_t>(((d + slab - 1) / slab) * slab,
+                                      64 * q8_lane_bytes(d));
   auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
   size_t off = 0;
   p.off_rowof = off;
@@ -1550,11 +1610,9 @@ hipError_t launch_spmm(int64_t n, int64_t nnz, const int64_t* rowptr,
 }
 
 bool q8_supported(int64_t n, int32_t N, int32_t K) {
-  const int kw = (K + 63) >> 6;
-  if (N <= 128 || N > 256 || K > 2048) return false;
-  if ((size_t)kw * 4 * 64 * 8 > 65536) return false;
-  return (uint64_t)n * 256u <= 0xFFFFFFFFull &&
-         (uint64_t)n * (uint64_t)((N + 7) / 8 * 8) * 2u <= 0xFFFFFFFFull;
+  if (N < 1 || N > 256 || K < 1 || K > 2048) return false;
+  const uint64_t row = 64u * (uint64_t)q8_lane_bytes(N);
+  return (uint64_t)n * row <= 0xFFFFFFFFull && (uint64_t)n * row * 2u <= 0xFFFFFFFFull;
 }
 
 hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
@@ -1563,16 +1621,24 @@ hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
                            float* g, hipStream_t stream) {
   if (M == 0) return hipSuccess;
   constexpr int RM = 4;
+  const int nb = q8_lane_bytes(N);
   const int kw = (K + 63) >> 6;
-  const size_t lds = (size_t)kw * 4 * 64 * sizeof(uint64_t);
+  const size_t lds = (size_t)kw * nb * 64 * sizeof(uint64_t);
   const int64_t tiles = (M + RM - 1) / RM;
   dim3 grid(grid_cap((tiles + kWavesPerBlock - 1) / kWavesPerBlock, 4096));
-  hipLaunchKernelGGL((k_bgemm_pop_q8<RM>), grid, dim3(kBlock), lds, stream, F, M, ldf,
-                     B, N, ldb, K, C8, ldc8, (_Float16*)C16, ldc16, g);
+#define BIGCN_Q8G(NBV)                                                                  \
+  hipLaunchKernelGGL((k_bgemm_pop_q8<RM, NBV>), grid, dim3(kBlock), lds, stream, F, M, \
+                     ldf, B, N, ldb, K, C8, ldc8, (_Float16*)C16, ldc16, g)
+  switch (nb) {
+    case 1: BIGCN_Q8G(1); break;
+    case 2: BIGCN_Q8G(2); break;
+    default: BIGCN_Q8G(4); break;
+  }
+#undef BIGCN_Q8G
   return hipGetLastError();
 }
 
-template <int NX>
+template <int NX, int NB, int NBN>
 hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
                       const int32_t* colidx, int mean, const float* g,
                       const int8_t* C8, int64_t ldc8, const void* C16, int64_t ldc16,
@@ -1593,21 +1659,40 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   nx.ldc16 = fn.ldc16;
   nx.g = fn.g;
   nx.sym = !mean;
-  const size_t lds = NX > 0 ? (size_t)((d + 63) >> 6) * 4 * 64 * sizeof(uint64_t) : 0;
+  const size_t lds = NX > 0 ? (size_t)((d + 63) >> 6) * NBN * 64 * sizeof(uint64_t) : 0;
   dim3 grid((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock));
-  hipLaunchKernelGGL((k_spmm_wave_q8<8, NX>), grid, dim3(kBlock), lds, stream, n, nnz,
-                     rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16, ldc16,
+  hipLaunchKernelGGL((k_spmm_wave_q8<8, NX, NB, NBN>), grid, dim3(kBlock), lds, stream, n,
+                     nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16, ldc16,
                      K & 1, d, alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,
                      row_of, tail_row, head, tail, nx, fn.wbits, fn.ldw);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t fix_waves = (p.workers + 3) / 4;
-  hipLaunchKernelGGL((k_spmm_fix_q8<NX>),
+  hipLaunchKernelGGL((k_spmm_fix_q8<NX, NB, NBN>),
                      dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
                      dim3(kBlock), lds, stream, rowptr, mean, d, alpha, bias, relu, out,
                      ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail, nx, fn.wbits,
                      fn.ldw);
   return hipGetLastError();
+}
+
+template <int NB>
+hipError_t spmm_q8_nb(int64_t n, int64_t nnz, const int64_t* rowptr,
+                      const int32_t* colidx, int mean, const float* g,
+                      const int8_t* C8, int64_t ldc8, const void* C16, int64_t ldc16,
+                      int32_t K, int32_t d, const float* alpha, const float* bias,
+                      int relu, float* out, int64_t ldo, const SpmmPlan& p, void* ws,
+                      const FusedNext& fn, hipStream_t stream) {
+#define BIGCN_Q8S(NX, NBN)                                                               \
+  return spmm_q8_nx<NX, NB, NBN>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, \
+                                 K, d, alpha, bias, relu, out, ldo, p, ws, fn, stream)
+  if (fn.kind == 0) BIGCN_Q8S(0, 1);
+  switch (q8_lane_bytes(fn.d_out)) {
+    case 1: BIGCN_Q8S(1, 1);
+    case 2: BIGCN_Q8S(1, 2);
+    default: BIGCN_Q8S(1, 4);
+  }
+#undef BIGCN_Q8S
 }
 
 hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
@@ -1626,15 +1711,15 @@ hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                        dim3(kBlock), 0, stream, n, d, bias, relu, out, ldo);
     return hipGetLastError();
   }
-  switch (fn.kind) {
+  switch (q8_lane_bytes(d)) {
     case 1:
-      return spmm_q8_nx<1>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
+      return spmm_q8_nb<1>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
                            alpha, bias, relu, out, ldo, p, ws, fn, stream);
     case 2:
-      return spmm_q8_nx<2>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
+      return spmm_q8_nb<2>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
                            alpha, bias, relu, out, ldo, p, ws, fn, stream);
     default:
-      return spmm_q8_nx<0>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
+      return spmm_q8_nb<4>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
                            alpha, bias, relu, out, ldo, p, ws, fn, stream);
   }
 }

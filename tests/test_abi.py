@@ -145,3 +145,63 @@ def test_forward_workspace_fits_the_workloads(cfg):
     hidden = max(dims[1:-1]) if len(dims) > 2 else 0
     assert ws >= n * 2 * max(dims[1:])           # the product matrix alone
     assert ws <= n * (8 * 64 + 2 * 4 * hidden + 4 * 256 + 64) + 8 * nnz + (64 << 20)
+
+
+def test_bgemm_q8_validation():
+    lib = bg.load()
+    f = lib.bigcn_bgemm_q8
+    #          F     M  ldf  B    N  ldb K    C8    ldc8 C16   ldc16 g
+    ok = [FAKE, 10, 1, FAKE, 50, 1, 64, FAKE, 64, FAKE, 64, FAKE, None]
+    for pos, val, want in [(8, 60, EINVAL),            # ldc8 < 64 (row of 50 columns)
+                           (8, 66, EINVAL),            # ldc8 not a multiple of 4
+                           (10, 32, EINVAL),           # ldc16 < 64
+                           (4, 0, EINVAL), (6, 0, EINVAL), (2, 0, EINVAL),
+                           (7, FAKE + 2, EALIGN), (9, FAKE + 4, EALIGN),
+                           (4, 300, EINVAL),           # 300 columns need 256-wide rows ...
+                           (6, 3000, EINVAL)]:         # ... and ldf >= 47
+        args = list(ok)
+        args[pos] = val
+        assert f(*args) == want, (pos, val)
+    wide = list(ok)
+    wide[4], wide[8], wide[10] = 300, 256, 256
+    assert f(*wide) == EUNSUPPORTED                     # more than 256 columns
+    longk = list(ok)
+    longk[2], longk[5], longk[6] = 47, 47, 3000
+    assert f(*longk) == EUNSUPPORTED                    # K > 2048
+    # the row width follows the column count: 65 columns need 128-wide rows
+    mid = list(ok)
+    mid[4] = 65
+    assert f(*mid) == EINVAL
+
+
+def test_spmm_csr_q8_validation():
+    lib = bg.load()
+    f = lib.bigcn_spmm_csr_q8
+    # n nnz rowptr colidx norm g C8 ldc8 C16 ldc16 K d alpha bias act out ldo ws bytes stream
+    ok = [10, 40, FAKE, FAKE, 0, FAKE, FAKE, 64, FAKE, 64, 100, 7, FAKE, None, 0, FAKE, 7,
+          FAKE, 1 << 20, None]
+    for pos, val, want in [(7, 32, EINVAL), (9, 60, EINVAL), (10, 0, EINVAL),
+                           (11, 0, EINVAL), (6, FAKE + 2, EALIGN)]:
+        args = list(ok)
+        args[pos] = val
+        assert f(*args) == want, (pos, val)
+    big = list(ok)
+    big[7], big[9], big[11], big[16] = 256, 260, 257, 257
+    assert f(*big) == EUNSUPPORTED
+    small_ws = list(ok)
+    small_ws[18] = 16
+    assert f(*small_ws) == EWORKSPACE
+
+
+def test_q8_layout_helpers():
+    """Rows of 64 NB entries; column k at NB (k % 64) + k // 64, a bijection
+    onto the first d... positions of the row for every width."""
+    for d in (1, 3, 63, 64, 65, 100, 128, 129, 200, 256):
+        nb = bg.q8_lane_bytes(d)
+        assert bg.q8_row(d) == 64 * nb and 64 * (nb // 2) < d <= 64 * nb
+        pos = [bg.q8_position(k, d) for k in range(d)]
+        assert len(set(pos)) == d and max(pos) < bg.q8_row(d)
+        assert all(p // nb == k % 64 for k, p in enumerate(pos))    # lane k % 64
+    assert [bg.q8_position(k, 64) for k in range(64)] == list(range(64))
+    assert bg.q8_supported(100, 256, 2048) and not bg.q8_supported(100, 257, 64)
+    assert not bg.q8_supported(100, 64, 2049) and bg.q8_supported(100, 1, 1)

@@ -229,8 +229,8 @@ def test_spmm_is_bitwise_reproducible(dev):
 def gpu_layer(dev, g, norm, h, wt, bias, act="none", mu=None, rstd=None,
               rowptr_t=None, colidx_t=None, ht=None):
     """pack -> bgemm -> spmm through the entry points, with the product
-    storage the forward pass picks for this shape (8-bit half-codes for
-    129..256 output columns, else exact 16-bit)."""
+    storage the forward pass picks for this shape (8-bit half-codes for up
+    to 256 output columns with K <= 2048, else exact 16-bit)."""
     n, K = h.shape if ht is None else ht.shape
     d = wt.shape[0]
     rowptr_t = _t(g.rowptr, dev) if rowptr_t is None else rowptr_t
@@ -248,7 +248,8 @@ def gpu_layer(dev, g, norm, h, wt, bias, act="none", mu=None, rstd=None,
     ws = torch.empty(bg.spmm_workspace_bytes(n, g.nnz, d), dtype=torch.uint8, device=dev)
     b = None if bias is None else _t(bias, dev)
     if bg.q8_supported(n, d, K):
-        C8 = torch.empty((n, 256), dtype=torch.int8, device=dev)
+        C8 = torch.empty((n, bg.q8_row(d)), dtype=torch.int8, device=dev)
+        C = torch.empty((n, bg.q8_row(d)), dtype=torch.float16, device=dev)
         bg.bigcn_bgemm_q8(F, wbits, K, C8, C, gs)
         bg.bigcn_spmm_csr_q8(rowptr_t, colidx_t, gs, C8, C, K, alpha, out, ws, b, norm,
                              act, d=d)
@@ -259,9 +260,8 @@ def gpu_layer(dev, g, norm, h, wt, bias, act="none", mu=None, rstd=None,
 
 
 def il_pos(d):
-    """Position of column k in a lane-interleaved 256-wide row."""
-    k = np.arange(d)
-    return 4 * (k % 64) + k // 64
+    """Positions of columns 0..d-1 in a row of the 8-bit layout."""
+    return np.array([bg.q8_position(k, d) for k in range(d)], dtype=np.int64)
 
 
 def decode_products(prod, K, d):
@@ -308,7 +308,9 @@ def test_layer_matches_oracle(dev, K, d, norm):
 
 Q8_SHAPES = [(1, 129, 64), (77, 200, 100), (1000, 256, 127), (513, 256, 128),
              (333, 256, 255), (400, 256, 256), (257, 130, 300), (300, 256, 602),
-             (64, 256, 1433), (65, 256, 2048)]
+             (64, 256, 1433), (65, 256, 2048),
+             (1, 1, 1), (50, 3, 64), (100, 7, 130), (257, 40, 256), (300, 64, 500),
+             (129, 65, 99), (200, 128, 1433), (70, 47, 2048), (999, 64, 255)]
 
 
 @pytest.mark.parametrize("M,N,K", Q8_SHAPES)
@@ -324,8 +326,9 @@ def test_bgemm_q8_matches_oracle(dev, M, N, K):
     gsc = rng.uniform(0.0, 2.0, M).astype(np.float32)
     gsc[::5] = 0.0
     Ft, Bt = _t(F.view(np.int64), dev), _t(B.view(np.int64), dev)
-    C8 = torch.full((M, 256 + 4), 99, dtype=torch.int8, device=dev)
-    C16 = torch.zeros((M, 256), dtype=torch.float16, device=dev)
+    W = bg.q8_row(N)
+    C8 = torch.full((M, W + 4), 99, dtype=torch.int8, device=dev)
+    C16 = torch.zeros((M, W), dtype=torch.float16, device=dev)
     gt = _t(gsc, dev)
     bg.bigcn_bgemm_q8(Ft, Bt, K, C8, C16, gt)
     torch.cuda.synchronize()
@@ -340,7 +343,10 @@ def test_bgemm_q8_matches_oracle(dev, M, N, K):
 
 @pytest.mark.parametrize("d,K,norm,act", [(129, 64, "sym", "none"), (200, 255, "mean", "relu"),
                                           (256, 256, "sym", "none"), (256, 602, "mean", "none"),
-                                          (256, 1433, "sym", "relu")])
+                                          (256, 1433, "sym", "relu"), (1, 5, "sym", "none"),
+                                          (3, 64, "sym", "none"), (7, 1433, "mean", "relu"),
+                                          (40, 256, "sym", "none"), (64, 500, "mean", "none"),
+                                          (65, 301, "sym", "relu"), (128, 256, "sym", "none")])
 def test_spmm_q8_matches_oracle(dev, d, K, norm, act):
     rng = np.random.default_rng(d + K)
     g = _star_plus_random(900, rng)
@@ -361,10 +367,11 @@ def test_spmm_q8_matches_oracle(dev, d, K, norm, act):
     gg[flag] = -np.abs(gg[flag])               # sign bit marks the exact rows
     codes = np.clip((dot - par) // 2, -128, 127).astype(np.int8)
     pos = il_pos(d)
-    c8 = np.zeros((g.n, 256), dtype=np.int8)
+    W = bg.q8_row(d)
+    c8 = np.zeros((g.n, W), dtype=np.int8)
     c8[:, pos] = codes
     C8 = _t(c8, dev)
-    c16 = np.zeros((g.n, 256), dtype=np.float16)
+    c16 = np.zeros((g.n, W), dtype=np.float16)
     c16[:, pos] = np.where(flag[:, None], dot, 0).astype(np.float16)
     C16 = _t(c16, dev)
     out = torch.full((g.n, d), float("nan"), dtype=torch.float32, device=dev)
