@@ -50,6 +50,7 @@ VALU_BITOP_PEAK = 256 * 4 * 16 * 2.4e9 * 16
 # Dense int8 MFMA: 5.0 P ops/s = 2.5 P multiply-adds/s, one sign product each.
 MFMA_I8_BITOP_PEAK = 2.5e15
 METRIC = "nodes/sec full Bi-GCN forward; bGEMM bit-ops/s; SpMM/pack HBM GB/s vs peak"
+COPY_BYTES = 256 << 20   # calibration copy of the byte counters
 
 
 def log(msg):
@@ -131,6 +132,79 @@ def bgemm_ab(shapes, reps, torch, bg, dev):
     return out
 
 
+def measured_traffic(workload_name, layer, entry):
+    """HBM bytes (read + written) of one entry-point call, from the committed
+    counter summary profiles/hbm_traffic_<workload>.md, or None when there is
+    none or the kernel / launch sources changed since it was taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.md" % workload_name)
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
+    if m is None:
+        return None
+    rec = json.loads(m.group(1))
+    h = hashlib.sha256()
+    for src in ("bigcn_kernels.hip", "bigcn_api.hip"):
+        with open(os.path.join(ROOT, "paper_2010_07565_amd", "csrc", src), "rb") as f:
+            h.update(f.read())
+    if rec.get("sources_sha256") != h.hexdigest():
+        return None
+    for e in rec["entries"]:
+        if e["layer"] == layer and e["entry"] == entry:
+            return e["fetch_bytes"] + e["write_bytes"]
+    return None
+
+
+def traffic_probe(w, model, x, rowptr, colidx, torch, bg, dev):
+    """One eager call of every per-layer entry point, in the order the
+    kernel table times them, then one 256 MiB device copy of known size."""
+    g = w.graph
+    kwmax = max(words(wt.shape[1]) for wt in w.weights_t)
+    ldF = (kwmax + 1) // 2 * 2
+    F = torch.empty((g.n, ldF), dtype=torch.int64, device=dev)
+    gs = torch.empty(g.n, dtype=torch.float32, device=dev)
+    ldc = max(256, (max(wt.shape[0] for wt in w.weights_t) + 7) // 8 * 8)
+    C = torch.empty((g.n, ldc), dtype=torch.float16, device=dev)
+    C8 = torch.empty((g.n, 256), dtype=torch.int8, device=dev)
+    ws = torch.empty(max(bg.spmm_workspace_bytes(g.n, g.nnz, wt.shape[0])
+                         for wt in w.weights_t), dtype=torch.uint8, device=dev)
+    mu_t = torch.from_numpy(w.mu).to(dev)
+    rstd_t = torch.from_numpy(w.rstd).to(dev)
+    h = x
+    for l, ly in enumerate(model.layers):
+        K, d = ly.d_in, ly.d_out
+        kw = words(K)
+        out = torch.empty((g.n, d), dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
+        log("probe layer %d: pack" % l)
+        bg.bigcn_binarize_pack(h, F[:, :kw], gs, mu_t if l == 0 else None,
+                               rstd_t if l == 0 else None, rowptr, w.norm)
+        if bg.q8_supported(g.n, d, K):
+            W = bg.q8_row(d)
+            c8 = C8.view(-1)[:g.n * W].view(g.n, W)
+            c16 = C.view(-1)[:g.n * W].view(g.n, W)
+            log("probe layer %d: bgemm_q8, spmm_q8" % l)
+            bg.bigcn_bgemm_q8(F[:, :kw], ly.wbits, K, c8, c16, gs)
+            bg.bigcn_spmm_csr_q8(rowptr, colidx, gs, c8, c16, K, ly.alpha, out, ws,
+                                 ly.bias, w.norm, ly.act, d=d)
+        else:
+            log("probe layer %d: bgemm, spmm" % l)
+            bg.bigcn_bgemm(F[:, :kw], ly.wbits, K, C[:, :d])
+            bg.bigcn_spmm_csr(rowptr, colidx, gs, C, ly.alpha, out, ws, ly.bias, w.norm,
+                              ly.act, d=d)
+        h = out
+    torch.cuda.synchronize()
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    log("probe: copy of %d bytes" % COPY_BYTES)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"traffic_probe": w.name, "copy_bytes": COPY_BYTES}), flush=True)
+
+
 def cpu_baseline(w, budget_s=10.0):
     """The oracle on this host: the whole forward pass for small graphs, else
     the dependency cones of a random set of output rows."""
@@ -195,6 +269,10 @@ def main():
     ap.add_argument("--forward-only", action="store_true",
                     help="time the forward pass only (no per-kernel table, no "
                          "algorithm comparison, no CPU baseline): for profiling")
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="call each entry point of the workload once, eagerly, then "
+                         "copy 256 MiB device to device (the counter calibration "
+                         "kernel): the program profiled for HBM byte counters")
     ap.add_argument("--bgemm-ab", action="store_true",
                     help="only compare the two binary-GEMM algorithms on every "
                          "workload's layer shapes")
@@ -236,6 +314,9 @@ def main():
     model = bg.BiGCN(rowptr, colidx, w.weights_t, w.biases, norm=w.norm, mu=w.mu,
                      rstd=w.rstd, device=dev)
     torch.cuda.synchronize()
+    if args.traffic_probe:
+        traffic_probe(w, model, x, rowptr, colidx, torch, bg, dev)
+        return
 
     # ---- the timed forward passes: eager calls, then the same pass replayed
     # from a HIP graph (the serving loop); the graph's output is checked
@@ -321,7 +402,7 @@ def main():
                  work=s["pack_bytes"]),
             dict(kernel="bgemm_q8" if q8 else "bgemm", layer=l, us=t_gemm * 1e6, bound="alu",
                  achieved=s["gemm_ops"] / t_gemm / 1e12, unit="Tbitop/s",
-                 peak=VALU_BITOP_PEAK / 1e12, work=s["gemm_ops"],
+                 peak=VALU_BITOP_PEAK / 1e12, work=s["gemm_ops"], bytes=s["gemm_bytes"],
                  hbm_gbs=s["gemm_bytes"] / t_gemm / 1e9),
             dict(kernel="spmm_q8" if q8 else "spmm", layer=l, us=t_spmm * 1e6, bound="hbm",
                  achieved=s["spmm_bytes"] / t_spmm / 1e9, unit="GB/s", peak=HBM_PEAK_GBS,
@@ -333,9 +414,14 @@ def main():
         log("  L%d %-5s %9.2f us  %8.1f %s  (%.1f%% of peak)" % (
             k["layer"], k["kernel"], k["us"], k["achieved"], k["unit"], 100 * k["frac"]))
     dom = max(kernels, key=lambda k: k["us"])
+    entry = dom["kernel"].split("_")[0]                  # pack / bgemm / spmm
+    traffic = measured_traffic(w.name, dom["layer"], entry)
     roofline = dict(kernel="%s (layer %d)" % (dom["kernel"], dom["layer"]), bound=dom["bound"],
                     achieved=round(dom["achieved"], 2), peak=dom["peak"], unit=dom["unit"],
-                    frac=round(dom["frac"], 4), traffic=None, avg_us=round(dom["us"], 3))
+                    frac=round(dom["frac"], 4), traffic=traffic,
+                    traffic_unit="bytes per call (HBM read + written)",
+                    algorithmic_bytes=dom["work"] if dom["bound"] == "hbm" else dom.get("bytes"),
+                    avg_us=round(dom["us"], 3))
 
     ab = bgemm_ab([(g.n, ly.d_out, ly.d_in) for ly in model.layers], reps, torch, bg, dev)
     assert all(r["equal"] for r in ab), "binary-GEMM algorithms disagree"

@@ -273,8 +273,6 @@ bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
     if (!aligned(workspace, 256)) return BIGCN_EALIGN;
   }
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = bigcn::launch_spmm_rows(n, nnz, rowptr, plan, workspace, s);
-  if (e != hipSuccess) return BIGCN_EHIP;
   return hip_status(bigcn::launch_spmm_q8(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN,
                                           g, C8, ldc8, C16, ldc16, K, d, alpha, bias,
                                           act == BIGCN_ACT_RELU, out, ldo, plan,
@@ -327,11 +325,18 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
   float* H[2] = {(float*)(ws + L.off_H0), (float*)(ws + L.off_H1)};
   void* wsp = ws + L.off_spmm;
 
-  // Per-worker start rows depend only on the graph and the chunk size, which
-  // is the same for every layer.
-  const bigcn::SpmmPlan plan0 = bigcn::spmm_plan(n, nnz, L.dmax);
-  hipError_t e = bigcn::launch_spmm_rows(n, nnz, rowptr, plan0, wsp, s);
-  if (e != hipSuccess) return BIGCN_EHIP;
+  // The exact-product aggregation needs per-worker start rows; they depend
+  // only on the graph and the chunk size (the same for every layer).  The
+  // 8-bit aggregation finds its rows itself.
+  hipError_t e = hipSuccess;
+  bool need_rows = false;
+  for (int32_t l = 0; l < n_layers; ++l)
+    need_rows |= !bigcn::q8_supported(n, layers[l].d_out, layers[l].d_in);
+  if (need_rows) {
+    const bigcn::SpmmPlan plan0 = bigcn::spmm_plan(n, nnz, L.dmax);
+    e = bigcn::launch_spmm_rows(n, nnz, rowptr, plan0, wsp, s);
+    if (e != hipSuccess) return BIGCN_EHIP;
+  }
 
   const float* hin = x;
   int64_t ldin = ldx;

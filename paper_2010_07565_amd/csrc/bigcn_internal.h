@@ -88,7 +88,8 @@ hipError_t launch_spmm(int64_t n, int64_t nnz, const int64_t* rowptr,
                        float* out, int64_t ldo, const SpmmPlan& plan,
                        void* workspace, hipStream_t stream);
 
-// Aggregation reading 8-bit half-codes (see launch_bgemm_q8); with a
+// Aggregation reading 8-bit half-codes (see launch_bgemm_q8; needs no row
+// plan: launch_spmm_rows is not required); with a
 // FusedNext of kind > 0 the output rows feed the next layer instead of (or,
 // if out != nullptr, besides) being written.
 hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,

@@ -36,11 +36,27 @@ __device__ inline int wave_index_in_block() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 }
 
+// DPP lane exchange within rows of 16 lanes (quad_perm, row_mirror and
+// row_half_mirror controls of gfx9 DPP).
+template <int CTRL>
+__device__ inline float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                       0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
 __device__ inline float wave_sum(float v) {
-  // Butterfly: every lane ends with the same, order-fixed sum.
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
+  // Order-fixed sum, the same in every lane: pairs (xor 1, xor 2), then the
+  // mirrored half rows and rows of 16 lanes, then the four rows' sums read
+  // out and added as (r0 + r1) + (r2 + r3).
+  v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp<0x141>(v);  // row_half_mirror
+  v += dpp<0x140>(v);  // row_mirror
+  const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float c = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float d = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return (a + b) + (c + d);
 }
 
 // ---------------------------------------------------------------- pack ----
@@ -165,9 +181,7 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
       }
     }
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1)
-#pragma unroll
-      for (int q = 0; q < RW; ++q) l1[q] += __shfl_xor(l1[q], off, 64);
+    for (int q = 0; q < RW; ++q) l1[q] = wave_sum(l1[q]);
 #pragma unroll
     for (int q = 0; q < RW; ++q) {
       const int64_t r = r0 + q;
@@ -974,6 +988,8 @@ __device__ inline float4_t load_partial(const float* p) {
 // With NX == 1 the output row is also written to out if out != nullptr.
 struct NextLayer {
   const uint64_t* sB;  // LDS: next weights, [kw'][NBN][64] interleaved columns
+  uint64_t wr[4];      // or, when NB * NBN <= 4, this lane's words in registers:
+                       // wr[w * NBN + c] = word w of column lane + 64c
   int32_t dn;          // next layer's output width d'
   int8_t* C8;          // codes [n][ldc8]
   int64_t ldc8;
@@ -1031,7 +1047,9 @@ __device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4
 #pragma unroll
     for (int w = 0; w < NB; ++w) {
       if (w >= kwn) break;
-      const uint64_t z = word[w] ^ nx.sB[(w * NBN + c) * 64 + lane];
+      const uint64_t bw = NB * NBN <= 4 ? nx.wr[(w * NBN + c) & 3]
+                                        : nx.sB[(w * NBN + c) * 64 + lane];
+      const uint64_t z = word[w] ^ bw;
       pc += __builtin_popcount((uint32_t)z);
       pc += __builtin_popcount((uint32_t)(z >> 32));
     }
@@ -1061,6 +1079,62 @@ __device__ inline void make_epi_il(EpiIL& ep, int lane, int32_t d,
   }
 }
 
+// The next layer's weights for finish_row: in registers when a lane needs
+// at most four words (NB * NBN <= 4; no LDS, no block barrier), else staged
+// in LDS by the whole block (stage_weights, which ends in a barrier).
+template <int NB, int NBN>
+__device__ inline void load_next_weights(NextLayer& nx, uint64_t* sBn,
+                                         const uint64_t* __restrict__ Bn, int64_t ldbn,
+                                         int32_t d, int lane) {
+  const int kwn = (d + 63) >> 6;
+  if constexpr (NB * NBN <= 4) {
+#pragma unroll
+    for (int w = 0; w < NB; ++w)
+#pragma unroll
+      for (int c = 0; c < NBN; ++c) {
+        const int col = lane + 64 * c;
+        nx.wr[(w * NBN + c) & 3] =
+            (w < kwn && col < nx.dn) ? Bn[(int64_t)col * ldbn + w] : 0ull;
+      }
+    nx.sB = nullptr;
+  } else {
+    stage_weights<NBN, true>(sBn, Bn, nx.dn, ldbn, kwn, 0);
+    nx.sB = sBn;
+  }
+}
+
+// The row holding edge s, rowptr[r] <= s < rowptr[r+1] (rows without
+// entries are skipped), by a wave-wide search: each step the 64 lanes probe
+// 64 evenly spaced row starts of the current range [lo, hi), which shrinks
+// 65-fold; once it is at most 64 rows wide, lane l loads the start and end
+// of row lo + l.  Returns r; lo, and this lane's start / end, are the window
+// the aggregation walks from.  Requires rowptr[0] <= s < rowptr[n].
+__device__ inline int64_t find_row(const int64_t* __restrict__ rowptr, int64_t n, int64_t s,
+                                   int lane, int64_t& lo_out, int64_t& start_l,
+                                   int64_t& end_l) {
+  int64_t lo = 0, hi = n;
+  while (hi - lo > 64) {
+    const int64_t step = (hi - lo + 64) / 65;
+    const int64_t p = lo + (int64_t)(lane + 1) * step;
+    const bool le = p < hi && rowptr[p] <= s;
+    const int c = (int)__builtin_popcountll(__builtin_amdgcn_ballot_w64(le));
+    const int64_t nhi = lo + (int64_t)(c + 1) * step;
+    lo += (int64_t)c * step;
+    if (nhi < hi) hi = nhi;
+  }
+  start_l = rowptr[lo + lane < n ? lo + lane : n];
+  end_l = rowptr[lo + 1 + lane < n ? lo + 1 + lane : n];
+  lo_out = lo;
+  const uint64_t done = __builtin_amdgcn_ballot_w64(lo + 1 + lane <= n && end_l <= s);
+  return lo + (int64_t)__builtin_popcountll(done);
+}
+
+__device__ inline int64_t readlane64(int64_t v, int l) {
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), l);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 // Whole-wave aggregation over 8-bit half-codes (see k_bgemm_pop_q8):
 //   sum_j g_j dot_jk = 2 * sum_j g_j code_jk + p * sum_j g_j.
 // An edge whose source row is flagged (sign bit of g_j) reads that row's
@@ -1068,7 +1142,9 @@ __device__ inline void make_epi_il(EpiIL& ep, int lane, int32_t d,
 // accumulator, so partial sums and the fix-up are the same as for exact
 // storage.  Lane l accumulates columns l + 64c (c < NB); partial rows are
 // stored in the same interleaved order.  Structure otherwise as
-// k_spmm_wave; finished rows go through finish_row<NX, NB, NBN>.
+// k_spmm_wave, except that each wave finds its first row itself
+// (find_row: no row plan is needed); finished rows go through
+// finish_row<NX, NB, NBN>.
 template <int U, int NX, int NB, int NBN>
 __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
     int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
@@ -1077,18 +1153,26 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
     int64_t ldc16, int par, int32_t d, const float* __restrict__ alpha,
     const float* __restrict__ bias, int relu, float* __restrict__ out,
     int64_t ldo, int64_t chunk, int64_t workers, int32_t dpad,
-    const int32_t* __restrict__ row_of, int32_t* __restrict__ tail_row,
-    float* __restrict__ head, float* __restrict__ tail, NextLayer nx,
-    const uint64_t* __restrict__ Bn, int64_t ldbn) {
+    int32_t* __restrict__ tail_row, float* __restrict__ head,
+    float* __restrict__ tail, NextLayer nx, const uint64_t* __restrict__ Bn,
+    int64_t ldbn) {
   static_assert(64 % U == 0, "group size");
   extern __shared__ uint64_t sBn[];
-  if (NX > 0) {
-    stage_weights<NBN, true>(sBn, Bn, nx.dn, ldbn, (d + 63) >> 6, 0);
-    nx.sB = sBn;
-  }
   const int lane = threadIdx.x & 63;
-  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
-  if (w >= workers) return;
+  const int64_t wv = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
+  const bool live = wv < workers;
+  const int64_t w = live ? wv : workers - 1;  // waves past the end only stage
+  const int64_t s = w * chunk;
+  const int nE = (int)((s + chunk < nnz ? s + chunk : nnz) - s);
+  const int64_t t = s + nE;
+  auto ld_idx = [&](int eb) -> int32_t {
+    const int x = eb + lane;
+    return colidx[s + (x < nE ? x : nE - 1)];
+  };
+  int32_t jA = ld_idx(0);  // issued first: independent of everything else
+  int32_t jB = ld_idx(64);
+  if (NX > 0) load_next_weights<NB, NBN>(nx, sBn, Bn, ldbn, d, lane);
+  if (!live) return;
   EpiIL ep;
   make_epi_il<NB>(ep, lane, d, alpha, bias, relu);
   const int rb8 = (int)ldc8;
@@ -1099,27 +1183,19 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
   const int voff16 = 2 * NB * lane;
   const float fpar = (float)par;
 
-  const int64_t s = w * chunk;
-  const int nE = (int)((s + chunk < nnz ? s + chunk : nnz) - s);
-  const int64_t t = s + nE;
   auto rel = [&](int64_t v) -> int {
     const int64_t x = v - s;
     return (int)(x < -1 ? -1 : (x > chunk + 1 ? chunk + 1 : x));
   };
-  auto ld_idx = [&](int eb) -> int32_t {
-    const int x = eb + lane;
-    return colidx[s + (x < nE ? x : nE - 1)];
-  };
-  int32_t jA = ld_idx(0);  // issued before the row lookups
-  int32_t jB = ld_idx(64);
-  int64_t r = row_of[w];
-  int64_t rbase = r;
-  int win = rel(rowptr[rbase + 1 + lane < n ? rbase + 1 + lane : n]);
+  float gA = g[jA];
+  int64_t rbase, start_l, end_l;
+  int64_t r = find_row(rowptr, n, s, lane, rbase, start_l, end_l);
+  int win = rel(end_l);
   int win_nx = rel(rowptr[rbase + 65 + lane < n ? rbase + 65 + lane : n]);
-  const int64_t beg0 = rowptr[r];
+  const int64_t beg0 = readlane64(start_l, (int)(r - rbase));
   bool before = beg0 < s;
   int cur_beg = rel(beg0);
-  int cur_end = __builtin_amdgcn_readlane(win, 0);
+  int cur_end = __builtin_amdgcn_readlane(win, (int)(r - rbase));
   const float4_t zero4 = {0.f, 0.f, 0.f, 0.f};
   if (!before) {
     for (int64_t q = r - 1; q >= 0 && rowptr[q] == s; --q)
@@ -1127,10 +1203,8 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
   }
   float4_t a0 = zero4, a1 = zero4;
   float gsum = 0.f;  // sum of g_j over the current row (for the parity term)
-  float gA = g[jA];
   float gB = g[jB];
   int32_t jCn = ld_idx(128);
-
   for (int eb = 0; eb < nE; eb += 64) {
     const uint64_t flagged = __builtin_amdgcn_ballot_w64(__builtin_bit_cast(int, gA) < 0);
     for (int m = 0; m < 64; m += U) {
@@ -1229,8 +1303,10 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
 }
 
 // Fix-up of the 8-bit path: rows cut by chunk boundaries, partial rows in
-// interleaved order, finished with the same finish_row.  One wave scans four
-// workers and finishes their cut rows in turn.
+// interleaved order, finished with the same finish_row.  One wave serves
+// four workers: their cut rows, row bounds and first two partial rows are
+// loaded together (lanes 0..3 fetch the per-worker scalars), then the rows
+// are finished in worker order.
 template <int NX, int NB, int NBN>
 __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
     const int64_t* __restrict__ rowptr, int mean, int32_t d,
@@ -1240,32 +1316,45 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
     const float* __restrict__ head, const float* __restrict__ tail, NextLayer nx,
     const uint64_t* __restrict__ Bn, int64_t ldbn) {
   extern __shared__ uint64_t sBn[];
-  if (NX > 0) {
-    stage_weights<NBN, true>(sBn, Bn, nx.dn, ldbn, (d + 63) >> 6, 0);
-    nx.sB = sBn;
-  }
   const int lane = threadIdx.x & 63;
+  if (NX > 0) load_next_weights<NB, NBN>(nx, sBn, Bn, ldbn, d, lane);
   const int64_t w0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * 4;
+  if (w0 >= workers) return;
   EpiIL ep;
   make_epi_il<NB>(ep, lane, d, alpha, bias, relu);
+  // lane q < 4: worker w0 + q's cut row and that row's bounds
+  const int64_t wq = w0 + (lane & 3);
+  const int32_t rq = wq < workers ? tail_row[wq] : -1;
+  const int64_t bq = rq >= 0 ? rowptr[rq] : 0;
+  const int64_t eq = rq >= 0 ? rowptr[rq + 1] : 0;
+  float4_t acc[4], nxt[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {  // tail of the worker and the next head
+    const int32_t r = __builtin_amdgcn_readlane(rq, q);
+    if (r >= 0) {
+      const int64_t w = w0 + q;
+      acc[q] = load_partial<NB>(tail + w * dpad + NB * lane);
+      nxt[q] = load_partial<NB>(head + (w + 1) * dpad + NB * lane);
+    }
+  }
+#pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int64_t w = w0 + q;
-    if (w >= workers) break;
-    const int32_t r = tail_row[w];
+    const int32_t r = __builtin_amdgcn_readlane(rq, q);
     if (r < 0) continue;
-    const int64_t wend = (rowptr[r + 1] - 1) / chunk;
-    float4_t acc = load_partial<NB>(tail + w * dpad + NB * lane);
-    int64_t v = w + 1;
+    const int64_t w = w0 + q;
+    const int64_t e = readlane64(eq, q);
+    const int64_t wend = (e - 1) / chunk;  // > w: a cut row continues past w
+    float4_t a = acc[q] + nxt[q];
+    int64_t v = w + 2;
     for (; v + 8 <= wend + 1; v += 8) {  // eight loads in flight, added in order
       float4_t h[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) h[u] = load_partial<NB>(head + (v + u) * dpad + NB * lane);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) acc += h[u];
+      for (int u = 0; u < 8; ++u) a += h[u];
     }
-    for (; v <= wend; ++v) acc += load_partial<NB>(head + v * dpad + NB * lane);
-    finish_row<NX, NB, NBN>(r, rowptr[r + 1] - rowptr[r], mean, acc, ep, out, ldo, nx,
-                            lane);
+    for (; v <= wend; ++v) a += load_partial<NB>(head + v * dpad + NB * lane);
+    finish_row<NX, NB, NBN>(r, e - readlane64(bq, q), mean, a, ep, out, ldo, nx, lane);
   }
 }
 
@@ -1646,7 +1735,6 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
                       int relu, float* out, int64_t ldo, const SpmmPlan& p, void* ws,
                       const FusedNext& fn, hipStream_t stream) {
   char* base = (char*)ws;
-  const int32_t* row_of = (const int32_t*)(base + p.off_rowof);
   int32_t* tail_row = (int32_t*)(base + p.off_tailrow);
   float* head = (float*)(base + p.off_head);
   float* tail = (float*)(base + p.off_tail);
@@ -1659,12 +1747,13 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   nx.ldc16 = fn.ldc16;
   nx.g = fn.g;
   nx.sym = !mean;
-  const size_t lds = NX > 0 ? (size_t)((d + 63) >> 6) * NBN * 64 * sizeof(uint64_t) : 0;
+  const size_t lds = (NX > 0 && NB * NBN > 4)
+                         ? (size_t)((d + 63) >> 6) * NBN * 64 * sizeof(uint64_t) : 0;
   dim3 grid((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock));
   hipLaunchKernelGGL((k_spmm_wave_q8<8, NX, NB, NBN>), grid, dim3(kBlock), lds, stream, n,
                      nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16, ldc16,
                      K & 1, d, alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,
-                     row_of, tail_row, head, tail, nx, fn.wbits, fn.ldw);
+                     tail_row, head, tail, nx, fn.wbits, fn.ldw);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t fix_waves = (p.workers + 3) / 4;
