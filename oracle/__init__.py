@@ -58,6 +58,10 @@ def _load():
         lib.oracle_layer.argtypes = [_i64, _p, _p, _int, _p, _i64, _i32, _p,
                                      _p, _p, _i32, _p, _int, _p, _i64, _p, _p,
                                      _p, _p]
+        lib.oracle_sage_layer.restype = _int
+        lib.oracle_sage_layer.argtypes = [_i64, _p, _p, _p, _i64, _i32, _p, _p, _p,
+                                          _p, _i32, _p, _int, _p, _i64, _p, _p, _p,
+                                          _p, _p]
         lib.oracle_threads.restype = _int
         lib.oracle_threads.argtypes = []
         _lib = lib
@@ -163,6 +167,52 @@ def layer(rowptr, colidx, norm, h, wt, bias=None, act="none", mu=None,
     if rc != 0:
         raise ValueError("oracle_layer failed (%d)" % rc)
     return z, mass, out, alpha
+
+
+def sage_layer(rowptr, colidx, h, wt_self, wt_neigh, bias=None, act="none",
+               mu=None, rstd=None, ids=None):
+    """Binarised two-weight GraphSAGE layer, mean aggregator over the CSR
+    rows (no self-loops expected), for the listed output rows.  Returns
+    (z fp64, mass fp64, out fp32, alpha_self fp64, alpha_neigh fp64)."""
+    rowptr = _c(rowptr, np.int64)
+    colidx = _c(colidx, np.int32)
+    h = _c(h, np.float32)
+    ws = _c(wt_self, np.float32)
+    wn = _c(wt_neigh, np.float32)
+    n, d_in = h.shape
+    d_out = ws.shape[0]
+    assert ws.shape == wn.shape == (d_out, d_in)
+    ids = _c(ids, np.int64)
+    n_out = n if ids is None else len(ids)
+    z = np.zeros((n_out, d_out), dtype=np.float64)
+    mass = np.zeros((n_out, d_out), dtype=np.float64)
+    out = np.zeros((n_out, d_out), dtype=np.float32)
+    a_s = np.zeros(d_out, dtype=np.float64)
+    a_n = np.zeros(d_out, dtype=np.float64)
+    rc = _load().oracle_sage_layer(n, rowptr.ctypes.data, colidx.ctypes.data,
+                                   h.ctypes.data, d_in, d_in, _ptr(_c(mu, np.float32)),
+                                   _ptr(_c(rstd, np.float32)), ws.ctypes.data,
+                                   wn.ctypes.data, d_out, _ptr(_c(bias, np.float32)),
+                                   ACTS[act], _ptr(ids), 0 if ids is None else len(ids),
+                                   z.ctypes.data, mass.ctypes.data, out.ctypes.data,
+                                   a_s.ctypes.data, a_n.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_sage_layer failed (%d)" % rc)
+    return z, mass, out, a_s, a_n
+
+
+def sage_forward(rowptr, colidx, x, weights_self_t, weights_neigh_t, biases,
+                 acts=None, mu=None, rstd=None):
+    """Free-running two-weight GraphSAGE forward; list of (z, mass, out)."""
+    acts = acts or ["none"] * len(weights_self_t)
+    h = x
+    res = []
+    for l, (ws, wn) in enumerate(zip(weights_self_t, weights_neigh_t)):
+        z, m, out, _, _ = sage_layer(rowptr, colidx, h, ws, wn, biases[l], acts[l],
+                                     mu if l == 0 else None, rstd if l == 0 else None)
+        res.append((z, m, out))
+        h = out
+    return res
 
 
 def forward(rowptr, colidx, norm, x, weights_t, biases, acts=None, mu=None,

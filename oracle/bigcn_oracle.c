@@ -38,6 +38,8 @@
  *   R6  No activation by default (the binarisation of the next layer's
  *       input acts as the non-linearity, Sec. 4.1); ReLU is optional.  A
  *       per-channel bias is optional.
+ *   R10 The two-weight GraphSAGE layer (oracle_sage_layer) transforms
+ *       before it aggregates, as Eq. (13) does; see that function.
  *
  * Every reduction runs sequentially in a fixed order in double precision;
  * OpenMP only splits independent rows, so results do not depend on the
@@ -272,6 +274,125 @@ done_w:
   free(wbits);
   free(alpha);
   free(slot);
+  return rc;
+}
+
+/* ---------------------------------------------------------------------
+ * oracle_sage_layer: a binarised two-weight GraphSAGE layer with the mean
+ * aggregator.  The paper binarises every feature-extraction step of the
+ * models it generalises (Sec. 6, Table 3); GraphSAGE has a self and a
+ * neighbour weight matrix (the model sizes of Table 3 are twice those of
+ * the one-matrix GCN), and its cycle-operation count charges the
+ * aggregation at the output width, i.e. the transform comes first as in
+ * Eq. (13) (reading R10):
+ *   ζs_ik = β_i α^s_k (F_i · B^s_k),   ζn_jk = β_j α^n_k (F_j · B^n_k)
+ *   z_ik  = ζs_ik + sum_{j in N(i)} ζn_jk / |N(i)| + b_k
+ * with N(i) the CSR row of i (the graph A without self-loops; an empty row
+ * contributes nothing), F, β, B, α from Eqs. (3)-(8).
+ *   mass_ik = |ζs_ik| + sum_j |ζn_jk| / |N(i)| + |b_k|;  out = fl32(act(z))
+ *   wt_self, wt_neigh  [d_out][d_in] fp32 = W^T of the two matrices
+ *   alpha_self / alpha_neigh  nullable [d_out] outputs
+ * Only the listed rows and their neighbours are binarised.  Returns 0, -1
+ * on a non-finite input, -2 on allocation failure.
+ * ------------------------------------------------------------------- */
+int oracle_sage_layer(int64_t n, const int64_t* rowptr, const int32_t* colidx,
+                      const float* h, int64_t ldh, int32_t d_in, const float* mu,
+                      const float* rstd, const float* wt_self,
+                      const float* wt_neigh, int32_t d_out, const float* bias,
+                      int act, const int64_t* ids, int64_t n_ids, double* z,
+                      double* mass, float* out, double* alpha_self_out,
+                      double* alpha_neigh_out) {
+  const int64_t ldw = (d_in + 63) / 64;
+  int64_t n_out = ids ? n_ids : n;
+  int rc = 0;
+  uint64_t* bs = calloc((size_t)d_out * ldw, sizeof(uint64_t));
+  uint64_t* bn = calloc((size_t)d_out * ldw, sizeof(uint64_t));
+  double* as = calloc((size_t)d_out, sizeof(double));
+  double* an = calloc((size_t)d_out, sizeof(double));
+  int64_t* slot = malloc((size_t)(n ? n : 1) * sizeof(int64_t));
+  int64_t* src_ids = NULL;
+  uint64_t* fbits = NULL;
+  double* beta = NULL;
+  int64_t *dots = NULL, *dotn = NULL;
+  if (!bs || !bn || !as || !an || !slot) {
+    rc = -2;
+    goto done;
+  }
+  /* Both weight matrices: B and α, one bucket per output channel. */
+  if (oracle_binarize(wt_self, d_out, d_in, d_in, NULL, NULL, NULL, 0, bs, ldw,
+                      as) != 0 ||
+      oracle_binarize(wt_neigh, d_out, d_in, d_in, NULL, NULL, NULL, 0, bn, ldw,
+                      an) != 0) {
+    rc = -1;
+    goto done;
+  }
+  if (alpha_self_out) memcpy(alpha_self_out, as, (size_t)d_out * sizeof(double));
+  if (alpha_neigh_out) memcpy(alpha_neigh_out, an, (size_t)d_out * sizeof(double));
+
+  /* Nodes needed: the listed rows (self term) and their neighbours. */
+  for (int64_t j = 0; j < n; ++j) slot[j] = -1;
+  for (int64_t r = 0; r < n_out; ++r) {
+    int64_t i = ids ? ids[r] : r;
+    slot[i] = 0;
+    for (int64_t e = rowptr[i]; e < rowptr[i + 1]; ++e) slot[colidx[e]] = 0;
+  }
+  int64_t n_src = 0;
+  for (int64_t j = 0; j < n; ++j) slot[j] = slot[j] == 0 ? n_src++ : -1;
+  src_ids = malloc((size_t)(n_src ? n_src : 1) * sizeof(int64_t));
+  fbits = calloc((size_t)(n_src ? n_src : 1) * ldw, sizeof(uint64_t));
+  beta = calloc((size_t)(n_src ? n_src : 1), sizeof(double));
+  dots = calloc((size_t)(n_src ? n_src : 1) * d_out, sizeof(int64_t));
+  dotn = calloc((size_t)(n_src ? n_src : 1) * d_out, sizeof(int64_t));
+  if (!src_ids || !fbits || !beta || !dots || !dotn) {
+    rc = -2;
+    goto done;
+  }
+  for (int64_t j = 0; j < n; ++j)
+    if (slot[j] >= 0) src_ids[slot[j]] = j;
+  /* Node features: F and β (Eqs. (7)-(8)); both ±1 products (Eq. (11)). */
+  if (oracle_binarize(h, n, d_in, ldh, mu, rstd, src_ids, n_src, fbits, ldw,
+                      beta) != 0) {
+    rc = -1;
+    goto done;
+  }
+  oracle_sign_dot(fbits, n_src, ldw, bs, d_out, ldw, d_in, dots, d_out);
+  oracle_sign_dot(fbits, n_src, ldw, bn, d_out, ldw, d_in, dotn, d_out);
+
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int64_t r = 0; r < n_out; ++r) {
+    int64_t i = ids ? ids[r] : r;
+    int64_t deg = rowptr[i + 1] - rowptr[i];
+    int64_t ci = slot[i];
+    for (int32_t k = 0; k < d_out; ++k) {
+      double self = beta[ci] * as[k] * (double)dots[ci * d_out + k];
+      double s = self, m = fabs(self);
+      for (int64_t e = rowptr[i]; e < rowptr[i + 1]; ++e) {
+        int64_t c = slot[colidx[e]];
+        double t = beta[c] * an[k] * (double)dotn[c * d_out + k] / (double)deg;
+        s += t;
+        m += fabs(t);
+      }
+      if (bias != NULL) {
+        s += (double)bias[k];
+        m += fabs((double)bias[k]);
+      }
+      double v = (act == ORACLE_ACT_RELU && s < 0.0) ? 0.0 : s;
+      z[r * d_out + k] = s;
+      mass[r * d_out + k] = m;
+      out[r * d_out + k] = (float)v;
+    }
+  }
+done:
+  free(bs);
+  free(bn);
+  free(as);
+  free(an);
+  free(slot);
+  free(src_ids);
+  free(fbits);
+  free(beta);
+  free(dots);
+  free(dotn);
   return rc;
 }
 

@@ -284,3 +284,80 @@ def test_thread_count_invariance():
         outs.append(subprocess.check_output([sys.executable, "-c", code],
                                             env=env, cwd=root).strip())
     assert outs[0] == outs[1]
+
+
+# ------------------------------------------ two-weight GraphSAGE layer (R10)
+
+def _sage_graph(n, edges):
+    return workloads.without_self_loops(workloads.graph_from_edges(n, edges))
+
+
+def test_without_self_loops():
+    g = workloads.graph_from_edges(5, [(0, 1), (1, 2), (3, 1)])
+    a = workloads.without_self_loops(g)
+    assert a.rowptr.tolist() == [0, 1, 4, 5, 6, 6]
+    assert a.colidx.tolist() == [1, 0, 2, 3, 1, 1]
+
+
+def test_hand_worked_sage_layer():
+    gv = _read_golden("tiny_sage.txt")
+    edges = [tuple(int(v) for v in e.split("-")) for e in gv["edges"].split()]
+    g = _sage_graph(int(gv["n"]), edges)
+    h = np.array(_rows(gv["h"]), dtype=np.float32)
+    ws = np.array(_rows(gv["ws"]), dtype=np.float32)
+    wn = np.array(_rows(gv["wn"]), dtype=np.float32)
+    bias = np.array(gv["bias"].split(), dtype=np.float32)
+    z, m, out, a_s, a_n = oracle.sage_layer(g.rowptr, g.colidx, h, ws, wn, bias)
+    assert a_s.tolist() == [float(gv["alpha_s"])] and a_n.tolist() == [float(gv["alpha_n"])]
+    assert z.tolist() == _rows(gv["z"]) and m.tolist() == _rows(gv["mass"])
+    _, _, out_r, _, _ = oracle.sage_layer(g.rowptr, g.colidx, h, ws, wn, bias, "relu")
+    assert out_r.tolist() == _rows(gv["relu"])
+
+
+@pytest.mark.parametrize("k", [64, 70, 300])
+def test_sage_reduces_to_graphsage_for_constant_magnitudes(k):
+    """With H = diag(c) S and both W = T diag(a) (S, T in {+-1}) the
+    binarisation is exact (Eqs. (5), (9)), so the layer equals the plain
+    two-weight GraphSAGE mean layer H Ws + D^-1 A H Wn + b, isolated nodes
+    contributing no neighbour term.  A swapped weight, a dropped self or
+    neighbour term, a self-loop counted in the mean or a wrong divisor all
+    break the equality."""
+    rng = np.random.default_rng(300 + k)
+    g = workloads.without_self_loops(workloads.random_small_graph(37, 80, rng, isolated=3))
+    d_out = 5
+    S = _signs(rng.standard_normal((g.n, k)))
+    c = rng.choice([0.25, 0.5, 1.0, 2.0, 4.0], size=g.n)
+    H = (c[:, None] * S).astype(np.float32)
+    Ws = (_signs(rng.standard_normal((k, d_out))) *
+          rng.choice([0.125, 0.375, 1.5], size=d_out)[None, :]).astype(np.float32)
+    Wn = (_signs(rng.standard_normal((k, d_out))) *
+          rng.choice([0.25, 0.75, 3.0], size=d_out)[None, :]).astype(np.float32)
+    bias = rng.uniform(-0.1, 0.1, d_out).astype(np.float32)
+    z, m, out, a_s, a_n = oracle.sage_layer(g.rowptr, g.colidx, H, Ws.T.copy(),
+                                            Wn.T.copy(), bias)
+    A = np.zeros((g.n, g.n))
+    for i in range(g.n):
+        for e in range(g.rowptr[i], g.rowptr[i + 1]):
+            A[i, g.colidx[e]] += 1.0
+    deg = A.sum(axis=1)
+    assert (deg == 0).sum() >= 3 and np.all(np.diag(A) == 0)
+    mean = np.where(deg[:, None] > 0, A / np.maximum(deg, 1)[:, None], 0.0)
+    H64 = H.astype(np.float64)
+    ref = H64 @ Ws.astype(np.float64) + mean @ (H64 @ Wn.astype(np.float64)) \
+        + bias.astype(np.float64)
+    assert np.allclose(z, ref, rtol=1e-12, atol=1e-12)
+    assert np.array_equal(out, z.astype(np.float32))      # no activation: fl32(z)
+
+
+def test_sage_subset_matches_full():
+    rng = np.random.default_rng(12)
+    g = workloads.without_self_loops(workloads.random_small_graph(60, 150, rng, isolated=4))
+    h = rng.standard_normal((g.n, 100)).astype(np.float32)
+    ws = rng.standard_normal((7, 100)).astype(np.float32)
+    wn = rng.standard_normal((7, 100)).astype(np.float32)
+    z, m, out, _, _ = oracle.sage_layer(g.rowptr, g.colidx, h, ws, wn, act="relu")
+    ids = np.array([59, 2, 2, 0, 31])
+    z2, m2, out2, _, _ = oracle.sage_layer(g.rowptr, g.colidx, h, ws, wn, act="relu",
+                                           ids=ids)
+    assert np.array_equal(z2, z[ids]) and np.array_equal(out2, out[ids])
+    assert np.all(out >= 0)

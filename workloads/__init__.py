@@ -58,7 +58,8 @@ def _load():
 
 @dataclass
 class Graph:
-    """CSR of A + I: int64 row pointers, int32 sorted column indices."""
+    """CSR of A + I (or of A, see without_self_loops): int64 row pointers,
+    int32 sorted column indices."""
     n: int
     rowptr: np.ndarray
     colidx: np.ndarray
@@ -101,6 +102,17 @@ def graph_from_edges(n: int, edges) -> Graph:
         cols.extend(row)
         rowptr[i + 1] = rowptr[i] + len(row)
     return Graph(n, rowptr, np.asarray(cols, dtype=np.int32))
+
+
+def without_self_loops(g: "Graph") -> "Graph":
+    """The CSR of A from that of A + I: every diagonal entry dropped (rows
+    keep their order; a node with no other neighbour gets an empty row)."""
+    rows = np.repeat(np.arange(g.n, dtype=np.int64), np.diff(g.rowptr))
+    keep = g.colidx.astype(np.int64) != rows
+    counts = np.bincount(rows[keep], minlength=g.n)
+    rowptr = np.zeros(g.n + 1, dtype=np.int64)
+    np.cumsum(counts, out=rowptr[1:])
+    return Graph(g.n, rowptr, np.ascontiguousarray(g.colidx[keep]))
 
 
 def random_small_graph(n: int, n_edges: int, rng: np.random.Generator,
