@@ -187,8 +187,13 @@ def traffic_probe(w, model, x, rowptr, colidx, torch, bg, dev):
             c16 = C.view(-1)[:g.n * W].view(g.n, W)
             log("probe layer %d: bgemm_q8, spmm_q8" % l)
             bg.bigcn_bgemm_q8(F[:, :kw], ly.wbits, K, c8, c16, gs)
-            bg.bigcn_spmm_csr_q8(rowptr, colidx, gs, c8, c16, K, ly.alpha, out, ws,
-                                 ly.bias, w.norm, ly.act, d=d)
+            if ly.wbits_self is not None:
+                Cs = torch.empty((g.n, (d + 7) // 8 * 8), dtype=torch.float16, device=dev)
+                bg.bigcn_spmm_csr_sage_q8(rowptr, colidx, gs, c8, c16, K, ly.alpha, Cs,
+                                          ly.alpha_self, out, ws, ly.bias, ly.act, d=d)
+            else:
+                bg.bigcn_spmm_csr_q8(rowptr, colidx, gs, c8, c16, K, ly.alpha, out, ws,
+                                     ly.bias, w.norm, ly.act, d=d)
         else:
             log("probe layer %d: bgemm, spmm" % l)
             bg.bigcn_bgemm(F[:, :kw], ly.wbits, K, C[:, :d])
@@ -241,9 +246,15 @@ def cpu_baseline(w, budget_s=10.0):
         h = w.x
         for l, wt in enumerate(w.weights_t):
             ids = need[l + 1]
-            _, _, out, _ = oracle.layer(g.rowptr, g.colidx, w.norm, h, wt, w.biases[l],
-                                        mu=w.mu if l == 0 else None,
-                                        rstd=w.rstd if l == 0 else None, ids=ids)
+            if w.weights_self_t is not None:
+                _, _, out, _, _ = oracle.sage_layer(g.rowptr, g.colidx, h, w.weights_self_t[l],
+                                                    wt, w.biases[l],
+                                                    mu=w.mu if l == 0 else None,
+                                                    rstd=w.rstd if l == 0 else None, ids=ids)
+            else:
+                _, _, out, _ = oracle.layer(g.rowptr, g.colidx, w.norm, h, wt, w.biases[l],
+                                            mu=w.mu if l == 0 else None,
+                                            rstd=w.rstd if l == 0 else None, ids=ids)
             if l + 1 < L:
                 h = np.zeros((g.n, wt.shape[0]), dtype=np.float32)
                 h[ids] = out
@@ -260,7 +271,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6])
     ap.add_argument("--kernel-reps", type=int, default=20)
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -312,7 +323,7 @@ def main():
     colidx = torch.from_numpy(g.colidx).to(dev)
     x = torch.from_numpy(w.x).to(dev)
     model = bg.BiGCN(rowptr, colidx, w.weights_t, w.biases, norm=w.norm, mu=w.mu,
-                     rstd=w.rstd, device=dev)
+                     rstd=w.rstd, device=dev, weights_self_t=w.weights_self_t)
     torch.cuda.synchronize()
     if args.traffic_probe:
         traffic_probe(w, model, x, rowptr, colidx, torch, bg, dev)
@@ -376,6 +387,8 @@ def main():
         t_pack = time_calls(lambda: bg.bigcn_binarize_pack(h, F[:, :kw], gs, m0, r0, rowptr,
                                                            w.norm), reps, torch)
         q8 = bg.q8_supported(g.n, d, K)
+        sage = ly.wbits_self is not None
+        t_self = None
         if q8:
             # the forward keeps these products as 8-bit half-codes, in rows
             # of q8_row(d) entries
@@ -384,10 +397,19 @@ def main():
             c16 = C.view(-1)[:g.n * W].view(g.n, W)
             t_gemm = time_calls(lambda: bg.bigcn_bgemm_q8(F[:, :kw], ly.wbits, K, c8, c16, gs),
                                 reps, torch)
-            t_spmm = time_calls(lambda: bg.bigcn_spmm_csr_q8(rowptr, colidx, gs, c8, c16, K,
-                                                             ly.alpha, out, ws, ly.bias,
-                                                             w.norm, ly.act, d=d),
-                                reps, torch)
+            if sage:   # the self products, exact in half, and the GraphSAGE aggregation
+                Cs = torch.empty((g.n, (d + 7) // 8 * 8), dtype=torch.float16, device=dev)
+                t_self = time_calls(lambda: bg.bigcn_bgemm(F[:, :kw], ly.wbits_self, K,
+                                                           Cs[:, :d]), reps, torch)
+                t_spmm = time_calls(lambda: bg.bigcn_spmm_csr_sage_q8(
+                    rowptr, colidx, gs, c8, c16, K, ly.alpha, Cs, ly.alpha_self, out, ws,
+                    ly.bias, ly.act, d=d), reps, torch)
+            else:
+                t_spmm = time_calls(lambda: bg.bigcn_spmm_csr_q8(rowptr, colidx, gs, c8, c16,
+                                                                 K, ly.alpha, out, ws,
+                                                                 ly.bias, w.norm, ly.act,
+                                                                 d=d),
+                                    reps, torch)
         else:
             t_gemm = time_calls(lambda: bg.bigcn_bgemm(F[:, :kw], ly.wbits, K, C[:, :d]),
                                 reps, torch)
@@ -404,10 +426,18 @@ def main():
                  achieved=s["gemm_ops"] / t_gemm / 1e12, unit="Tbitop/s",
                  peak=VALU_BITOP_PEAK / 1e12, work=s["gemm_ops"], bytes=s["gemm_bytes"],
                  hbm_gbs=s["gemm_bytes"] / t_gemm / 1e9),
-            dict(kernel="spmm_q8" if q8 else "spmm", layer=l, us=t_spmm * 1e6, bound="hbm",
-                 achieved=s["spmm_bytes"] / t_spmm / 1e9, unit="GB/s", peak=HBM_PEAK_GBS,
-                 work=s["spmm_bytes"]),
+            dict(kernel=("spmm_sage_q8" if sage else "spmm_q8") if q8 else "spmm", layer=l,
+                 us=t_spmm * 1e6, bound="hbm",
+                 achieved=(s["spmm_bytes"] + (g.n * d * 2 if sage else 0)) / t_spmm / 1e9,
+                 unit="GB/s", peak=HBM_PEAK_GBS,
+                 work=s["spmm_bytes"] + (g.n * d * 2 if sage else 0)),
         ]
+        if t_self is not None:
+            kernels.append(dict(kernel="bgemm_self", layer=l, us=t_self * 1e6, bound="alu",
+                                achieved=s["gemm_ops"] / t_self / 1e12, unit="Tbitop/s",
+                                peak=VALU_BITOP_PEAK / 1e12, work=s["gemm_ops"],
+                                bytes=g.n * kw * 8 + d * kw * 8 + g.n * d * 2,
+                                hbm_gbs=(g.n * kw * 8 + g.n * d * 2) / t_self / 1e9))
         h = out
     for k in kernels:
         k["frac"] = k["achieved"] / k["peak"]
@@ -435,7 +465,10 @@ def main():
     dims = [w.weights_t[0].shape[1]] + [wt.shape[0] for wt in w.weights_t]
     from paper_2010_07565_amd import costmodel
     undirected = (g.nnz - g.n) // 2
-    theory = costmodel.theoretical_ratios(g.n, undirected, dims)
+    wpl = 2 if w.weights_self_t is not None else 1
+    if w.weights_self_t is not None:
+        undirected = g.nnz // 2                          # A has no self-loops
+    theory = costmodel.theoretical_ratios(g.n, undirected, dims, wpl)
     paper = {
         "kind": "the paper's analytic counts (Sec. 5: cycle operations, model and "
                 "feature sizes, full precision over binarized) for this workload; "

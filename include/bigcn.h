@@ -193,6 +193,35 @@ bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                                void* workspace, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * bigcn_spmm_csr_sage_q8 -- aggregation of a binarised two-weight GraphSAGE
+ * layer with the mean aggregator.  The paper binarises every feature-
+ * extraction step of the GNNs it generalises (Sec. 6, Table 3, whose model
+ * sizes count a self and a neighbour matrix); both products are formed
+ * before aggregating, as in Eq. (13):
+ *   out[i][k] = act( alpha_neigh[k] / |N(i)| * sum_{j in N(i)} g[j] dot_n[j][k]
+ *                    + |g[i]| * alpha_self[k] * dot_s[i][k] + b_k )
+ * with N(i) row i of the CSR given (the graph A, normally without
+ * self-loops; an empty row has no neighbour term), g the scales of
+ * bigcn_binarize_pack with norm MEAN (beta), flagged by bigcn_bgemm_q8 for
+ * the neighbour products C8 / C16 exactly as for bigcn_spmm_csr_q8, and
+ * dot_s the node's own products with the self weights:
+ *   Cself  [n][ldself] IEEE half, ldself >= d, natural column order (as
+ *          written by bigcn_bgemm with ctype F16), 2-byte aligned.
+ *   alpha_self  fp32[d].
+ * Errors: as bigcn_spmm_csr_q8, plus EINVAL for a NULL Cself / alpha_self
+ *         or ldself < d.
+ * ------------------------------------------------------------------------- */
+bigcn_status bigcn_spmm_csr_sage_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                    const int32_t* colidx, const float* g,
+                                    const int8_t* C8, int64_t ldc8, const void* C16,
+                                    int64_t ldc16, int32_t K, int32_t d,
+                                    const float* alpha_neigh, const void* Cself,
+                                    int64_t ldself, const float* alpha_self,
+                                    const float* bias, bigcn_act act, float* out,
+                                    int64_t ldo, void* workspace, size_t ws_bytes,
+                                    void* stream);
+
+/* ---------------------------------------------------------------------------
  * bigcn_forward -- the whole multi-layer forward pass (Sec. 4.1):
  *     H^(0) = X,  H^(l+1) = act_l( Ã ζ^(l) + b_l ),  l = 0 .. n_layers-1,
  * every layer binarised (features and weights).  Layer 0 standardises X with
@@ -218,8 +247,14 @@ bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
  * hidden activations are never written to memory.  The result is
  * bit-identical to chaining the per-step entry points (bigcn_binarize_pack,
  * bigcn_bgemm_q8, bigcn_spmm_csr_q8 for 8-bit layers).
+ * A layer with wbits_self set is a two-weight GraphSAGE layer: the graph
+ * given is then A (the neighbour sets, normally without self-loops) and
+ * norm must be MEAN; its products stay unfused (8-bit neighbour codes, exact
+ * half self products, then bigcn_spmm_csr_sage_q8's aggregation).
  * Errors: as the per-step calls, plus EINVAL for inconsistent layer widths
- *         or n_layers < 1, EUNSUPPORTED for d_in > 8192 on a layer.
+ *         or n_layers < 1, or a GraphSAGE layer with norm SYM, EUNSUPPORTED
+ *         for d_in > 8192 on a layer or a GraphSAGE layer outside the 8-bit
+ *         shapes (d_out <= 256, d_in <= 2048).
  * ------------------------------------------------------------------------- */
 typedef struct {
   int32_t d_in;
@@ -229,6 +264,12 @@ typedef struct {
   const float* alpha;
   const float* bias;
   bigcn_act act;
+  /* NULL for a graph-convolution layer.  Otherwise the layer is a two-weight
+   * GraphSAGE layer (see bigcn_spmm_csr_sage_q8): wbits / alpha are the
+   * neighbour weights, these the self weights, packed the same way. */
+  const uint64_t* wbits_self;
+  int64_t ldw_self;
+  const float* alpha_self;
 } bigcn_layer;
 
 size_t bigcn_forward_workspace_bytes(int64_t n, int64_t nnz,

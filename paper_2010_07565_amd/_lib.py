@@ -28,6 +28,7 @@ ALGOS = {"auto": 0, "popcount": 1, "mfma_i8": 2}
 # Every entry point declared in include/bigcn.h.
 EXPORTS = ("bigcn_binarize_pack", "bigcn_bgemm", "bigcn_spmm_workspace_bytes",
            "bigcn_spmm_csr", "bigcn_bgemm_q8", "bigcn_spmm_csr_q8",
+           "bigcn_spmm_csr_sage_q8",
            "bigcn_forward_workspace_bytes", "bigcn_forward", "bigcn_status_string")
 
 
@@ -41,7 +42,8 @@ class _Layer(ctypes.Structure):
     _fields_ = [("d_in", ctypes.c_int32), ("d_out", ctypes.c_int32),
                 ("wbits", ctypes.c_void_p), ("ldw", ctypes.c_int64),
                 ("alpha", ctypes.c_void_p), ("bias", ctypes.c_void_p),
-                ("act", ctypes.c_int)]
+                ("act", ctypes.c_int), ("wbits_self", ctypes.c_void_p),
+                ("ldw_self", ctypes.c_int64), ("alpha_self", ctypes.c_void_p)]
 
 
 _lib = None
@@ -74,6 +76,10 @@ def load() -> ctypes.CDLL:
     lib.bigcn_bgemm_q8.restype = _int
     lib.bigcn_bgemm_q8.argtypes = [_p, _i64, _i64, _p, _i32, _i64, _i32, _p, _i64, _p,
                                    _i64, _p, _p]
+    lib.bigcn_spmm_csr_sage_q8.restype = _int
+    lib.bigcn_spmm_csr_sage_q8.argtypes = [_i64, _i64, _p, _p, _p, _p, _i64, _p, _i64,
+                                           _i32, _i32, _p, _p, _i64, _p, _p, _int, _p,
+                                           _i64, _p, _sz, _p]
     lib.bigcn_spmm_csr_q8.restype = _int
     lib.bigcn_spmm_csr_q8.argtypes = [_i64, _i64, _p, _p, _int, _p, _p, _i64, _p, _i64,
                                       _i32, _i32, _p, _p, _int, _p, _i64, _p, _sz, _p]
@@ -211,6 +217,30 @@ def bigcn_spmm_csr_q8(rowptr: torch.Tensor, colidx: torch.Tensor, g: torch.Tenso
     _check("bigcn_spmm_csr_q8", st)
 
 
+def bigcn_spmm_csr_sage_q8(rowptr: torch.Tensor, colidx: torch.Tensor, g: torch.Tensor,
+                           C8: torch.Tensor, C16: torch.Tensor, K: int,
+                           alpha_neigh: torch.Tensor, Cself: torch.Tensor,
+                           alpha_self: torch.Tensor, out: torch.Tensor,
+                           workspace: torch.Tensor, bias=None, act: str = "none",
+                           d: Optional[int] = None, nnz: Optional[int] = None,
+                           stream=None) -> None:
+    """Two-weight GraphSAGE aggregation (mean over the CSR rows) with the
+    self term from the exact half products Cself."""
+    n = rowptr.shape[0] - 1
+    d = alpha_neigh.shape[0] if d is None else d
+    nnz = colidx.shape[0] if nnz is None else nnz
+    st = load().bigcn_spmm_csr_sage_q8(
+        n, nnz, _dev(rowptr, torch.int64, "rowptr"), _dev(colidx, torch.int32, "colidx"),
+        _dev(g, torch.float32, "g"), _dev(C8, torch.int8, "C8"), _ld(C8, "C8"),
+        _dev(C16, torch.float16, "C16"), _ld(C16, "C16"), K, d,
+        _dev(alpha_neigh, torch.float32, "alpha_neigh"), _dev(Cself, torch.float16, "Cself"),
+        _ld(Cself, "Cself"), _dev(alpha_self, torch.float32, "alpha_self"),
+        _dev(bias, torch.float32, "bias"), ACTS[act], _dev(out, torch.float32, "out"),
+        _ld(out, "out"), _dev(workspace, torch.uint8, "workspace"),
+        workspace.numel() if workspace is not None else 0, _stream(stream))
+    _check("bigcn_spmm_csr_sage_q8", st)
+
+
 def q8_lane_bytes(d: int) -> int:
     """Bytes per lane of the 8-bit layout for d output columns."""
     return 1 if d <= 64 else 2 if d <= 128 else 4
@@ -234,18 +264,26 @@ def q8_supported(n: int, d: int, K: int) -> bool:
 
 @dataclass
 class Layer:
-    """A binarised layer: packed signs of W^T, alpha, optional bias."""
+    """A binarised layer: packed signs of W^T, alpha, optional bias; with
+    wbits_self / alpha_self a two-weight GraphSAGE layer (wbits / alpha are
+    then the neighbour weights)."""
     d_in: int
     d_out: int
     wbits: torch.Tensor            # int64 [d_out, ldw] (uint64 words)
     alpha: torch.Tensor            # fp32 [d_out]
     bias: Optional[torch.Tensor] = None
     act: str = "none"
+    wbits_self: Optional[torch.Tensor] = None
+    alpha_self: Optional[torch.Tensor] = None
 
     def _c(self) -> _Layer:
+        sage = self.wbits_self is not None
         return _Layer(self.d_in, self.d_out, _dev(self.wbits, torch.int64, "wbits"),
                       _ld(self.wbits, "wbits"), _dev(self.alpha, torch.float32, "alpha"),
-                      _dev(self.bias, torch.float32, "bias"), ACTS[self.act])
+                      _dev(self.bias, torch.float32, "bias"), ACTS[self.act],
+                      _dev(self.wbits_self, torch.int64, "wbits_self") if sage else None,
+                      _ld(self.wbits_self, "wbits_self") if sage else 0,
+                      _dev(self.alpha_self, torch.float32, "alpha_self") if sage else None)
 
 
 def _layers(layers: Sequence[Layer]):
@@ -293,10 +331,14 @@ class BiGCN:
     """A binarized GCN bound to one graph on one device.
 
     Weights are packed once at construction; ``forward`` runs the whole pass
-    into a preallocated output with a preallocated workspace."""
+    into a preallocated output with a preallocated workspace.  With
+    ``weights_self_t`` (one W^T per layer, or None) the layers given are
+    two-weight GraphSAGE layers: ``weights_t`` holds their neighbour
+    weights, the graph is A and ``norm`` must be "mean"."""
 
     def __init__(self, rowptr, colidx, weights_t, biases=None, acts=None,
-                 norm: str = "sym", mu=None, rstd=None, device="cuda"):
+                 norm: str = "sym", mu=None, rstd=None, device="cuda",
+                 weights_self_t=None):
         self.device = torch.device(device)
         self.rowptr = torch.as_tensor(rowptr, dtype=torch.int64, device=self.device)
         self.colidx = torch.as_tensor(colidx, dtype=torch.int32, device=self.device)
@@ -309,13 +351,18 @@ class BiGCN:
                                                               device=self.device)
         biases = biases or [None] * len(weights_t)
         acts = acts or ["none"] * len(weights_t)
+        selfs = weights_self_t or [None] * len(weights_t)
         self.layers = []
-        for wt, b, a in zip(weights_t, biases, acts):
+        for wt, b, a, ws in zip(weights_t, biases, acts, selfs):
             wt = torch.as_tensor(wt, dtype=torch.float32, device=self.device).contiguous()
             wbits, alpha = pack_weights(wt)
             bt = None if b is None else torch.as_tensor(b, dtype=torch.float32,
                                                         device=self.device)
-            self.layers.append(Layer(wt.shape[1], wt.shape[0], wbits, alpha, bt, a))
+            wbs = als = None
+            if ws is not None:     # two-weight GraphSAGE layer: wt is the neighbour W^T
+                ws = torch.as_tensor(ws, dtype=torch.float32, device=self.device).contiguous()
+                wbs, als = pack_weights(ws)
+            self.layers.append(Layer(wt.shape[1], wt.shape[0], wbits, alpha, bt, a, wbs, als))
         self.ws = torch.empty(forward_workspace_bytes(self.n, self.nnz, self.layers),
                               dtype=torch.uint8, device=self.device)
         self.out = torch.empty((self.n, self.layers[-1].d_out), dtype=torch.float32,

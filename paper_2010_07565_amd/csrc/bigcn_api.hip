@@ -105,8 +105,8 @@ hipError_t run_bgemm(const uint64_t* F, int64_t M, int64_t ldf, const uint64_t* 
 // next layer's products while its own are being read.  ldc8 / ldc16 are the
 // capacities per node; an 8-bit layer uses rows of q8_row(d_out).
 struct ForwardLayout {
-  int64_t ldF, ldh, ldc8, ldc16;
-  size_t off_F, off_g[2], off_C8[2], off_C16[2], off_H0, off_H1, off_spmm, bytes;
+  int64_t ldF, ldh, ldc8, ldc16, ldS;
+  size_t off_F, off_g[2], off_C8[2], off_C16[2], off_H0, off_H1, off_S, off_spmm, bytes;
   int32_t dmax;
 };
 
@@ -116,6 +116,7 @@ int fuse_kind(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t nl, int
   if (l + 1 >= nl || nnz == 0) return 0;
   const bigcn_layer& a = layers[l];
   const bigcn_layer& b = layers[l + 1];
+  if (a.wbits_self != nullptr || b.wbits_self != nullptr) return 0;  // GraphSAGE layers
   if (!bigcn::q8_supported(n, a.d_out, a.d_in)) return 0;  // producer: 8-bit wave kernel
   return bigcn::q8_supported(n, b.d_out, b.d_in) ? 1 : 0;
 }
@@ -126,12 +127,14 @@ inline int64_t q8_row(int32_t d) { return 64 * bigcn::q8_lane_bytes(d); }
 
 bool forward_layout(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t nl,
                     ForwardLayout* L) {
-  int64_t kwmax = 1, dmax = 1, hmax = 1;
+  int64_t kwmax = 1, dmax = 1, hmax = 1, smax = 0;
   for (int32_t l = 0; l < nl; ++l) {
     kwmax = std::max<int64_t>(kwmax, words(layers[l].d_in));
     dmax = std::max<int64_t>(dmax, layers[l].d_out);
     if (l + 1 < nl) hmax = std::max<int64_t>(hmax, layers[l].d_out);
+    if (layers[l].wbits_self != nullptr) smax = std::max<int64_t>(smax, layers[l].d_out);
   }
+  L->ldS = (smax + 7) / 8 * 8;
   L->ldF = (kwmax + 1) / 2 * 2;
   L->ldh = (hmax + 3) / 4 * 4;
   L->ldc8 = 256;
@@ -152,6 +155,8 @@ bool forward_layout(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t n
   if (nl >= 2) off += up256((size_t)n * L->ldh * 4);
   L->off_H1 = off;
   if (nl >= 3) off += up256((size_t)n * L->ldh * 4);
+  L->off_S = off;
+  off += up256((size_t)n * L->ldS * 2);
   L->off_spmm = off;
   off += bigcn::spmm_plan(n, nnz, (int32_t)dmax).bytes;
   L->bytes = off;
@@ -279,6 +284,44 @@ bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                                           workspace, nullptr, s));
 }
 
+bigcn_status bigcn_spmm_csr_sage_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                    const int32_t* colidx, const float* g,
+                                    const int8_t* C8, int64_t ldc8, const void* C16,
+                                    int64_t ldc16, int32_t K, int32_t d,
+                                    const float* alpha_neigh, const void* Cself,
+                                    int64_t ldself, const float* alpha_self,
+                                    const float* bias, bigcn_act act, float* out,
+                                    int64_t ldo, void* workspace, size_t ws_bytes,
+                                    void* stream) {
+  bigcn_status st = check_graph(n, nnz, rowptr, colidx, BIGCN_NORM_MEAN);
+  if (st != BIGCN_OK) return st;
+  if (K < 1 || d < 1 || ldc8 < q8_row(d) || ldc8 % 4 != 0 || ldc16 < q8_row(d))
+    return BIGCN_EINVAL;
+  st = check_spmm_operands(n, g, C16, BIGCN_F16, d, ldc16, alpha_neigh, bias, act, out,
+                           ldo);
+  if (st != BIGCN_OK) return st;
+  if (ldself < d || alpha_self == nullptr || (n > 0 && (C8 == nullptr || Cself == nullptr)))
+    return BIGCN_EINVAL;
+  if (!aligned(C8, 4) || !aligned(Cself, 2) || !aligned(alpha_self, 4)) return BIGCN_EALIGN;
+  if (!bigcn::q8_supported(n, d, K) || (uint64_t)n * ldc8 > 0xFFFFFFFFull ||
+      (uint64_t)n * ldc16 * 2 > 0xFFFFFFFFull)
+    return BIGCN_EUNSUPPORTED;
+  const bigcn::SpmmPlan plan = bigcn::spmm_plan(n, nnz, d);
+  if (n > 0 && nnz > 0) {
+    if (workspace == nullptr || ws_bytes < plan.bytes) return BIGCN_EWORKSPACE;
+    if (!aligned(workspace, 256)) return BIGCN_EALIGN;
+  }
+  bigcn::FusedNext fn = {};
+  fn.kind = 2;
+  fn.Cself = Cself;
+  fn.ldself = ldself;
+  fn.alpha_self = alpha_self;
+  return hip_status(bigcn::launch_spmm_q8(n, nnz, rowptr, colidx, 1, g, C8, ldc8, C16, ldc16,
+                                          K, d, alpha_neigh, bias, act == BIGCN_ACT_RELU,
+                                          out, ldo, plan, workspace, &fn,
+                                          (hipStream_t)stream));
+}
+
 size_t bigcn_forward_workspace_bytes(int64_t n, int64_t nnz,
                                      const bigcn_layer* layers, int32_t n_layers) {
   if (n < 0 || nnz < 0 || layers == nullptr || n_layers < 1) return 0;
@@ -307,6 +350,12 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
     if (!aligned(ly.wbits, 8) || !aligned(ly.alpha, 4) || !aligned(ly.bias, 4))
       return BIGCN_EALIGN;
     if (ly.d_in > kMaxBgemmK) return BIGCN_EUNSUPPORTED;
+    if (ly.wbits_self != nullptr) {  // two-weight GraphSAGE layer
+      if (ly.alpha_self == nullptr || ly.ldw_self < words(ly.d_in)) return BIGCN_EINVAL;
+      if (!aligned(ly.wbits_self, 8) || !aligned(ly.alpha_self, 4)) return BIGCN_EALIGN;
+      if (norm != BIGCN_NORM_MEAN) return BIGCN_EINVAL;
+      if (!bigcn::q8_supported(n, ly.d_out, ly.d_in)) return BIGCN_EUNSUPPORTED;
+    }
   }
   if (ldx < layers[0].d_in || ldo < layers[n_layers - 1].d_out) return BIGCN_EINVAL;
   if ((mu == nullptr) != (rstd == nullptr)) return BIGCN_EINVAL;
@@ -362,6 +411,11 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
         e = run_bgemm(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C16, ct, L.ldc16,
                       BIGCN_BGEMM_AUTO, s);
       if (e != hipSuccess) return BIGCN_EHIP;
+      if (ly.wbits_self != nullptr) {  // the node's own products, exact in half
+        e = run_bgemm(F, n, L.ldF, ly.wbits_self, ly.d_out, ly.ldw_self, ly.d_in,
+                      ws + L.off_S, IType::F16, L.ldS, BIGCN_BGEMM_AUTO, s);
+        if (e != hipSuccess) return BIGCN_EHIP;
+      }
     }
     const int kind = fuse_kind(n, nnz, layers, n_layers, l);
     float* hout = last ? out : (kind != 0 ? nullptr : H[l & 1]);
@@ -370,7 +424,12 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
     if (q8) {
       bigcn::FusedNext fn = {};
       fn.kind = kind;
-      if (kind != 0) {
+      if (ly.wbits_self != nullptr) {
+        fn.kind = 2;
+        fn.Cself = ws + L.off_S;
+        fn.ldself = L.ldS;
+        fn.alpha_self = ly.alpha_self;
+      } else if (kind != 0) {
         const bigcn_layer& nxt = layers[l + 1];
         const int nset = (l + 1) & 1;
         fn.wbits = nxt.wbits;

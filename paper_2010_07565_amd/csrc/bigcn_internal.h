@@ -51,6 +51,9 @@ hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
 //   kind 0: none (the output rows are written);
 //   kind 1: next products as 8-bit half-codes (C8, C16 fallback, flags in g),
 //           rows of 64*q8_lane_bytes(d_out) codes / halves.
+//   kind 2: no next layer; the rows get the self term of a two-weight
+//           GraphSAGE layer, |g_i| alpha_self[k] Cself[i][k], before bias and
+//           activation (Cself: exact half products with the self weights).
 // g receives the next layer's per-node scale.
 struct FusedNext {
   int kind;
@@ -62,6 +65,9 @@ struct FusedNext {
   void* C16;
   int64_t ldc16;
   float* g;
+  const void* Cself;      // kind 2
+  int64_t ldself;
+  const float* alpha_self;
 };
 
 // Aggregation over the CSR of Â with the fused rescale / bias / activation

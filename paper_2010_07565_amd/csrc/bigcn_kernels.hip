@@ -978,6 +978,9 @@ __device__ inline float4_t load_partial(const float* p) {
 // What the aggregation does with a finished output row in the 8-bit path.
 // Lane l holds columns l + 64c of the row (c < NB, interleaved).
 //   NX == 0: write act(rowfac*alpha*acc + b) to out (columns l + 64c).
+//   NX == 2: as 0, plus the self term of a two-weight GraphSAGE layer:
+//            |g_r| * alpha_self[k] * Cself[r][k] (exact half products of the
+//            node's own features with the self weights) before bias / act.
 //   NX == 1: the next layer (K' = d inputs, d' <= 256 outputs, NBN bytes per
 //            lane) is fused: its sign bits are the ballots of the output
 //            values (word c = ballot of slot c, because lane l holds element
@@ -997,10 +1000,14 @@ struct NextLayer {
   int64_t ldc16;
   float* g;            // next layer's per-node scale
   int sym;             // fold D̂^-1/2 into the next scale
+  const _Float16* Cself;  // NX == 2: self products [n][ldself], natural order
+  int64_t ldself;
+  const float* gself;     // NX == 2: per-node scale (its magnitude is β_i)
 };
 
 struct EpiIL {
   float alpha[4], bias[4];
+  float alpha_s[4];    // self weights' α (NX == 2)
   bool valid[4];       // column lane + 64c < d
   int relu;
   int32_t d;
@@ -1011,18 +1018,27 @@ __device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4
                                   const EpiIL& ep, float* __restrict__ out, int64_t ldo,
                                   const NextLayer& nx, int lane) {
   const float rowfac = deg > 0 ? row_factor_deg(deg, mean) : 0.f;
+  float self[NB];
+  if (NX == 2) {
+    const float gi = fabsf(nx.gself[r]);
+#pragma unroll
+    for (int c = 0; c < NB; ++c)
+      self[c] = ep.valid[c] ? gi * ep.alpha_s[c] * (float)nx.Cself[r * nx.ldself + lane + 64 * c]
+                            : 0.f;
+  }
   float v[NB];
 #pragma unroll
   for (int c = 0; c < NB; ++c) {
-    const float t = deg > 0 ? fmaf(acc[c], rowfac * ep.alpha[c], ep.bias[c]) : ep.bias[c];
+    float t = deg > 0 ? fmaf(acc[c], rowfac * ep.alpha[c], ep.bias[c]) : ep.bias[c];
+    if (NX == 2) t += self[c];
     v[c] = act(t, ep.relu);
   }
-  if (NX == 0 || out != nullptr) {
+  if (NX != 1 || out != nullptr) {
 #pragma unroll
     for (int c = 0; c < NB; ++c)
       if (ep.valid[c]) out[r * ldo + lane + 64 * c] = v[c];
   }
-  if (NX == 0) return;
+  if (NX != 1) return;
   // Next layer: signs (one ballot per 64 elements = one packed word) and
   // mean magnitude, exactly as the pack kernel forms them.
   uint64_t word[NB];
@@ -1067,7 +1083,8 @@ __device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4
 template <int NB>
 __device__ inline void make_epi_il(EpiIL& ep, int lane, int32_t d,
                                    const float* __restrict__ alpha,
-                                   const float* __restrict__ bias, int relu) {
+                                   const float* __restrict__ bias, int relu,
+                                   const float* __restrict__ alpha_s = nullptr) {
   ep.relu = relu;
   ep.d = d;
 #pragma unroll
@@ -1076,6 +1093,7 @@ __device__ inline void make_epi_il(EpiIL& ep, int lane, int32_t d,
     ep.valid[c] = c < NB && k < d;
     ep.alpha[c] = ep.valid[c] ? alpha[k] : 0.f;
     ep.bias[c] = (ep.valid[c] && bias != nullptr) ? bias[k] : 0.f;
+    ep.alpha_s[c] = (ep.valid[c] && alpha_s != nullptr) ? alpha_s[k] : 0.f;
   }
 }
 
@@ -1155,7 +1173,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
     int64_t ldo, int64_t chunk, int64_t workers, int32_t dpad,
     int32_t* __restrict__ tail_row, float* __restrict__ head,
     float* __restrict__ tail, NextLayer nx, const uint64_t* __restrict__ Bn,
-    int64_t ldbn) {
+    int64_t ldbn, const float* __restrict__ alpha_s) {
   static_assert(64 % U == 0, "group size");
   extern __shared__ uint64_t sBn[];
   const int lane = threadIdx.x & 63;
@@ -1171,10 +1189,10 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
   };
   int32_t jA = ld_idx(0);  // issued first: independent of everything else
   int32_t jB = ld_idx(64);
-  if (NX > 0) load_next_weights<NB, NBN>(nx, sBn, Bn, ldbn, d, lane);
+  if (NX == 1) load_next_weights<NB, NBN>(nx, sBn, Bn, ldbn, d, lane);
   if (!live) return;
   EpiIL ep;
-  make_epi_il<NB>(ep, lane, d, alpha, bias, relu);
+  make_epi_il<NB>(ep, lane, d, alpha, bias, relu, alpha_s);
   const int rb8 = (int)ldc8;
   const int rb16 = (int)(ldc16 * 2);
   const __amdgpu_buffer_rsrc_t rs8 = raw_rsrc(C8, (uint32_t)(n * rb8));
@@ -1314,14 +1332,14 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
     float* __restrict__ out, int64_t ldo, int64_t chunk, int64_t workers,
     int32_t dpad, const int32_t* __restrict__ tail_row,
     const float* __restrict__ head, const float* __restrict__ tail, NextLayer nx,
-    const uint64_t* __restrict__ Bn, int64_t ldbn) {
+    const uint64_t* __restrict__ Bn, int64_t ldbn, const float* __restrict__ alpha_s) {
   extern __shared__ uint64_t sBn[];
   const int lane = threadIdx.x & 63;
-  if (NX > 0) load_next_weights<NB, NBN>(nx, sBn, Bn, ldbn, d, lane);
+  if (NX == 1) load_next_weights<NB, NBN>(nx, sBn, Bn, ldbn, d, lane);
   const int64_t w0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * 4;
   if (w0 >= workers) return;
   EpiIL ep;
-  make_epi_il<NB>(ep, lane, d, alpha, bias, relu);
+  make_epi_il<NB>(ep, lane, d, alpha, bias, relu, alpha_s);
   // lane q < 4: worker w0 + q's cut row and that row's bounds
   const int64_t wq = w0 + (lane & 3);
   const int32_t rq = wq < workers ? tail_row[wq] : -1;
@@ -1424,6 +1442,21 @@ __global__ __launch_bounds__(kBlock) void k_spmm_rows(
   const int64_t a = rowptr[r], b = rowptr[r + 1];
   if (b <= a) return;
   for (int64_t w = (a + chunk - 1) / chunk; w * chunk < b; ++w) row_of[w] = (int32_t)r;
+}
+
+// Two-weight GraphSAGE layer on a graph without edges: every row is its
+// self term, act(b_k + |g_i| alpha_self[k] Cself[i][k]).
+__global__ __launch_bounds__(kBlock) void k_sage_self_only(
+    int64_t n, int32_t d, const float* __restrict__ g, const _Float16* __restrict__ Cself,
+    int64_t ldself, const float* __restrict__ alpha_s, const float* __restrict__ bias,
+    int relu, float* __restrict__ out, int64_t ldo) {
+  const int64_t idx = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (idx >= n * (int64_t)d) return;
+  const int64_t i = idx / d;
+  const int k = (int)(idx - i * d);
+  const float self = fabsf(g[i]) * alpha_s[k] * (float)Cself[i * ldself + k];
+  const float t = (bias != nullptr ? bias[k] : 0.f) + self;
+  out[i * ldo + k] = act(t, relu);
 }
 
 // Graph without edges: every row is act(bias).
@@ -1747,13 +1780,16 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   nx.ldc16 = fn.ldc16;
   nx.g = fn.g;
   nx.sym = !mean;
+  nx.Cself = (const _Float16*)fn.Cself;
+  nx.ldself = fn.ldself;
+  nx.gself = g;
   const size_t lds = (NX > 0 && NB * NBN > 4)
                          ? (size_t)((d + 63) >> 6) * NBN * 64 * sizeof(uint64_t) : 0;
   dim3 grid((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock));
   hipLaunchKernelGGL((k_spmm_wave_q8<8, NX, NB, NBN>), grid, dim3(kBlock), lds, stream, n,
                      nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16, ldc16,
                      K & 1, d, alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,
-                     tail_row, head, tail, nx, fn.wbits, fn.ldw);
+                     tail_row, head, tail, nx, fn.wbits, fn.ldw, fn.alpha_self);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t fix_waves = (p.workers + 3) / 4;
@@ -1761,7 +1797,7 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
                      dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
                      dim3(kBlock), lds, stream, rowptr, mean, d, alpha, bias, relu, out,
                      ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail, nx, fn.wbits,
-                     fn.ldw);
+                     fn.ldw, fn.alpha_self);
   return hipGetLastError();
 }
 
@@ -1776,6 +1812,7 @@ hipError_t spmm_q8_nb(int64_t n, int64_t nnz, const int64_t* rowptr,
   return spmm_q8_nx<NX, NB, NBN>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, \
                                  K, d, alpha, bias, relu, out, ldo, p, ws, fn, stream)
   if (fn.kind == 0) BIGCN_Q8S(0, 1);
+  if (fn.kind == 2) BIGCN_Q8S(2, 1);
   switch (q8_lane_bytes(fn.d_out)) {
     case 1: BIGCN_Q8S(1, 1);
     case 2: BIGCN_Q8S(1, 2);
@@ -1794,6 +1831,13 @@ hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
   if (n == 0) return hipSuccess;
   FusedNext none = {};
   const FusedNext& fn = next != nullptr ? *next : none;
+  if (nnz == 0 && fn.kind == 2) {
+    const int64_t total = n * (int64_t)d;
+    hipLaunchKernelGGL(k_sage_self_only, dim3((unsigned)((total + kBlock - 1) / kBlock)),
+                       dim3(kBlock), 0, stream, n, d, g, (const _Float16*)fn.Cself,
+                       fn.ldself, fn.alpha_self, bias, relu, out, ldo);
+    return hipGetLastError();
+  }
   if (nnz == 0 && fn.kind == 0) {
     const int64_t total = n * (int64_t)d;
     hipLaunchKernelGGL(k_spmm_empty, dim3((unsigned)((total + kBlock - 1) / kBlock)),

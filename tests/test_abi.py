@@ -130,21 +130,27 @@ def test_workspace_queries_grow_with_size():
     assert bg.spmm_workspace_bytes(-1, 10, 4) == 0
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_forward_workspace_fits_the_workloads(cfg):
     """The workspace needed by each workload stays a small multiple of the
     node data (well inside 288 GB)."""
     import workloads
     c = workloads.CONFIGS[cfg]
-    n, nnz = c["n"], 2 * c["undirected"] + c["n"]
+    sage = bool(c.get("sage"))
+    n, nnz = c["n"], 2 * c["undirected"] + (0 if sage else c["n"])
     dims = c["dims"]
     L = _lib._Layer
     arr = (L * (len(dims) - 1))(*[L(dims[i], dims[i + 1], FAKE, (dims[i] + 63) // 64,
-                                    FAKE, None, 0) for i in range(len(dims) - 1)])
+                                    FAKE, None, 0, FAKE if sage else None,
+                                    (dims[i] + 63) // 64 if sage else 0,
+                                    FAKE if sage else None)
+                                  for i in range(len(dims) - 1)])
     ws = bg.load().bigcn_forward_workspace_bytes(n, nnz, arr, len(dims) - 1)
     hidden = max(dims[1:-1]) if len(dims) > 2 else 0
-    assert ws >= n * 2 * max(dims[1:])           # the product matrix alone
-    assert ws <= n * (8 * 64 + 2 * 4 * hidden + 4 * 256 + 64) + 8 * nnz + (64 << 20)
+    self_products = 2 * max(dims[1:]) if sage else 0
+    assert ws >= n * (2 * max(dims[1:]) + self_products)   # the product matrices
+    assert ws <= n * (8 * 64 + 2 * 4 * hidden + 4 * 256 + 64 + self_products) + 8 * nnz \
+        + (64 << 20)
 
 
 def test_bgemm_q8_validation():
@@ -205,3 +211,35 @@ def test_q8_layout_helpers():
     assert [bg.q8_position(k, 64) for k in range(64)] == list(range(64))
     assert bg.q8_supported(100, 256, 2048) and not bg.q8_supported(100, 257, 64)
     assert not bg.q8_supported(100, 64, 2049) and bg.q8_supported(100, 1, 1)
+
+
+def test_spmm_csr_sage_q8_validation():
+    lib = bg.load()
+    f = lib.bigcn_spmm_csr_sage_q8
+    # n nnz rowptr colidx g C8 ldc8 C16 ldc16 K d alpha_n Cself ldself alpha_s bias act
+    # out ldo ws bytes stream
+    ok = [10, 40, FAKE, FAKE, FAKE, FAKE, 64, FAKE, 64, 100, 7, FAKE, FAKE, 8, FAKE, None, 0,
+          FAKE, 7, FAKE, 1 << 20, None]
+    for pos, val, want in [(13, 6, EINVAL),            # ldself < d
+                           (12, None, EINVAL),         # no self products
+                           (14, None, EINVAL),         # no self alphas
+                           (12, FAKE + 1, EALIGN), (6, 32, EINVAL), (10, 0, EINVAL)]:
+        args = list(ok)
+        args[pos] = val
+        assert f(*args) == want, (pos, val)
+    wide = list(ok)
+    wide[6], wide[8], wide[10], wide[13], wide[18] = 256, 260, 257, 260, 257
+    assert f(*wide) == EUNSUPPORTED
+
+
+def test_forward_rejects_sage_layer_with_symmetric_norm():
+    lib = bg.load()
+    L = _lib._Layer
+    layers = (L * 1)(L(100, 16, FAKE, 2, FAKE, None, 0, FAKE, 2, FAKE))
+    need = lib.bigcn_forward_workspace_bytes(50, 200, layers, 1)
+    args = [50, 200, FAKE, FAKE, 0, FAKE, 100, None, None, layers, 1, FAKE, 16, FAKE,
+            need, None]
+    assert lib.bigcn_forward(*args) == EINVAL        # GraphSAGE needs norm MEAN
+    short = (L * 1)(L(100, 16, FAKE, 2, FAKE, None, 0, FAKE, 1, FAKE))
+    args[4], args[9] = 1, short
+    assert lib.bigcn_forward(*args) == EINVAL        # ldw_self < ceil(100/64)

@@ -418,3 +418,132 @@ def test_captured_forward_replays_match_eager(dev):
         ref = ref_model.forward(_t(xi, dev)).clone()
         torch.cuda.synchronize()
         assert torch.equal(got, ref), "replay %d differs from eager" % it
+
+
+# ------------------------------------------- two-weight GraphSAGE (8-bit path)
+
+def gpu_sage_layer(dev, g, h, wt_self, wt_neigh, bias, act="none", mu=None, rstd=None,
+                   rowptr_t=None, colidx_t=None, ht=None):
+    """pack (mean) -> 8-bit GEMM with the neighbour weights + exact half GEMM
+    with the self weights -> GraphSAGE aggregation, through the entry points
+    (the steps the forward pass runs for such a layer)."""
+    n, K = h.shape if ht is None else ht.shape
+    d = wt_self.shape[0]
+    rowptr_t = _t(g.rowptr, dev) if rowptr_t is None else rowptr_t
+    colidx_t = _t(g.colidx, dev) if colidx_t is None else colidx_t
+    ht = _t(h, dev) if ht is None else ht
+    wbs, a_s = bg.pack_weights(_t(wt_self, dev))
+    wbn, a_n = bg.pack_weights(_t(wt_neigh, dev))
+    kw = (K + 63) // 64
+    F = torch.empty((n, kw), dtype=torch.int64, device=dev)
+    gs = torch.empty(n, dtype=torch.float32, device=dev)
+    bg.bigcn_binarize_pack(ht, F, gs, None if mu is None else _t(mu, dev),
+                           None if rstd is None else _t(rstd, dev), rowptr_t, "mean")
+    W = bg.q8_row(d)
+    C8 = torch.empty((n, W), dtype=torch.int8, device=dev)
+    C16 = torch.empty((n, W), dtype=torch.float16, device=dev)
+    Cs = torch.empty((n, (d + 7) // 8 * 8), dtype=torch.float16, device=dev)
+    bg.bigcn_bgemm_q8(F, wbn, K, C8, C16, gs)
+    bg.bigcn_bgemm(F, wbs, K, Cs[:, :d])
+    out = torch.empty((n, d), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(1, bg.spmm_workspace_bytes(n, g.nnz, d)), dtype=torch.uint8,
+                     device=dev)
+    b = None if bias is None else _t(bias, dev)
+    bg.bigcn_spmm_csr_sage_q8(rowptr_t, colidx_t, gs, C8, C16, K, a_n, Cs, a_s, out, ws,
+                              b, act, d=d, nnz=g.nnz)
+    return out, F, (C8, C16, gs), Cs[:, :d], a_s, a_n
+
+
+def _sage_graph(n, rng, isolated=5):
+    return workloads.without_self_loops(_star_plus_random(n, rng)) if isolated else \
+        workloads.without_self_loops(workloads.random_small_graph(n, 3 * n, rng))
+
+
+@pytest.mark.parametrize("K,d,act", [(130, 7, "none"), (64, 64, "relu"), (100, 65, "none"),
+                                     (602, 200, "none"), (256, 256, "relu"),
+                                     (1433, 41, "none"), (63, 3, "none"), (300, 128, "none")])
+def test_sage_layer_matches_oracle(dev, K, d, act):
+    rng = np.random.default_rng(7 * K + d)
+    g = _sage_graph(700, rng)
+    assert np.all(g.colidx != np.repeat(np.arange(g.n), np.diff(g.rowptr)))
+    assert (np.diff(g.rowptr) == 0).sum() >= 5            # isolated nodes
+    x = rng.standard_normal((g.n, K)).astype(np.float32)
+    mu, rstd = workloads.bn_stats(x)
+    wts = workloads.glorot_t(K, d, rng)
+    wtn = workloads.glorot_t(K, d, rng)
+    b = rng.uniform(-0.1, 0.1, d).astype(np.float32)
+    out, F, prod, Cs, a_s, a_n = gpu_sage_layer(dev, g, x, wts, wtn, b, act, mu, rstd)
+    torch.cuda.synchronize()
+    z, m, _, as_ref, an_ref = oracle.sage_layer(g.rowptr, g.colidx, x, wts, wtn, b, act,
+                                                mu, rstd)
+    fb, _ = oracle.binarize(x, mu, rstd)
+    assert np.array_equal(u64(F), fb)
+    assert np.array_equal(decode_products(prod, K, d),
+                          oracle.sign_dot(fb, oracle.binarize(wtn)[0], K))
+    assert np.array_equal(Cs.cpu().numpy().astype(np.int64),
+                          oracle.sign_dot(fb, oracle.binarize(wts)[0], K))
+    assert np.allclose(a_s.cpu().numpy(), as_ref, rtol=1e-5, atol=0)
+    assert np.allclose(a_n.cpu().numpy(), an_ref, rtol=1e-5, atol=0)
+    err = mass_error(out.cpu().numpy(), z, m, relu=act == "relu")
+    assert err <= TOL, err
+
+
+def test_sage_layer_without_edges(dev):
+    """A graph with no edges: every output row is its self term plus bias."""
+    rng = np.random.default_rng(5)
+    n, K, d = 90, 70, 33
+    g = workloads.Graph(n, np.zeros(n + 1, dtype=np.int64), np.zeros(0, dtype=np.int32))
+    x = rng.standard_normal((n, K)).astype(np.float32)
+    wts, wtn = workloads.glorot_t(K, d, rng), workloads.glorot_t(K, d, rng)
+    b = rng.uniform(-0.1, 0.1, d).astype(np.float32)
+    out, *_ = gpu_sage_layer(dev, g, x, wts, wtn, b, colidx_t=torch.zeros(1, dtype=torch.int32,
+                                                                         device=dev))
+    torch.cuda.synchronize()
+    z, m, *_ = oracle.sage_layer(g.rowptr, g.colidx, x, wts, wtn, b)
+    assert mass_error(out.cpu().numpy(), z, m) <= TOL
+
+
+def test_sage_forward_equals_chained_and_oracle(dev):
+    """A 3-layer two-weight GraphSAGE model through bigcn_forward equals the
+    chained entry points bit for bit, and matches the oracle's free-running
+    forward (hidden sign flips only at legitimate near-zeros)."""
+    rng = np.random.default_rng(66)
+    g = _sage_graph(900, rng)
+    dims = [200, 128, 64, 9]
+    x = rng.standard_normal((g.n, dims[0])).astype(np.float32)
+    mu, rstd = workloads.bn_stats(x)
+    wn = [workloads.glorot_t(dims[i], dims[i + 1], rng) for i in range(3)]
+    wsf = [workloads.glorot_t(dims[i], dims[i + 1], rng) for i in range(3)]
+    bs = [rng.uniform(-0.1, 0.1, dims[i + 1]).astype(np.float32) for i in range(3)]
+    rowptr_t, colidx_t = _t(g.rowptr, dev), _t(g.colidx, dev)
+    model = bg.BiGCN(rowptr_t, colidx_t, wn, bs, norm="mean", mu=mu, rstd=rstd, device=dev,
+                     weights_self_t=wsf)
+    xt = _t(x, dev)
+    got = model.forward(xt).clone()
+    h = xt
+    for l in range(3):
+        h, *_ = gpu_sage_layer(dev, g, None, wsf[l], wn[l], bs[l],
+                               mu=mu if l == 0 else None, rstd=rstd if l == 0 else None,
+                               rowptr_t=rowptr_t, colidx_t=colidx_t, ht=h)
+    torch.cuda.synchronize()
+    assert torch.equal(got, h), "forward differs from the chained entry points"
+    ref = oracle.sage_forward(g.rowptr, g.colidx, x, wsf, wn, bs, mu=mu, rstd=rstd)
+    # layer by layer from the GPU's own chain: hidden signs may differ from
+    # the oracle's only where the oracle's value is within rounding of zero
+    h = xt
+    flipped = np.zeros(g.n, dtype=bool)
+    src = np.repeat(np.arange(g.n), np.diff(g.rowptr))
+    for l in range(3):
+        h, *_ = gpu_sage_layer(dev, g, None, wsf[l], wn[l], bs[l],
+                               mu=mu if l == 0 else None, rstd=rstd if l == 0 else None,
+                               rowptr_t=rowptr_t, colidx_t=colidx_t, ht=h)
+        out = h.cpu().numpy()
+        z, m, o = ref[l]
+        tainted = flipped.copy()                       # own row (self term) ...
+        tainted[np.unique(src[flipped[g.colidx]])] = True   # ... or a neighbour
+        clean = ~tainted
+        assert mass_error(out[clean], z[clean], m[clean]) <= TOL
+        flips = (out >= 0) != (o >= 0)
+        fc = flips & clean[:, None]
+        assert np.all(np.abs(z[fc]) <= TOL * m[fc] + 1e-30), "sign flip away from zero"
+        flipped = flipped | flips.any(axis=1)

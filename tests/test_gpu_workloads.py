@@ -1,4 +1,5 @@
-"""The five synthetic workloads at full size, on the GPU, against the oracle.
+"""The synthetic workloads at full size, on the GPU, against the oracle
+(the five graph-convolution workloads and the two-weight GraphSAGE one).
 
 Per layer, the GPU layer (pack -> bgemm -> spmm through the C ABI, all rows,
 the launch shapes the forward pass uses) is compared with the oracle on
@@ -19,7 +20,7 @@ import oracle
 import workloads
 import paper_2010_07565_amd as bg
 from helpers import TOL, mass_error, plain_rel_error, sample_rows, u64
-from test_gpu_parity import _t, decode_products, gpu_layer
+from test_gpu_parity import _t, decode_products, gpu_layer, gpu_sage_layer
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -47,12 +48,13 @@ def workload(cfg):
 
 
 @pytest.mark.timeout(1200)
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_workload_layers_match_oracle(dev, cfg):
     w = workload(cfg)
     g = w.graph
     rowptr_t, colidx_t = _t(g.rowptr, dev), _t(g.colidx, dev)
     ids = None if cfg <= 2 else sample_rows(g, 256, seed=cfg)
+    sage = w.weights_self_t is not None
     for l, wt in enumerate(w.weights_t):
         K, d = wt.shape[1], wt.shape[0]
         if l == 0:
@@ -60,6 +62,9 @@ def test_workload_layers_match_oracle(dev, cfg):
         else:
             h, mu, rstd = workloads.layer_input(g.n, K, seed=1000 * cfg + l), None, None
         log("cfg %d layer %d: %d -> %d, n=%d nnz=%d" % (cfg, l, K, d, g.n, g.nnz))
+        if sage:
+            check_sage_layer(dev, w, l, h, mu, rstd, ids, rowptr_t, colidx_t)
+            continue
         out, F, C, alpha = gpu_layer(dev, g, w.norm, h, wt, w.biases[l], mu=mu, rstd=rstd,
                                      rowptr_t=rowptr_t, colidx_t=colidx_t)
         torch.cuda.synchronize()
@@ -85,25 +90,60 @@ def test_workload_layers_match_oracle(dev, cfg):
         del out, F, C
 
 
+def check_sage_layer(dev, w, l, h, mu, rstd, ids, rowptr_t, colidx_t):
+    g = w.graph
+    ws, wn = w.weights_self_t[l], w.weights_t[l]
+    K, d = wn.shape[1], wn.shape[0]
+    out, F, prod, Cs, a_s, a_n = gpu_sage_layer(dev, g, h, ws, wn, w.biases[l], mu=mu,
+                                                rstd=rstd, rowptr_t=rowptr_t,
+                                                colidx_t=colidx_t)
+    torch.cuda.synchronize()
+    fb, _ = oracle.binarize(h, mu, rstd)
+    assert np.array_equal(u64(F), fb), "packed bits differ"
+    rows = np.arange(g.n) if ids is None else ids
+    assert np.array_equal(decode_products(prod, K, d)[rows],
+                          oracle.sign_dot(fb[rows], oracle.binarize(wn)[0], K))
+    assert np.array_equal(Cs.cpu().numpy().astype(np.int64)[rows],
+                          oracle.sign_dot(fb[rows], oracle.binarize(ws)[0], K))
+    t = time.time()
+    z, m, _, as_ref, an_ref = oracle.sage_layer(g.rowptr, g.colidx, h, ws, wn, w.biases[l],
+                                                mu=mu, rstd=rstd, ids=ids)
+    got = out.cpu().numpy() if ids is None else out[torch.from_numpy(ids).to(dev)].cpu().numpy()
+    assert bool(torch.isfinite(out).all())
+    err = mass_error(got, z, m)
+    log("  oracle %.1f s; mass-normalised err %.2e, plain rel err %.2e, rows %d" % (
+        time.time() - t, err, plain_rel_error(got, z, m), len(got)))
+    assert np.allclose(a_s.cpu().numpy(), as_ref, rtol=1e-5, atol=0)
+    assert np.allclose(a_n.cpu().numpy(), an_ref, rtol=1e-5, atol=0)
+    assert err <= TOL
+
+
 def chained(dev, w, rowptr_t, colidx_t, xt):
     h = xt
     for l, wt in enumerate(w.weights_t):
-        out, _, _, _ = gpu_layer(dev, w.graph, w.norm, None, wt, w.biases[l],
-                                 mu=w.mu if l == 0 else None, rstd=w.rstd if l == 0 else None,
-                                 rowptr_t=rowptr_t, colidx_t=colidx_t, ht=h)
+        if w.weights_self_t is not None:
+            out, *_ = gpu_sage_layer(dev, w.graph, None, w.weights_self_t[l], wt,
+                                     w.biases[l], mu=w.mu if l == 0 else None,
+                                     rstd=w.rstd if l == 0 else None,
+                                     rowptr_t=rowptr_t, colidx_t=colidx_t, ht=h)
+        else:
+            out, _, _, _ = gpu_layer(dev, w.graph, w.norm, None, wt, w.biases[l],
+                                     mu=w.mu if l == 0 else None,
+                                     rstd=w.rstd if l == 0 else None,
+                                     rowptr_t=rowptr_t, colidx_t=colidx_t, ht=h)
         h = out
     return h
 
 
 @pytest.mark.timeout(1200)
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_forward_equals_chained_layers(dev, cfg):
     w = workload(cfg)
     g = w.graph
     rowptr_t, colidx_t = _t(g.rowptr, dev), _t(g.colidx, dev)
     xt = _t(w.x, dev)
     model = bg.BiGCN(rowptr_t, colidx_t, w.weights_t, w.biases, norm=w.norm,
-                     mu=w.mu, rstd=w.rstd, device=dev)
+                     mu=w.mu, rstd=w.rstd, device=dev, weights_self_t=w.weights_self_t)
     out = model.forward(xt).clone()
     out2 = model.forward(xt).clone()
     ref = chained(dev, w, rowptr_t, colidx_t, xt)

@@ -22,6 +22,7 @@ import subprocess
 from dataclasses import dataclass, field
 
 import numpy as np
+from typing import Optional
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "graphgen.cpp")
@@ -142,6 +143,9 @@ class Workload:
     weights_t: list = field(default_factory=list)   # fp32 W^T [d_out, d_in]
     biases: list = field(default_factory=list)      # fp32 [d_out]
     seeds: dict = field(default_factory=dict)
+    # two-weight GraphSAGE: self-weight W^T per layer (weights_t then holds
+    # the neighbour weights and graph is A without self-loops); else None
+    weights_self_t: Optional[list] = None
 
     @property
     def n(self) -> int:
@@ -165,6 +169,10 @@ CONFIGS = {
             dims=[602, 256, 41], norm="sym", feat="normal"),
     5: dict(name="products-like", n=2449029, undirected=61_850_000,
             dims=[100, 256, 256, 47], norm="mean", feat="normal"),
+    # Two-weight GraphSAGE (self + neighbour matrices, mean over the
+    # neighbours without self-loops) on the arxiv-shaped graph.
+    6: dict(name="arxiv-like-sage", n=169343, undirected=1_150_000,
+            dims=[128, 256, 256, 40], norm="mean", feat="normal", sage=True),
 }
 
 BN_EPS = 1e-5
@@ -213,8 +221,12 @@ def make_workload(index: int, with_bias: bool = True) -> Workload:
     ws = [glorot_t(dims[i], dims[i + 1], rng_w) for i in range(len(dims) - 1)]
     bs = [rng_b.uniform(-0.1, 0.1, size=dims[i + 1]).astype(np.float32)
           if with_bias else None for i in range(len(dims) - 1)]
+    wself = None
+    if cfg.get("sage"):
+        g = without_self_loops(g)
+        wself = [glorot_t(dims[i], dims[i + 1], rng_w) for i in range(len(dims) - 1)]
     return Workload(cfg["name"], index, cfg["norm"], g, x, mu, rstd, ws, bs,
-                    seeds=dict(config_seed=index - 1, graph=gseed))
+                    seeds=dict(config_seed=index - 1, graph=gseed), weights_self_t=wself)
 
 
 def layer_input(n: int, d: int, seed: int) -> np.ndarray:
