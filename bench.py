@@ -4,7 +4,9 @@
 
 A step is one whole forward pass (every layer: sign pack, binary GEMM, CSR
 aggregation) over a seeded synthetic workload whose inputs, packed weights
-and workspace are already resident in device memory.  The default workload
+and workspace are already resident in device memory.  The pass is timed
+twice, as eager calls and as a HIP-graph replay (checked bit-equal to the
+eager pass first); the faster loop gives the reported value (--mode).  The default workload
 is the PubMed-shaped citation graph (19,717 nodes, 500 -> 64 -> 3); the other
 four are selectable with --workload.
 
@@ -275,8 +277,9 @@ def main():
     ap.add_argument("--kernel-reps", type=int, default=20)
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--eager", action="store_true",
-                    help="report eager calls instead of the HIP-graph replay")
+    ap.add_argument("--mode", choices=["best", "graph", "eager"], default="best",
+                    help="which timed loop gives the reported value: the faster of "
+                         "the two (default), the HIP-graph replay, or eager calls")
     ap.add_argument("--forward-only", action="store_true",
                     help="time the forward pass only (no per-kernel table, no "
                          "algorithm comparison, no CPU baseline): for profiling")
@@ -349,7 +352,11 @@ def main():
     torch.cuda.synchronize()
     assert torch.equal(model.out, eager_out), "graph replay differs from the eager pass"
     graph_s = timed(replay, args.steps, args.warmup)
-    step_s = graph_s if not args.eager else eager_s
+    if args.mode == "best":
+        mode = "hip_graph_replay" if graph_s <= eager_s else "eager"
+    else:
+        mode = "hip_graph_replay" if args.mode == "graph" else "eager"
+    step_s = graph_s if mode == "hip_graph_replay" else eager_s
     ms = step_s * 1e3
     nodes_per_s = g.n / step_s
     log("forward: eager %.4f ms/step, graph replay %.4f ms/step -> %.4g nodes/s" % (
@@ -358,7 +365,8 @@ def main():
     if args.forward_only:
         print(json.dumps({"metric": METRIC, "value": round(nodes_per_s, 1), "unit": "nodes/s",
                           "ms_per_step": round(ms, 5), "workload": w.name,
-                          "mode": "eager" if args.eager else "hip_graph_replay"}), flush=True)
+                          "mode": mode, "eager_ms_per_step": round(eager_s * 1e3, 5),
+                          "graph_ms_per_step": round(graph_s * 1e3, 5)}), flush=True)
         return
 
     # ---- each kernel alone, through its entry point, same shapes and ld's
@@ -490,7 +498,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 5),
-        "mode": "eager" if args.eager else "hip_graph_replay",
+        "mode": mode,
+        "graph_ms_per_step": round(graph_s * 1e3, 5),
         "eager_ms_per_step": round(eager_s * 1e3, 5),
         "higher_is_better": True,
         "scaling": "weak",
