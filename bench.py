@@ -8,7 +8,7 @@ and workspace are already resident in device memory.  The pass is timed
 twice, as eager calls and as a HIP-graph replay (checked bit-equal to the
 eager pass first); the faster loop gives the reported value (--mode).  The default workload
 is the PubMed-shaped citation graph (19,717 nodes, 500 -> 64 -> 3); the other
-four are selectable with --workload.
+five (the sixth a two-weight GraphSAGE model) are selectable with --workload.
 
 Prints one JSON line.  Besides the forward-pass throughput it carries
  - "kernels":  each layer's steps timed alone through their entry points
