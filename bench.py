@@ -16,8 +16,11 @@ Prints one JSON line.  Besides the forward-pass throughput it carries
    the launch stream); the aggregation step is its three kernels (row plan,
    aggregation, fix-up of rows cut by chunk boundaries);
  - "roofline": the dominant kernel (largest share of a forward pass) against
-   its bound: HBM bytes for pack / aggregation, bit operations on the vector
-   ALUs for the binary GEMM;
+   its bound: HBM bytes for pack / aggregation (each array counted once;
+   the aggregation entries also carry the gather model, every edge reading
+   its source's whole product row), bit operations on the vector ALUs for
+   the binary GEMM; "traffic" is the counter-measured HBM bytes of that call
+   (profiles/hbm_traffic_<workload>.md) while the kernel sources match;
  - "bgemm_ab": the binary GEMM of every layer shape run with both
    algorithms (XOR + bit count on the vector ALUs, +-1 int8 on the matrix
    cores) on the same random sign bits, checked equal, each against its
@@ -438,7 +441,13 @@ def main():
                  us=t_spmm * 1e6, bound="hbm",
                  achieved=(s["spmm_bytes"] + (g.n * d * 2 if sage else 0)) / t_spmm / 1e9,
                  unit="GB/s", peak=HBM_PEAK_GBS,
-                 work=s["spmm_bytes"] + (g.n * d * 2 if sage else 0)),
+                 work=s["spmm_bytes"] + (g.n * d * 2 if sage else 0),
+                 # every edge re-reads its source's product row (whole row of
+                 # the stored layout), column index and scale
+                 gather_bytes=g.nnz * (8 + (bg.q8_row(d) if q8 else 2 * ((d + 7) // 8 * 8)))
+                 + g.n * d * 4,
+                 gather_gbs=(g.nnz * (8 + (bg.q8_row(d) if q8 else 2 * ((d + 7) // 8 * 8)))
+                             + g.n * d * 4) / t_spmm / 1e9),
         ]
         if t_self is not None:
             kernels.append(dict(kernel="bgemm_self", layer=l, us=t_self * 1e6, bound="alu",
