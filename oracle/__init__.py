@@ -62,6 +62,9 @@ def _load():
         lib.oracle_sage_layer.argtypes = [_i64, _p, _p, _p, _i64, _i32, _p, _p, _p,
                                           _p, _i32, _p, _int, _p, _i64, _p, _p, _p,
                                           _p, _p]
+        lib.oracle_layer_backward.restype = _int
+        lib.oracle_layer_backward.argtypes = [_i64, _p, _p, _int, _p, _i64, _i32, _p,
+                                              _i32, _p, _p, _int] + [_p] * 9
         lib.oracle_threads.restype = _int
         lib.oracle_threads.argtypes = []
         _lib = lib
@@ -213,6 +216,37 @@ def sage_forward(rowptr, colidx, x, weights_self_t, weights_neigh_t, biases,
         res.append((z, m, out))
         h = out
     return res
+
+
+def layer_backward(rowptr, colidx, norm, h, wt, gout, out=None, act="none"):
+    """Back propagation of one binarised layer (Alg. 1, Eqs. (14)-(15)).
+    Returns a dict of fp64 arrays: dzeta, mass_dzeta [n, d_out]; dwt_tilde,
+    mass_dwt, dwt [d_out, d_in] (W^T layout); dh_tilde, mass_dh, dh
+    [n, d_in]; db [d_out]."""
+    rowptr = _c(rowptr, np.int64)
+    colidx = _c(colidx, np.int32)
+    h = _c(h, np.float32)
+    wt = _c(wt, np.float32)
+    gout = _c(gout, np.float32)
+    n, d_in = h.shape
+    d_out = wt.shape[0]
+    assert wt.shape[1] == d_in and gout.shape == (n, d_out)
+    if act == "relu":
+        out = _c(out, np.float32)
+        assert out.shape == (n, d_out)
+    r = {k: np.zeros(shape, dtype=np.float64) for k, shape in (
+        ("dzeta", (n, d_out)), ("mass_dzeta", (n, d_out)), ("dwt_tilde", (d_out, d_in)),
+        ("mass_dwt", (d_out, d_in)), ("dh_tilde", (n, d_in)), ("mass_dh", (n, d_in)),
+        ("dh", (n, d_in)), ("dwt", (d_out, d_in)), ("db", (d_out,)))}
+    rc = _load().oracle_layer_backward(
+        n, rowptr.ctypes.data, colidx.ctypes.data, NORMS[norm], h.ctypes.data, d_in, d_in,
+        wt.ctypes.data, d_out, gout.ctypes.data, _ptr(out if act == "relu" else None),
+        ACTS[act], *[r[k].ctypes.data for k in ("dzeta", "mass_dzeta", "dwt_tilde",
+                                                 "mass_dwt", "dh_tilde", "mass_dh", "dh",
+                                                 "dwt", "db")])
+    if rc != 0:
+        raise ValueError("oracle_layer_backward failed (%d)" % rc)
+    return r
 
 
 def forward(rowptr, colidx, norm, x, weights_t, biases, acts=None, mu=None,

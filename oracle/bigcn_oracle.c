@@ -40,6 +40,10 @@
  *       per-channel bias is optional.
  *   R10 The two-weight GraphSAGE layer (oracle_sage_layer) transforms
  *       before it aggregates, as Eq. (13) does; see that function.
+ *   R12 Back propagation (oracle_layer_backward): Eq. (14) as printed,
+ *       the indicator on the magnitude of dL/dH~ itself; no term for the
+ *       dependence of β on H (Eq. (14) has none); the straight-through
+ *       estimator 1[|W| < 1] for dB/dW in Eq. (15).
  *
  * Every reduction runs sequentially in a fixed order in double precision;
  * OpenMP only splits independent rows, so results do not depend on the
@@ -393,6 +397,133 @@ done:
   free(beta);
   free(dots);
   free(dotn);
+  return rc;
+}
+
+/* ---------------------------------------------------------------------
+ * oracle_layer_backward: the back propagation of one binarised layer,
+ * Alg. 1 with Eqs. (14)-(15), in the order the algorithm states it:
+ *   G      = dL/dH^(l+1), masked by 1[out > 0] when the layer has ReLU
+ *   db_k   = sum_i G_ik                         (the optional bias)
+ *   dζ     = Ã^T G                              (first step of Alg. 1)
+ *   dW~    = H~^T dζ,   H~ = diag(β) F          (Eqs. (7)-(8))
+ *   dH~    = dζ W~^T,   W~ = B diag(α)          (Eqs. (3)-(4))
+ *   dH     = dH~ * 1[|dH~| < 1]                 (Eq. (14), reading R12)
+ *   dW_ij  = (1/d_in) B_ij sum_k dW~_kj B_kj + α_j dW~_ij 1[|W_ij| < 1]
+ *                                               (Eq. (15), straight-through
+ *                                                estimator for sign)
+ * Ã^T is taken on the CSR of Â, which must be structurally symmetric (an
+ * undirected graph with self-loops): (Ã^T G)_j = sum_{i in N(j)} Ã_ij G_i.
+ * Every sum runs sequentially in a fixed order in double precision.
+ *   h     [n][ldh] fp32 layer input H (before binarisation)
+ *   wt    [d_out][d_in] fp32 W^T;  gout [n][d_out] fp32 dL/dH^(l+1)
+ *   out   [n][d_out] fp32 forward output (read only for ReLU; nullable else)
+ * Outputs (doubles):  dzeta, mass_dzeta [n][d_out]; dwt_tilde, mass_dwt
+ *   [d_out][d_in] (W^T layout); dh_tilde, mass_dh [n][d_in]; dh [n][d_in];
+ *   dwt [d_out][d_in]; db [d_out].  mass_* hold the sum of the absolute
+ *   values of the terms of each entry.
+ * Returns 0, -1 on a non-finite input, -2 on allocation failure.
+ * ------------------------------------------------------------------- */
+int oracle_layer_backward(int64_t n, const int64_t* rowptr, const int32_t* colidx,
+                          int norm, const float* h, int64_t ldh, int32_t d_in,
+                          const float* wt, int32_t d_out, const float* gout,
+                          const float* out, int act, double* dzeta,
+                          double* mass_dzeta, double* dwt_tilde, double* mass_dwt,
+                          double* dh_tilde, double* mass_dh, double* dh, double* dwt,
+                          double* db) {
+  const int64_t ldw = (d_in + 63) / 64;
+  int rc = 0;
+  uint64_t* fbits = calloc((size_t)(n ? n : 1) * ldw, sizeof(uint64_t));
+  double* beta = calloc((size_t)(n ? n : 1), sizeof(double));
+  uint64_t* wbits = calloc((size_t)d_out * ldw, sizeof(uint64_t));
+  double* alpha = calloc((size_t)d_out, sizeof(double));
+  double* G = calloc((size_t)(n ? n : 1) * d_out, sizeof(double));
+  if (!fbits || !beta || !wbits || !alpha || !G) {
+    rc = -2;
+    goto done;
+  }
+  if (oracle_binarize(h, n, d_in, ldh, NULL, NULL, NULL, 0, fbits, ldw, beta) != 0 ||
+      oracle_binarize(wt, d_out, d_in, d_in, NULL, NULL, NULL, 0, wbits, ldw, alpha) != 0) {
+    rc = -1;
+    goto done;
+  }
+  /* The incoming gradient, through the activation. */
+  for (int64_t i = 0; i < n; ++i)
+    for (int32_t k = 0; k < d_out; ++k) {
+      double gv = (double)gout[i * d_out + k];
+      if (act == ORACLE_ACT_RELU && !(out[i * d_out + k] > 0.0f)) gv = 0.0;
+      G[i * d_out + k] = gv;
+    }
+  /* Bias: dL/db_k = sum_i G_ik. */
+  for (int32_t k = 0; k < d_out; ++k) {
+    double s = 0.0;
+    for (int64_t i = 0; i < n; ++i) s += G[i * d_out + k];
+    db[k] = s;
+  }
+  /* dζ = Ã^T G, row j gathering the rows i of its (symmetric) neighbourhood. */
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int64_t j = 0; j < n; ++j) {
+    int64_t deg_j = rowptr[j + 1] - rowptr[j];
+    for (int32_t k = 0; k < d_out; ++k) {
+      double s = 0.0, m = 0.0;
+      for (int64_t e = rowptr[j]; e < rowptr[j + 1]; ++e) {
+        int64_t i = colidx[e];
+        int64_t deg_i = rowptr[i + 1] - rowptr[i];
+        double t = atilde(norm, deg_i, deg_j) * G[i * d_out + k];  /* Ã_ij G_ik */
+        s += t;
+        m += fabs(t);
+      }
+      dzeta[j * d_out + k] = s;
+      mass_dzeta[j * d_out + k] = m;
+    }
+  }
+  /* dW~ = H~^T dζ: entry (k in d_in, j in d_out), stored at [j][k]. */
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int32_t j = 0; j < d_out; ++j)
+    for (int32_t k = 0; k < d_in; ++k) {
+      double s = 0.0, m = 0.0;
+      for (int64_t i = 0; i < n; ++i) {
+        double ht = beta[i] * (double)sign_at(fbits + i * ldw, k);  /* H~_ik */
+        double t = ht * dzeta[i * d_out + j];
+        s += t;
+        m += fabs(t);
+      }
+      dwt_tilde[(int64_t)j * d_in + k] = s;
+      mass_dwt[(int64_t)j * d_in + k] = m;
+    }
+  /* dH~ = dζ W~^T and Eq. (14). */
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int64_t i = 0; i < n; ++i)
+    for (int32_t k = 0; k < d_in; ++k) {
+      double s = 0.0, m = 0.0;
+      for (int32_t j = 0; j < d_out; ++j) {
+        double wtl = (double)sign_at(wbits + (int64_t)j * ldw, k) * alpha[j];  /* W~_kj */
+        double t = dzeta[i * d_out + j] * wtl;
+        s += t;
+        m += fabs(t);
+      }
+      dh_tilde[i * d_in + k] = s;
+      mass_dh[i * d_in + k] = m;
+      dh[i * d_in + k] = fabs(s) < 1.0 ? s : 0.0;
+    }
+  /* Eq. (15) per weight, W_ij = wt[j][i]. */
+  for (int32_t j = 0; j < d_out; ++j) {
+    double colsum = 0.0;  /* sum_k dW~_kj B_kj */
+    for (int32_t k = 0; k < d_in; ++k)
+      colsum += dwt_tilde[(int64_t)j * d_in + k] * (double)sign_at(wbits + (int64_t)j * ldw, k);
+    for (int32_t i = 0; i < d_in; ++i) {
+      double bij = (double)sign_at(wbits + (int64_t)j * ldw, i);
+      double ste = fabs((double)wt[(int64_t)j * d_in + i]) < 1.0 ? 1.0 : 0.0;
+      dwt[(int64_t)j * d_in + i] = bij * colsum / (double)d_in +
+                                   alpha[j] * dwt_tilde[(int64_t)j * d_in + i] * ste;
+    }
+  }
+done:
+  free(fbits);
+  free(beta);
+  free(wbits);
+  free(alpha);
+  free(G);
   return rc;
 }
 
