@@ -222,6 +222,54 @@ bigcn_status bigcn_spmm_csr_sage_q8(int64_t n, int64_t nnz, const int64_t* rowpt
                                     void* stream);
 
 /* ---------------------------------------------------------------------------
+ * bigcn_layer_backward -- back propagation of one binarised graph-convolution
+ * layer (Alg. 1 with Eqs. (14)-(15); training is outside the forward path,
+ * this is the gradient the paper's algorithm defines):
+ *   G     = gout, masked by 1[out > 0] when act is RELU
+ *   db    = sum_i G_i                       dζ = Ã^T G
+ *   dW~   = H~^T dζ,   H~ = diag(β) sign(H) (Eqs. (7)-(8))
+ *   dH~   = dζ W~^T,   W~ = sign(W) diag(α) (Eqs. (3)-(4))
+ *   dH    = dH~ * 1[|dH~| < 1]              (Eq. (14), the indicator taken
+ *                                            on |dH~| as printed)
+ *   dW_ij = B_ij / d_in * sum_k dW~_kj B_kj + α_j dW~_ij 1[|W_ij| < 1]
+ *                                           (Eq. (15), straight-through
+ *                                            estimator for sign)
+ * The CSR of Â must be structurally symmetric (an undirected graph with its
+ * self-loops, as for the forward); Ã and its normalisation as for
+ * bigcn_spmm_csr.
+ *   h      [n][ldh] fp32 layer input (before binarisation), ldh >= d_in
+ *   wt     [d_out][ldwt] fp32 W^T; wbits [d_out][ldw], alpha fp32[d_out]:
+ *          W^T packed by bigcn_binarize_pack
+ *   gout   [n][ldg] fp32 dL/dH^(l+1); out [n][ldo] the forward output of
+ *          the layer (read for RELU only, may be NULL otherwise)
+ *   dwt    [d_out][lddw] fp32 dL/dW in the W^T layout (required)
+ *   dh, dh_tilde  [n][ld] fp32 dL/dH and dL/dH~, each nullable
+ *   dwt_tilde [d_out][lddwt] fp32 dL/dW~ (W^T layout), db fp32[d_out],
+ *          dzeta [n][lddz] fp32 dL/dζ: each nullable
+ *   workspace  bigcn_layer_backward_workspace_bytes(n, nnz, d_in, d_out)
+ *          bytes, 256-byte aligned; contents on entry are ignored.
+ * Sums over nodes (db, dW~) are formed in fp64 over fixed chunks of rows
+ * and added in order; every result is reproducible bit for bit.
+ * Errors: EINVAL (bad sizes, NULL required pointers, short leading
+ *         dimensions, bad norm / act), EALIGN (pointers not aligned to their
+ *         element size, workspace not 256-byte aligned), EWORKSPACE,
+ *         EUNSUPPORTED (d_in > 2048 or d_out > 256).
+ * ------------------------------------------------------------------------- */
+size_t bigcn_layer_backward_workspace_bytes(int64_t n, int64_t nnz, int32_t d_in,
+                                            int32_t d_out);
+bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                  const int32_t* colidx, bigcn_norm norm, const float* h,
+                                  int64_t ldh, int32_t d_in, const float* wt, int64_t ldwt,
+                                  const uint64_t* wbits, int64_t ldw, const float* alpha,
+                                  int32_t d_out, const float* gout, int64_t ldg,
+                                  const float* out, int64_t ldo, bigcn_act act,
+                                  float* dh, int64_t lddh, float* dh_tilde,
+                                  int64_t lddht, float* dwt, int64_t lddw,
+                                  float* dwt_tilde, int64_t lddwt, float* db,
+                                  float* dzeta, int64_t lddz, void* workspace,
+                                  size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * bigcn_forward -- the whole multi-layer forward pass (Sec. 4.1):
  *     H^(0) = X,  H^(l+1) = act_l( Ã ζ^(l) + b_l ),  l = 0 .. n_layers-1,
  * every layer binarised (features and weights).  Layer 0 standardises X with

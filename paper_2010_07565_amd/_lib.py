@@ -28,7 +28,8 @@ ALGOS = {"auto": 0, "popcount": 1, "mfma_i8": 2}
 # Every entry point declared in include/bigcn.h.
 EXPORTS = ("bigcn_binarize_pack", "bigcn_bgemm", "bigcn_spmm_workspace_bytes",
            "bigcn_spmm_csr", "bigcn_bgemm_q8", "bigcn_spmm_csr_q8",
-           "bigcn_spmm_csr_sage_q8",
+           "bigcn_spmm_csr_sage_q8", "bigcn_layer_backward_workspace_bytes",
+           "bigcn_layer_backward",
            "bigcn_forward_workspace_bytes", "bigcn_forward", "bigcn_status_string")
 
 
@@ -80,6 +81,12 @@ def load() -> ctypes.CDLL:
     lib.bigcn_spmm_csr_sage_q8.argtypes = [_i64, _i64, _p, _p, _p, _p, _i64, _p, _i64,
                                            _i32, _i32, _p, _p, _i64, _p, _p, _int, _p,
                                            _i64, _p, _sz, _p]
+    lib.bigcn_layer_backward_workspace_bytes.restype = _sz
+    lib.bigcn_layer_backward_workspace_bytes.argtypes = [_i64, _i64, _i32, _i32]
+    lib.bigcn_layer_backward.restype = _int
+    lib.bigcn_layer_backward.argtypes = ([_i64, _i64, _p, _p, _int, _p, _i64, _i32, _p, _i64,
+                                          _p, _i64, _p, _i32, _p, _i64, _p, _i64, _int]
+                                         + [_p, _i64] * 4 + [_p, _p, _i64, _p, _sz, _p])
     lib.bigcn_spmm_csr_q8.restype = _int
     lib.bigcn_spmm_csr_q8.argtypes = [_i64, _i64, _p, _p, _int, _p, _p, _i64, _p, _i64,
                                       _i32, _i32, _p, _p, _int, _p, _i64, _p, _sz, _p]
@@ -239,6 +246,38 @@ def bigcn_spmm_csr_sage_q8(rowptr: torch.Tensor, colidx: torch.Tensor, g: torch.
         _ld(out, "out"), _dev(workspace, torch.uint8, "workspace"),
         workspace.numel() if workspace is not None else 0, _stream(stream))
     _check("bigcn_spmm_csr_sage_q8", st)
+
+
+def layer_backward_workspace_bytes(n: int, nnz: int, d_in: int, d_out: int) -> int:
+    return load().bigcn_layer_backward_workspace_bytes(n, nnz, d_in, d_out)
+
+
+def _ldn(t, name):
+    return (None, 0) if t is None else (_dev(t, torch.float32, name), _ld(t, name))
+
+
+def bigcn_layer_backward(rowptr: torch.Tensor, colidx: torch.Tensor, h: torch.Tensor,
+                         wt: torch.Tensor, wbits: torch.Tensor, alpha: torch.Tensor,
+                         gout: torch.Tensor, dwt: torch.Tensor, workspace: torch.Tensor,
+                         norm: str = "sym", act: str = "none", out=None, dh=None,
+                         dh_tilde=None, dwt_tilde=None, db=None, dzeta=None,
+                         nnz: Optional[int] = None, stream=None) -> None:
+    """Back propagation of one binarised layer (Alg. 1, Eqs. (14)-(15))."""
+    n, d_in = h.shape
+    d_out = wt.shape[0]
+    nnz = colidx.shape[0] if nnz is None else nnz
+    o = _ldn(out, "out")
+    st = load().bigcn_layer_backward(
+        n, nnz, _dev(rowptr, torch.int64, "rowptr"), _dev(colidx, torch.int32, "colidx"),
+        NORMS[norm], _dev(h, torch.float32, "h"), _ld(h, "h"), d_in,
+        _dev(wt, torch.float32, "wt"), _ld(wt, "wt"), _dev(wbits, torch.int64, "wbits"),
+        _ld(wbits, "wbits"), _dev(alpha, torch.float32, "alpha"), d_out,
+        _dev(gout, torch.float32, "gout"), _ld(gout, "gout"), o[0], o[1], ACTS[act],
+        *_ldn(dh, "dh"), *_ldn(dh_tilde, "dh_tilde"), _dev(dwt, torch.float32, "dwt"),
+        _ld(dwt, "dwt"), *_ldn(dwt_tilde, "dwt_tilde"),
+        None if db is None else _dev(db, torch.float32, "db"), *_ldn(dzeta, "dzeta"),
+        _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    _check("bigcn_layer_backward", st)
 
 
 def q8_lane_bytes(d: int) -> int:

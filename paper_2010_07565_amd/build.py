@@ -7,7 +7,8 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libbigcn.so")
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("bigcn_kernels.hip", "bigcn_api.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f)
+           for f in ("bigcn_kernels.hip", "bigcn_api.hip", "bigcn_backward.hip")]
 
 # -packed-fp32-ops keeps the compiler from emitting packed fp32 VALU ops.
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

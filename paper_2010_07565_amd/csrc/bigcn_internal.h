@@ -9,10 +9,11 @@
 
 namespace bigcn {
 
-// Element storage of binary-GEMM products (same values as bigcn_itype).
-enum class IType : int { I32 = 0, I16 = 1, F16 = 2 };
+// Element storage of binary-GEMM products (same values as bigcn_itype), and
+// fp32 rows for the aggregation of gradients (internal only).
+enum class IType : int { I32 = 0, I16 = 1, F16 = 2, F32 = 3 };
 
-inline size_t itype_size(IType t) { return t == IType::I32 ? 4 : 2; }
+inline size_t itype_size(IType t) { return (t == IType::I32 || t == IType::F32) ? 4 : 2; }
 
 // Sign-pack rows of x; see bigcn_binarize_pack.  sym != 0 folds D̂^-1/2 into
 // the scale when rowptr is given.
@@ -87,6 +88,7 @@ hipError_t launch_spmm_rows(int64_t n, int64_t nnz, const int64_t* rowptr,
                             const SpmmPlan& plan, void* workspace,
                             hipStream_t stream);
 // Aggregation proper; requires launch_spmm_rows to have run on `workspace`.
+// mean: 0 symmetric, 1 mean, 2 no destination factor (see row_factor_deg).
 hipError_t launch_spmm(int64_t n, int64_t nnz, const int64_t* rowptr,
                        const int32_t* colidx, int mean, const float* g,
                        const void* C, IType ct, int32_t d, int64_t ldc,

@@ -211,6 +211,8 @@ template <>
 struct Vec4<int16_t> { typedef short4_t type; };
 template <>
 struct Vec4<int32_t> { typedef int4_t type; };
+template <>
+struct Vec4<float> { typedef float4_t type; };
 
 template <typename T>
 __device__ inline T from_int(int v) { return (T)v; }
@@ -578,9 +580,12 @@ __device__ inline void write_empty(float* __restrict__ out, int64_t ldo,
   store_out(out + r * ldo + c0, ep, v);
 }
 
+// Destination-side factor of Ã for a row with deg entries: D̂^-1/2 (mean 0,
+// symmetric), D̂^-1 (mean 1), or none (mean 2: the transpose of the mean
+// normalisation, whose factor sits on the source side).
 __device__ inline float row_factor_deg(int64_t deg, int mean) {
   const float dg = (float)deg;
-  return mean ? 1.0f / dg : 1.0f / sqrtf(dg);
+  return mean == 2 ? 1.0f : mean ? 1.0f / dg : 1.0f / sqrtf(dg);
 }
 
 __device__ inline float row_factor(const int64_t* __restrict__ rowptr, int64_t r,
@@ -742,6 +747,12 @@ template <>
 struct Gather<int32_t> {
   __device__ static int4_t load(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
     return __builtin_bit_cast(int4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0));
+  }
+};
+template <>
+struct Gather<float> {
+  __device__ static float4_t load(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
+    return __builtin_bit_cast(float4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0));
   }
 };
 
@@ -1724,6 +1735,10 @@ hipError_t launch_spmm(int64_t n, int64_t nnz, const int64_t* rowptr,
       return spmm_dispatch_l<int16_t>(n, nnz, rowptr, colidx, mean, g,
                                       (const int16_t*)C, d, ldc, alpha, bias,
                                       relu, out, ldo, plan, workspace, stream);
+    case IType::F32:
+      return spmm_dispatch_l<float>(n, nnz, rowptr, colidx, mean, g, (const float*)C, d,
+                                    ldc, alpha, bias, relu, out, ldo, plan, workspace,
+                                    stream);
     default:
       return spmm_dispatch_l<int32_t>(n, nnz, rowptr, colidx, mean, g,
                                       (const int32_t*)C, d, ldc, alpha, bias,

@@ -243,3 +243,32 @@ def test_forward_rejects_sage_layer_with_symmetric_norm():
     short = (L * 1)(L(100, 16, FAKE, 2, FAKE, None, 0, FAKE, 1, FAKE))
     args[4], args[9] = 1, short
     assert lib.bigcn_forward(*args) == EINVAL        # ldw_self < ceil(100/64)
+
+
+def test_layer_backward_validation():
+    lib = bg.load()
+    f = lib.bigcn_layer_backward
+    n, nnz, d_in, d_out = 10, 40, 100, 7
+    need = lib.bigcn_layer_backward_workspace_bytes(n, nnz, d_in, d_out)
+    assert need > 0
+    assert lib.bigcn_layer_backward_workspace_bytes(n, nnz, 0, d_out) == 0
+    # n nnz rowptr colidx norm h ldh d_in wt ldwt wbits ldw alpha d_out gout ldg out ldo act
+    # dh lddh dht lddht dwt lddw dwtt lddwt db dzeta lddz ws bytes stream
+    ok = [n, nnz, FAKE, FAKE, 0, FAKE, d_in, d_in, FAKE, d_in, FAKE, 2, FAKE, d_out, FAKE,
+          d_out, None, 0, 0, FAKE, d_in, None, 0, FAKE, d_in, None, 0, None, None, 0, FAKE,
+          need, None]
+    for pos, val, want in [(6, 99, EINVAL), (11, 1, EINVAL), (15, 6, EINVAL),
+                           (18, 1, EINVAL),            # ReLU without the forward output
+                           (23, None, EINVAL), (24, 99, EINVAL), (4, 7, EINVAL),
+                           (31, need - 1, EWORKSPACE), (30, FAKE + 64, EALIGN),
+                           (5, FAKE + 2, EALIGN), (10, FAKE + 4, EALIGN)]:
+        args = list(ok)
+        args[pos] = val
+        assert f(*args) == want, (pos, val)
+    big = list(ok)
+    big[7], big[6], big[9], big[20], big[24] = 3000, 3000, 3000, 3000, 3000
+    big[11] = 47
+    assert f(*big) == EUNSUPPORTED
+    wide = list(ok)
+    wide[13], wide[15] = 300, 300
+    assert f(*wide) == EUNSUPPORTED
