@@ -34,7 +34,11 @@ Prints one JSON line.  Besides the forward-pass throughput it carries
     python bench.py --bgemm-ab
 
 runs only the two-algorithm comparison, over the layer shapes of all five
-workloads, and prints it as one JSON line.
+workloads, and prints it as one JSON line;
+
+    python bench.py --backward [--workload N]
+
+times the back propagation of every layer (bigcn_layer_backward) instead.
 """
 from __future__ import annotations
 
@@ -160,6 +164,51 @@ def measured_traffic(workload_name, layer, entry):
         if e["layer"] == layer and e["entry"] == entry:
             return e["fetch_bytes"] + e["write_bytes"]
     return None
+
+
+def backward_bench(w, model, x, rowptr, colidx, args, torch, bg, dev):
+    """Every layer's bigcn_layer_backward on the workload's shapes: layer 0
+    reads the features, deeper layers a seeded N(0,1) stand-in input, the
+    incoming gradient is seeded N(0, 0.05^2).  All outputs are requested
+    (dH, dH~, dW, dW~, db, dzeta).  Per-layer durations from time_calls; a
+    step is the whole backward pass (the sum)."""
+    import numpy as np
+    import workloads
+    g = w.graph
+    if w.weights_self_t is not None:
+        raise SystemExit("bench.py --backward: the back propagation covers the "
+                         "graph-convolution layer (workloads 1-5)")
+    layers = []
+    total = 0.0
+    for l, wt in enumerate(w.weights_t):
+        d_out, d_in = wt.shape
+        h = x if l == 0 else torch.from_numpy(
+            workloads.layer_input(g.n, d_in, seed=3000 + l)).to(dev)
+        G = torch.from_numpy((np.random.default_rng(50 + l).standard_normal(
+            (g.n, d_out)) * 0.05).astype(np.float32)).to(dev)
+        wt_t = torch.from_numpy(wt).to(dev)
+        ly = model.layers[l]
+        outs = dict(dh=torch.empty((g.n, d_in), device=dev),
+                    dh_tilde=torch.empty((g.n, d_in), device=dev),
+                    dwt_tilde=torch.empty((d_out, d_in), device=dev),
+                    db=torch.empty(d_out, device=dev),
+                    dzeta=torch.empty((g.n, d_out), device=dev))
+        dwt = torch.empty((d_out, d_in), device=dev)
+        ws = torch.empty(bg.layer_backward_workspace_bytes(g.n, g.nnz, d_in, d_out),
+                         dtype=torch.uint8, device=dev)
+        t = time_calls(lambda: bg.bigcn_layer_backward(rowptr, colidx, h, wt_t, ly.wbits,
+                                                       ly.alpha, G, dwt, ws, w.norm, **outs),
+                       args.kernel_reps, torch)
+        total += t
+        flops = 2.0 * 2.0 * g.n * d_in * d_out          # dW~ and dH~ products
+        layers.append(dict(layer=l, d_in=d_in, d_out=d_out, us=round(t * 1e6, 3),
+                           gflops=round(flops / t / 1e9, 1)))
+        log("  backward L%d %d->%d: %.2f us (%.0f GFLOP/s for dW~ and dH~)" % (
+            l, d_in, d_out, t * 1e6, flops / t / 1e9))
+    return {"metric": "nodes/sec full Bi-GCN backward (Alg. 1, Eqs. (14)-(15))",
+            "value": round(g.n / total, 1), "unit": "nodes/s",
+            "ms_per_step": round(total * 1e3, 5), "workload": w.name, "layers": layers,
+            "data": "synthetic (seeded inputs and incoming gradients)"}
 
 
 def traffic_probe(w, model, x, rowptr, colidx, torch, bg, dev):
@@ -290,6 +339,9 @@ def main():
                     help="call each entry point of the workload once, eagerly, then "
                          "copy 256 MiB device to device (the counter calibration "
                          "kernel): the program profiled for HBM byte counters")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the back propagation of every layer of the workload "
+                         "(Alg. 1, Eqs. (14)-(15)) instead of the forward pass")
     ap.add_argument("--bgemm-ab", action="store_true",
                     help="only compare the two binary-GEMM algorithms on every "
                          "workload's layer shapes")
@@ -333,6 +385,10 @@ def main():
     torch.cuda.synchronize()
     if args.traffic_probe:
         traffic_probe(w, model, x, rowptr, colidx, torch, bg, dev)
+        return
+    if args.backward:
+        print(json.dumps(backward_bench(w, model, x, rowptr, colidx, args, torch, bg, dev)),
+              flush=True)
         return
 
     # ---- the timed forward passes: eager calls, then the same pass replayed

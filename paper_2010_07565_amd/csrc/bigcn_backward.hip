@@ -55,7 +55,7 @@ __global__ __launch_bounds__(kB) void k_bwd_prep(
 }
 
 // Column sums of Gm over a chunk of R rows (block = chunk), fp64, rows in
-// order; then the chunks in order.
+// order (eight loads in flight); then the chunks in order.
 __global__ __launch_bounds__(kB) void k_bwd_colsum_part(
     int64_t n, int32_t d, const float* __restrict__ Gm, int64_t ldm, int64_t R,
     double* __restrict__ part) {
@@ -63,7 +63,15 @@ __global__ __launch_bounds__(kB) void k_bwd_colsum_part(
   const int64_t i0 = c * R, i1 = std::min<int64_t>(n, i0 + R);
   for (int k = threadIdx.x; k < d; k += kB) {
     double acc = 0.0;
-    for (int64_t i = i0; i < i1; ++i) acc += (double)Gm[i * ldm + k];
+    int64_t i = i0;
+    for (; i + 8 <= i1; i += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = Gm[(i + u) * ldm + k];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc += (double)v[u];
+    }
+    for (; i < i1; ++i) acc += (double)Gm[i * ldm + k];
     part[c * d + k] = acc;
   }
 }
@@ -73,36 +81,69 @@ __global__ __launch_bounds__(kB) void k_bwd_colsum_final(
   const int k = blockIdx.x * kB + threadIdx.x;
   if (k >= d) return;
   double acc = 0.0;
-  for (int64_t c = 0; c < chunks; ++c) acc += part[c * d + k];
+  int64_t c = 0;
+  for (; c + 8 <= chunks; c += 8) {  // eight loads in flight, added in order
+    double v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = part[(c + u) * d + k];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += v[u];
+  }
+  for (; c < chunks; ++c) acc += part[c * d + k];
   db[k] = (float)acc;
 }
 
 // Partial sums of dW~^T over a chunk of R rows:
 //   part[c][j][64w + b] = sum_{i in chunk c} s(F_i, 64w + b) * β_i dζ_ij.
-// Block (chunk c, word w, 256 columns); thread = column j; 64 fp64
-// accumulators, one per bit of the word.  Row words are wave-uniform.
+// Block (chunk c, word w, 64 columns): thread (column j, bit group q) owns
+// bits 16q .. 16q+15 of the word for column j.  Each run of 64 rows is
+// summed in fp32 (at most 64 terms) and added to fp64 accumulators, in row
+// order.  Row words are wave-uniform.
 __global__ __launch_bounds__(kB) void k_bwd_wtilde_part(
     int64_t n, int32_t d_in, int32_t d_out, const uint64_t* __restrict__ F, int64_t ldf,
     const float* __restrict__ beta, const float* __restrict__ dz, int64_t lddz,
     int64_t R, double* __restrict__ part) {
   const int64_t c = blockIdx.x;
   const int w = blockIdx.y;
-  const int j = blockIdx.z * kB + threadIdx.x;
-  if (j >= d_out) return;  // no barrier in this kernel
+  const int j = blockIdx.z * 64 + (threadIdx.x & 63);
+  const int q = threadIdx.x >> 6;  // wave index: bit group
+  if (j >= d_out) return;          // no barrier in this kernel
   const int64_t i0 = c * R, i1 = std::min<int64_t>(n, i0 + R);
-  double acc[64];
+  double acc[16];
 #pragma unroll
-  for (int b = 0; b < 64; ++b) acc[b] = 0.0;
-  for (int64_t i = i0; i < i1; ++i) {
-    const double x = (double)(beta[i] * dz[i * lddz + j]);
-    const uint64_t word = F[i * ldf + w];
+  for (int b = 0; b < 16; ++b) acc[b] = 0.0;
+  for (int64_t r0 = i0; r0 < i1; r0 += 64) {
+    const int64_t r1 = std::min<int64_t>(i1, r0 + 64);
+    float sub[16];
 #pragma unroll
-    for (int b = 0; b < 64; ++b) acc[b] += ((word >> b) & 1ull) ? x : -x;
+    for (int b = 0; b < 16; ++b) sub[b] = 0.f;
+    int64_t i = r0;
+    for (; i + 8 <= r1; i += 8) {  // eight rows' loads in flight, summed in order
+      float x[8];
+      uint32_t bits[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        x[u] = beta[i + u] * dz[(i + u) * lddz + j];
+        bits[u] = (uint32_t)(F[(i + u) * ldf + w] >> (16 * q)) & 0xFFFFu;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int b = 0; b < 16; ++b) sub[b] += ((bits[u] >> b) & 1u) ? x[u] : -x[u];
+    }
+    for (; i < r1; ++i) {
+      const float x = beta[i] * dz[i * lddz + j];
+      const uint32_t bits = (uint32_t)(F[i * ldf + w] >> (16 * q)) & 0xFFFFu;
+#pragma unroll
+      for (int b = 0; b < 16; ++b) sub[b] += ((bits >> b) & 1u) ? x : -x;
+    }
+#pragma unroll
+    for (int b = 0; b < 16; ++b) acc[b] += (double)sub[b];
   }
-  double* dst = part + ((int64_t)c * d_out + j) * d_in + 64 * w;
-  const int nb = std::min(64, d_in - 64 * w);
+  double* dst = part + ((int64_t)c * d_out + j) * d_in + 64 * w + 16 * q;
+  const int nb = std::min(16, d_in - 64 * w - 16 * q);
 #pragma unroll
-  for (int b = 0; b < 64; ++b)
+  for (int b = 0; b < 16; ++b)
     if (b < nb) dst[b] = acc[b];
 }
 
@@ -115,7 +156,15 @@ __global__ __launch_bounds__(kB) void k_bwd_wtilde_final(
   if (idx >= (int64_t)d_in * d_out) return;
   const int64_t j = idx / d_in, k = idx - j * d_in;
   double acc = 0.0;
-  for (int64_t c = 0; c < chunks; ++c) acc += part[(c * d_out + j) * d_in + k];
+  int64_t c = 0;
+  for (; c + 8 <= chunks; c += 8) {  // eight loads in flight, added in order
+    double v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = part[((c + u) * d_out + j) * d_in + k];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += v[u];
+  }
+  for (; c < chunks; ++c) acc += part[(c * d_out + j) * d_in + k];
   wtd[idx] = acc;
   if (out != nullptr) out[j * ldout + k] = (float)acc;
 }
@@ -209,9 +258,15 @@ BwdLayout bwd_layout(int64_t n, int64_t nnz, int32_t d_in, int32_t d_out) {
   BwdLayout L;
   L.kw = words(d_in);
   L.ldm = (d_out + 3) / 4 * 4;
-  L.R = std::max<int64_t>(256, (n + 255) / 256);  // at most 256 row chunks
+  // Row chunks of the dW~ partial sums: about 2048 blocks of (chunk, word,
+  // 64 columns), chunks of at least 64 rows, partial sums within 512 MB.
+  const int64_t per_chunk = L.kw * ((d_out + 63) / 64);
+  int64_t chunks = std::max<int64_t>(1, 2048 / per_chunk);
+  chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, (n + 63) / 64));
+  chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, (512ll << 20) / ((int64_t)d_out * d_in * 8)));
+  L.R = std::max<int64_t>(1, (n + chunks - 1) / chunks);
   L.chunks = std::max<int64_t>(1, (n + L.R - 1) / L.R);
-  L.Rdb = 4096;
+  L.Rdb = std::max<int64_t>(64, (n + 4095) / 4096);  // at most 4096 row chunks
   L.chunks_db = std::max<int64_t>(1, (n + L.Rdb - 1) / L.Rdb);
   size_t off = 0;
   L.off_F = off;
@@ -344,7 +399,7 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
   }
   // dW~^T, then Eq. (15).
   hipLaunchKernelGGL(k_bwd_wtilde_part, dim3((unsigned)L.chunks, (unsigned)L.kw,
-                                             (unsigned)((d_out + kB - 1) / kB)),
+                                             (unsigned)((d_out + 63) / 64)),
                      dim3(kB), 0, s, n, d_in, d_out, F, L.kw, beta, dz, L.ldm, L.R, pw);
   hipLaunchKernelGGL(k_bwd_wtilde_final, dim3(grid_of((int64_t)d_in * d_out)), dim3(kB), 0,
                      s, d_in, d_out, L.chunks, pw, wtd, dwt_tilde, lddwt);
