@@ -149,6 +149,13 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
   const int64_t step = (int64_t)gridDim.x * kWavesPerBlock * RW;
   for (int64_t r0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * RW;
        r0 < rows; r0 += step) {
+    // lane q < RW: the normalisation factor of row r0 + q, loaded together
+    // with the rows so that the end of the group does not wait for it
+    float colf = 1.f;
+    if (rowptr != nullptr && sym && lane < RW && r0 + lane < rows) {
+      const int64_t dg = rowptr[r0 + lane + 1] - rowptr[r0 + lane];
+      colf = dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f;
+    }
     float v[RW][KWT];
 #pragma unroll
     for (int q = 0; q < RW; ++q) {
@@ -191,10 +198,7 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
         if (wb + lane < ldw) br[wb + lane] = wb == 0 ? mine[q] : 0ull;
       if (lane == q) {
         float sc = l1[q] / (float)cols;
-        if (rowptr != nullptr && sym) {
-          const int64_t dg = rowptr[r + 1] - rowptr[r];
-          sc = sc * (dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f);
-        }
+        if (rowptr != nullptr && sym) sc = sc * colf;
         scale[r] = sc;
       }
     }
