@@ -21,6 +21,8 @@
 
 #include <hip/hip_fp16.h>
 
+#include <type_traits>
+
 namespace bigcn {
 namespace {
 
@@ -331,6 +333,7 @@ __global__ __launch_bounds__(kBlock) void k_bgemm_pop(
 // decided per row with a ballot.
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float2_t __attribute__((ext_vector_type(2)));
 
 template <int NB>
@@ -1391,6 +1394,522 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
   }
 }
 
+// ------------------------------------------------ narrow 8-bit aggregation ----
+//
+// Layers of at most 64 output columns keep one code byte per column (column
+// k at byte k of a 64-byte row).  In the k_spmm_wave_q8 layout a wave then
+// spends one gather instruction per edge on one byte per lane.  Here a slot
+// of G lanes covers a row's columns instead, CPL codes per lane (one 4-, 8-
+// or 16-byte gather), so a wave works on S = 64 / G rows or edges at once.
+//
+// Work split: block b owns rows [b*R, b*R + R), R <= 64, and cuts their edge
+// range into four equal shares, one per wave.  A wave takes the rows that
+// start in its share and, as a partial, the row in progress where its share
+// begins.  Rows are dealt to the slots in rounds of S.  In a round a row with
+// at most kNarrowShort edges in the share is summed by its own slot, edge by
+// edge in CSR order (row-parallel); a longer one by all slots together, slot
+// q taking edges q, q + S, ... (edge-parallel), followed by a butterfly over
+// the slots.  Complete rows are then finished by their slots in parallel.
+// A row cut by a share boundary leaves its pieces in LDS; after a block
+// barrier the wave where it starts adds them in share order and finishes
+// it.  No atomics and no second kernel: the sums, and hence the results, do
+// not depend on timing.
+constexpr int kNarrowShort = 16;  // edges in a share up to which a row is row-parallel
+// rows landed per lane and batch (1 KB of LDS per wave and row for 16-byte
+// pieces, 256 B for 4-byte ones)
+template <int CPL>
+constexpr int narrow_batch() { return CPL == 4 ? 16 : 8; }
+constexpr uint32_t kPastEnd = 0x80000000u;  // buffer offset past every range: loads give 0
+
+__device__ inline int wave_max_i32(int v) {
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) v = max(v, __shfl_xor(v, m));
+  return v;
+}
+
+__device__ inline uint64_t shfl_xor_u64(uint64_t v, int m) {
+  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
+  const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Gathered code rows land in LDS (buffer loads with the lds modifier: lane
+// l's bytes go to base + size * l, a range past the buffer gives zeros), so
+// a wave keeps NB rows per lane in flight without holding them in
+// registers.  4-byte pieces for CPL == 4, else 16 bytes (CPL == 8 uses half).
+typedef __attribute__((address_space(3))) void lds_void_t;
+template <int CPL>
+struct Landed {
+  typedef typename std::conditional<CPL == 4, uint32_t, uint4>::type type;
+  static constexpr int bytes = CPL == 4 ? 4 : 16;
+};
+
+// One landed piece per lane (wave-uniform LDS destination).
+__device__ inline void land_piece16(__amdgpu_buffer_rsrc_t rs, void* lds, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)lds, 16, voff, 0, 0, 0);
+}
+__device__ inline void land_piece4(__amdgpu_buffer_rsrc_t rs, void* lds, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)lds, 4, voff, 0, 0, 0);
+}
+template <int CPL, typename T>
+__device__ inline void land_piece(__amdgpu_buffer_rsrc_t rs, T* lds, uint32_t voff) {
+  if constexpr (CPL == 4)
+    land_piece4(rs, (void*)lds, voff);
+  else
+    land_piece16(rs, (void*)lds, voff);
+}
+
+// Wait until this wave's landed rows are in LDS (vmcnt(0), other counters
+// left alone), and keep the compiler from moving LDS reads above it.
+__device__ inline void wait_landed() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __asm__ volatile("" ::: "memory");
+}
+
+__device__ inline float code_of(uint32_t w, int k) {
+  return (float)(int)(int8_t)((w >> (8 * k)) & 0xff);
+}
+
+template <int CPL>
+__device__ inline float landed_code(const typename Landed<CPL>::type& x, int k) {
+  if constexpr (CPL == 4) {
+    return code_of(x, k);
+  } else {
+    const uint32_t w = (k >> 2) == 0 ? x.x : (k >> 2) == 1 ? x.y : (k >> 2) == 2 ? x.z : x.w;
+    return code_of(w, k & 3);
+  }
+}
+
+// (dot - p) / 2 for CPL consecutive columns of a flagged row's exact products
+// (halves; row offset voff bytes).
+template <int CPL>
+__device__ inline void gather_row_exact(float (&v)[CPL], __amdgpu_buffer_rsrc_t rs,
+                                        uint32_t voff, float fpar) {
+  // whole-vector bit casts (filling a local half array dword by dword has
+  // been seen to compile into a single-dword load replicated across columns)
+  if constexpr (CPL == 16) {
+    const half8_t a = __builtin_bit_cast(half8_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                      rs, (int)voff, 0, 0));
+    const half8_t b = __builtin_bit_cast(half8_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                      rs, (int)(voff + 16), 0, 0));
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      v[k] = ((float)a[k] - fpar) * 0.5f;
+      v[8 + k] = ((float)b[k] - fpar) * 0.5f;
+    }
+  } else if constexpr (CPL == 8) {
+    const half8_t a = __builtin_bit_cast(half8_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                      rs, (int)voff, 0, 0));
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = ((float)a[k] - fpar) * 0.5f;
+  } else {
+    const half4_t a = __builtin_bit_cast(half4_t, __builtin_amdgcn_raw_buffer_load_b64(
+                                                      rs, (int)voff, 0, 0));
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = ((float)a[k] - fpar) * 0.5f;
+  }
+}
+
+// One slot's batch of landed rows added to its sums: acc[k] += g_j code_jk
+// and gs += g_j over the batch in edge order, where a flagged row (sign bit
+// of g_j) counts with weight zero; then, only if the batch holds flagged rows,
+// their exact products (dot - p) / 2 are added with weight |g_j|, again in
+// edge order.  The fixed order keeps the sums reproducible.
+template <int CPL, int NB>
+__device__ inline void narrow_accumulate(float (&acc)[CPL], float& gs,
+                                         const typename Landed<CPL>::type* base, int lane,
+                                         const float (&gv)[NB], const uint32_t (&jv)[NB],
+                                         __amdgpu_buffer_rsrc_t rs16, uint32_t rb16,
+                                         uint32_t coff16, float fpar) {
+  bool flagged = false;
+#pragma unroll
+  for (int u = 0; u < NB; ++u) {
+    const bool f = __builtin_bit_cast(int, gv[u]) < 0;
+    flagged |= f;
+    const float gj = f ? 0.f : gv[u];
+    const typename Landed<CPL>::type x = base[u * 64 + lane];
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) acc[k] = fmaf(landed_code<CPL>(x, k), gj, acc[k]);
+    gs += gj;
+  }
+  if (__builtin_amdgcn_ballot_w64(flagged) == 0) return;
+#pragma unroll
+  for (int u = 0; u < NB; ++u) {
+    const bool f = __builtin_bit_cast(int, gv[u]) < 0;
+    if (__builtin_amdgcn_ballot_w64(f) == 0) continue;
+    if (f) {
+      const float gj = fabsf(gv[u]);
+      float v[CPL];
+      gather_row_exact<CPL>(v, rs16, jv[u] * rb16 + coff16, fpar);
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) acc[k] = fmaf(v[k], gj, acc[k]);
+      gs += gj;
+    }
+    // one edge at a time, so the exact loads are not all hoisted (and held
+    // in registers) ahead of the first
+    __asm__ volatile("" ::: "memory");
+  }
+}
+
+// Epilogue constants of the narrow layout: alpha, bias and (NX == 2) the self
+// weights' alpha per column, staged in LDS by the block (zero past d); lane
+// c of a slot reads columns CPL*c + k.
+struct NarrowEpi {
+  const float* s_alpha;  // LDS [3][64]: alpha, bias, alpha_self
+  uint32_t valid;        // bit k: column CPL*c + k < d
+  int relu;
+  int32_t d;
+};
+
+// A finished row in one slot: the same epilogue as finish_row (rescale,
+// bias, self term, activation), the output written or, for NX == 1, the
+// next layer formed in place.  Its scale is the mean |value| summed in the
+// order of the pack kernel's wave reduction (lane c holds elements
+// 16c .. 16c + 15, one 16-lane row of that reduction: a balanced tree inside
+// the lane, then (row0 + row1) + (row2 + row3) across the slot), so fused and
+// chained layers agree bit for bit.  With K' = d <= 64 every next product
+// |dot| <= 64 fits an 8-bit half-code: no exact fallback is needed.
+template <int G, int CPL, int NX>
+__device__ inline void finish_slot(int64_t r, int64_t deg, int mean, const float (&sum)[CPL],
+                                   const NarrowEpi& ep, int c, float* __restrict__ out,
+                                   int64_t ldo, const NextLayer& nx, int nbn,
+                                   const uint64_t* s_bn) {
+  static_assert(CPL * G <= 64 && CPL <= 16, "narrow layout");
+  const float rowfac = deg > 0 ? row_factor_deg(deg, mean) : 0.f;
+  float gi = 0.f;
+  if (NX == 2) gi = fabsf(nx.gself[r]);
+  const float* al = ep.s_alpha + CPL * c;
+  float v[CPL];
+#pragma unroll
+  for (int k = 0; k < CPL; ++k) {
+    const bool ok = (ep.valid >> k) & 1;
+    float t = deg > 0 ? fmaf(sum[k], rowfac * al[k], al[64 + k]) : al[64 + k];
+    if (NX == 2)
+      t += ok ? gi * al[128 + k] * (float)nx.Cself[r * nx.ldself + CPL * c + k] : 0.f;
+    v[k] = act(t, ep.relu);
+  }
+  if (NX != 1 || out != nullptr) {
+#pragma unroll
+    for (int k = 0; k < CPL; ++k)
+      if ((ep.valid >> k) & 1) out[r * ldo + CPL * c + k] = v[k];
+  }
+  if (NX != 1) return;
+  uint32_t m = 0;
+  float a[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const bool ok = k < CPL && ((ep.valid >> k) & 1);
+    if (k < CPL) m |= (uint32_t)(ok && v[k] >= 0.f) << k;
+    a[k] = ok ? fabsf(v[k < CPL ? k : 0]) : 0.f;
+  }
+  uint64_t word = (uint64_t)m << (CPL * c);
+  if (G >= 2) word |= shfl_xor_u64(word, 1);
+  if (G >= 4) word |= shfl_xor_u64(word, 2);
+  float qd[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    qd[i] = (a[4 * i] + a[4 * i + 1]) + (a[4 * i + 2] + a[4 * i + 3]);
+  float l1 = (qd[0] + qd[1]) + (qd[2] + qd[3]);
+  if (G >= 2) l1 = l1 + __shfl_xor(l1, 1);
+  if (G >= 4) l1 = l1 + __shfl_xor(l1, 2);
+  float sc = l1 / (float)ep.d;
+  if (nx.sym) sc = sc * (deg > 0 ? 1.0f / sqrtf((float)deg) : 0.f);
+  const int Kn = ep.d;
+  const int par = Kn & 1;
+  for (int kq = c; kq < nx.dn; kq += G) {
+    const uint64_t z = word ^ s_bn[kq];
+    const int pc = __builtin_popcount((uint32_t)z) + __builtin_popcount((uint32_t)(z >> 32));
+    const int code = ((Kn - 2 * pc) - par) >> 1;
+    nx.C8[r * nx.ldc8 + nbn * (kq & 63) + (kq >> 6)] = (int8_t)code;
+  }
+  if (c == 0) nx.g[r] = sc;
+}
+
+template <int G, int CPL, int NX>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void k_spmm_narrow(
+    int64_t n, const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
+    int mean, const float* __restrict__ g, const int8_t* __restrict__ C8, int64_t ldc8,
+    const _Float16* __restrict__ C16, int64_t ldc16, int par, int32_t d,
+    const float* __restrict__ alpha, const float* __restrict__ bias, int relu,
+    float* __restrict__ out, int64_t ldo, int32_t rpb, NextLayer nx, int nbn,
+    const uint64_t* __restrict__ Bn, int64_t ldbn, const float* __restrict__ alpha_s) {
+  constexpr int S = 64 / G;
+  extern __shared__ uint64_t s_bn[];  // NX == 1: word 0 of each next weight column
+  __shared__ float s_part[2][kWavesPerBlock][64];  // [0] head pieces, [1] tail pieces
+  __shared__ float s_epi[3][64];                   // alpha, bias, alpha_self
+  // A chunk of CH edges lands in LDS through NLI instructions of EPI = 64 / G
+  // edges each (lane l: edge EPI i + l / G, bytes CPL (l % G) ..); chunk edge
+  // k's piece c sits at landed index G k + c, its scale at s_gk[k].
+  constexpr int EPI = 64 / G;
+  constexpr int NLI = G == 4 ? 8 : 4;
+  constexpr int CH = NLI * EPI;
+  constexpr int JR = CH / 64;
+  typedef typename Landed<CPL>::type LandT;
+  __shared__ LandT s_land[kWavesPerBlock][NLI * 64];
+  __shared__ float s_gk[kWavesPerBlock][CH];
+  const int lane = threadIdx.x & 63;
+  const int wv = wave_index_in_block();
+  const int q = lane / G;
+  const int c = lane % G;
+  const int64_t r_lo = (int64_t)blockIdx.x * rpb;
+  const int nr = (int)(n - r_lo < rpb ? n - r_lo : rpb);
+  // lane l < nr: bounds of row r_lo + l (lanes past nr repeat the last row)
+  const int64_t rl = r_lo + (lane < nr ? lane : nr - 1);
+  const int64_t st = rowptr[rl];
+  const int64_t en = rowptr[rl + 1];
+  if (NX == 1) {
+    for (int i = threadIdx.x; i < nx.dn; i += kBlock) s_bn[i] = Bn[(int64_t)i * ldbn];
+  }
+  if (threadIdx.x < 64) {
+    const int k = threadIdx.x;
+    s_epi[0][k] = k < d ? alpha[k] : 0.f;
+    s_epi[1][k] = (k < d && bias != nullptr) ? bias[k] : 0.f;
+    s_epi[2][k] = (NX == 2 && k < d) ? alpha_s[k] : 0.f;
+  }
+  NarrowEpi ep;
+  ep.s_alpha = &s_epi[0][0];
+  ep.relu = relu;
+  ep.d = d;
+  ep.valid = 0;
+#pragma unroll
+  for (int k = 0; k < CPL; ++k) ep.valid |= (uint32_t)(CPL * c + k < d) << k;
+  const int64_t eb = readlane64(st, 0);
+  const int64_t ee = readlane64(en, nr - 1);
+  const int total = (int)(ee - eb);
+  const int L = (total + kWavesPerBlock - 1) / kWavesPerBlock;
+  const bool last = wv == kWavesPerBlock - 1;
+  const int ws = min(wv * L, total);
+  const int we = last ? total : min(ws + L, total);
+  const int rs_l = (int)(st - eb);
+  const int re_l = (int)(en - eb);
+  const int o_b = (int)__builtin_popcountll(__builtin_amdgcn_ballot_w64(lane < nr && rs_l < ws));
+  const int o_e = last ? nr
+                       : (int)__builtin_popcountll(
+                             __builtin_amdgcn_ballot_w64(lane < nr && rs_l < we));
+  int h = o_b;
+  if (o_b > 0 && __builtin_amdgcn_readlane(re_l, o_b - 1) > ws) h = o_b - 1;
+  const float fpar = (float)par;
+  const uint32_t rb8 = (uint32_t)ldc8;
+  const uint32_t rb16 = (uint32_t)(ldc16 * 2);
+  const uint32_t coff8 = (uint32_t)(CPL * c);
+  const uint32_t coff16 = (uint32_t)(2 * CPL * c);
+  const __amdgpu_buffer_rsrc_t rs8 = raw_rsrc(C8, (uint32_t)(n * (int64_t)rb8));
+  const __amdgpu_buffer_rsrc_t rs16 = raw_rsrc(C16, (uint32_t)(n * (int64_t)rb16));
+  const __amdgpu_buffer_rsrc_t rsi = raw_rsrc(colidx + eb, (uint32_t)total * 4u);
+  const __amdgpu_buffer_rsrc_t rsg = raw_rsrc(g, (uint32_t)(n * 4));
+  __syncthreads();  // s_epi and s_bn are read by finish_slot
+
+  LandT* land = &s_land[wv][0];
+  float* sgk = &s_gk[wv][0];
+  // Lands chunk edges [0, nk) whose indices lane l holds in jr[r] (edge
+  // 64 r + l): their scales into sgk, their code pieces into land.
+  auto land_chunk = [&](const uint32_t (&jr)[JR], int nk) {
+    float gk[JR];
+#pragma unroll
+    for (int r = 0; r < JR; ++r)
+      gk[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                            rsg, (int)(64 * r + lane < nk ? jr[r] * 4u : kPastEnd),
+                                            0, 0));
+#pragma unroll
+    for (int i = 0; i < NLI; ++i) {
+      if (EPI * i >= nk) break;  // wave-uniform
+      const int k = EPI * i + lane / G;
+      const uint32_t j = (uint32_t)__shfl((int)jr[(EPI * i) / 64], (EPI * i) % 64 + lane / G);
+      land_piece<CPL>(rs8, land + i * 64, k < nk ? j * rb8 + coff8 : kPastEnd);
+    }
+    wait_landed();
+#pragma unroll
+    for (int r = 0; r < JR; ++r)
+      if (64 * r < nk) sgk[64 * r + lane] = gk[r];
+  };
+  // Adds chunk edges k[u] (those with ok[u]) to a slot's sums, in order u =
+  // 0..3; all four LDS reads are issued before the first is used.  A flagged
+  // source row (sign bit of g) adds its exact products instead, its index
+  // read back from colidx at byte offset ipos[u].
+  auto add_edges4 = [&](float (&a)[CPL], float& sg, const int (&k)[4], const bool (&ok)[4],
+                        const uint32_t (&ipos)[4]) {
+    LandT x[4];
+    float gv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      x[u] = land[G * k[u] + c];
+      gv[u] = ok[u] ? sgk[k[u]] : 0.f;
+    }
+    bool any = false;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const bool f = __builtin_bit_cast(int, gv[u]) < 0;
+      any |= f;
+      const float gw = f ? 0.f : gv[u];
+#pragma unroll
+      for (int kk = 0; kk < CPL; ++kk) a[kk] = fmaf(landed_code<CPL>(x[u], kk), gw, a[kk]);
+      sg += gw;
+    }
+    if (__builtin_amdgcn_ballot_w64(any) == 0) return;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const bool f = __builtin_bit_cast(int, gv[u]) < 0;
+      if (__builtin_amdgcn_ballot_w64(f) == 0) continue;
+      if (f) {
+        const uint32_t j = __builtin_amdgcn_raw_buffer_load_b32(rsi, (int)ipos[u], 0, 0);
+        float v[CPL];
+        gather_row_exact<CPL>(v, rs16, j * rb16 + coff16, fpar);
+        const float ga = fabsf(gv[u]);
+#pragma unroll
+        for (int kk = 0; kk < CPL; ++kk) a[kk] = fmaf(v[kk], ga, a[kk]);
+        sg += ga;
+      }
+      __asm__ volatile("" ::: "memory");
+    }
+  };
+  for (int base = h; base < o_e; base += S) {
+    const int idx = base + q;
+    const bool on = idx < o_e;
+    const int ix = on ? idx : base;
+    const int rs = __shfl(rs_l, ix);
+    const int re = __shfl(re_l, ix);
+    const int cb = rs > ws ? rs : ws;
+    const int ce = re < we ? re : we;
+    const int len = (on && ce > cb) ? ce - cb : 0;
+    const bool lng = len > kNarrowShort;
+    const int plen = lng ? 0 : len;  // edges of this slot's short row
+    float acc[CPL];
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) acc[k] = 0.f;
+    float gs = 0.f;
+    // Row-parallel part: the short rows' edges, concatenated in slot order
+    // (slot q's at [pq, pq + plen)), land chunk by chunk with every lane of
+    // the landing busy; each slot then walks its own row in LDS.
+    int incl = c == 0 ? plen : 0;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int v = __shfl_up(incl, off);
+      if (lane >= off) incl += v;
+    }
+    const int nshort = __shfl(incl, 63);
+    const int pq = __shfl(incl, q * G) - plen;
+    const int endq = pq + plen;
+    for (int cbase = 0; cbase < nshort; cbase += CH) {
+      const int nk = min(CH, nshort - cbase);
+      uint32_t jr[JR];
+#pragma unroll
+      for (int r = 0; r < JR; ++r) {
+        // slot holding concatenated edge kk: the first whose end exceeds it
+        const int kk = cbase + 64 * r + lane;
+        int lo = 0, hi = S - 1;
+#pragma unroll
+        for (int st = S; st > 1; st >>= 1) {
+          const int mid = (lo + hi) >> 1;
+          const int em = __shfl(endq, mid * G);
+          if (em <= kk) lo = mid + 1; else hi = mid;
+        }
+        const int pk = __shfl(pq, lo * G);
+        const int ck = __shfl(cb, lo * G);
+        jr[r] = __builtin_amdgcn_raw_buffer_load_b32(
+            rsi, (int)(64 * r + lane < nk ? (uint32_t)(ck + kk - pk) * 4u : kPastEnd), 0, 0);
+      }
+      land_chunk(jr, nk);
+      const int a0 = max(pq, cbase);
+      const int a1 = min(endq, cbase + nk);
+      const int cnt = a1 > a0 ? a1 - a0 : 0;
+      const int mc = wave_max_i32(cnt);
+      for (int t = 0; t < mc; t += 4) {
+        int k[4];
+        bool ok[4];
+        uint32_t ip[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          ok[u] = t + u < cnt;
+          k[u] = ok[u] ? a0 + t + u - cbase : 0;
+          ip[u] = (uint32_t)(cb + a0 + t + u - pq) * 4u;
+        }
+        add_edges4(acc, gs, k, ok, ip);
+      }
+    }
+    // Edge-parallel part: long rows one at a time, landed contiguously, slot
+    // q adding edges q, q + S, ...; a butterfly over the slots gives the total.
+    uint64_t lm = __builtin_amdgcn_ballot_w64(c == 0 && lng);
+    while (lm != 0) {
+      const int ld = (int)__builtin_ctzll(lm);
+      lm &= lm - 1;
+      const int lcb = __builtin_amdgcn_readlane(cb, ld);
+      const int llen = __builtin_amdgcn_readlane(len, ld);
+      float tmp[CPL];
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) tmp[k] = 0.f;
+      float tg = 0.f;
+      for (int cbase = 0; cbase < llen; cbase += CH) {
+        const int nk = min(CH, llen - cbase);
+        uint32_t jr[JR];
+#pragma unroll
+        for (int r = 0; r < JR; ++r)
+          jr[r] = __builtin_amdgcn_raw_buffer_load_b32(
+              rsi, (int)(64 * r + lane < nk ? (uint32_t)(lcb + cbase + 64 * r + lane) * 4u : kPastEnd),
+              0, 0);
+        land_chunk(jr, nk);
+        const int mt = (nk + S - 1) / S;
+        for (int t = 0; t < mt; t += 4) {
+          int k[4];
+          bool ok[4];
+          uint32_t ip[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int kq = q + S * (t + u);
+            ok[u] = kq < nk;
+            k[u] = ok[u] ? kq : 0;
+            ip[u] = (uint32_t)(lcb + cbase + kq) * 4u;
+          }
+          add_edges4(tmp, tg, k, ok, ip);
+        }
+      }
+#pragma unroll
+      for (int m = G; m < 64; m <<= 1) {
+#pragma unroll
+        for (int k = 0; k < CPL; ++k) tmp[k] += __shfl_xor(tmp[k], m);
+        tg += __shfl_xor(tg, m);
+      }
+      if (q == ld / G) {
+#pragma unroll
+        for (int k = 0; k < CPL; ++k) acc[k] = tmp[k];
+        gs = tg;
+      }
+    }
+    float sum[CPL];
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) sum[k] = 2.f * acc[k] + fpar * gs;
+    const bool headp = on && rs < ws;
+    const bool tailp = on && !headp && re > we;
+    if (headp || tailp) {
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) s_part[tailp ? 1 : 0][wv][CPL * c + k] = sum[k];
+    }
+    if (on && !headp && !tailp)
+      finish_slot<G, CPL, NX>(r_lo + idx, re - rs, mean, sum, ep, c, out, ldo, nx, nbn, s_bn);
+  }
+  __syncthreads();
+  // The row this wave started that runs past its share: its pieces, in share
+  // order, from this wave (tail) and the waves that follow (heads).
+  if (!last && o_e > o_b && L > 0) {
+    const int it = o_e - 1;
+    const int rs = __builtin_amdgcn_readlane(rs_l, it);
+    const int re = __builtin_amdgcn_readlane(re_l, it);
+    if (re > we) {
+      const int kend = min((re - 1) / L, kWavesPerBlock - 1);
+      if (lane < G) {
+        float sum[CPL];
+#pragma unroll
+        for (int k = 0; k < CPL; ++k) sum[k] = s_part[1][wv][CPL * c + k];
+        for (int m = wv + 1; m <= kend; ++m) {
+#pragma unroll
+          for (int k = 0; k < CPL; ++k) sum[k] += s_part[0][m][CPL * c + k];
+        }
+        finish_slot<G, CPL, NX>(r_lo + it, re - rs, mean, sum, ep, c, out, ldo, nx, nbn,
+                                s_bn);
+      }
+    }
+  }
+}
+
 // Rows cut by chunk boundaries: tail of the owning worker, then the heads of
 // the following workers, added in order.  A group of LC lanes (LC a power of
 // two covering the layer width, at most 64) serves one worker, so every cut
@@ -1840,6 +2359,70 @@ hipError_t spmm_q8_nb(int64_t n, int64_t nnz, const int64_t* rowptr,
 #undef BIGCN_Q8S
 }
 
+// Rows per block of the narrow aggregation: enough blocks to cover the chip
+// on small graphs, at most one row per lane of the block's row window.
+int32_t narrow_rows_per_block(int64_t n) {
+  const int64_t r = n / 1024;
+  return (int32_t)(r < 8 ? 8 : r > 64 ? 64 : r);
+}
+
+template <int G, int CPL>
+hipError_t spmm_narrow_gc(int64_t n, const int64_t* rowptr, const int32_t* colidx,
+                          int mean, const float* g, const int8_t* C8, int64_t ldc8,
+                          const void* C16, int64_t ldc16, int32_t K, int32_t d,
+                          const float* alpha, const float* bias, int relu, float* out,
+                          int64_t ldo, const FusedNext& fn, hipStream_t stream) {
+  NextLayer nx = {};
+  nx.dn = fn.d_out;
+  nx.C8 = fn.C8;
+  nx.ldc8 = fn.ldc8;
+  nx.C16 = (_Float16*)fn.C16;
+  nx.ldc16 = fn.ldc16;
+  nx.g = fn.g;
+  nx.sym = !mean;
+  nx.Cself = (const _Float16*)fn.Cself;
+  nx.ldself = fn.ldself;
+  nx.gself = g;
+  const int32_t rpb = narrow_rows_per_block(n);
+  const dim3 grid((unsigned)((n + rpb - 1) / rpb));
+  const int nbn = fn.kind == 1 ? q8_lane_bytes(fn.d_out) : 1;
+  const size_t lds = fn.kind == 1 ? (size_t)fn.d_out * sizeof(uint64_t) : 0;
+#define BIGCN_NARROW(NX)                                                                   \
+  hipLaunchKernelGGL((k_spmm_narrow<G, CPL, NX>), grid, dim3(kBlock), lds, stream, n,      \
+                     rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16, ldc16, K & 1, \
+                     d, alpha, bias, relu, out, ldo, rpb, nx, nbn, fn.wbits, fn.ldw,        \
+                     fn.alpha_self)
+  switch (fn.kind) {
+    case 1: BIGCN_NARROW(1); break;
+    case 2: BIGCN_NARROW(2); break;
+    default: BIGCN_NARROW(0); break;
+  }
+#undef BIGCN_NARROW
+  return hipGetLastError();
+}
+
+// Layers of at most 64 columns: lanes per slot and codes per lane by width.
+hipError_t spmm_narrow(int64_t n, const int64_t* rowptr, const int32_t* colidx, int mean,
+                       const float* g, const int8_t* C8, int64_t ldc8, const void* C16,
+                       int64_t ldc16, int32_t K, int32_t d, const float* alpha,
+                       const float* bias, int relu, float* out, int64_t ldo,
+                       const FusedNext& fn, hipStream_t stream) {
+  if (d <= 4)
+    return spmm_narrow_gc<1, 4>(n, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
+                                alpha, bias, relu, out, ldo, fn, stream);
+  if (d <= 8)
+    return spmm_narrow_gc<1, 8>(n, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
+                                alpha, bias, relu, out, ldo, fn, stream);
+  if (d <= 16)
+    return spmm_narrow_gc<1, 16>(n, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
+                                 alpha, bias, relu, out, ldo, fn, stream);
+  if (d <= 32)
+    return spmm_narrow_gc<2, 16>(n, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
+                                 alpha, bias, relu, out, ldo, fn, stream);
+  return spmm_narrow_gc<4, 16>(n, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
+                               alpha, bias, relu, out, ldo, fn, stream);
+}
+
 hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                           const int32_t* colidx, int mean, const float* g,
                           const int8_t* C8, int64_t ldc8, const void* C16,
@@ -1863,6 +2446,9 @@ hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                        dim3(kBlock), 0, stream, n, d, bias, relu, out, ldo);
     return hipGetLastError();
   }
+  if (q8_lane_bytes(d) == 1 && nnz < ((int64_t)1 << 31))
+    return spmm_narrow(n, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d, alpha, bias,
+                       relu, out, ldo, fn, stream);
   switch (q8_lane_bytes(d)) {
     case 1:
       return spmm_q8_nb<1>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
