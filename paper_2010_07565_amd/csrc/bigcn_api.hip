@@ -399,7 +399,14 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
     void* C16 = ws + L.off_C16[set];
     const bool q8 = bigcn::q8_supported(n, ly.d_out, ly.d_in);
     const IType ct = forward_itype(ly.d_in);
-    if (!have_products) {
+    if (!have_products && q8 && ly.wbits_self == nullptr &&
+        bigcn::pack_bgemm_q8_supported(ly.d_in, ly.d_out)) {
+      e = bigcn::launch_pack_bgemm_q8(hin, n, ly.d_in, ldin, l == 0 ? mu : nullptr,
+                                      l == 0 ? rstd : nullptr, rowptr,
+                                      norm == BIGCN_NORM_SYM, ly.wbits, ly.d_out, ly.ldw,
+                                      C8, q8_row(ly.d_out), C16, q8_row(ly.d_out), g, s);
+      if (e != hipSuccess) return BIGCN_EHIP;
+    } else if (!have_products) {
       e = bigcn::launch_pack(hin, n, ly.d_in, ldin, l == 0 ? mu : nullptr,
                              l == 0 ? rstd : nullptr, rowptr, norm == BIGCN_NORM_SYM,
                              F, L.ldF, g, s);

@@ -42,6 +42,16 @@ hipError_t launch_bgemm_mfma(const uint64_t* F, int64_t M, int64_t ldf,
 // order, 64*NB per row) to C16 and flagged by the sign bit of g.
 constexpr int q8_lane_bytes(int32_t N) { return N <= 64 ? 1 : N <= 128 ? 2 : 4; }
 bool q8_supported(int64_t n, int32_t N, int32_t K);
+// The pack of a layer's input followed, in the same kernel, by its binary
+// GEMM into 8-bit half-codes (layers of N <= 64 outputs and at most 2048
+// inputs): the codes, exact rows and flagged scale of launch_pack +
+// launch_bgemm_q8, bit for bit, without writing the packed bits.
+bool pack_bgemm_q8_supported(int32_t cols, int32_t N);
+hipError_t launch_pack_bgemm_q8(const float* x, int64_t rows, int32_t cols, int64_t ldx,
+                                const float* mu, const float* rstd, const int64_t* rowptr,
+                                int sym, const uint64_t* B, int32_t N, int64_t ldb,
+                                int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
+                                float* g, hipStream_t stream);
 hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
                            const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
                            int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,

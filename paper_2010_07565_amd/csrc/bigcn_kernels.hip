@@ -132,12 +132,18 @@ __global__ __launch_bounds__(kBlock) void k_pack(
 // Same computation with RW rows per wave in flight: all RW*kw loads of a
 // row group are issued before the first ballot, the per-column mean / rstd
 // sit in LDS, and the RW row sums are reduced together.  kw <= KWT <= 32.
-template <bool STD, int RW, int KWT>
+// With FQ the binary GEMM of a layer of N <= 64 outputs follows in place
+// (lane j: output j, its weight words in registers, the row's words being
+// the ballots): the 8-bit half-codes, exact rows and flags of
+// k_bgemm_pop_q8 (one byte per column) are written instead of the bits.
+template <bool STD, int RW, int KWT, bool FQ>
 __global__ __launch_bounds__(kBlock) void k_pack_rows(
     const float* __restrict__ x, int64_t rows, int32_t cols, int64_t ldx,
     const float* __restrict__ mu, const float* __restrict__ rstd,
     const int64_t* __restrict__ rowptr, int sym, uint64_t* __restrict__ bits,
-    int64_t ldw, float* __restrict__ scale) {
+    int64_t ldw, float* __restrict__ scale, const uint64_t* __restrict__ B, int32_t N,
+    int64_t ldb, int8_t* __restrict__ C8, int64_t ldc8, _Float16* __restrict__ C16,
+    int64_t ldc16) {
   extern __shared__ float s_norm[];  // mu[0..cols), rstd[cols..2 cols)
   if (STD) {
     for (int i = threadIdx.x; i < cols; i += kBlock) {
@@ -149,6 +155,21 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
   const int lane = threadIdx.x & 63;
   const int kw = (cols + 63) >> 6;
   const int64_t step = (int64_t)gridDim.x * kWavesPerBlock * RW;
+  // FQ: lane j's weight words, in registers (KWT <= 16) or, for the widest
+  // inputs, in LDS after the row statistics ([w][64] words)
+  constexpr bool kWLds = FQ && KWT > 16;
+  uint64_t wr[FQ && !kWLds ? KWT : 1];
+#pragma unroll
+  for (int w = 0; w < (FQ && !kWLds ? KWT : 1); ++w)
+    wr[w] = (FQ && !kWLds && lane < N && w < kw) ? B[(int64_t)lane * ldb + w] : 0ull;
+  uint64_t* s_w = reinterpret_cast<uint64_t*>(s_norm + (STD ? 2 * cols + (cols & 1) : 0));
+  if (kWLds) {
+    for (int i = threadIdx.x; i < kw * 64; i += kBlock) {
+      const int w = i >> 6, j = i & 63;
+      s_w[i] = j < N ? B[(int64_t)j * ldb + w] : 0ull;
+    }
+    __syncthreads();
+  }
   for (int64_t r0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * RW;
        r0 < rows; r0 += step) {
     // lane q < RW: the normalisation factor of row r0 + q, loaded together
@@ -170,10 +191,12 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
     }
     float l1[RW];
     uint64_t mine[RW];
+    int pc[RW];  // FQ: lane j's popcount of row XOR weights
 #pragma unroll
     for (int q = 0; q < RW; ++q) {
       l1[q] = 0.f;
       mine[q] = 0;
+      pc[q] = 0;
 #pragma unroll
       for (int w = 0; w < KWT; ++w) {
         if (w >= kw) break;  // wave-uniform
@@ -187,6 +210,10 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
         const uint64_t b = __builtin_amdgcn_ballot_w64(ok && y >= 0.f);
         l1[q] += ok ? fabsf(y) : 0.f;
         if (lane == w) mine[q] = b;
+        if constexpr (FQ) {
+          const uint64_t z = b ^ (kWLds ? s_w[w * 64 + lane] : wr[w]);
+          pc[q] += __builtin_popcount((uint32_t)z) + __builtin_popcount((uint32_t)(z >> 32));
+        }
       }
     }
 #pragma unroll
@@ -195,13 +222,27 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
     for (int q = 0; q < RW; ++q) {
       const int64_t r = r0 + q;
       if (r >= rows) break;  // wave-uniform
-      uint64_t* br = bits + r * ldw;
-      for (int64_t wb = 0; wb < ldw; wb += 64)
-        if (wb + lane < ldw) br[wb + lane] = wb == 0 ? mine[q] : 0ull;
-      if (lane == q) {
-        float sc = l1[q] / (float)cols;
-        if (rowptr != nullptr && sym) sc = sc * colf;
-        scale[r] = sc;
+      if constexpr (FQ) {
+        const int dot = cols - 2 * pc[q];
+        const int code = (dot - (cols & 1)) >> 1;
+        C8[r * ldc8 + lane] = (int8_t)code;
+        const bool flag =
+            __builtin_amdgcn_ballot_w64(lane < N && (code < -128 || code > 127)) != 0;
+        if (flag) C16[r * ldc16 + lane] = (_Float16)dot;
+        if (lane == q) {
+          float sc = l1[q] / (float)cols;
+          if (rowptr != nullptr && sym) sc = sc * colf;
+          scale[r] = flag ? -fabsf(sc) : sc;
+        }
+      } else {
+        uint64_t* br = bits + r * ldw;
+        for (int64_t wb = 0; wb < ldw; wb += 64)
+          if (wb + lane < ldw) br[wb + lane] = wb == 0 ? mine[q] : 0ull;
+        if (lane == q) {
+          float sc = l1[q] / (float)cols;
+          if (rowptr != nullptr && sym) sc = sc * colf;
+          scale[r] = sc;
+        }
       }
     }
   }
@@ -2126,28 +2167,41 @@ hipError_t spmm_dispatch_l(int64_t n, int64_t nnz, const int64_t* rowptr,
 #undef BIGCN_SPMM_L
 }
 
-template <bool STD, int RW, int KWT>
+// Fused binary GEMM of the FQ variant (unused otherwise).
+struct PackQ8 {
+  const uint64_t* B = nullptr;
+  int32_t N = 0;
+  int64_t ldb = 0;
+  int8_t* C8 = nullptr;
+  int64_t ldc8 = 0;
+  _Float16* C16 = nullptr;
+  int64_t ldc16 = 0;
+};
+
+template <bool STD, int RW, int KWT, bool FQ>
 hipError_t pack_rows_launch(const float* x, int64_t rows, int32_t cols, int64_t ldx,
                             const float* mu, const float* rstd, const int64_t* rowptr,
                             int sym, uint64_t* bits, int64_t ldw, float* scale,
-                            hipStream_t stream) {
+                            const PackQ8& pq, hipStream_t stream) {
   const int64_t groups = (rows + RW - 1) / RW;
   dim3 grid(grid_cap((groups + kWavesPerBlock - 1) / kWavesPerBlock, 8192));
-  const size_t lds = STD ? (size_t)2 * cols * sizeof(float) : 0;
-  hipLaunchKernelGGL((k_pack_rows<STD, RW, KWT>), grid, dim3(kBlock), lds, stream, x,
-                     rows, cols, ldx, mu, rstd, rowptr, sym, bits, ldw, scale);
+  size_t lds = STD ? (size_t)(2 * cols + (cols & 1)) * sizeof(float) : 0;
+  if (FQ && KWT > 16) lds += (size_t)((cols + 63) / 64) * 64 * sizeof(uint64_t);
+  hipLaunchKernelGGL((k_pack_rows<STD, RW, KWT, FQ>), grid, dim3(kBlock), lds, stream, x,
+                     rows, cols, ldx, mu, rstd, rowptr, sym, bits, ldw, scale, pq.B, pq.N,
+                     pq.ldb, pq.C8, pq.ldc8, pq.C16, pq.ldc16);
   return hipGetLastError();
 }
 
-template <bool STD>
+template <bool STD, bool FQ = false>
 hipError_t pack_rows_dispatch(const float* x, int64_t rows, int32_t cols, int64_t ldx,
                               const float* mu, const float* rstd, const int64_t* rowptr,
                               int sym, uint64_t* bits, int64_t ldw, float* scale,
-                              hipStream_t stream) {
+                              hipStream_t stream, const PackQ8& pq = PackQ8()) {
   const int kw = (cols + 63) >> 6;
-#define BIGCN_PACK(RWV, KWV)                                                          \
-  return pack_rows_launch<STD, RWV, KWV>(x, rows, cols, ldx, mu, rstd, rowptr, sym, \
-                                         bits, ldw, scale, stream)
+#define BIGCN_PACK(RWV, KWV)                                                              \
+  return pack_rows_launch<STD, RWV, KWV, FQ>(x, rows, cols, ldx, mu, rstd, rowptr, sym, \
+                                             bits, ldw, scale, pq, stream)
   if (kw <= 1) BIGCN_PACK(8, 1);
   if (kw <= 2) BIGCN_PACK(8, 2);
   if (kw <= 4) BIGCN_PACK(4, 4);
@@ -2182,6 +2236,31 @@ hipError_t launch_pack(const float* x, int64_t rows, int32_t cols, int64_t ldx,
     hipLaunchKernelGGL(k_pack<false>, grid, dim3(kBlock), 0, stream, x, rows,
                        cols, ldx, mu, rstd, rowptr, sym, bits, ldw, scale);
   return hipGetLastError();
+}
+
+bool pack_bgemm_q8_supported(int32_t cols, int32_t N) {
+  return cols >= 1 && (cols + 63) / 64 <= 32 && N >= 1 && N <= 64;
+}
+
+hipError_t launch_pack_bgemm_q8(const float* x, int64_t rows, int32_t cols, int64_t ldx,
+                                const float* mu, const float* rstd, const int64_t* rowptr,
+                                int sym, const uint64_t* B, int32_t N, int64_t ldb,
+                                int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
+                                float* g, hipStream_t stream) {
+  if (rows == 0) return hipSuccess;
+  PackQ8 pq;
+  pq.B = B;
+  pq.N = N;
+  pq.ldb = ldb;
+  pq.C8 = C8;
+  pq.ldc8 = ldc8;
+  pq.C16 = (_Float16*)C16;
+  pq.ldc16 = ldc16;
+  if (mu != nullptr)
+    return pack_rows_dispatch<true, true>(x, rows, cols, ldx, mu, rstd, rowptr, sym, nullptr,
+                                          0, g, stream, pq);
+  return pack_rows_dispatch<false, true>(x, rows, cols, ldx, mu, rstd, rowptr, sym, nullptr, 0,
+                                         g, stream, pq);
 }
 
 hipError_t launch_bgemm_popcount(const uint64_t* F, int64_t M, int64_t ldf,
