@@ -1743,8 +1743,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   LandT* land = &s_land[wv][0];
   float* sgk = &s_gk[wv][0];
   // Lands chunk edges [0, nk) whose indices lane l holds in jr[r] (edge
-  // 64 r + l): their scales into sgk, their code pieces into land.
-  auto land_chunk = [&](const uint32_t (&jr)[JR], int nk) {
+  // 64 r + l): their scales into sgk, their code pieces into land; issued()
+  // runs once the loads are in flight, before the wait.
+  auto land_chunk = [&](const uint32_t (&jr)[JR], int nk, auto&& issued) {
     float gk[JR];
 #pragma unroll
     for (int r = 0; r < JR; ++r)
@@ -1758,6 +1759,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       const uint32_t j = (uint32_t)__shfl((int)jr[(EPI * i) / 64], (EPI * i) % 64 + lane / G);
       land_piece<CPL>(rs8, land + i * 64, k < nk ? j * rb8 + coff8 : kPastEnd);
     }
+    issued();
     wait_landed();
 #pragma unroll
     for (int r = 0; r < JR; ++r)
@@ -1813,82 +1815,69 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     const int ce = re < we ? re : we;
     const int len = (on && ce > cb) ? ce - cb : 0;
     const bool lng = len > kNarrowShort;
-    const int plen = lng ? 0 : len;  // edges of this slot's short row
     float acc[CPL];
 #pragma unroll
     for (int k = 0; k < CPL; ++k) acc[k] = 0.f;
     float gs = 0.f;
-    // Row-parallel part: the short rows' edges, concatenated in slot order
-    // (slot q's at [pq, pq + plen)), land chunk by chunk with every lane of
-    // the landing busy; each slot then walks its own row in LDS.
-    int incl = c == 0 ? plen : 0;
+    // The round's rows own one contiguous edge range [r0, r1) (within the
+    // share); it lands chunk by chunk, every lane of a landing busy, the next
+    // chunk's indices loading while this one lands.  Short rows then walk
+    // their own edges in LDS (row-parallel); each long row is summed
+    // edge-parallel per chunk (slot q on edges q, q + S, ..., then a
+    // butterfly) and its owner adds the chunk totals in chunk order.
+    const int nrow = min(S, o_e - base);
+    const int r0 = __builtin_amdgcn_readfirstlane(cb);
+    const int r1 = __builtin_amdgcn_readlane(ce, (nrow - 1) * G);
+    uint32_t jn[JR];
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int v = __shfl_up(incl, off);
-      if (lane >= off) incl += v;
-    }
-    const int nshort = __shfl(incl, 63);
-    const int pq = __shfl(incl, q * G) - plen;
-    const int endq = pq + plen;
-    for (int cbase = 0; cbase < nshort; cbase += CH) {
-      const int nk = min(CH, nshort - cbase);
+    for (int r = 0; r < JR; ++r)
+      jn[r] = __builtin_amdgcn_raw_buffer_load_b32(
+          rsi, (int)(r0 + 64 * r + lane < r1 ? (uint32_t)(r0 + 64 * r + lane) * 4u : kPastEnd),
+          0, 0);
+    // running strided sums of the long row in progress (it may continue
+    // into the next chunk: rows are contiguous, so at most one does)
+    float tmp[CPL];
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) tmp[k] = 0.f;
+    float tg = 0.f;
+    for (int cbase = r0; cbase < r1; cbase += CH) {
+      const int nk = min(CH, r1 - cbase);
       uint32_t jr[JR];
 #pragma unroll
-      for (int r = 0; r < JR; ++r) {
-        // slot holding concatenated edge kk: the first whose end exceeds it
-        const int kk = cbase + 64 * r + lane;
-        int lo = 0, hi = S - 1;
+      for (int r = 0; r < JR; ++r) jr[r] = jn[r];
+      land_chunk(jr, nk, [&]() {
 #pragma unroll
-        for (int st = S; st > 1; st >>= 1) {
-          const int mid = (lo + hi) >> 1;
-          const int em = __shfl(endq, mid * G);
-          if (em <= kk) lo = mid + 1; else hi = mid;
+        for (int r = 0; r < JR; ++r) {
+          const int e = cbase + CH + 64 * r + lane;
+          jn[r] = __builtin_amdgcn_raw_buffer_load_b32(
+              rsi, (int)(e < r1 ? (uint32_t)e * 4u : kPastEnd), 0, 0);
         }
-        const int pk = __shfl(pq, lo * G);
-        const int ck = __shfl(cb, lo * G);
-        jr[r] = __builtin_amdgcn_raw_buffer_load_b32(
-            rsi, (int)(64 * r + lane < nk ? (uint32_t)(ck + kk - pk) * 4u : kPastEnd), 0, 0);
-      }
-      land_chunk(jr, nk);
-      const int a0 = max(pq, cbase);
-      const int a1 = min(endq, cbase + nk);
-      const int cnt = a1 > a0 ? a1 - a0 : 0;
-      const int mc = wave_max_i32(cnt);
-      for (int t = 0; t < mc; t += 4) {
-        int k[4];
-        bool ok[4];
-        uint32_t ip[4];
+      });
+      const int a0 = max(cb, cbase);
+      const int a1 = min(ce, cbase + nk);
+      const int cnt = (on && a1 > a0) ? a1 - a0 : 0;
+      if (__builtin_amdgcn_ballot_w64(!lng && cnt > 0) != 0) {
+        const int mc = wave_max_i32(lng ? 0 : cnt);
+        for (int t = 0; t < mc; t += 4) {
+          int k[4];
+          bool ok[4];
+          uint32_t ip[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          ok[u] = t + u < cnt;
-          k[u] = ok[u] ? a0 + t + u - cbase : 0;
-          ip[u] = (uint32_t)(cb + a0 + t + u - pq) * 4u;
+          for (int u = 0; u < 4; ++u) {
+            ok[u] = !lng && t + u < cnt;
+            k[u] = ok[u] ? a0 + t + u - cbase : 0;
+            ip[u] = (uint32_t)(a0 + t + u) * 4u;
+          }
+          add_edges4(acc, gs, k, ok, ip);
         }
-        add_edges4(acc, gs, k, ok, ip);
       }
-    }
-    // Edge-parallel part: long rows one at a time, landed contiguously, slot
-    // q adding edges q, q + S, ...; a butterfly over the slots gives the total.
-    uint64_t lm = __builtin_amdgcn_ballot_w64(c == 0 && lng);
-    while (lm != 0) {
-      const int ld = (int)__builtin_ctzll(lm);
-      lm &= lm - 1;
-      const int lcb = __builtin_amdgcn_readlane(cb, ld);
-      const int llen = __builtin_amdgcn_readlane(len, ld);
-      float tmp[CPL];
-#pragma unroll
-      for (int k = 0; k < CPL; ++k) tmp[k] = 0.f;
-      float tg = 0.f;
-      for (int cbase = 0; cbase < llen; cbase += CH) {
-        const int nk = min(CH, llen - cbase);
-        uint32_t jr[JR];
-#pragma unroll
-        for (int r = 0; r < JR; ++r)
-          jr[r] = __builtin_amdgcn_raw_buffer_load_b32(
-              rsi, (int)(64 * r + lane < nk ? (uint32_t)(lcb + cbase + 64 * r + lane) * 4u : kPastEnd),
-              0, 0);
-        land_chunk(jr, nk);
-        const int mt = (nk + S - 1) / S;
+      uint64_t lm = __builtin_amdgcn_ballot_w64(c == 0 && lng && cnt > 0);
+      while (lm != 0) {
+        const int ld = (int)__builtin_ctzll(lm);
+        lm &= lm - 1;
+        const int la = __builtin_amdgcn_readlane(a0, ld) - cbase;
+        const int ln = __builtin_amdgcn_readlane(cnt, ld);
+        const int mt = (ln + S - 1) / S;
         for (int t = 0; t < mt; t += 4) {
           int k[4];
           bool ok[4];
@@ -1896,23 +1885,28 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
             const int kq = q + S * (t + u);
-            ok[u] = kq < nk;
-            k[u] = ok[u] ? kq : 0;
-            ip[u] = (uint32_t)(lcb + cbase + kq) * 4u;
+            ok[u] = kq < ln;
+            k[u] = ok[u] ? la + kq : 0;
+            ip[u] = (uint32_t)(cbase + la + kq) * 4u;
           }
           add_edges4(tmp, tg, k, ok, ip);
         }
-      }
+        if (__builtin_amdgcn_readlane(ce, ld) <= cbase + nk) {  // the row ends here
 #pragma unroll
-      for (int m = G; m < 64; m <<= 1) {
+          for (int m = G; m < 64; m <<= 1) {
 #pragma unroll
-        for (int k = 0; k < CPL; ++k) tmp[k] += __shfl_xor(tmp[k], m);
-        tg += __shfl_xor(tg, m);
-      }
-      if (q == ld / G) {
+            for (int k = 0; k < CPL; ++k) tmp[k] += __shfl_xor(tmp[k], m);
+            tg += __shfl_xor(tg, m);
+          }
+          if (q == ld / G) {
 #pragma unroll
-        for (int k = 0; k < CPL; ++k) acc[k] = tmp[k];
-        gs = tg;
+            for (int k = 0; k < CPL; ++k) acc[k] = tmp[k];
+            gs = tg;
+          }
+#pragma unroll
+          for (int k = 0; k < CPL; ++k) tmp[k] = 0.f;
+          tg = 0.f;
+        }
       }
     }
     float sum[CPL];
