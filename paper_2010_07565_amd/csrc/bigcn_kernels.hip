@@ -144,16 +144,28 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
     int64_t ldw, float* __restrict__ scale, const uint64_t* __restrict__ B, int32_t N,
     int64_t ldb, int8_t* __restrict__ C8, int64_t ldc8, _Float16* __restrict__ C16,
     int64_t ldc16) {
-  extern __shared__ float s_norm[];  // mu[0..cols), rstd[cols..2 cols)
-  if (STD) {
+  // Column statistics: in registers (lane l keeps columns 64 w + l) up to
+  // 16 words, so the first row loads need not wait for a block barrier;
+  // in LDS (mu[0..cols), rstd[cols..2 cols)) for wider rows.
+  extern __shared__ float s_norm[];
+  constexpr bool kNLds = STD && KWT > 16;
+  const int lane = threadIdx.x & 63;
+  const int kw = (cols + 63) >> 6;
+  float mr[STD && !kNLds ? KWT : 1], rr[STD && !kNLds ? KWT : 1];
+#pragma unroll
+  for (int w = 0; w < (STD && !kNLds ? KWT : 1); ++w) {
+    const int k = w * 64 + lane;
+    const bool ok = STD && !kNLds && w < kw && k < cols;
+    mr[w] = ok ? mu[k] : 0.f;
+    rr[w] = ok ? rstd[k] : 0.f;
+  }
+  if (kNLds) {
     for (int i = threadIdx.x; i < cols; i += kBlock) {
       s_norm[i] = mu[i];
       s_norm[cols + i] = rstd[i];
     }
     __syncthreads();
   }
-  const int lane = threadIdx.x & 63;
-  const int kw = (cols + 63) >> 6;
   const int64_t step = (int64_t)gridDim.x * kWavesPerBlock * RW;
   // FQ: lane j's weight words, in registers (KWT <= 16) or, for the widest
   // inputs, in LDS after the row statistics ([w][64] words)
@@ -162,7 +174,7 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
 #pragma unroll
   for (int w = 0; w < (FQ && !kWLds ? KWT : 1); ++w)
     wr[w] = (FQ && !kWLds && lane < N && w < kw) ? B[(int64_t)lane * ldb + w] : 0ull;
-  uint64_t* s_w = reinterpret_cast<uint64_t*>(s_norm + (STD ? 2 * cols + (cols & 1) : 0));
+  uint64_t* s_w = reinterpret_cast<uint64_t*>(s_norm + (kNLds ? 2 * cols + (cols & 1) : 0));
   if (kWLds) {
     for (int i = threadIdx.x; i < kw * 64; i += kBlock) {
       const int w = i >> 6, j = i & 63;
@@ -204,8 +216,9 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
         const bool ok = k < cols;
         float y = v[q][w];
         if (STD && ok) {
-          const float t = y - s_norm[k];  // two separate fp32 roundings
-          y = t * s_norm[cols + k];
+          // two separate fp32 roundings
+          const float t = y - (kNLds ? s_norm[k] : mr[w]);
+          y = t * (kNLds ? s_norm[cols + k] : rr[w]);
         }
         const uint64_t b = __builtin_amdgcn_ballot_w64(ok && y >= 0.f);
         l1[q] += ok ? fabsf(y) : 0.f;
@@ -2179,7 +2192,7 @@ hipError_t pack_rows_launch(const float* x, int64_t rows, int32_t cols, int64_t 
                             const PackQ8& pq, hipStream_t stream) {
   const int64_t groups = (rows + RW - 1) / RW;
   dim3 grid(grid_cap((groups + kWavesPerBlock - 1) / kWavesPerBlock, 8192));
-  size_t lds = STD ? (size_t)(2 * cols + (cols & 1)) * sizeof(float) : 0;
+  size_t lds = (STD && KWT > 16) ? (size_t)(2 * cols + (cols & 1)) * sizeof(float) : 0;
   if (FQ && KWT > 16) lds += (size_t)((cols + 63) / 64) * 64 * sizeof(uint64_t);
   hipLaunchKernelGGL((k_pack_rows<STD, RW, KWT, FQ>), grid, dim3(kBlock), lds, stream, x,
                      rows, cols, ldx, mu, rstd, rowptr, sym, bits, ldw, scale, pq.B, pq.N,
