@@ -43,7 +43,7 @@ hipError_t launch_bgemm_mfma(const uint64_t* F, int64_t M, int64_t ldf,
 constexpr int q8_lane_bytes(int32_t N) { return N <= 64 ? 1 : N <= 128 ? 2 : 4; }
 bool q8_supported(int64_t n, int32_t N, int32_t K);
 // The pack of a layer's input followed, in the same kernel, by its binary
-// GEMM into 8-bit half-codes (layers of N <= 64 outputs and at most 2048
+// GEMM into 8-bit half-codes (layers of N <= 64 outputs and at most 1024
 // inputs): the codes, exact rows and flagged scale of launch_pack +
 // launch_bgemm_q8, bit for bit, without writing the packed bits.
 bool pack_bgemm_q8_supported(int32_t cols, int32_t N);
