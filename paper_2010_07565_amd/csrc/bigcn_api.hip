@@ -400,7 +400,7 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
     const bool q8 = bigcn::q8_supported(n, ly.d_out, ly.d_in);
     const IType ct = forward_itype(ly.d_in);
     if (!have_products && q8 && ly.wbits_self == nullptr &&
-        bigcn::pack_bgemm_q8_supported(ly.d_in, ly.d_out)) {
+        bigcn::pack_bgemm_q8_supported(ly.d_in, ly.d_out, ldin)) {
       e = bigcn::launch_pack_bgemm_q8(hin, n, ly.d_in, ldin, l == 0 ? mu : nullptr,
                                       l == 0 ? rstd : nullptr, rowptr,
                                       norm == BIGCN_NORM_SYM, ly.wbits, ly.d_out, ly.ldw,

@@ -34,6 +34,17 @@ typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef int int4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
+// Buffer resource for raw (unformatted) loads: base, stride 0, byte range,
+// and the gfx9 default of the fourth descriptor word.  Loads past the range
+// return zero.
+template <typename T>
+__device__ inline __amdgpu_buffer_rsrc_t raw_rsrc(const T* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(p), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+constexpr uint32_t kPastEnd = 0x80000000u;  // buffer offset past every range: loads give 0
+
 __device__ inline int wave_index_in_block() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 }
@@ -136,6 +147,10 @@ __global__ __launch_bounds__(kBlock) void k_pack(
 // in place (lane j: output j, its weight words in registers, the row's words
 // being the ballots): the 8-bit half-codes, exact rows and flags of
 // k_bgemm_pop_q8 (one byte per column) are written instead of the bits.
+// Row stride limit of k_pack_rows, whose RW-row groups are addressed with
+// 32-bit buffer offsets.
+constexpr int64_t kPackRowsMaxLd = (int64_t)1 << 24;
+
 template <bool STD, int RW, int KWT, bool FQ>
 __global__ __launch_bounds__(kBlock) void k_pack_rows(
     const float* __restrict__ x, int64_t rows, int32_t cols, int64_t ldx,
@@ -152,12 +167,16 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
   const int lane = threadIdx.x & 63;
   const int kw = (cols + 63) >> 6;
   float mr[STD && !kNLds ? KWT : 1], rr[STD && !kNLds ? KWT : 1];
+  if constexpr (STD && !kNLds) {
+    // columns past cols fall outside the ranges and read as zero
+    const __amdgpu_buffer_rsrc_t rsm = raw_rsrc(mu, (uint32_t)cols * 4u);
+    const __amdgpu_buffer_rsrc_t rsr = raw_rsrc(rstd, (uint32_t)cols * 4u);
 #pragma unroll
-  for (int w = 0; w < (STD && !kNLds ? KWT : 1); ++w) {
-    const int k = w * 64 + lane;
-    const bool ok = STD && !kNLds && w < kw && k < cols;
-    mr[w] = ok ? mu[k] : 0.f;
-    rr[w] = ok ? rstd[k] : 0.f;
+    for (int w = 0; w < KWT; ++w) {
+      const uint32_t off = w < kw ? (uint32_t)(w * 64 + lane) * 4u : kPastEnd;
+      mr[w] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsm, (int)off, 0, 0));
+      rr[w] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsr, (int)off, 0, 0));
+    }
   }
   if (kNLds) {
     for (int i = threadIdx.x; i < cols; i += kBlock) {
@@ -169,27 +188,38 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
   const int64_t step = (int64_t)gridDim.x * kWavesPerBlock * RW;
   static_assert(!FQ || KWT <= 16, "fused GEMM keeps its weight words in registers");
   uint64_t wr[FQ ? KWT : 1];  // FQ: lane j's weight words
+  if constexpr (FQ) {
+    const __amdgpu_buffer_rsrc_t rsb = raw_rsrc(B, (uint32_t)(N * ldb * 8));
 #pragma unroll
-  for (int w = 0; w < (FQ ? KWT : 1); ++w)
-    wr[w] = (FQ && lane < N && w < kw) ? B[(int64_t)lane * ldb + w] : 0ull;
+    for (int w = 0; w < KWT; ++w) {
+      const uint32_t off = (lane < N && w < kw) ? (uint32_t)(lane * ldb + w) * 8u : kPastEnd;
+      wr[w] = __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(rsb, (int)off, 0, 0));
+    }
+  }
   for (int64_t r0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * RW;
        r0 < rows; r0 += step) {
-    // lane q < RW: the normalisation factor of row r0 + q, loaded together
-    // with the rows so that the end of the group does not wait for it
-    float colf = 1.f;
-    if (rowptr != nullptr && sym && lane < RW && r0 + lane < rows) {
-      const int64_t dg = rowptr[r0 + lane + 1] - rowptr[r0 + lane];
-      colf = dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f;
-    }
+    // The group's nq rows as one raw buffer ending with the last row's
+    // element cols - 1 (element (q, k) at byte 4 (q ldx + k)), so rows past
+    // the matrix read as zero; elements past cols in a row are loaded but
+    // masked below.  Every load is issued before any result is used.
+    const int nq = (int)(rows - r0 < RW ? rows - r0 : RW);
+    const __amdgpu_buffer_rsrc_t rsx =
+        raw_rsrc(x + r0 * ldx, (uint32_t)(((nq - 1) * ldx + cols) * 4));
     float v[RW][KWT];
 #pragma unroll
     for (int q = 0; q < RW; ++q) {
-      const int64_t r = r0 + q < rows ? r0 + q : rows - 1;
+      const uint32_t vo = (uint32_t)(q * ldx + lane) * 4u;
 #pragma unroll
-      for (int w = 0; w < KWT; ++w) {
-        const int k = w * 64 + lane;
-        v[q][w] = (w < kw && k < cols) ? x[r * ldx + k] : 0.f;
-      }
+      for (int w = 0; w < KWT; ++w)
+        v[q][w] = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(rsx, (int)(vo + 256u * w), 0, 0));
+    }
+    // lane q < nq: the degree of row r0 + q (for the normalisation factor),
+    // loaded after the rows so that waiting for it does not hold them back
+    int64_t dg = 0;
+    if (rowptr != nullptr && sym) {
+      const int64_t rq = r0 + (lane < nq ? lane : 0);
+      dg = rowptr[rq + 1] - rowptr[rq];
     }
     float l1[RW];
     uint64_t mine[RW];
@@ -234,7 +264,7 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
         if (flag) C16[r * ldc16 + lane] = (_Float16)dot;
         if (lane == q) {
           float sc = l1[q] / (float)cols;
-          if (rowptr != nullptr && sym) sc = sc * colf;
+          if (rowptr != nullptr && sym) sc = sc * (dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f);
           scale[r] = flag ? -fabsf(sc) : sc;
         }
       } else {
@@ -243,7 +273,7 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
           if (wb + lane < ldw) br[wb + lane] = wb == 0 ? mine[q] : 0ull;
         if (lane == q) {
           float sc = l1[q] / (float)cols;
-          if (rowptr != nullptr && sym) sc = sc * colf;
+          if (rowptr != nullptr && sym) sc = sc * (dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f);
           scale[r] = sc;
         }
       }
@@ -769,15 +799,6 @@ __global__ __launch_bounds__(kBlock) void k_spmm(
     if (load_cols) *reinterpret_cast<float4_t*>(tail + w * dpad + c0) = sum;
     if (sub == 0 && blockIdx.y == 0) tail_row[w] = (int32_t)r;
   }
-}
-
-// Buffer resource for raw (unformatted) loads: base, stride 0, byte range,
-// and the gfx9 default of the fourth descriptor word.  Loads past the range
-// return zero.
-template <typename T>
-__device__ inline __amdgpu_buffer_rsrc_t raw_rsrc(const T* p, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(p), (short)0, (int)bytes,
-                                           0x00020000);
 }
 
 template <typename T>
@@ -1463,7 +1484,6 @@ constexpr int kNarrowShort = 16;  // edges in a share up to which a row is row-p
 // pieces, 256 B for 4-byte ones)
 template <int CPL>
 constexpr int narrow_batch() { return CPL == 4 ? 16 : 8; }
-constexpr uint32_t kPastEnd = 0x80000000u;  // buffer offset past every range: loads give 0
 
 __device__ inline int wave_max_i32(int v) {
 #pragma unroll
@@ -2218,7 +2238,7 @@ hipError_t launch_pack(const float* x, int64_t rows, int32_t cols, int64_t ldx,
                        int64_t ldw, float* scale, hipStream_t stream) {
   if (rows == 0) return hipSuccess;
   const int kw = (cols + 63) >> 6;
-  if (kw <= 32) {
+  if (kw <= 32 && ldx <= kPackRowsMaxLd) {
     if (mu != nullptr)
       return pack_rows_dispatch<true>(x, rows, cols, ldx, mu, rstd, rowptr, sym, bits,
                                       ldw, scale, stream);
@@ -2238,8 +2258,9 @@ hipError_t launch_pack(const float* x, int64_t rows, int32_t cols, int64_t ldx,
 // Inputs of more than 16 words keep the weights in LDS inside a loop the
 // compiler does not unroll; there the separate pack and GEMM are faster
 // (1433 inputs: 15.1 us fused against 8.0 + 5.2 us).
-bool pack_bgemm_q8_supported(int32_t cols, int32_t N) {
-  return cols >= 1 && (cols + 63) / 64 <= 16 && N >= 1 && N <= 64;
+bool pack_bgemm_q8_supported(int32_t cols, int32_t N, int64_t ldx) {
+  return cols >= 1 && (cols + 63) / 64 <= 16 && N >= 1 && N <= 64 && ldx >= cols &&
+         ldx <= kPackRowsMaxLd;
 }
 
 hipError_t launch_pack_bgemm_q8(const float* x, int64_t rows, int32_t cols, int64_t ldx,
