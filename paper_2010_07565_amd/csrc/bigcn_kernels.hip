@@ -140,16 +140,19 @@ __global__ __launch_bounds__(kBlock) void k_pack(
   }
 }
 
+// Row stride limit of k_pack_rows, whose RW-row groups are addressed with
+// 32-bit buffer offsets.
+constexpr int64_t kPackRowsMaxLd = (int64_t)1 << 24;
+
 // Same computation with RW rows per wave in flight: all RW*kw loads of a
-// row group are issued before the first ballot, the per-column mean / rstd
-// sit in LDS, and the RW row sums are reduced together.  kw <= KWT <= 32.
+// row group are issued before the first ballot, and the RW row sums are
+// reduced together.  kw <= KWT <= 32 and RW * ldw <= 64: lane RW q + w
+// collects word w of row q, so the group's words (rows r0.. contiguous at
+// stride ldw) and scales leave in one store each.
 // With FQ (KWT <= 16) the binary GEMM of a layer of N <= 64 outputs follows
 // in place (lane j: output j, its weight words in registers, the row's words
 // being the ballots): the 8-bit half-codes, exact rows and flags of
 // k_bgemm_pop_q8 (one byte per column) are written instead of the bits.
-// Row stride limit of k_pack_rows, whose RW-row groups are addressed with
-// 32-bit buffer offsets.
-constexpr int64_t kPackRowsMaxLd = (int64_t)1 << 24;
 
 template <bool STD, int RW, int KWT, bool FQ>
 __global__ __launch_bounds__(kBlock) void k_pack_rows(
@@ -222,39 +225,51 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
       dg = rowptr[rq + 1] - rowptr[rq];
     }
     float l1[RW];
-    uint64_t mine[RW];
+    uint64_t mine = 0;  // lane ldw q + w: word w of row q (pad words stay zero)
     int pc[RW];  // FQ: lane j's popcount of row XOR weights
 #pragma unroll
     for (int q = 0; q < RW; ++q) {
       l1[q] = 0.f;
-      mine[q] = 0;
       pc[q] = 0;
 #pragma unroll
       for (int w = 0; w < KWT; ++w) {
         if (w >= kw) break;  // wave-uniform
-        const int k = w * 64 + lane;
-        const bool ok = k < cols;
+        // Lanes past cols hold junk (the next row or zero): the last word's
+        // lane mask drops their bits and its sum skips them.
+        const bool full = (w + 1) * 64 <= cols;  // wave-uniform
         float y = v[q][w];
-        if (STD && ok) {
+        if constexpr (STD) {
           // two separate fp32 roundings
-          const float t = y - (kNLds ? s_norm[k] : mr[w]);
-          y = t * (kNLds ? s_norm[cols + k] : rr[w]);
+          const int k = w * 64 + lane;
+          const int kk = kNLds && k >= cols ? 0 : k;
+          const float t = y - (kNLds ? s_norm[kk] : mr[w]);
+          y = t * (kNLds ? s_norm[cols + kk] : rr[w]);
         }
-        const uint64_t b = __builtin_amdgcn_ballot_w64(ok && y >= 0.f);
-        l1[q] += ok ? fabsf(y) : 0.f;
-        if (lane == w) mine[q] = b;
+        uint64_t b = __builtin_amdgcn_fcmpf(y, 0.f, 3 /* ordered >= */);
+        if (full) {
+          l1[q] += fabsf(y);
+        } else {
+          b &= (1ull << (cols & 63)) - 1;
+          l1[q] += lane < (cols & 63) ? fabsf(y) : 0.f;
+        }
+        if (!FQ && lane == q * ldw + w) mine = b;
         if constexpr (FQ) {
           const uint64_t z = b ^ wr[w];
-          pc[q] += __builtin_popcount((uint32_t)z) + __builtin_popcount((uint32_t)(z >> 32));
+          pc[q] = __builtin_popcount((uint32_t)(z >> 32)) +
+                  (__builtin_popcount((uint32_t)z) + pc[q]);
         }
       }
     }
 #pragma unroll
     for (int q = 0; q < RW; ++q) l1[q] = wave_sum(l1[q]);
+    // lane q < nq: row r0 + q's sum and (FQ) overflow flag
+    float myl1 = 0.f;
+    bool myflag = false;
 #pragma unroll
     for (int q = 0; q < RW; ++q) {
       const int64_t r = r0 + q;
       if (r >= rows) break;  // wave-uniform
+      if (lane == q) myl1 = l1[q];
       if constexpr (FQ) {
         const int dot = cols - 2 * pc[q];
         const int code = (dot - (cols & 1)) >> 1;
@@ -262,21 +277,14 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
         const bool flag =
             __builtin_amdgcn_ballot_w64(lane < N && (code < -128 || code > 127)) != 0;
         if (flag) C16[r * ldc16 + lane] = (_Float16)dot;
-        if (lane == q) {
-          float sc = l1[q] / (float)cols;
-          if (rowptr != nullptr && sym) sc = sc * (dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f);
-          scale[r] = flag ? -fabsf(sc) : sc;
-        }
-      } else {
-        uint64_t* br = bits + r * ldw;
-        for (int64_t wb = 0; wb < ldw; wb += 64)
-          if (wb + lane < ldw) br[wb + lane] = wb == 0 ? mine[q] : 0ull;
-        if (lane == q) {
-          float sc = l1[q] / (float)cols;
-          if (rowptr != nullptr && sym) sc = sc * (dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f);
-          scale[r] = sc;
-        }
+        if (lane == q) myflag = flag;
       }
+    }
+    if (!FQ && lane < nq * ldw) bits[r0 * ldw + lane] = mine;
+    if (lane < nq) {
+      float sc = myl1 / (float)cols;
+      if (rowptr != nullptr && sym) sc = sc * (dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f);
+      scale[r0 + lane] = myflag ? -fabsf(sc) : sc;
     }
   }
 }
@@ -1491,9 +1499,12 @@ __device__ inline int wave_max_i32(int v) {
   return v;
 }
 
-__device__ inline uint64_t shfl_xor_u64(uint64_t v, int m) {
-  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
-  const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
+// 64-bit lane exchange within quads (DPP quad_perm control CTRL).
+template <int CTRL>
+__device__ inline uint64_t dpp_u64(uint64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, 0xF, 0xF, false);
+  const uint32_t hi =
+      (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, 0xF, 0xF, false);
   return ((uint64_t)hi << 32) | lo;
 }
 
@@ -1623,6 +1634,7 @@ struct NarrowEpi {
   uint32_t valid;        // bit k: column CPL*c + k < d
   int relu;
   int32_t d;
+  bool vec;              // out 16-byte aligned with ldo % 4 == 0
 };
 
 // A finished row in one slot: the same epilogue as finish_row (rescale,
@@ -1638,24 +1650,52 @@ __device__ inline void finish_slot(int64_t r, int64_t deg, int mean, const float
                                    const NarrowEpi& ep, int c, float* __restrict__ out,
                                    int64_t ldo, const NextLayer& nx, int nbn,
                                    const uint64_t* s_bn) {
-  static_assert(CPL * G <= 64 && CPL <= 16, "narrow layout");
+  static_assert(CPL * G <= 64 && CPL <= 16 && CPL % 4 == 0, "narrow layout");
   const float rowfac = deg > 0 ? row_factor_deg(deg, mean) : 0.f;
   float gi = 0.f;
   if (NX == 2) gi = fabsf(nx.gself[r]);
+  // this lane's constants in 16-byte LDS reads, all issued before any use
   const float* al = ep.s_alpha + CPL * c;
+  float av[CPL], bv[CPL], sv[NX == 2 ? CPL : 1];
+#pragma unroll
+  for (int k = 0; k < CPL; k += 4) {
+    const float4_t a4 = *reinterpret_cast<const float4_t*>(al + k);
+    const float4_t b4 = *reinterpret_cast<const float4_t*>(al + 64 + k);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      av[k + u] = a4[u];
+      bv[k + u] = b4[u];
+    }
+    if constexpr (NX == 2) {
+      const float4_t s4 = *reinterpret_cast<const float4_t*>(al + 128 + k);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sv[k + u] = s4[u];
+    }
+  }
   float v[CPL];
 #pragma unroll
   for (int k = 0; k < CPL; ++k) {
     const bool ok = (ep.valid >> k) & 1;
-    float t = deg > 0 ? fmaf(sum[k], rowfac * al[k], al[64 + k]) : al[64 + k];
+    float t = deg > 0 ? fmaf(sum[k], rowfac * av[k], bv[k]) : bv[k];
     if (NX == 2)
-      t += ok ? gi * al[128 + k] * (float)nx.Cself[r * nx.ldself + CPL * c + k] : 0.f;
+      t += ok ? gi * sv[k] * (float)nx.Cself[r * nx.ldself + CPL * c + k] : 0.f;
     v[k] = act(t, ep.relu);
   }
   if (NX != 1 || out != nullptr) {
+    float* o = out + r * ldo + CPL * c;
+    if (ep.vec && ep.valid == (1u << CPL) - 1) {
 #pragma unroll
-    for (int k = 0; k < CPL; ++k)
-      if ((ep.valid >> k) & 1) out[r * ldo + CPL * c + k] = v[k];
+      for (int k = 0; k < CPL; k += 4) {
+        float4_t q4;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) q4[u] = v[k + u];
+        *reinterpret_cast<float4_t*>(o + k) = q4;
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < CPL; ++k)
+        if ((ep.valid >> k) & 1) o[k] = v[k];
+    }
   }
   if (NX != 1) return;
   uint32_t m = 0;
@@ -1666,18 +1706,25 @@ __device__ inline void finish_slot(int64_t r, int64_t deg, int mean, const float
     if (k < CPL) m |= (uint32_t)(ok && v[k] >= 0.f) << k;
     a[k] = ok ? fabsf(v[k < CPL ? k : 0]) : 0.f;
   }
+  // the slot's G lanes are one quad or part of one: DPP quad exchanges
   uint64_t word = (uint64_t)m << (CPL * c);
-  if (G >= 2) word |= shfl_xor_u64(word, 1);
-  if (G >= 4) word |= shfl_xor_u64(word, 2);
+  if (G >= 2) word |= dpp_u64<0xB1>(word);  // quad_perm [1,0,3,2]: lane ^ 1
+  if (G >= 4) word |= dpp_u64<0x4E>(word);  // quad_perm [2,3,0,1]: lane ^ 2
   float qd[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
     qd[i] = (a[4 * i] + a[4 * i + 1]) + (a[4 * i + 2] + a[4 * i + 3]);
   float l1 = (qd[0] + qd[1]) + (qd[2] + qd[3]);
-  if (G >= 2) l1 = l1 + __shfl_xor(l1, 1);
-  if (G >= 4) l1 = l1 + __shfl_xor(l1, 2);
+  if (G >= 2) l1 = l1 + dpp<0xB1>(l1);
+  if (G >= 4) l1 = l1 + dpp<0x4E>(l1);
   float sc = l1 / (float)ep.d;
-  if (nx.sym) sc = sc * (deg > 0 ? 1.0f / sqrtf((float)deg) : 0.f);
+  if (nx.sym) {
+    // D-hat^-1/2 of this row: the symmetric row factor itself when this
+    // layer is symmetric too
+    const float isd =
+        mean == 0 ? rowfac : (deg > 0 ? 1.0f / sqrtf((float)deg) : 0.f);
+    sc = sc * isd;
+  }
   const int Kn = ep.d;
   const int par = Kn & 1;
   for (int kq = c; kq < nx.dn; kq += G) {
@@ -1700,7 +1747,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   constexpr int S = 64 / G;
   extern __shared__ uint64_t s_bn[];  // NX == 1: word 0 of each next weight column
   __shared__ float s_part[2][kWavesPerBlock][64];  // [0] head pieces, [1] tail pieces
-  __shared__ float s_epi[3][64];                   // alpha, bias, alpha_self
+  __shared__ __attribute__((aligned(16))) float s_epi[3][64];  // alpha, bias, alpha_self
   // A chunk of CH edges lands in LDS through NLI instructions of EPI = 64 / G
   // edges each (lane l: edge EPI i + l / G, bytes CPL (l % G) ..); chunk edge
   // k's piece c sits at landed index G k + c, its scale at s_gk[k].
@@ -1734,6 +1781,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   ep.s_alpha = &s_epi[0][0];
   ep.relu = relu;
   ep.d = d;
+  ep.vec = ((uintptr_t)out & 15) == 0 && (ldo & 3) == 0;
   ep.valid = 0;
 #pragma unroll
   for (int k = 0; k < CPL; ++k) ep.valid |= (uint32_t)(CPL * c + k < d) << k;
@@ -2201,7 +2249,10 @@ hipError_t pack_rows_launch(const float* x, int64_t rows, int32_t cols, int64_t 
                             int sym, uint64_t* bits, int64_t ldw, float* scale,
                             const PackQ8& pq, hipStream_t stream) {
   const int64_t groups = (rows + RW - 1) / RW;
-  dim3 grid(grid_cap((groups + kWavesPerBlock - 1) / kWavesPerBlock, 8192));
+  // The fused GEMM's waves each load their weight words (and the column
+  // statistics): fewer waves, taking several row groups each, measured
+  // faster (500 inputs, 64 outputs: 10.3 us at 1024 blocks, 12.4 us at 2465).
+  dim3 grid(grid_cap((groups + kWavesPerBlock - 1) / kWavesPerBlock, FQ ? 1024 : 8192));
   const size_t lds = (STD && KWT > 16) ? (size_t)2 * cols * sizeof(float) : 0;
   hipLaunchKernelGGL((k_pack_rows<STD, RW, KWT, FQ>), grid, dim3(kBlock), lds, stream, x,
                      rows, cols, ldx, mu, rstd, rowptr, sym, bits, ldw, scale, pq.B, pq.N,
@@ -2238,7 +2289,10 @@ hipError_t launch_pack(const float* x, int64_t rows, int32_t cols, int64_t ldx,
                        int64_t ldw, float* scale, hipStream_t stream) {
   if (rows == 0) return hipSuccess;
   const int kw = (cols + 63) >> 6;
-  if (kw <= 32 && ldx <= kPackRowsMaxLd) {
+  // k_pack_rows writes a group's words with one lane per word (RW * ldw <=
+  // 64 for the RW its dispatch picks from kw)
+  const int rw = kw <= 2 ? 8 : kw <= 4 ? 4 : kw <= 8 ? 2 : 1;
+  if (kw <= 32 && ldx <= kPackRowsMaxLd && rw * ldw <= 64) {
     if (mu != nullptr)
       return pack_rows_dispatch<true>(x, rows, cols, ldx, mu, rstd, rowptr, sym, bits,
                                       ldw, scale, stream);
