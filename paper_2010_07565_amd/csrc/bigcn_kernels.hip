@@ -1809,6 +1809,20 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   const __amdgpu_buffer_rsrc_t rs16 = raw_rsrc(C16, (uint32_t)(n * (int64_t)rb16));
   const __amdgpu_buffer_rsrc_t rsi = raw_rsrc(colidx + eb, (uint32_t)total * 4u);
   const __amdgpu_buffer_rsrc_t rsg = raw_rsrc(g, (uint32_t)(n * 4));
+  // The first round's first batch of edge indices is requested before the
+  // block barrier (its range is the one the round loop computes for base h).
+  uint32_t jpre[JR];
+#pragma unroll
+  for (int r = 0; r < JR; ++r) jpre[r] = 0;
+  if (h < o_e) {
+    const int p0 = max(__builtin_amdgcn_readlane(rs_l, h), ws);
+    const int p1 = min(__builtin_amdgcn_readlane(re_l, min(h + S, o_e) - 1), we);
+#pragma unroll
+    for (int r = 0; r < JR; ++r)
+      jpre[r] = __builtin_amdgcn_raw_buffer_load_b32(
+          rsi, (int)(p0 + 64 * r + lane < p1 ? (uint32_t)(p0 + 64 * r + lane) * 4u : kPastEnd),
+          0, 0);
+  }
   __syncthreads();  // s_epi and s_bn are read by finish_slot
 
   LandT* land = &s_land[wv][0];
@@ -1900,11 +1914,16 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     const int r0 = __builtin_amdgcn_readfirstlane(cb);
     const int r1 = __builtin_amdgcn_readlane(ce, (nrow - 1) * G);
     uint32_t jn[JR];
+    if (base == h) {
 #pragma unroll
-    for (int r = 0; r < JR; ++r)
-      jn[r] = __builtin_amdgcn_raw_buffer_load_b32(
-          rsi, (int)(r0 + 64 * r + lane < r1 ? (uint32_t)(r0 + 64 * r + lane) * 4u : kPastEnd),
-          0, 0);
+      for (int r = 0; r < JR; ++r) jn[r] = jpre[r];
+    } else {
+#pragma unroll
+      for (int r = 0; r < JR; ++r)
+        jn[r] = __builtin_amdgcn_raw_buffer_load_b32(
+            rsi, (int)(r0 + 64 * r + lane < r1 ? (uint32_t)(r0 + 64 * r + lane) * 4u : kPastEnd),
+            0, 0);
+    }
     // running strided sums of the long row in progress (it may continue
     // into the next chunk: rows are contiguous, so at most one does)
     float tmp[CPL];
