@@ -1493,12 +1493,6 @@ constexpr int kNarrowShort = 16;  // edges in a share up to which a row is row-p
 template <int CPL>
 constexpr int narrow_batch() { return CPL == 4 ? 16 : 8; }
 
-__device__ inline int wave_max_i32(int v) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) v = max(v, __shfl_xor(v, m));
-  return v;
-}
-
 // 64-bit lane exchange within quads (DPP quad_perm control CTRL).
 template <int CTRL>
 __device__ inline uint64_t dpp_u64(uint64_t v) {
@@ -1837,12 +1831,18 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       gk[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
                                             rsg, (int)(64 * r + lane < nk ? jr[r] * 4u : kPastEnd),
                                             0, 0));
+    // every lane exchange first, so their latencies overlap; then the loads
+    uint32_t lo[NLI];
+#pragma unroll
+    for (int i = 0; i < NLI; ++i) {
+      const int k = EPI * i + lane / G;
+      const uint32_t j = (uint32_t)__shfl((int)jr[(EPI * i) / 64], (EPI * i) % 64 + lane / G);
+      lo[i] = k < nk ? j * rb8 + coff8 : kPastEnd;
+    }
 #pragma unroll
     for (int i = 0; i < NLI; ++i) {
       if (EPI * i >= nk) break;  // wave-uniform
-      const int k = EPI * i + lane / G;
-      const uint32_t j = (uint32_t)__shfl((int)jr[(EPI * i) / 64], (EPI * i) % 64 + lane / G);
-      land_piece<CPL>(rs8, land + i * 64, k < nk ? j * rb8 + coff8 : kPastEnd);
+      land_piece<CPL>(rs8, land + i * 64, lo[i]);
     }
     issued();
     wait_landed();
@@ -1946,9 +1946,12 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       const int a0 = max(cb, cbase);
       const int a1 = min(ce, cbase + nk);
       const int cnt = (on && a1 > a0) ? a1 - a0 : 0;
-      if (__builtin_amdgcn_ballot_w64(!lng && cnt > 0) != 0) {
-        const int mc = wave_max_i32(lng ? 0 : cnt);
-        for (int t = 0; t < mc; t += 4) {
+      {
+        // short rows: batches of four edges while any slot has edges left
+        // (at most kNarrowShort per row in this chunk)
+        const int sc = lng ? 0 : cnt;
+        for (int t = 0; t < kNarrowShort; t += 4) {
+          if (__builtin_amdgcn_ballot_w64(sc > t) == 0) break;
           int k[4];
           bool ok[4];
           uint32_t ip[4];
