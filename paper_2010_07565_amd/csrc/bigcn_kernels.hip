@@ -1782,12 +1782,41 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   const int64_t eb = readlane64(st, 0);
   const int64_t ee = readlane64(en, nr - 1);
   const int total = (int)(ee - eb);
-  const int L = (total + kWavesPerBlock - 1) / kWavesPerBlock;
   const bool last = wv == kWavesPerBlock - 1;
-  const int ws = min(wv * L, total);
-  const int we = last ? total : min(ws + L, total);
   const int rs_l = (int)(st - eb);
   const int re_l = (int)(en - eb);
+  // Share boundaries bnd[0..4] (relative edge positions, nondecreasing):
+  // each share takes an equal part of the edges still unassigned, except
+  // that a share whose rows (the row cut at its start and those starting in
+  // it) would number more than S ends at the start of the row that would be
+  // its (S+1)-th, saving its wave a second round of rows, as long as the
+  // shares after it then stay within one landing chunk of the equal split.
+  const int L = (total + kWavesPerBlock - 1) / kWavesPerBlock;
+  int bnd[kWavesPerBlock + 1];
+  bnd[0] = 0;
+  bnd[kWavesPerBlock] = total;
+#pragma unroll
+  for (int i = 1; i < kWavesPerBlock; ++i) {
+    const int lo = bnd[i - 1];
+    const int rem = kWavesPerBlock - i + 1;  // shares left, this one included
+    int b = lo + (total - lo + rem - 1) / rem;
+    const int first =
+        (int)__builtin_popcountll(__builtin_amdgcn_ballot_w64(lane < nr && rs_l < lo));
+    const int cut = (first > 0 && __builtin_amdgcn_readlane(re_l, first - 1) > lo) ? 1 : 0;
+    const int ends =
+        (int)__builtin_popcountll(__builtin_amdgcn_ballot_w64(lane < nr && rs_l < b));
+    if (ends - first + cut > S) {
+      const int bc = __builtin_amdgcn_readlane(rs_l, first + S - cut);
+      if (total - bc <= (rem - 1) * (L + CH)) b = bc;
+    }
+    bnd[i] = b;
+  }
+  int ws = 0, we = total;  // bnd[wv], bnd[wv + 1]
+#pragma unroll
+  for (int i = 0; i < kWavesPerBlock; ++i) {
+    if (i == wv) ws = bnd[i];
+    if (i == wv + 1) we = bnd[i];
+  }
   const int o_b = (int)__builtin_popcountll(__builtin_amdgcn_ballot_w64(lane < nr && rs_l < ws));
   const int o_e = last ? nr
                        : (int)__builtin_popcountll(
@@ -2017,12 +2046,16 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   __syncthreads();
   // The row this wave started that runs past its share: its pieces, in share
   // order, from this wave (tail) and the waves that follow (heads).
-  if (!last && o_e > o_b && L > 0) {
+  if (!last && o_e > o_b && total > 0) {
     const int it = o_e - 1;
     const int rs = __builtin_amdgcn_readlane(rs_l, it);
     const int re = __builtin_amdgcn_readlane(re_l, it);
     if (re > we) {
-      const int kend = min((re - 1) / L, kWavesPerBlock - 1);
+      // the last wave whose share starts inside the row
+      int kend = wv;
+#pragma unroll
+      for (int m = 1; m < kWavesPerBlock; ++m)
+        if (m > wv && bnd[m] < re) kend = m;
       if (lane < G) {
         float sum[CPL];
 #pragma unroll
