@@ -1493,6 +1493,14 @@ constexpr int kNarrowShort = 16;  // edges in a share up to which a row is row-p
 template <int CPL>
 constexpr int narrow_batch() { return CPL == 4 ? 16 : 8; }
 
+// Block barrier for data exchanged through LDS only: this wave's LDS
+// operations complete first (lgkmcnt 0), while its global loads and stores
+// may stay in flight (no vmcnt wait, unlike __syncthreads).
+__device__ inline void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // vmcnt 63, expcnt 7, lgkmcnt 0
+  __builtin_amdgcn_s_barrier();
+}
+
 // 64-bit lane exchange within quads (DPP quad_perm control CTRL).
 template <int CTRL>
 __device__ inline uint64_t dpp_u64(uint64_t v) {
@@ -1760,16 +1768,39 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   const int nr = (int)(n - r_lo < rpb ? n - r_lo : rpb);
   // lane l < nr: bounds of row r_lo + l (lanes past nr repeat the last row)
   const int64_t rl = r_lo + (lane < nr ? lane : nr - 1);
-  const int64_t st = rowptr[rl];
-  const int64_t en = rowptr[rl + 1];
-  if (NX == 1) {
-    for (int i = threadIdx.x; i < nx.dn; i += kBlock) s_bn[i] = Bn[(int64_t)i * ldbn];
-  }
-  if (threadIdx.x < 64) {
-    const int k = threadIdx.x;
-    s_epi[0][k] = k < d ? alpha[k] : 0.f;
-    s_epi[1][k] = (k < d && bias != nullptr) ? bias[k] : 0.f;
-    s_epi[2][k] = (NX == 2 && k < d) ? alpha_s[k] : 0.f;
+  int64_t st, en;
+  {
+    // The block's constants and the row bounds, every load issued before
+    // the first LDS store:
+    // thread t < 64 fetches column t's alpha, bias and alpha_self (zero past
+    // d, the byte ranges ending there), and with NX == 1 thread t < d' word
+    // 0 of next weight column t (d' <= 256 threads).
+    const int t = threadIdx.x;
+    const uint32_t eo = t < 64 ? (uint32_t)t * 4u : kPastEnd;
+    const uint32_t eb4 = (uint32_t)d * 4u;
+    const float e_al = __builtin_bit_cast(
+        float, __builtin_amdgcn_raw_buffer_load_b32(raw_rsrc(alpha, eb4), (int)eo, 0, 0));
+    const float e_bi = __builtin_bit_cast(
+        float, __builtin_amdgcn_raw_buffer_load_b32(raw_rsrc(bias, bias != nullptr ? eb4 : 0u),
+                                                    (int)eo, 0, 0));
+    float e_as = 0.f;
+    if constexpr (NX == 2)
+      e_as = __builtin_bit_cast(
+          float, __builtin_amdgcn_raw_buffer_load_b32(raw_rsrc(alpha_s, eb4), (int)eo, 0, 0));
+    uint64_t e_bn = 0;
+    if constexpr (NX == 1)
+      e_bn = __builtin_bit_cast(
+          uint64_t, __builtin_amdgcn_raw_buffer_load_b64(
+                        raw_rsrc(Bn, (uint32_t)(nx.dn * ldbn * 8)),
+                        (int)(t < nx.dn ? (uint32_t)(t * ldbn) * 8u : kPastEnd), 0, 0));
+    st = rowptr[rl];
+    en = rowptr[rl + 1];
+    if (t < 64) {
+      s_epi[0][t] = e_al;
+      s_epi[1][t] = e_bi;
+      s_epi[2][t] = e_as;
+    }
+    if (NX == 1 && t < nx.dn) s_bn[t] = e_bn;
   }
   NarrowEpi ep;
   ep.s_alpha = &s_epi[0][0];
@@ -1846,7 +1877,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
           rsi, (int)(p0 + 64 * r + lane < p1 ? (uint32_t)(p0 + 64 * r + lane) * 4u : kPastEnd),
           0, 0);
   }
-  __syncthreads();  // s_epi and s_bn are read by finish_slot
+  lds_barrier();  // s_epi and s_bn are read by finish_slot
 
   LandT* land = &s_land[wv][0];
   float* sgk = &s_gk[wv][0];
@@ -2043,7 +2074,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     if (on && !headp && !tailp)
       finish_slot<G, CPL, NX>(r_lo + idx, re - rs, mean, sum, ep, c, out, ldo, nx, nbn, s_bn);
   }
-  __syncthreads();
+  lds_barrier();
   // The row this wave started that runs past its share: its pieces, in share
   // order, from this wave (tail) and the waves that follow (heads).
   if (!last && o_e > o_b && total > 0) {
@@ -2596,6 +2627,8 @@ hipError_t spmm_narrow_gc(int64_t n, const int64_t* rowptr, const int32_t* colid
   const int32_t rpb = narrow_rows_per_block(n);
   const dim3 grid((unsigned)((n + rpb - 1) / rpb));
   const int nbn = fn.kind == 1 ? q8_lane_bytes(fn.d_out) : 1;
+  // one thread per next weight column stages its first word
+  if (fn.kind == 1 && fn.d_out > kBlock) return hipErrorInvalidValue;
   const size_t lds = fn.kind == 1 ? (size_t)fn.d_out * sizeof(uint64_t) : 0;
 #define BIGCN_NARROW(NX)                                                                   \
   hipLaunchKernelGGL((k_spmm_narrow<G, CPL, NX>), grid, dim3(kBlock), lds, stream, n,      \
