@@ -8,9 +8,11 @@
 //   dζ    = Ã^T G                                (the edge-chunked aggregation
 //                                                 of bigcn_kernels.hip on fp32
 //                                                 rows; Â structurally symmetric)
-//   dW~^T = (H~^T dζ)^T,  H~ = diag(β) F         (fp64 partial sums per chunk
+//   dW~^T = (H~^T dζ)^T,  H~ = diag(β) F         (fp32 MFMA, 64-row runs added
+//                                                 to fp64 partial sums per chunk
 //                                                 of rows, summed in order)
-//   dH~   = dζ W~^T,      W~ = B diag(α);  dH = dH~ 1[|dH~| < 1]   (Eq. (14))
+//   dH~   = dζ W~^T,      W~ = B diag(α);  dH = dH~ 1[|dH~| < 1]   (Eq. (14);
+//                                                 fp32 MFMA)
 //   dW    = Eq. (15) with 1[|W| < 1] for the derivative of sign.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -93,58 +95,94 @@ __global__ __launch_bounds__(kB) void k_bwd_colsum_final(
   db[k] = (float)acc;
 }
 
-// Partial sums of dW~^T over a chunk of R rows:
-//   part[c][j][64w + b] = sum_{i in chunk c} s(F_i, 64w + b) * β_i dζ_ij.
-// Block (chunk c, word w, 64 columns): thread (column j, bit group q) owns
-// bits 16q .. 16q+15 of the word for column j.  Each run of 64 rows is
-// summed in fp32 (at most 64 terms) and added to fp64 accumulators, in row
-// order.  Row words are wave-uniform.
-__global__ __launch_bounds__(kB) void k_bwd_wtilde_part(
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float float4_t __attribute__((ext_vector_type(4)));
+
+// ±1 in fp32 from bit sh of dw: a set bit (sign +1) gives +1.0f, a clear bit
+// -1.0f (the bit moved to the sign position, then flipped with the pattern
+// of -1.0f).
+__device__ inline float pm1(uint32_t dw, int sh) {
+  return __builtin_bit_cast(float, ((dw >> sh) << 31) ^ 0xBF800000u);
+}
+
+// Bit k of a packed row, ±1: word k/64 of the row, already loaded in w[].
+__device__ inline float pm1_word(uint64_t w, int sh) {
+  return pm1(sh < 32 ? (uint32_t)w : (uint32_t)(w >> 32), sh & 31);
+}
+
+// Partial sums of dW~^T over a chunk of R rows, on the matrix cores:
+//   part[c][j][k] = sum_{i in chunk c} s(F_i, k) * β_i dζ_ij.
+// One wave per (chunk c, 16 columns j, 16*NT bits k): fp32 MFMA 16x16x4 with
+// A[j][q] = β_i dζ_ij and B[q][k] = s(F_i, k) for the four rows i = r0+4s+q
+// of step s (lane group q); the products are exact (one operand is ±1).
+// Each run of 64 rows is summed in fp32 (64 terms per output) and added to
+// fp64 accumulators, runs in row order.  Lane (n, q) ends holding outputs
+// (4q + r, n) of each 16x16 tile.
+template <int NT>
+__global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
     int64_t n, int32_t d_in, int32_t d_out, const uint64_t* __restrict__ F, int64_t ldf,
     const float* __restrict__ beta, const float* __restrict__ dz, int64_t lddz,
-    int64_t R, double* __restrict__ part) {
-  const int64_t c = blockIdx.x;
-  const int w = blockIdx.y;
-  const int j = blockIdx.z * 64 + (threadIdx.x & 63);
-  const int q = threadIdx.x >> 6;  // wave index: bit group
-  if (j >= d_out) return;          // no barrier in this kernel
+    int64_t R, int32_t jtiles, int32_t kgroups, int64_t tasks, double* __restrict__ part) {
+  constexpr int NW = NT >= 4 ? NT / 4 : 1;  // packed words a lane reads per row
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * (kB / 64) +
+                    __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (t >= tasks) return;  // no barrier in this kernel
+  const int kg = (int)(t % kgroups);
+  const int jt = (int)((t / kgroups) % jtiles);
+  const int64_t c = t / ((int64_t)kgroups * jtiles);
+  const int m = lane & 15, q = lane >> 4;
+  const int j = jt * 16 + m;  // this lane's A column
+  const int k0 = kg * 16 * NT;
+  const int w0 = k0 >> 6;
+  const int kw = (d_in + 63) >> 6;
   const int64_t i0 = c * R, i1 = std::min<int64_t>(n, i0 + R);
-  double acc[16];
+  f32x4_t acc[NT];
+  double acc64[NT][4];
 #pragma unroll
-  for (int b = 0; b < 16; ++b) acc[b] = 0.0;
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc64[nt][r] = 0.0;
   for (int64_t r0 = i0; r0 < i1; r0 += 64) {
-    const int64_t r1 = std::min<int64_t>(i1, r0 + 64);
-    float sub[16];
 #pragma unroll
-    for (int b = 0; b < 16; ++b) sub[b] = 0.f;
-    int64_t i = r0;
-    for (; i + 8 <= r1; i += 8) {  // eight rows' loads in flight, summed in order
-      float x[8];
-      uint32_t bits[8];
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < 16; s0 += 8) {  // eight steps (32 rows) of loads in flight
+      float a[8];
+      uint64_t wd[8][NW];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        x[u] = beta[i + u] * dz[(i + u) * lddz + j];
-        bits[u] = (uint32_t)(F[(i + u) * ldf + w] >> (16 * q)) & 0xFFFFu;
+        const int64_t row = r0 + 4 * (s0 + u) + q;
+        const bool ok = row < i1;
+        a[u] = ok && j < d_out ? beta[row] * dz[row * lddz + j] : 0.f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+          wd[u][w] = ok && w0 + w < kw ? F[row * ldf + w0 + w] : 0ull;
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u)
 #pragma unroll
-        for (int b = 0; b < 16; ++b) sub[b] += ((bits[u] >> b) & 1u) ? x[u] : -x[u];
-    }
-    for (; i < r1; ++i) {
-      const float x = beta[i] * dz[i * lddz + j];
-      const uint32_t bits = (uint32_t)(F[i * ldf + w] >> (16 * q)) & 0xFFFFu;
-#pragma unroll
-      for (int b = 0; b < 16; ++b) sub[b] += ((bits >> b) & 1u) ? x : -x;
+        for (int nt = 0; nt < NT; ++nt) {
+          const int sh = (k0 & 63) + 16 * (nt & 3) + m;
+          const float b = pm1_word(wd[u][nt >> 2], sh);
+          acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u], b, acc[nt], 0, 0, 0);
+        }
     }
 #pragma unroll
-    for (int b = 0; b < 16; ++b) acc[b] += (double)sub[b];
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc64[nt][r] += (double)acc[nt][r];
   }
-  double* dst = part + ((int64_t)c * d_out + j) * d_in + 64 * w + 16 * q;
-  const int nb = std::min(16, d_in - 64 * w - 16 * q);
 #pragma unroll
-  for (int b = 0; b < 16; ++b)
-    if (b < nb) dst[b] = acc[b];
+  for (int r = 0; r < 4; ++r) {
+    const int jo = jt * 16 + 4 * q + r;
+    if (jo >= d_out) break;
+    double* dst = part + ((int64_t)c * d_out + jo) * d_in;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int k = k0 + 16 * nt + m;
+      if (k < d_in) dst[k] = acc64[nt][r];
+    }
+  }
 }
 
 // dW~^T[j][k] = sum over chunks in order; fp64 kept for Eq. (15), fp32 copy
@@ -197,48 +235,82 @@ __global__ __launch_bounds__(kB) void k_bwd_weights(
   }
 }
 
-// dH~[i][k] = sum_j dζ_ij α_j s(B_j, k), j in order, and Eq. (14).  One
-// wave per row; lane l owns columns 64w + l (w < kw <= KW); the packed
-// weight words sit in LDS ([d_out][kw]) and are read as wave broadcasts.
-template <int KW>
-__global__ __launch_bounds__(kB) void k_bwd_htilde(
+// dH~[i][k] = sum_j α_j dζ_ij s(B_j, k) and Eq. (14), on the matrix cores.
+// One wave per (16 rows, 16*NT columns k): fp32 MFMA 16x16x4 with
+// A[i][q] = α_j dζ_ij and B[q][k] = s(B_j, k) (exact products).  Step s of a
+// 32-wide chunk of j gives lane group q the index j = j0 + 8q + s, so a
+// lane's eight A values are two 16-byte loads of its row.  The packed weight
+// words and α sit in LDS (rows padded to a multiple of 32 with zeros).  The
+// sum over j runs in fp32, as a sequential sum would.
+template <int NT>
+__global__ __launch_bounds__(kB) void k_bwd_htilde_mfma(
     int64_t n, int32_t d_in, int32_t d_out, const float* __restrict__ dz, int64_t lddz,
     const uint64_t* __restrict__ B, int64_t ldb, const float* __restrict__ alpha,
-    float* __restrict__ dht, int64_t lddht, float* __restrict__ dh, int64_t lddh) {
-  extern __shared__ uint64_t sB[];
+    int32_t kgroups, float* __restrict__ dht, int64_t lddht, float* __restrict__ dh,
+    int64_t lddh) {
+  constexpr int NW = NT >= 4 ? NT / 4 : 1;
+  extern __shared__ uint64_t sB[];  // [jpad][kw] words, then α [jpad]
   const int kw = (d_in + 63) >> 6;
-  for (int idx = threadIdx.x; idx < d_out * kw; idx += kB)
-    sB[idx] = B[(int64_t)(idx / kw) * ldb + idx % kw];
+  const int jpad = (d_out + 31) & ~31;
+  float* sA = reinterpret_cast<float*>(sB + (size_t)jpad * kw);
+  for (int idx = threadIdx.x; idx < jpad * kw; idx += kB) {
+    const int jj = idx / kw;
+    sB[idx] = jj < d_out ? B[(int64_t)jj * ldb + idx % kw] : 0ull;
+  }
+  for (int jj = threadIdx.x; jj < jpad; jj += kB) sA[jj] = jj < d_out ? alpha[jj] : 0.f;
   __syncthreads();
   const int lane = threadIdx.x & 63;
+  const int m = lane & 15, q = lane >> 4;
+  const int64_t tasks = (n + 15) / 16 * kgroups;
   const int64_t nwaves = (int64_t)gridDim.x * (kB / 64);
-  for (int64_t i = (int64_t)blockIdx.x * (kB / 64) +
+  for (int64_t t = (int64_t)blockIdx.x * (kB / 64) +
                    __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-       i < n; i += nwaves) {
-    float acc[KW];
+       t < tasks; t += nwaves) {
+    const int kg = (int)(t % kgroups);
+    const int64_t i0 = (t / kgroups) * 16;
+    const int64_t row = i0 + m;  // this lane's A row
+    const int k0 = kg * 16 * NT;
+    const int w0 = k0 >> 6;
+    f32x4_t acc[NT];
 #pragma unroll
-    for (int w = 0; w < KW; ++w) acc[w] = 0.f;
-    for (int j0 = 0; j0 < d_out; j0 += 64) {
-      const int jl = j0 + lane;
-      const float v = jl < d_out ? alpha[jl] * dz[i * lddz + jl] : 0.f;
-      const int jn = std::min(64, d_out - j0);
-      for (int jj = 0; jj < jn; ++jj) {
-        const float vj = __builtin_bit_cast(
-            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), jj));
-        const uint64_t* row = sB + (j0 + jj) * kw;
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j0 = 0; j0 < d_out; j0 += 32) {
+      const int jb = j0 + 8 * q;
+      float4_t v0 = {0.f, 0.f, 0.f, 0.f}, v1 = {0.f, 0.f, 0.f, 0.f};
+      if (row < n && jb < d_out) v0 = *reinterpret_cast<const float4_t*>(dz + row * lddz + jb);
+      if (row < n && jb + 4 < d_out)
+        v1 = *reinterpret_cast<const float4_t*>(dz + row * lddz + jb + 4);
+      float a[8];
 #pragma unroll
-        for (int w = 0; w < KW; ++w) {
-          if (w >= kw) break;
-          acc[w] += ((row[w] >> lane) & 1ull) ? vj : -vj;
+      for (int s = 0; s < 8; ++s) {
+        const float v = s < 4 ? v0[s] : v1[s - 4];
+        a[s] = jb + s < d_out ? sA[jb + s] * v : 0.f;
+      }
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        uint64_t wd[NW];
+#pragma unroll
+        for (int w = 0; w < NW; ++w) wd[w] = w0 + w < kw ? sB[(jb + s) * kw + w0 + w] : 0ull;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int sh = (k0 & 63) + 16 * (nt & 3) + m;
+          const float b = pm1_word(wd[nt >> 2], sh);
+          acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b, acc[nt], 0, 0, 0);
         }
       }
     }
 #pragma unroll
-    for (int w = 0; w < KW; ++w) {
-      const int k = 64 * w + lane;
-      if (w >= kw || k >= d_in) break;
-      if (dht != nullptr) dht[i * lddht + k] = acc[w];
-      if (dh != nullptr) dh[i * lddh + k] = fabsf(acc[w]) < 1.f ? acc[w] : 0.f;
+    for (int r = 0; r < 4; ++r) {
+      const int64_t ro = i0 + 4 * q + r;
+      if (ro >= n) break;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int k = k0 + 16 * nt + m;
+        if (k >= d_in) continue;
+        const float v = acc[nt][r];
+        if (dht != nullptr) dht[ro * lddht + k] = v;
+        if (dh != nullptr) dh[ro * lddh + k] = fabsf(v) < 1.f ? v : 0.f;
+      }
     }
   }
 }
@@ -247,9 +319,19 @@ inline unsigned grid_of(int64_t threads) {
   return (unsigned)std::max<int64_t>(1, (threads + kB - 1) / kB);
 }
 
-// Workspace layout of bigcn_layer_backward.
+// Power of two >= v, at most cap.
+inline int pow2_at_least(int v, int cap) {
+  int p = 1;
+  while (p < v && p < cap) p <<= 1;
+  return p;
+}
+
+// Workspace layout of bigcn_layer_backward, and the tiling of the two
+// matrix-core products: dW~ takes 16 x 16*ntw tiles (ntw <= 8), dH~
+// 16 x 16*nth tiles (nth <= 16), each with kgroups tiles across d_in.
 struct BwdLayout {
   int64_t kw, ldm, R, chunks, Rdb, chunks_db;
+  int ntw, kgw, jtw, nth, kgh;
   size_t off_F, off_beta, off_s, off_ones, off_Gm, off_dz, off_pdb, off_pw, off_wtd,
       off_spmm, bytes;
 };
@@ -258,11 +340,18 @@ BwdLayout bwd_layout(int64_t n, int64_t nnz, int32_t d_in, int32_t d_out) {
   BwdLayout L;
   L.kw = words(d_in);
   L.ldm = (d_out + 3) / 4 * 4;
-  // Row chunks of the dW~ partial sums: about 2048 blocks of (chunk, word,
-  // 64 columns), chunks of at least 64 rows, partial sums within 512 MB.
-  const int64_t per_chunk = L.kw * ((d_out + 63) / 64);
-  int64_t chunks = std::max<int64_t>(1, 2048 / per_chunk);
-  chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, (n + 63) / 64));
+  const int ktiles = (d_in + 15) / 16;
+  L.ntw = pow2_at_least(ktiles, 8);
+  L.kgw = (ktiles + L.ntw - 1) / L.ntw;
+  L.jtw = (d_out + 15) / 16;
+  L.nth = pow2_at_least(ktiles, 16);
+  L.kgh = (ktiles + L.nth - 1) / L.nth;
+  // Row chunks of the dW~ partial sums: about 4096 waves of (chunk, 16
+  // columns, 16*ntw bits), chunks of at least 256 rows, partial sums within
+  // 512 MB.
+  const int64_t per_chunk = (int64_t)L.jtw * L.kgw;
+  int64_t chunks = std::max<int64_t>(1, 4096 / per_chunk);
+  chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, (n + 255) / 256));
   chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, (512ll << 20) / ((int64_t)d_out * d_in * 8)));
   L.R = std::max<int64_t>(1, (n + chunks - 1) / chunks);
   L.chunks = std::max<int64_t>(1, (n + L.R - 1) / L.R);
@@ -295,15 +384,27 @@ BwdLayout bwd_layout(int64_t n, int64_t nnz, int32_t d_in, int32_t d_out) {
 
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-template <int KW>
-void launch_htilde(int64_t n, int32_t d_in, int32_t d_out, const float* dz, int64_t lddz,
-                   const uint64_t* B, int64_t ldb, const float* alpha, float* dht,
-                   int64_t lddht, float* dh, int64_t lddh, hipStream_t s) {
-  const size_t lds = (size_t)d_out * words(d_in) * 8;
-  const int64_t blocks = std::min<int64_t>((n + 3) / 4, 8192);
-  hipLaunchKernelGGL((k_bwd_htilde<KW>), dim3((unsigned)std::max<int64_t>(1, blocks)),
-                     dim3(kB), lds, s, n, d_in, d_out, dz, lddz, B, ldb, alpha, dht, lddht,
-                     dh, lddh);
+template <int NT>
+void launch_htilde(int64_t n, int32_t d_in, int32_t d_out, int32_t kgroups, const float* dz,
+                   int64_t lddz, const uint64_t* B, int64_t ldb, const float* alpha,
+                   float* dht, int64_t lddht, float* dh, int64_t lddh, hipStream_t s) {
+  const int jpad = (d_out + 31) & ~31;
+  const size_t lds = (size_t)jpad * words(d_in) * 8 + (size_t)jpad * 4;
+  const int64_t tasks = (n + 15) / 16 * kgroups;
+  const int64_t blocks = std::min<int64_t>((tasks + 3) / 4, 2048);
+  hipLaunchKernelGGL((k_bwd_htilde_mfma<NT>), dim3((unsigned)std::max<int64_t>(1, blocks)),
+                     dim3(kB), lds, s, n, d_in, d_out, dz, lddz, B, ldb, alpha, kgroups, dht,
+                     lddht, dh, lddh);
+}
+
+template <int NT>
+void launch_wtilde(int64_t n, int32_t d_in, int32_t d_out, const BwdLayout& L,
+                   const uint64_t* F, const float* beta, const float* dz, double* part,
+                   hipStream_t s) {
+  const int64_t tasks = L.chunks * L.jtw * L.kgw;
+  hipLaunchKernelGGL((k_bwd_wtilde_mfma<NT>), dim3((unsigned)((tasks + 3) / 4)), dim3(kB), 0,
+                     s, n, d_in, d_out, F, L.kw, beta, dz, L.ldm, L.R, L.jtw, L.kgw, tasks,
+                     part);
 }
 
 }  // namespace
@@ -398,9 +499,12 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
                                    hipMemcpyDeviceToDevice, s));
   }
   // dW~^T, then Eq. (15).
-  hipLaunchKernelGGL(k_bwd_wtilde_part, dim3((unsigned)L.chunks, (unsigned)L.kw,
-                                             (unsigned)((d_out + 63) / 64)),
-                     dim3(kB), 0, s, n, d_in, d_out, F, L.kw, beta, dz, L.ldm, L.R, pw);
+  switch (L.ntw) {
+    case 1: launch_wtilde<1>(n, d_in, d_out, L, F, beta, dz, pw, s); break;
+    case 2: launch_wtilde<2>(n, d_in, d_out, L, F, beta, dz, pw, s); break;
+    case 4: launch_wtilde<4>(n, d_in, d_out, L, F, beta, dz, pw, s); break;
+    default: launch_wtilde<8>(n, d_in, d_out, L, F, beta, dz, pw, s); break;
+  }
   hipLaunchKernelGGL(k_bwd_wtilde_final, dim3(grid_of((int64_t)d_in * d_out)), dim3(kB), 0,
                      s, d_in, d_out, L.chunks, pw, wtd, dwt_tilde, lddwt);
   hipLaunchKernelGGL(k_bwd_weights, dim3((unsigned)d_out), dim3(kB), 0, s, d_in, wtd, wbits,
@@ -408,16 +512,16 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
   BIGCN_CHECK(hipGetLastError());
   // dH~ and dH (Eq. (14)).
   if (n > 0 && (dh != nullptr || dh_tilde != nullptr)) {
-    const int kw = (int)L.kw;
-#define BIGCN_HT(KWV)                                                                     \
-  launch_htilde<KWV>(n, d_in, d_out, dz, L.ldm, wbits, ldw, alpha, dh_tilde, lddht, dh, \
-                     lddh, s)
-    if (kw <= 1) BIGCN_HT(1);
-    else if (kw <= 2) BIGCN_HT(2);
-    else if (kw <= 4) BIGCN_HT(4);
-    else if (kw <= 8) BIGCN_HT(8);
-    else if (kw <= 16) BIGCN_HT(16);
-    else BIGCN_HT(32);
+#define BIGCN_HT(NTV)                                                                  \
+  launch_htilde<NTV>(n, d_in, d_out, L.kgh, dz, L.ldm, wbits, ldw, alpha, dh_tilde, lddht, \
+                     dh, lddh, s)
+    switch (L.nth) {
+      case 1: BIGCN_HT(1); break;
+      case 2: BIGCN_HT(2); break;
+      case 4: BIGCN_HT(4); break;
+      case 8: BIGCN_HT(8); break;
+      default: BIGCN_HT(16); break;
+    }
 #undef BIGCN_HT
     BIGCN_CHECK(hipGetLastError());
   }
