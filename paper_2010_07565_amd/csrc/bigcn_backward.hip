@@ -133,6 +133,7 @@ __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
   const int64_t c = t / ((int64_t)kgroups * jtiles);
   const int m = lane & 15, q = lane >> 4;
   const int j = jt * 16 + m;  // this lane's A column
+  const int jc = j < d_out ? j : d_out - 1;
   const int k0 = kg * 16 * NT;
   const int w0 = k0 >> 6;
   const int kw = (d_in + 63) >> 6;
@@ -147,17 +148,21 @@ __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     for (int s0 = 0; s0 < 16; s0 += 8) {  // eight steps (32 rows) of loads in flight
+      // Loads at clamped (in-range) addresses with no branch, so all of the
+      // batch's loads are in flight together; rows past the chunk and
+      // columns past d_out are then zeroed by a 0/1 factor (a select would
+      // let the compiler move the loads into a branch and wait on each).
       float a[8];
       uint64_t wd[8][NW];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int64_t row = r0 + 4 * (s0 + u) + q;
-        const bool ok = row < i1;
-        a[u] = ok && j < d_out ? beta[row] * dz[row * lddz + j] : 0.f;
+        const int64_t rc = row < i1 ? row : i1 - 1;
+        a[u] = beta[rc] * dz[rc * lddz + jc] * (row < i1 && j < d_out ? 1.f : 0.f);
 #pragma unroll
-        for (int w = 0; w < NW; ++w)
-          wd[u][w] = ok && w0 + w < kw ? F[row * ldf + w0 + w] : 0ull;
+        for (int w = 0; w < NW; ++w) wd[u][w] = F[rc * ldf + (w0 + w < kw ? w0 + w : kw - 1)];
       }
+      __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any MFMA
 #pragma unroll
       for (int u = 0; u < 8; ++u)
 #pragma unroll
@@ -249,7 +254,7 @@ __global__ __launch_bounds__(kB) void k_bwd_htilde_mfma(
     int32_t kgroups, float* __restrict__ dht, int64_t lddht, float* __restrict__ dh,
     int64_t lddh) {
   constexpr int NW = NT >= 4 ? NT / 4 : 1;
-  extern __shared__ uint64_t sB[];  // [jpad][kw] words, then α [jpad]
+  extern __shared__ uint64_t sB[];  // [jpad][kw] words, then α [jpad] (16-byte aligned)
   const int kw = (d_in + 63) >> 6;
   const int jpad = (d_out + 31) & ~31;
   float* sA = reinterpret_cast<float*>(sB + (size_t)jpad * kw);
@@ -274,17 +279,30 @@ __global__ __launch_bounds__(kB) void k_bwd_htilde_mfma(
     f32x4_t acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // The next chunk's two 16-byte loads (clamped to valid addresses: a row
+    // past n repeats row n-1, whose outputs are never stored; columns past
+    // d_out are zeroed below) are issued before this chunk's MFMAs.
+    const float* zr = dz + (row < n ? row : n - 1) * lddz;
+    auto load_chunk = [&](int jn, float4_t& u0, float4_t& u1) {
+      const int c = jn + 8 * q;
+      u0 = *reinterpret_cast<const float4_t*>(zr + (c < d_out ? c : 0));
+      u1 = *reinterpret_cast<const float4_t*>(zr + (c + 4 < d_out ? c + 4 : 0));
+    };
+    float4_t n0, n1;
+    load_chunk(0, n0, n1);
     for (int j0 = 0; j0 < d_out; j0 += 32) {
       const int jb = j0 + 8 * q;
-      float4_t v0 = {0.f, 0.f, 0.f, 0.f}, v1 = {0.f, 0.f, 0.f, 0.f};
-      if (row < n && jb < d_out) v0 = *reinterpret_cast<const float4_t*>(dz + row * lddz + jb);
-      if (row < n && jb + 4 < d_out)
-        v1 = *reinterpret_cast<const float4_t*>(dz + row * lddz + jb + 4);
+      const float4_t v0 = n0, v1 = n1;
+      if (j0 + 32 < d_out) load_chunk(j0 + 32, n0, n1);
+      __builtin_amdgcn_sched_barrier(0);
+      const float4_t al0 = *reinterpret_cast<const float4_t*>(sA + jb);
+      const float4_t al1 = *reinterpret_cast<const float4_t*>(sA + jb + 4);
       float a[8];
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
         const float v = s < 4 ? v0[s] : v1[s - 4];
-        a[s] = jb + s < d_out ? sA[jb + s] * v : 0.f;
+        const float al = s < 4 ? al0[s] : al1[s - 4];
+        a[s] = jb + s < d_out ? al * v : 0.f;
       }
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
