@@ -30,15 +30,16 @@ inline size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
 inline int64_t words(int64_t k) { return (k + 63) / 64; }
 
 // Gm = G (zero where the ReLU output is not positive, and in the pad columns
-// up to ldm); s_i = the source-side factor of Ã^T (D̂_ii^-1/2 symmetric,
-// D̂_ii^-1 mean); ones = 1 (the per-column scale of the aggregation).
+// up to ldm), unless Gm is null (G is then aggregated in place); s_i = the
+// source-side factor of Ã^T (D̂_ii^-1/2 symmetric, D̂_ii^-1 mean); ones = 1
+// (the per-column scale of the aggregation).
 __global__ __launch_bounds__(kB) void k_bwd_prep(
     int64_t n, int32_t d, const float* __restrict__ G, int64_t ldg,
     const float* __restrict__ out, int64_t ldo, int relu, float* __restrict__ Gm,
     int64_t ldm, const int64_t* __restrict__ rowptr, int mean, float* __restrict__ s,
     float* __restrict__ ones) {
   const int64_t idx = (int64_t)blockIdx.x * kB + threadIdx.x;
-  if (idx < n * ldm) {
+  if (Gm != nullptr && idx < n * ldm) {
     const int64_t i = idx / ldm;
     const int64_t k = idx - i * ldm;
     float v = 0.f;
@@ -417,11 +418,11 @@ void launch_htilde(int64_t n, int32_t d_in, int32_t d_out, int32_t kgroups, cons
 
 template <int NT>
 void launch_wtilde(int64_t n, int32_t d_in, int32_t d_out, const BwdLayout& L,
-                   const uint64_t* F, const float* beta, const float* dz, double* part,
-                   hipStream_t s) {
+                   const uint64_t* F, const float* beta, const float* dz, int64_t lddz,
+                   double* part, hipStream_t s) {
   const int64_t tasks = L.chunks * L.jtw * L.kgw;
   hipLaunchKernelGGL((k_bwd_wtilde_mfma<NT>), dim3((unsigned)((tasks + 3) / 4)), dim3(kB), 0,
-                     s, n, d_in, d_out, F, L.kw, beta, dz, L.ldm, L.R, L.jtw, L.kgw, tasks,
+                     s, n, d_in, d_out, F, L.kw, beta, dz, lddz, L.R, L.jtw, L.kgw, tasks,
                      part);
 }
 
@@ -475,8 +476,16 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
   float* beta = (float*)(ws + L.off_beta);
   float* sc = (float*)(ws + L.off_s);
   float* ones = (float*)(ws + L.off_ones);
-  float* Gm = (float*)(ws + L.off_Gm);
-  float* dz = (float*)(ws + L.off_dz);
+  // G is aggregated in place when no ReLU mask applies and its rows suit the
+  // aggregation's 16-byte loads; dζ is written straight to the caller's
+  // buffer under the same condition (else to the workspace, then copied).
+  const bool g_direct = act != BIGCN_ACT_RELU && ldg % 4 == 0 && aligned(gout, 16);
+  const bool z_direct = dzeta != nullptr && lddz % 4 == 0 && aligned(dzeta, 16);
+  float* Gm = g_direct ? nullptr : (float*)(ws + L.off_Gm);
+  const float* Gsrc = g_direct ? gout : Gm;
+  const int64_t ldsrc = g_direct ? ldg : L.ldm;
+  float* dz = z_direct ? dzeta : (float*)(ws + L.off_dz);
+  const int64_t ldz = z_direct ? lddz : L.ldm;
   double* pdb = (double*)(ws + L.off_pdb);
   double* pw = (double*)(ws + L.off_pw);
   double* wtd = (double*)(ws + L.off_wtd);
@@ -493,13 +502,14 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
   if (n > 0)
     BIGCN_CHECK(bigcn::launch_pack(h, n, d_in, ldh, nullptr, nullptr, nullptr, 0, F, L.kw,
                                    beta, s));
-  hipLaunchKernelGGL(k_bwd_prep, dim3(grid_of(std::max<int64_t>(n * L.ldm, L.ldm))),
+  hipLaunchKernelGGL(k_bwd_prep,
+                     dim3(grid_of(std::max<int64_t>(g_direct ? n : n * L.ldm, L.ldm))),
                      dim3(kB), 0, s, n, d_out, gout, ldg, out, ldo,
                      act == BIGCN_ACT_RELU ? 1 : 0, Gm, L.ldm, rowptr, mean, sc, ones);
   BIGCN_CHECK(hipGetLastError());
   if (db != nullptr) {
     hipLaunchKernelGGL(k_bwd_colsum_part, dim3((unsigned)L.chunks_db), dim3(kB), 0, s, n,
-                       d_out, Gm, L.ldm, L.Rdb, pdb);
+                       d_out, Gsrc, ldsrc, L.Rdb, pdb);
     hipLaunchKernelGGL(k_bwd_colsum_final, dim3(grid_of(d_out)), dim3(kB), 0, s, d_out,
                        L.chunks_db, pdb, db);
     BIGCN_CHECK(hipGetLastError());
@@ -509,19 +519,19 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
   if (n > 0) {
     const bigcn::SpmmPlan plan = bigcn::spmm_plan(n, nnz, d_out);
     BIGCN_CHECK(bigcn::launch_spmm_rows(n, nnz, rowptr, plan, wsp, s));
-    BIGCN_CHECK(bigcn::launch_spmm(n, nnz, rowptr, colidx, mean ? 2 : 0, sc, Gm,
-                                   bigcn::IType::F32, d_out, L.ldm, ones, nullptr, 0, dz,
-                                   L.ldm, plan, wsp, s));
-    if (dzeta != nullptr)
+    BIGCN_CHECK(bigcn::launch_spmm(n, nnz, rowptr, colidx, mean ? 2 : 0, sc, Gsrc,
+                                   bigcn::IType::F32, d_out, ldsrc, ones, nullptr, 0, dz,
+                                   ldz, plan, wsp, s));
+    if (dzeta != nullptr && !z_direct)
       BIGCN_CHECK(hipMemcpy2DAsync(dzeta, lddz * 4, dz, L.ldm * 4, (size_t)d_out * 4, n,
                                    hipMemcpyDeviceToDevice, s));
   }
   // dW~^T, then Eq. (15).
   switch (L.ntw) {
-    case 1: launch_wtilde<1>(n, d_in, d_out, L, F, beta, dz, pw, s); break;
-    case 2: launch_wtilde<2>(n, d_in, d_out, L, F, beta, dz, pw, s); break;
-    case 4: launch_wtilde<4>(n, d_in, d_out, L, F, beta, dz, pw, s); break;
-    default: launch_wtilde<8>(n, d_in, d_out, L, F, beta, dz, pw, s); break;
+    case 1: launch_wtilde<1>(n, d_in, d_out, L, F, beta, dz, ldz, pw, s); break;
+    case 2: launch_wtilde<2>(n, d_in, d_out, L, F, beta, dz, ldz, pw, s); break;
+    case 4: launch_wtilde<4>(n, d_in, d_out, L, F, beta, dz, ldz, pw, s); break;
+    default: launch_wtilde<8>(n, d_in, d_out, L, F, beta, dz, ldz, pw, s); break;
   }
   hipLaunchKernelGGL(k_bwd_wtilde_final, dim3(grid_of((int64_t)d_in * d_out)), dim3(kB), 0,
                      s, d_in, d_out, L.chunks, pw, wtd, dwt_tilde, lddwt);
@@ -531,7 +541,7 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
   // dH~ and dH (Eq. (14)).
   if (n > 0 && (dh != nullptr || dh_tilde != nullptr)) {
 #define BIGCN_HT(NTV)                                                                  \
-  launch_htilde<NTV>(n, d_in, d_out, L.kgh, dz, L.ldm, wbits, ldw, alpha, dh_tilde, lddht, \
+  launch_htilde<NTV>(n, d_in, d_out, L.kgh, dz, ldz, wbits, ldw, alpha, dh_tilde, lddht, \
                      dh, lddh, s)
     switch (L.nth) {
       case 1: BIGCN_HT(1); break;
