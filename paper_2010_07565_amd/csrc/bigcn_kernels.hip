@@ -1253,8 +1253,9 @@ __device__ inline int64_t readlane64(int64_t v, int l) {
 // stored in the same interleaved order.  Structure otherwise as
 // k_spmm_wave, except that each wave finds its first row itself
 // (find_row: no row plan is needed); finished rows go through
-// finish_row<NX, NB, NBN>.
-template <int U, int NX, int NB, int NBN>
+// finish_row<NX, NB, NBN>.  P = K mod 2 (the parity p): for even K the
+// p * sum g term is zero and its running sum is not kept.
+template <int U, int NX, int NB, int NBN, int P>
 __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
     int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, int mean, const float* __restrict__ g,
@@ -1336,7 +1337,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
             fma_n<NB>(a1, gg[u], codes_to_float<NB>(vv[u]));
           else
             fma_n<NB>(a0, gg[u], codes_to_float<NB>(vv[u]));
-          gsum += gg[u];
+          if constexpr (P != 0) gsum += gg[u];
         }
         continue;
       }
@@ -1345,7 +1346,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
         const int eu = e0 + u;
         if (eu >= nE) break;
         if (eu == cur_end) {
-          const float4_t sum = 2.f * (a0 + a1) + fpar * gsum;
+          const float4_t sum = P != 0 ? 2.f * (a0 + a1) + fpar * gsum : 2.f * (a0 + a1);
           if (before) {
             store_partial<NB>(head + w * dpad + NB * lane, sum);
           } else {
@@ -1382,7 +1383,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
           fma_n<NB>(a1, gj, v);
         else
           fma_n<NB>(a0, gj, v);
-        gsum += gj;
+        if constexpr (P != 0) gsum += gj;
       }
     }
     jA = jB;
@@ -1391,7 +1392,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
     gB = g[jB];
     jCn = ld_idx(eb + 192);
   }
-  const float4_t sum = 2.f * (a0 + a1) + fpar * gsum;
+  const float4_t sum = P != 0 ? 2.f * (a0 + a1) + fpar * gsum : 2.f * (a0 + a1);
   if (cur_end == nE) {
     if (before) {
       store_partial<NB>(head + w * dpad + NB * lane, sum);
@@ -2564,10 +2565,16 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   const size_t lds = (NX > 0 && NB * NBN > 4)
                          ? (size_t)((d + 63) >> 6) * NBN * 64 * sizeof(uint64_t) : 0;
   dim3 grid((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock));
-  hipLaunchKernelGGL((k_spmm_wave_q8<8, NX, NB, NBN>), grid, dim3(kBlock), lds, stream, n,
-                     nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16, ldc16,
-                     K & 1, d, alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,
-                     tail_row, head, tail, nx, fn.wbits, fn.ldw, fn.alpha_self);
+  if (K & 1)
+    hipLaunchKernelGGL((k_spmm_wave_q8<8, NX, NB, NBN, 1>), grid, dim3(kBlock), lds, stream,
+                       n, nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16,
+                       ldc16, 1, d, alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,
+                       tail_row, head, tail, nx, fn.wbits, fn.ldw, fn.alpha_self);
+  else
+    hipLaunchKernelGGL((k_spmm_wave_q8<8, NX, NB, NBN, 0>), grid, dim3(kBlock), lds, stream,
+                       n, nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16,
+                       ldc16, 0, d, alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,
+                       tail_row, head, tail, nx, fn.wbits, fn.ldw, fn.alpha_self);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t fix_waves = (p.workers + 3) / 4;
