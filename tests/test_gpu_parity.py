@@ -420,6 +420,54 @@ def test_captured_forward_replays_match_eager(dev):
         assert torch.equal(got, ref), "replay %d differs from eager" % it
 
 
+# --------------------------------------- forward across the storage paths --
+
+@pytest.mark.parametrize("dims,acts", [([2100, 300, 47], ["relu", "none"]),
+                                       ([130, 300, 260, 5], ["none", "relu", "none"])])
+def test_forward_exact_path_layers(dev, dims, acts):
+    """bigcn_forward with layers outside the 8-bit path (K > 2048: exact
+    16-bit products; more than 256 outputs: exact half products) next to
+    8-bit ones: equal to the chained entry points bit for bit, and to the
+    oracle's free-running forward (hidden sign flips only where the oracle's
+    value is within rounding of zero)."""
+    rng = np.random.default_rng(sum(dims))
+    g = _star_plus_random(700, rng)
+    L = len(dims) - 1
+    x = rng.standard_normal((g.n, dims[0])).astype(np.float32)
+    mu, rstd = workloads.bn_stats(x)
+    wts = [workloads.glorot_t(dims[i], dims[i + 1], rng) for i in range(L)]
+    bs = [rng.uniform(-0.1, 0.1, dims[i + 1]).astype(np.float32) for i in range(L)]
+    assert not bg.q8_supported(g.n, dims[1], dims[0])
+    rowptr_t, colidx_t = _t(g.rowptr, dev), _t(g.colidx, dev)
+    model = bg.BiGCN(rowptr_t, colidx_t, wts, bs, acts=acts, norm="sym", mu=mu, rstd=rstd,
+                     device=dev)
+    xt = _t(x, dev)
+    got = model.forward(xt).clone()
+    h = xt
+    outs = []
+    for l in range(L):
+        h, *_ = gpu_layer(dev, g, "sym", None, wts[l], bs[l], act=acts[l],
+                          mu=mu if l == 0 else None, rstd=rstd if l == 0 else None,
+                          rowptr_t=rowptr_t, colidx_t=colidx_t, ht=h)
+        outs.append(h.cpu().numpy())
+    torch.cuda.synchronize()
+    assert torch.equal(got, h), "forward differs from the chained entry points"
+    ref = oracle.forward(g.rowptr, g.colidx, "sym", x, wts, bs, acts=acts, mu=mu, rstd=rstd)
+    flipped = np.zeros(g.n, dtype=bool)
+    src = np.repeat(np.arange(g.n), np.diff(g.rowptr))
+    for l in range(L):
+        out = outs[l]
+        z, m, o = ref[l]
+        tainted = np.zeros(g.n, dtype=bool)
+        tainted[np.unique(src[flipped[g.colidx]])] = True
+        clean = ~tainted
+        assert mass_error(out[clean], z[clean], m[clean], relu=acts[l] == "relu") <= TOL
+        flips = (out >= 0) != (o >= 0)
+        fc = flips & clean[:, None]
+        assert np.all(np.abs(z[fc]) <= TOL * m[fc] + 1e-30), "sign flip away from zero"
+        flipped = flipped | flips.any(axis=1) | tainted
+
+
 # ------------------------------------------- two-weight GraphSAGE (8-bit path)
 
 def gpu_sage_layer(dev, g, h, wt_self, wt_neigh, bias, act="none", mu=None, rstd=None,
