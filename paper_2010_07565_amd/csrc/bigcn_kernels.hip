@@ -1484,10 +1484,12 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
 // edge in CSR order (row-parallel); a longer one by all slots together, slot
 // q taking edges q, q + S, ... (edge-parallel), followed by a butterfly over
 // the slots.  Complete rows are then finished by their slots in parallel.
-// A row cut by a share boundary leaves its pieces in LDS; after a block
-// barrier the wave where it starts adds them in share order and finishes
-// it.  No atomics and no second kernel: the sums, and hence the results, do
-// not depend on timing.
+// A row cut by a share boundary leaves its head pieces in LDS; after a
+// block barrier the wave where it starts adds them, in share order, to the
+// tail it holds in its slot.  A wave's last round of rows is finished after
+// that barrier, together with its cut row, so the epilogue runs once per
+// wave.  No atomics and no second kernel: the sums, and hence the results,
+// do not depend on timing.
 constexpr int kNarrowShort = 16;  // edges in a share up to which a row is row-parallel
 // rows landed per lane and batch (1 KB of LDS per wave and row for 16-byte
 // pieces, 256 B for 4-byte ones)
@@ -1749,7 +1751,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     const uint64_t* __restrict__ Bn, int64_t ldbn, const float* __restrict__ alpha_s) {
   constexpr int S = 64 / G;
   extern __shared__ uint64_t s_bn[];  // NX == 1: word 0 of each next weight column
-  __shared__ float s_part[2][kWavesPerBlock][64];  // [0] head pieces, [1] tail pieces
+  __shared__ float s_head[kWavesPerBlock][64];  // the piece of a row cut at a share's start
   __shared__ __attribute__((aligned(16))) float s_epi[3][64];  // alpha, bias, alpha_self
   // A chunk of CH edges lands in LDS through NLI instructions of EPI = 64 / G
   // edges each (lane l: edge EPI i + l / G, bytes CPL (l % G) ..); chunk edge
@@ -1951,6 +1953,15 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       __asm__ volatile("" ::: "memory");
     }
   };
+  // The last round's rows are finished after the block barrier, together
+  // with the row cut at this share's end (its pieces from the following
+  // waves added into its slot): one epilogue for them all.  Their sums wait
+  // in this wave's landing buffer (idle by then; CPL floats per lane fit).
+  static_assert(64 * CPL * 4 <= NLI * 64 * (int)sizeof(LandT), "sums fit the landing buffer");
+  float* keep_lds = reinterpret_cast<float*>(&s_land[wv][0]) + CPL * lane;
+  bool keep_fin = false, keep_tail = false;
+  int64_t keep_row = 0;
+  int keep_rs = 0, keep_re = 0;
   for (int base = h; base < o_e; base += S) {
     const int idx = base + q;
     const bool on = idx < o_e;
@@ -2068,39 +2079,45 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     for (int k = 0; k < CPL; ++k) sum[k] = 2.f * acc[k] + fpar * gs;
     const bool headp = on && rs < ws;
     const bool tailp = on && !headp && re > we;
-    if (headp || tailp) {
+    if (headp) {
 #pragma unroll
-      for (int k = 0; k < CPL; ++k) s_part[tailp ? 1 : 0][wv][CPL * c + k] = sum[k];
+      for (int k = 0; k < CPL; ++k) s_head[wv][CPL * c + k] = sum[k];
     }
-    if (on && !headp && !tailp)
-      finish_slot<G, CPL, NX>(r_lo + idx, re - rs, mean, sum, ep, c, out, ldo, nx, nbn, s_bn);
+    const bool fin = on && !headp && !tailp;
+    if (base + S < o_e) {
+      if (fin)
+        finish_slot<G, CPL, NX>(r_lo + idx, re - rs, mean, sum, ep, c, out, ldo, nx, nbn,
+                                s_bn);
+    } else {
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) keep_lds[k] = sum[k];
+      keep_fin = fin || tailp;
+      keep_tail = tailp;
+      keep_row = r_lo + idx;
+      keep_rs = rs;
+      keep_re = re;
+    }
   }
   lds_barrier();
-  // The row this wave started that runs past its share: its pieces, in share
-  // order, from this wave (tail) and the waves that follow (heads).
-  if (!last && o_e > o_b && total > 0) {
-    const int it = o_e - 1;
-    const int rs = __builtin_amdgcn_readlane(rs_l, it);
-    const int re = __builtin_amdgcn_readlane(re_l, it);
-    if (re > we) {
-      // the last wave whose share starts inside the row
-      int kend = wv;
+  float keep[CPL];
 #pragma unroll
-      for (int m = 1; m < kWavesPerBlock; ++m)
-        if (m > wv && bnd[m] < re) kend = m;
-      if (lane < G) {
-        float sum[CPL];
+  for (int k = 0; k < CPL; ++k) keep[k] = keep_lds[k];
+  // The row this wave started that runs past its share (the tail slot of
+  // the last round): the heads of the waves whose shares start inside it,
+  // added in share order.
+  if (keep_tail) {
+    int kend = wv;
 #pragma unroll
-        for (int k = 0; k < CPL; ++k) sum[k] = s_part[1][wv][CPL * c + k];
-        for (int m = wv + 1; m <= kend; ++m) {
+    for (int m = 1; m < kWavesPerBlock; ++m)
+      if (m > wv && bnd[m] < keep_re) kend = m;
+    for (int m = wv + 1; m <= kend; ++m) {
 #pragma unroll
-          for (int k = 0; k < CPL; ++k) sum[k] += s_part[0][m][CPL * c + k];
-        }
-        finish_slot<G, CPL, NX>(r_lo + it, re - rs, mean, sum, ep, c, out, ldo, nx, nbn,
-                                s_bn);
-      }
+      for (int k = 0; k < CPL; ++k) keep[k] += s_head[m][CPL * c + k];
     }
   }
+  if (__builtin_amdgcn_ballot_w64(keep_fin) != 0 && keep_fin)
+    finish_slot<G, CPL, NX>(keep_row, keep_re - keep_rs, mean, keep, ep, c, out, ldo, nx, nbn,
+                            s_bn);
 }
 
 // Rows cut by chunk boundaries: tail of the owning worker, then the heads of
