@@ -420,6 +420,59 @@ def test_captured_forward_replays_match_eager(dev):
         assert torch.equal(got, ref), "replay %d differs from eager" % it
 
 
+# ------------------------------------------------------- degenerate graphs --
+
+def test_zero_nodes(dev):
+    """A graph with no nodes: every entry point accepts it, launches nothing
+    and leaves its outputs alone; the weight gradient of the backward is 0."""
+    K, d = 130, 7
+    rowptr = torch.zeros(1, dtype=torch.int64, device=dev)
+    colidx = torch.zeros(0, dtype=torch.int32, device=dev)
+    wt = _t(workloads.glorot_t(K, d, np.random.default_rng(0)), dev)
+    wbits, alpha = bg.pack_weights(wt)
+    x = torch.empty((0, K), device=dev)
+    F = torch.empty((0, 4), dtype=torch.int64, device=dev)
+    gs = torch.empty(0, device=dev)
+    bg.bigcn_binarize_pack(x, F[:, :3], gs, None, None, rowptr, "sym")
+    C = torch.empty((0, 8), dtype=torch.float16, device=dev)
+    bg.bigcn_bgemm(F[:, :3], wbits, K, C[:, :d])
+    W = bg.q8_row(d)
+    C8 = torch.empty((0, W), dtype=torch.int8, device=dev)
+    C16 = torch.empty((0, W), dtype=torch.float16, device=dev)
+    bg.bigcn_bgemm_q8(F[:, :3], wbits, K, C8, C16, gs)
+    out = torch.empty((0, d), device=dev)
+    ws = torch.empty(max(1, bg.spmm_workspace_bytes(0, 0, d)), dtype=torch.uint8, device=dev)
+    bg.bigcn_spmm_csr(rowptr, colidx, gs, C, alpha, out, ws, d=d)
+    bg.bigcn_spmm_csr_q8(rowptr, colidx, gs, C8, C16, K, alpha, out, ws, d=d)
+    model = bg.BiGCN(rowptr, colidx, [workloads.glorot_t(K, d, np.random.default_rng(1))],
+                     norm="sym", device=dev)
+    assert model.forward(x).shape == (0, d)
+    dwt = torch.full((d, K), np.nan, device=dev)
+    bws = torch.empty(max(1, bg.layer_backward_workspace_bytes(0, 0, K, d)),
+                      dtype=torch.uint8, device=dev)
+    bg.bigcn_layer_backward(rowptr, colidx, x, wt, wbits, alpha, torch.empty((0, d), device=dev),
+                            dwt, bws, "sym", nnz=0)
+    torch.cuda.synchronize()
+    assert bool((dwt == 0).all())
+
+
+@pytest.mark.parametrize("dims", [[70, 5, 3], [1, 1]])
+def test_single_node(dev, dims):
+    """One node whose only entry is its self-loop (D̂ = 1, so Ã = 1): the
+    forward pass against the oracle, down to layers of one input and one
+    output."""
+    rng = np.random.default_rng(len(dims))
+    g = workloads.Graph(1, np.array([0, 1], dtype=np.int64), np.array([0], dtype=np.int32))
+    L = len(dims) - 1
+    x = rng.standard_normal((1, dims[0])).astype(np.float32)
+    wts = [workloads.glorot_t(dims[i], dims[i + 1], rng) for i in range(L)]
+    bs = [rng.uniform(-0.1, 0.1, dims[i + 1]).astype(np.float32) for i in range(L)]
+    model = bg.BiGCN(g.rowptr, g.colidx, wts, bs, norm="sym", device=dev)
+    got = model.forward(_t(x, dev)).cpu().numpy()
+    z, m, _ = oracle.forward(g.rowptr, g.colidx, "sym", x, wts, bs)[-1]
+    assert mass_error(got, z, m) <= TOL
+
+
 # --------------------------------------- forward across the storage paths --
 
 @pytest.mark.parametrize("dims,acts", [([2100, 300, 47], ["relu", "none"]),
