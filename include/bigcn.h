@@ -331,6 +331,28 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
                            void* workspace, size_t ws_bytes, void* stream);
 
 /* Human-readable text of a status code (static storage). */
+/* ---------------------------------------------------------------------------
+ * bigcn_check_csr -- validates the contents of a CSR graph on the device
+ * (the entry points above take them on trust: a bad row pointer or column
+ * index there is an out-of-range access).  The graph is the input every
+ * aggregation reads (Sec. 3.1: the rows of Â, or of A for the GraphSAGE
+ * layer); a caller checks it once, before its first use.
+ *
+ *   n, nnz   rows and entries (host values).
+ *   rowptr   int64[n + 1] (device), colidx int32[nnz] (device); only read,
+ *            each element once, at positions < n + 1 and < nnz.
+ *   flags    int32[1] (device, caller-owned): set to the OR of
+ *              1  rowptr[0] != 0
+ *              2  rowptr[n] != nnz
+ *              4  rowptr decreases somewhere
+ *              8  a column index outside [0, n)
+ *            and 0 for a valid graph.  Ready when `stream` is synchronised.
+ * Errors: EINVAL (n < 0, nnz < 0, n > INT32_MAX, NULL flags, NULL rowptr,
+ *         or NULL colidx with nnz > 0), EALIGN, EHIP.
+ * ------------------------------------------------------------------------- */
+bigcn_status bigcn_check_csr(int64_t n, int64_t nnz, const int64_t* rowptr,
+                             const int32_t* colidx, int32_t* flags, void* stream);
+
 const char* bigcn_status_string(bigcn_status s);
 
 #ifdef __cplusplus

@@ -30,7 +30,8 @@ EXPORTS = ("bigcn_binarize_pack", "bigcn_bgemm", "bigcn_spmm_workspace_bytes",
            "bigcn_spmm_csr", "bigcn_bgemm_q8", "bigcn_spmm_csr_q8",
            "bigcn_spmm_csr_sage_q8", "bigcn_layer_backward_workspace_bytes",
            "bigcn_layer_backward",
-           "bigcn_forward_workspace_bytes", "bigcn_forward", "bigcn_status_string")
+           "bigcn_forward_workspace_bytes", "bigcn_forward", "bigcn_check_csr",
+           "bigcn_status_string")
 
 
 class BigcnError(RuntimeError):
@@ -93,6 +94,8 @@ def load() -> ctypes.CDLL:
     lib.bigcn_forward_workspace_bytes.restype = _sz
     lib.bigcn_forward_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(_Layer),
                                                   _i32]
+    lib.bigcn_check_csr.restype = _int
+    lib.bigcn_check_csr.argtypes = [_i64, _i64, _p, _p, _p, _p]
     lib.bigcn_forward.restype = _int
     lib.bigcn_forward.argtypes = [_i64, _i64, _p, _p, _int, _p, _i64, _p, _p,
                                   ctypes.POINTER(_Layer), _i32, _p, _i64, _p, _sz, _p]
@@ -354,6 +357,28 @@ def bigcn_forward(rowptr: torch.Tensor, colidx: torch.Tensor, x: torch.Tensor,
     _check("bigcn_forward", st)
 
 
+CSR_FLAGS = {1: "rowptr[0] != 0", 2: "rowptr[n] != nnz", 4: "rowptr decreases",
+             8: "column index outside [0, n)"}
+
+
+def bigcn_check_csr(rowptr: torch.Tensor, colidx: torch.Tensor, nnz: Optional[int] = None,
+                    stream=None) -> int:
+    """Validates a CSR graph on the device; returns the flags of
+    include/bigcn.h (0 = valid).  Synchronises the stream to read them."""
+    n = rowptr.shape[0] - 1
+    nnz = colidx.shape[0] if nnz is None else nnz
+    flags = torch.empty(1, dtype=torch.int32, device=rowptr.device)
+    st = load().bigcn_check_csr(n, nnz, _dev(rowptr, torch.int64, "rowptr"),
+                                _dev(colidx, torch.int32, "colidx"),
+                                _dev(flags, torch.int32, "flags"), _stream(stream))
+    _check("bigcn_check_csr", st)
+    if stream is not None and hasattr(stream, "synchronize"):
+        stream.synchronize()
+    else:
+        torch.cuda.synchronize(rowptr.device)
+    return int(flags.item())
+
+
 # ----------------------------------------------------------------- helpers --
 
 def pack_weights(wt: torch.Tensor, ldw: Optional[int] = None, stream=None):
@@ -383,6 +408,10 @@ class BiGCN:
         self.colidx = torch.as_tensor(colidx, dtype=torch.int32, device=self.device)
         self.n = self.rowptr.shape[0] - 1
         self.nnz = self.colidx.shape[0]
+        bad = bigcn_check_csr(self.rowptr, self.colidx, self.nnz)
+        if bad:
+            raise ValueError("invalid CSR graph: " +
+                             ", ".join(t for f, t in CSR_FLAGS.items() if bad & f))
         self.norm = norm
         self.mu = None if mu is None else torch.as_tensor(mu, dtype=torch.float32,
                                                           device=self.device)

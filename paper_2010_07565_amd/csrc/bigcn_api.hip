@@ -165,7 +165,51 @@ bool forward_layout(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t n
 
 }  // namespace
 
+namespace {
+
+// Contents of a CSR graph, flags as bigcn_check_csr documents: one kernel
+// clears the flags word, the next (stream-ordered after it) ORs in what
+// each thread finds; every element is read once, in range.
+__global__ void k_csr_clear(int32_t* flags) { *flags = 0; }
+
+__global__ void k_csr_check(int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
+                            const int32_t* __restrict__ colidx, int32_t* flags) {
+  int32_t f = 0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i <= n || i < nnz;
+       i += stride) {
+    if (i <= n) {
+      const int64_t r = rowptr[i];
+      if (i == 0 && r != 0) f |= 1;
+      if (i == n && r != nnz) f |= 2;
+      if (i < n && rowptr[i + 1] < r) f |= 4;
+    }
+    if (i < nnz) {
+      const int32_t c = colidx[i];
+      if (c < 0 || (int64_t)c >= n) f |= 8;
+    }
+  }
+  if (f != 0) atomicOr(flags, f);
+}
+
+}  // namespace
+
 extern "C" {
+
+bigcn_status bigcn_check_csr(int64_t n, int64_t nnz, const int64_t* rowptr,
+                             const int32_t* colidx, int32_t* flags, void* stream) {
+  if (n < 0 || nnz < 0 || n > INT32_MAX || flags == nullptr || rowptr == nullptr ||
+      (nnz > 0 && colidx == nullptr))
+    return BIGCN_EINVAL;
+  if (!aligned(rowptr, 8) || !aligned(colidx, 4) || !aligned(flags, 4)) return BIGCN_EALIGN;
+  hipStream_t s = (hipStream_t)stream;
+  hipLaunchKernelGGL(k_csr_clear, dim3(1), dim3(1), 0, s, flags);
+  const int64_t items = std::max<int64_t>(n + 1, nnz);
+  const int64_t blocks = std::min<int64_t>((items + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_csr_check, dim3((unsigned)blocks), dim3(256), 0, s, n, nnz, rowptr,
+                     colidx, flags);
+  return hipGetLastError() == hipSuccess ? BIGCN_OK : BIGCN_EHIP;
+}
 
 const char* bigcn_status_string(bigcn_status s) {
   switch (s) {

@@ -91,6 +91,18 @@ def test_spmm_validation():
         assert f(*args) == want, (pos, val)
 
 
+def test_check_csr_validation():
+    f = bg.load().bigcn_check_csr
+    base = [10, 40, FAKE, FAKE, FAKE, None]
+    for pos, val, want in [(0, -1, EINVAL), (0, 1 << 31, EINVAL), (1, -1, EINVAL),
+                           (2, None, EINVAL), (3, None, EINVAL), (4, None, EINVAL),
+                           (2, FAKE + 4, EALIGN), (3, FAKE + 2, EALIGN),
+                           (4, FAKE + 2, EALIGN)]:
+        args = list(base)
+        args[pos] = val
+        assert f(*args) == want, (pos, val)
+
+
 def test_forward_validation():
     lib = bg.load()
     L = _lib._Layer

@@ -420,6 +420,34 @@ def test_captured_forward_replays_match_eager(dev):
         assert torch.equal(got, ref), "replay %d differs from eager" % it
 
 
+# ------------------------------------------------------------ graph checks --
+
+def _flags(dev, rowptr, colidx, nnz=None):
+    return bg.bigcn_check_csr(torch.tensor(rowptr, dtype=torch.int64, device=dev),
+                              torch.tensor(colidx, dtype=torch.int32, device=dev), nnz=nnz)
+
+
+def test_check_csr_accepts_valid_graphs(dev):
+    rng = np.random.default_rng(4)
+    for g in (_star_plus_random(600, rng), _with_empty_rows(rng), workloads.make_workload(2).graph):
+        assert _flags(dev, g.rowptr, g.colidx) == 0
+    assert _flags(dev, [0], []) == 0
+    assert _flags(dev, [0, 0, 0], []) == 0
+
+
+def test_check_csr_flags_each_defect(dev):
+    # each malformed graph is only read by the checker itself
+    assert _flags(dev, [1, 2, 3], [0, 1]) == 1 | 2      # starts at 1; rowptr[n] = 3 != 2
+    assert _flags(dev, [0, 1, 2], [0, 1, 1]) == 2       # rowptr[n] = 2, nnz = 3
+    assert _flags(dev, [0, 2, 1, 3], [0, 1, 2]) == 4    # decreases
+    assert _flags(dev, [0, 1, 2], [0, 2]) == 8          # column 2 of a 2-node graph
+    assert _flags(dev, [0, 1, 2], [-1, 0]) == 8
+    assert _flags(dev, [0, 3, 1], [5, 0, 0]) == 2 | 4 | 8
+    with pytest.raises(ValueError, match="column index outside"):
+        bg.BiGCN(np.array([0, 1, 2]), np.array([0, 7], dtype=np.int32),
+                 [workloads.glorot_t(8, 3, np.random.default_rng(0))], device=dev)
+
+
 # ------------------------------------------------------- degenerate graphs --
 
 def test_zero_nodes(dev):
