@@ -242,13 +242,14 @@ __global__ __launch_bounds__(kB) void k_bwd_weights(
 }
 
 // dH~[i][k] = sum_j α_j dζ_ij s(B_j, k) and Eq. (14), on the matrix cores.
-// One wave per (16 rows, 16*NT columns k): fp32 MFMA 16x16x4 with
-// A[i][q] = α_j dζ_ij and B[q][k] = s(B_j, k) (exact products).  Step s of a
-// 32-wide chunk of j gives lane group q the index j = j0 + 8q + s, so a
-// lane's eight A values are two 16-byte loads of its row.  The packed weight
-// words and α sit in LDS (rows padded to a multiple of 32 with zeros).  The
-// sum over j runs in fp32, as a sequential sum would.
-template <int NT>
+// One wave per (16*RT rows, 16*NT columns k): fp32 MFMA 16x16x4 with
+// A[i][q] = α_j dζ_ij and B[q][k] = s(B_j, k) (exact products); each ±1
+// operand is built once and used by the RT row tiles.  Step s of a 32-wide
+// chunk of j gives lane group q the index j = j0 + 8q + s, so a lane's eight
+// A values of a row tile are two 16-byte loads of its row.  The packed
+// weight words and α sit in LDS (rows padded to a multiple of 32 with
+// zeros).  The sum over j runs in fp32, as a sequential sum would.
+template <int NT, int RT>
 __global__ __launch_bounds__(kB) void k_bwd_htilde_mfma(
     int64_t n, int32_t d_in, int32_t d_out, const float* __restrict__ dz, int64_t lddz,
     const uint64_t* __restrict__ B, int64_t ldb, const float* __restrict__ alpha,
@@ -267,44 +268,60 @@ __global__ __launch_bounds__(kB) void k_bwd_htilde_mfma(
   __syncthreads();
   const int lane = threadIdx.x & 63;
   const int m = lane & 15, q = lane >> 4;
-  const int64_t tasks = (n + 15) / 16 * kgroups;
+  const int64_t tasks = (n + 16 * RT - 1) / (16 * RT) * kgroups;
   const int64_t nwaves = (int64_t)gridDim.x * (kB / 64);
   for (int64_t t = (int64_t)blockIdx.x * (kB / 64) +
                    __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
        t < tasks; t += nwaves) {
     const int kg = (int)(t % kgroups);
-    const int64_t i0 = (t / kgroups) * 16;
-    const int64_t row = i0 + m;  // this lane's A row
+    const int64_t i0 = (t / kgroups) * 16 * RT;
     const int k0 = kg * 16 * NT;
     const int w0 = k0 >> 6;
-    f32x4_t acc[NT];
+    f32x4_t acc[RT][NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    // The next chunk's two 16-byte loads (clamped to valid addresses: a row
-    // past n repeats row n-1, whose outputs are never stored; columns past
-    // d_out are zeroed below) are issued before this chunk's MFMAs.
-    const float* zr = dz + (row < n ? row : n - 1) * lddz;
-    auto load_chunk = [&](int jn, float4_t& u0, float4_t& u1) {
+    for (int r = 0; r < RT; ++r)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[r][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // The next chunk's 16-byte loads (clamped to valid addresses: a row past
+    // n repeats row n-1, whose outputs are never stored; columns past d_out
+    // are zeroed below) are issued before this chunk's MFMAs.
+    const float* zr[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      const int64_t row = i0 + 16 * r + m;  // this lane's A row in tile r
+      zr[r] = dz + (row < n ? row : n - 1) * lddz;
+    }
+    auto load_chunk = [&](int jn, float4_t (&u0)[RT], float4_t (&u1)[RT]) {
       const int c = jn + 8 * q;
-      u0 = *reinterpret_cast<const float4_t*>(zr + (c < d_out ? c : 0));
-      u1 = *reinterpret_cast<const float4_t*>(zr + (c + 4 < d_out ? c + 4 : 0));
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        u0[r] = *reinterpret_cast<const float4_t*>(zr[r] + (c < d_out ? c : 0));
+        u1[r] = *reinterpret_cast<const float4_t*>(zr[r] + (c + 4 < d_out ? c + 4 : 0));
+      }
     };
-    float4_t n0, n1;
+    float4_t n0[RT], n1[RT];
     load_chunk(0, n0, n1);
     for (int j0 = 0; j0 < d_out; j0 += 32) {
       const int jb = j0 + 8 * q;
-      const float4_t v0 = n0, v1 = n1;
+      float4_t v0[RT], v1[RT];
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        v0[r] = n0[r];
+        v1[r] = n1[r];
+      }
       if (j0 + 32 < d_out) load_chunk(j0 + 32, n0, n1);
       __builtin_amdgcn_sched_barrier(0);
       const float4_t al0 = *reinterpret_cast<const float4_t*>(sA + jb);
       const float4_t al1 = *reinterpret_cast<const float4_t*>(sA + jb + 4);
-      float a[8];
+      float a[RT][8];
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const float v = s < 4 ? v0[s] : v1[s - 4];
-        const float al = s < 4 ? al0[s] : al1[s - 4];
-        a[s] = jb + s < d_out ? al * v : 0.f;
-      }
+      for (int r = 0; r < RT; ++r)
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const float v = s < 4 ? v0[r][s] : v1[r][s - 4];
+          const float al = s < 4 ? al0[s] : al1[s - 4];
+          a[r][s] = jb + s < d_out ? al * v : 0.f;
+        }
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
         uint64_t wd[NW];
@@ -314,23 +331,27 @@ __global__ __launch_bounds__(kB) void k_bwd_htilde_mfma(
         for (int nt = 0; nt < NT; ++nt) {
           const int sh = (k0 & 63) + 16 * (nt & 3) + m;
           const float b = pm1_word(wd[nt >> 2], sh);
-          acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b, acc[nt], 0, 0, 0);
+#pragma unroll
+          for (int r = 0; r < RT; ++r)
+            acc[r][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[r][s], b, acc[r][nt], 0, 0, 0);
         }
       }
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int64_t ro = i0 + 4 * q + r;
-      if (ro >= n) break;
+    for (int r = 0; r < RT; ++r)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int k = k0 + 16 * nt + m;
-        if (k >= d_in) continue;
-        const float v = acc[nt][r];
-        if (dht != nullptr) dht[ro * lddht + k] = v;
-        if (dh != nullptr) dh[ro * lddh + k] = fabsf(v) < 1.f ? v : 0.f;
+      for (int rr = 0; rr < 4; ++rr) {
+        const int64_t ro = i0 + 16 * r + 4 * q + rr;
+        if (ro >= n) break;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int k = k0 + 16 * nt + m;
+          if (k >= d_in) continue;
+          const float v = acc[r][nt][rr];
+          if (dht != nullptr) dht[ro * lddht + k] = v;
+          if (dh != nullptr) dh[ro * lddh + k] = fabsf(v) < 1.f ? v : 0.f;
+        }
       }
-    }
   }
 }
 
@@ -347,7 +368,8 @@ inline int pow2_at_least(int v, int cap) {
 
 // Workspace layout of bigcn_layer_backward, and the tiling of the two
 // matrix-core products: dW~ takes 16 x 16*ntw tiles (ntw <= 8), dH~
-// 16 x 16*nth tiles (nth <= 16), each with kgroups tiles across d_in.
+// 32 x 16*nth tiles (nth <= 8: two row tiles share each ±1 operand), each
+// with kgroups tiles across d_in.
 struct BwdLayout {
   int64_t kw, ldm, R, chunks, Rdb, chunks_db;
   int ntw, kgw, jtw, nth, kgh;
@@ -363,7 +385,7 @@ BwdLayout bwd_layout(int64_t n, int64_t nnz, int32_t d_in, int32_t d_out) {
   L.ntw = pow2_at_least(ktiles, 8);
   L.kgw = (ktiles + L.ntw - 1) / L.ntw;
   L.jtw = (d_out + 15) / 16;
-  L.nth = pow2_at_least(ktiles, 16);
+  L.nth = pow2_at_least(ktiles, 8);
   L.kgh = (ktiles + L.nth - 1) / L.nth;
   // Row chunks of the dW~ partial sums: about 4096 waves of (chunk, 16
   // columns, 16*ntw bits), chunks of at least 256 rows, partial sums within
@@ -403,15 +425,18 @@ BwdLayout bwd_layout(int64_t n, int64_t nnz, int32_t d_in, int32_t d_out) {
 
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
+constexpr int kHtildeRowTiles = 2;  // 16-row tiles per wave sharing each ±1 operand
+
 template <int NT>
 void launch_htilde(int64_t n, int32_t d_in, int32_t d_out, int32_t kgroups, const float* dz,
                    int64_t lddz, const uint64_t* B, int64_t ldb, const float* alpha,
                    float* dht, int64_t lddht, float* dh, int64_t lddh, hipStream_t s) {
   const int jpad = (d_out + 31) & ~31;
   const size_t lds = (size_t)jpad * words(d_in) * 8 + (size_t)jpad * 4;
-  const int64_t tasks = (n + 15) / 16 * kgroups;
+  constexpr int RT = kHtildeRowTiles;
+  const int64_t tasks = (n + 16 * RT - 1) / (16 * RT) * kgroups;
   const int64_t blocks = std::min<int64_t>((tasks + 3) / 4, 2048);
-  hipLaunchKernelGGL((k_bwd_htilde_mfma<NT>), dim3((unsigned)std::max<int64_t>(1, blocks)),
+  hipLaunchKernelGGL((k_bwd_htilde_mfma<NT, RT>), dim3((unsigned)std::max<int64_t>(1, blocks)),
                      dim3(kB), lds, s, n, d_in, d_out, dz, lddz, B, ldb, alpha, kgroups, dht,
                      lddht, dh, lddh);
 }
@@ -547,8 +572,7 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
       case 1: BIGCN_HT(1); break;
       case 2: BIGCN_HT(2); break;
       case 4: BIGCN_HT(4); break;
-      case 8: BIGCN_HT(8); break;
-      default: BIGCN_HT(16); break;
+      default: BIGCN_HT(8); break;
     }
 #undef BIGCN_HT
     BIGCN_CHECK(hipGetLastError());
