@@ -396,7 +396,7 @@ BwdLayout bwd_layout(int64_t n, int64_t nnz, int32_t d_in, int32_t d_out) {
   chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, (512ll << 20) / ((int64_t)d_out * d_in * 8)));
   L.R = std::max<int64_t>(1, (n + chunks - 1) / chunks);
   L.chunks = std::max<int64_t>(1, (n + L.R - 1) / L.R);
-  L.Rdb = std::max<int64_t>(64, (n + 4095) / 4096);  // at most 4096 row chunks
+  L.Rdb = std::max<int64_t>(64, (n + 1023) / 1024);  // at most 1024 row chunks
   L.chunks_db = std::max<int64_t>(1, (n + L.Rdb - 1) / L.Rdb);
   size_t off = 0;
   L.off_F = off;
