@@ -119,6 +119,8 @@ __device__ inline float pm1_word(uint64_t w, int sh) {
 // Each run of 64 rows is summed in fp32 (64 terms per output) and added to
 // fp64 accumulators, runs in row order.  Lane (n, q) ends holding outputs
 // (4q + r, n) of each 16x16 tile.
+constexpr int kWtBatch = 16;  // row steps (4 rows each) whose loads are issued together
+
 template <int NT>
 __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
     int64_t n, int32_t d_in, int32_t d_out, const uint64_t* __restrict__ F, int64_t ldf,
@@ -148,15 +150,15 @@ __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
   for (int64_t r0 = i0; r0 < i1; r0 += 64) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < 16; s0 += 8) {  // eight steps (32 rows) of loads in flight
+    for (int s0 = 0; s0 < 16; s0 += kWtBatch) {  // kWtBatch steps of loads in flight
       // Loads at clamped (in-range) addresses with no branch, so all of the
       // batch's loads are in flight together; rows past the chunk and
       // columns past d_out are then zeroed by a 0/1 factor (a select would
       // let the compiler move the loads into a branch and wait on each).
-      float a[8];
-      uint64_t wd[8][NW];
+      float a[kWtBatch];
+      uint64_t wd[kWtBatch][NW];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < kWtBatch; ++u) {
         const int64_t row = r0 + 4 * (s0 + u) + q;
         const int64_t rc = row < i1 ? row : i1 - 1;
         a[u] = beta[rc] * dz[rc * lddz + jc] * (row < i1 && j < d_out ? 1.f : 0.f);
@@ -165,7 +167,7 @@ __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
       }
       __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any MFMA
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
+      for (int u = 0; u < kWtBatch; ++u)
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
           const int sh = (k0 & 63) + 16 * (nt & 3) + m;
