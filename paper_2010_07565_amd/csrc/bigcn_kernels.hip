@@ -1256,7 +1256,7 @@ __device__ inline int64_t readlane64(int64_t v, int l) {
 // finish_row<NX, NB, NBN>.  P = K mod 2 (the parity p): for even K the
 // p * sum g term is zero and its running sum is not kept.
 template <int U, int NX, int NB, int NBN, int P>
-__global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) void k_spmm_wave_q8(
     int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, int mean, const float* __restrict__ g,
     const int8_t* __restrict__ C8, int64_t ldc8, const _Float16* __restrict__ C16,
@@ -1268,6 +1268,8 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
     int64_t ldbn, const float* __restrict__ alpha_s) {
   static_assert(64 % U == 0, "group size");
   extern __shared__ uint64_t sBn[];
+  // the scales of the window's 64 edges, read back as 16-byte broadcasts
+  __shared__ __attribute__((aligned(16))) float s_gw[kWavesPerBlock][64];
   const int lane = threadIdx.x & 63;
   const int64_t wv = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
   const bool live = wv < workers;
@@ -1315,22 +1317,30 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
   float gsum = 0.f;  // sum of g_j over the current row (for the parity term)
   float gB = g[jB];
   int32_t jCn = ld_idx(128);
+  float* gw = &s_gw[wave_index_in_block()][0];
   for (int eb = 0; eb < nE; eb += 64) {
     const uint64_t flagged = __builtin_amdgcn_ballot_w64(__builtin_bit_cast(int, gA) < 0);
+    gw[lane] = gA;
     for (int m = 0; m < 64; m += U) {
       const int e0 = eb + m;
       if (e0 >= nE) break;
       uint32_t vv[U];
-      float gg[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int j = __builtin_amdgcn_readlane(jA, m + u);
-        gg[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                              __builtin_bit_cast(int, gA), m + u));
         vv[u] = gather_codes<NB>(rs8, voff8, (int)((uint32_t)j * (uint32_t)rb8));
       }
       const bool any_flag = ((flagged >> m) & ((1ull << U) - 1)) != 0;
       if (e0 + U <= nE && cur_end >= e0 + U && !any_flag) {
+        // a group inside one row: its scales (the same in every lane) as
+        // LDS broadcasts, whose latency hides behind the gathers
+        float gg[U];
+#pragma unroll
+        for (int u = 0; u < U; u += 4) {
+          const float4_t g4 = *reinterpret_cast<const float4_t*>(gw + m + u);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) gg[u + v] = g4[v];
+        }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           if (u & 1)
@@ -1369,7 +1379,8 @@ __global__ __launch_bounds__(kBlock) void k_spmm_wave_q8(
               finish_row<NX, NB, NBN>(r, 0, mean, zero4, ep, out, ldo, nx, lane);
           } while (cur_end == eu);
         }
-        float gj = gg[u];
+        float gj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                 __builtin_bit_cast(int, gA), m + u));
         float4_t v;
         if (__builtin_bit_cast(int, gj) < 0) {
           // Flagged source row: its exact products, as (dot - p) / 2.
