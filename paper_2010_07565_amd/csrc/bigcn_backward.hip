@@ -96,7 +96,6 @@ __global__ __launch_bounds__(kB) void k_bwd_colsum_final(
   db[k] = (float)acc;
 }
 
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
 // ±1 in fp32 from bit sh of dw: a set bit (sign +1) gives +1.0f, a clear bit
@@ -141,7 +140,7 @@ __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
   const int w0 = k0 >> 6;
   const int kw = (d_in + 63) >> 6;
   const int64_t i0 = c * R, i1 = std::min<int64_t>(n, i0 + R);
-  f32x4_t acc[NT];
+  float4_t acc[NT];
   double acc64[NT][4];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
@@ -149,7 +148,7 @@ __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
     for (int r = 0; r < 4; ++r) acc64[nt][r] = 0.0;
   for (int64_t r0 = i0; r0 < i1; r0 += 64) {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = float4_t{0.f, 0.f, 0.f, 0.f};
     for (int s0 = 0; s0 < 16; s0 += kWtBatch) {  // kWtBatch steps of loads in flight
       // Loads at clamped (in-range) addresses with no branch, so all of the
       // batch's loads are in flight together; rows past the chunk and
@@ -279,11 +278,11 @@ __global__ __launch_bounds__(kB) void k_bwd_htilde_mfma(
     const int64_t i0 = (t / kgroups) * 16 * RT;
     const int k0 = kg * 16 * NT;
     const int w0 = k0 >> 6;
-    f32x4_t acc[RT][NT];
+    float4_t acc[RT][NT];
 #pragma unroll
     for (int r = 0; r < RT; ++r)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[r][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int nt = 0; nt < NT; ++nt) acc[r][nt] = float4_t{0.f, 0.f, 0.f, 0.f};
     // The next chunk's 16-byte loads (clamped to valid addresses: a row past
     // n repeats row n-1, whose outputs are never stored; columns past d_out
     // are zeroed below) are issued before this chunk's MFMAs.
