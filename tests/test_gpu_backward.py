@@ -128,6 +128,22 @@ def test_pubmed_like_layer_backward(dev, layer):
     check_backward(got, ref, G, wt, d_in)
 
 
+@pytest.mark.timeout(600)
+def test_arxiv_like_layer_backward(dev):
+    """Full-size arxiv-like 256 -> 256 layer (169,343 nodes, 2.47 M entries),
+    every entry: the matrix-core products at the tiling large layers use."""
+    w = workloads.make_workload(3)
+    g = w.graph
+    wt = w.weights_t[1]
+    d_out, d_in = wt.shape
+    h = workloads.layer_input(g.n, d_in, seed=2001)
+    rng = np.random.default_rng(41)
+    G = (rng.standard_normal((g.n, d_out)) * 0.05).astype(np.float32)
+    ref = oracle.layer_backward(g.rowptr, g.colidx, w.norm, h, wt, G)
+    got = gpu_backward(dev, g, w.norm, h, wt, G)
+    check_backward(got, ref, G, wt, d_in)
+
+
 def test_backward_reproducible(dev):
     rng = np.random.default_rng(21)
     g = _star(900, rng)
