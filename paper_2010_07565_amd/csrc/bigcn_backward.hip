@@ -426,6 +426,19 @@ BwdLayout bwd_layout(int64_t n, int64_t nnz, int32_t d_in, int32_t d_out) {
 
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
+// The bytes of a row-major fp32 matrix argument ([rows][ld], cols used; a
+// null pointer or no rows is empty), for overlap tests between arguments.
+struct Span {
+  const void* p;
+  int64_t rows, cols, ld;
+  uintptr_t lo() const { return (uintptr_t)p; }
+  uintptr_t hi() const { return lo() + (uintptr_t)(((rows - 1) * ld + cols) * 4); }
+  bool empty() const { return p == nullptr || rows <= 0 || cols <= 0; }
+  bool overlaps(const Span& o) const {
+    return !empty() && !o.empty() && lo() < o.hi() && o.lo() < hi();
+  }
+};
+
 constexpr int kHtildeRowTiles = 2;  // 16-row tiles per wave sharing each ±1 operand
 
 template <int NT>
@@ -502,11 +515,23 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
   float* beta = (float*)(ws + L.off_beta);
   float* sc = (float*)(ws + L.off_s);
   float* ones = (float*)(ws + L.off_ones);
-  // G is aggregated in place when no ReLU mask applies and its rows suit the
-  // aggregation's 16-byte loads; dζ is written straight to the caller's
-  // buffer under the same condition (else to the workspace, then copied).
-  const bool g_direct = act != BIGCN_ACT_RELU && ldg % 4 == 0 && aligned(gout, 16);
-  const bool z_direct = dzeta != nullptr && lddz % 4 == 0 && aligned(dzeta, 16);
+  // G is aggregated in place when no ReLU mask applies, its rows suit the
+  // aggregation's 16-byte loads and db (written before) does not overlap it;
+  // dζ is written straight to the caller's buffer when its rows suit those
+  // loads and it overlaps no other argument (else to the workspace, then
+  // copied): the earlier path's results for any arguments.
+  const Span sg{gout, n, d_out, ldg}, sz{dzeta, n, d_out, lddz};
+  const Span others[] = {{h, n, d_in, ldh},          {gout, n, d_out, ldg},
+                         {out, n, d_out, ldo},       {dh, n, d_in, lddh},
+                         {dh_tilde, n, d_in, lddht}, {dwt, d_out, d_in, lddw},
+                         {dwt_tilde, d_out, d_in, lddwt}, {db, 1, d_out, d_out},
+                         {wt, d_out, d_in, ldwt}};
+  bool z_alone = true;
+  for (const Span& o : others) z_alone = z_alone && !sz.overlaps(o);
+  const bool g_direct = act != BIGCN_ACT_RELU && ldg % 4 == 0 && aligned(gout, 16) &&
+                        !sg.overlaps(Span{db, 1, d_out, d_out});
+  const bool z_direct =
+      dzeta != nullptr && lddz % 4 == 0 && aligned(dzeta, 16) && z_alone;
   float* Gm = g_direct ? nullptr : (float*)(ws + L.off_Gm);
   const float* Gsrc = g_direct ? gout : Gm;
   const int64_t ldsrc = g_direct ? ldg : L.ldm;

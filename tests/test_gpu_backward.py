@@ -144,6 +144,42 @@ def test_arxiv_like_layer_backward(dev):
     check_backward(got, ref, G, wt, d_in)
 
 
+def test_backward_dzeta_in_place_of_gout(dev):
+    """dζ written over the incoming gradient's own buffer: every result equal,
+    bit for bit, to the call with separate buffers."""
+    rng = np.random.default_rng(8)
+    g = _star(500, rng)
+    n, d_in, d_out = g.n, 96, 64
+    h = _t(rng.standard_normal((n, d_in)).astype(np.float32), dev)
+    wt = _t(rng.standard_normal((d_out, d_in)).astype(np.float32), dev)
+    G = _t((rng.standard_normal((n, d_out)) * 0.1).astype(np.float32), dev)
+    wbits, alpha = bg.pack_weights(wt)
+    ws = torch.empty(bg.layer_backward_workspace_bytes(n, g.nnz, d_in, d_out),
+                     dtype=torch.uint8, device=dev)
+    rowptr, colidx = _t(g.rowptr, dev), _t(g.colidx, dev)
+
+    def run(gout, dzeta):
+        r = dict(dh=torch.empty((n, d_in), device=dev),
+                 dh_tilde=torch.empty((n, d_in), device=dev),
+                 dwt=torch.empty((d_out, d_in), device=dev),
+                 dwt_tilde=torch.empty((d_out, d_in), device=dev),
+                 db=torch.empty(d_out, device=dev))
+        bg.bigcn_layer_backward(rowptr, colidx, h, wt, wbits, alpha, gout, r["dwt"], ws,
+                                "sym", dh=r["dh"], dh_tilde=r["dh_tilde"],
+                                dwt_tilde=r["dwt_tilde"], db=r["db"], dzeta=dzeta,
+                                nnz=g.nnz)
+        torch.cuda.synchronize()
+        return r
+
+    ref_dz = torch.empty((n, d_out), device=dev)
+    ref = run(G.clone(), ref_dz)
+    G2 = G.clone()
+    got = run(G2, G2)
+    for k in ref:
+        assert torch.equal(ref[k], got[k]), k
+    assert torch.equal(G2, ref_dz)
+
+
 def test_backward_reproducible(dev):
     rng = np.random.default_rng(21)
     g = _star(900, rng)
