@@ -6,21 +6,26 @@ A step is one whole forward pass (every layer: sign pack, binary GEMM, CSR
 aggregation) over a seeded synthetic workload whose inputs, packed weights
 and workspace are already resident in device memory.  The pass is timed
 twice, as eager calls and as a HIP-graph replay (checked bit-equal to the
-eager pass first); the faster loop gives the reported value (--mode).  The default workload
+eager pass first); the faster loop gives the reported value (--mode).  A
+third timing ("cold_ms_per_step") runs each pass after a 512 MiB write that
+evicts the last-level cache and the L2s, so the inputs come from HBM; it is
+reported beside the value, not as it.  The default workload
 is the PubMed-shaped citation graph (19,717 nodes, 500 -> 64 -> 3); the other
 five (the sixth a two-weight GraphSAGE model) are selectable with --workload.
 
 Prints one JSON line.  Besides the forward-pass throughput it carries
  - "kernels":  each layer's steps timed alone through their entry points
    (HIP events around a graph replay of --kernel-reps back-to-back calls on
-   the launch stream); the aggregation step is its three kernels (row plan,
-   aggregation, fix-up of rows cut by chunk boundaries);
+   the launch stream); an aggregation step is all of its kernels (one for
+   layers of at most 64 columns, aggregation and fix-up for wider 8-bit
+   layers, plus a row plan on the exact-product path);
  - "roofline": the dominant kernel (largest share of a forward pass) against
    its bound: HBM bytes for pack / aggregation (each array counted once;
    the aggregation entries also carry the gather model, every edge reading
    its source's whole product row), bit operations on the vector ALUs for
    the binary GEMM; "traffic" is the counter-measured HBM bytes of that call
    (profiles/hbm_traffic_<workload>.md) while the kernel sources match;
+   "cold" is the same entry point timed after cache-evicting writes;
  - "bgemm_ab": the binary GEMM of every layer shape run with both
    algorithms (XOR + bit count on the vector ALUs, +-1 int8 on the matrix
    cores) on the same random sign bits, checked equal, each against its
@@ -29,7 +34,8 @@ Prints one JSON line.  Besides the forward-pass throughput it carries
    ratios for this workload (theory, quoted as such), beside the ratio of
    the fp32 features to the packed sign words this library stores;
  - "cpu_baseline": the plain CPU oracle timed on this host on a bounded
-   sample of the same workload.
+   sample of the same workload: whole forward passes up to 200 K nodes,
+   else each layer's two steps on row samples scaled to all rows.
 
     python bench.py --bgemm-ab
 
