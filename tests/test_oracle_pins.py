@@ -361,3 +361,153 @@ def test_sage_subset_matches_full():
                                            ids=ids)
     assert np.array_equal(z2, z[ids]) and np.array_equal(out2, out[ids])
     assert np.all(out >= 0)
+
+
+# ------------------------------------ multi-layer chain (Sec. 4.1, Sec. 6.2)
+
+def _expr_rows(text):
+    """Rows of exact expressions (fractions, powers of two) as float64."""
+    env = {"__builtins__": {}}
+    return np.array([[float(eval(t, env)) for t in r.split()] for r in text.split(";")],
+                    dtype=np.float64)
+
+
+def _forward_fixture():
+    gv = _read_golden("tiny_forward.txt")
+    edges = [tuple(int(v) for v in e.split("-")) for e in gv["edges"].split()]
+    g = workloads.graph_from_edges(int(gv["n"]), edges)
+    f32 = lambda k: _expr_rows(gv[k]).astype(np.float32)
+    fx = dict(g=g, norm=gv["norm"], x=f32("x"), mu=f32("mu")[0], rstd=f32("rstd")[0],
+              wts=[f32("wt0"), f32("wt1")], bs=[f32("bias0")[0], f32("bias1")[0]])
+    return gv, fx
+
+
+def _check_forward(gv, fx, forward):
+    """The hand-worked chain: True iff every expected value is reproduced."""
+    g = fx["g"]
+    run = lambda acts: forward(g.rowptr, g.colidx, fx["norm"], fx["x"], fx["wts"], fx["bs"],
+                               acts=acts, mu=fx["mu"], rstd=fx["rstd"])
+    ok = True
+    res = run(["none", "none"])
+    ok &= np.allclose(res[0][0], _expr_rows(gv["z0"]), rtol=1e-15, atol=0)
+    ok &= np.array_equal(res[0][2].astype(np.float64), _expr_rows(gv["out0"]))
+    ok &= np.allclose(res[1][0], _expr_rows(gv["z1"]), rtol=1e-15, atol=0)
+    res = run(["relu", "none"])
+    ok &= np.array_equal(res[0][2].astype(np.float64), _expr_rows(gv["relu_none_out0"]))
+    ok &= np.allclose(res[1][0], _expr_rows(gv["relu_none_z1"]), rtol=1e-15, atol=0)
+    res = run(["none", "relu"])
+    ok &= np.array_equal(res[1][2].astype(np.float64), _expr_rows(gv["none_relu_out1"]))
+    return bool(ok)
+
+
+def _sage_fixture():
+    gv = _read_golden("tiny_sage_forward.txt")
+    edges = [tuple(int(v) for v in e.split("-")) for e in gv["edges"].split()]
+    g = _sage_graph(int(gv["n"]), edges)
+    f32 = lambda k: _expr_rows(gv[k]).astype(np.float32)
+    fx = dict(g=g, x=f32("x"), mu=f32("mu")[0], rstd=f32("rstd")[0],
+              ws=[f32("ws0"), f32("ws1")], wn=[f32("wn0"), f32("wn1")],
+              bs=[f32("bias0")[0], f32("bias1")[0]])
+    return gv, fx
+
+
+def _check_sage_forward(gv, fx, forward):
+    g = fx["g"]
+    run = lambda acts: forward(g.rowptr, g.colidx, fx["x"], fx["ws"], fx["wn"], fx["bs"],
+                               acts=acts, mu=fx["mu"], rstd=fx["rstd"])
+    ok = True
+    res = run(["none", "none"])
+    ok &= np.array_equal(res[0][0], _expr_rows(gv["z0"]))        # every value dyadic
+    ok &= np.array_equal(res[0][2].astype(np.float64), _expr_rows(gv["out0"]))
+    ok &= np.array_equal(res[1][0], _expr_rows(gv["z1"]))
+    ok &= np.array_equal(res[1][1], _expr_rows(gv["mass1"]))
+    res = run(["relu", "none"])
+    ok &= np.array_equal(res[0][2].astype(np.float64), _expr_rows(gv["relu_none_out0"]))
+    ok &= np.array_equal(res[1][0], _expr_rows(gv["relu_none_z1"]))
+    res = run(["none", "relu"])
+    ok &= np.array_equal(res[1][2].astype(np.float64), _expr_rows(gv["none_relu_out1"]))
+    return bool(ok)
+
+
+def test_fixture_fp32_roundings_are_what_the_text_derives():
+    """The fixtures' hand roundings, checked against the IEEE conversion."""
+    assert float(np.float32(7 / 12)) == 9786709 / 2 ** 24
+    assert float(np.float32(5 / 12)) == 13981013 / 2 ** 25
+    for v in (-8, 3, -12, 1):
+        assert float(np.float32(v + 2.0 ** -26)) == v
+    b1 = 33554431 / 2 ** 26
+    assert [float(np.float32(v)) for v in ((0.75 + 3 * b1) / 2 + 0.125,
+                                           (0.75 + 3 * b1) / 3 + 0.125,
+                                           1.5 * b1 + 0.125)] == [1.25, 0.875, 0.875]
+
+
+def test_hand_worked_two_layer_forward():
+    gv, fx = _forward_fixture()
+    assert _check_forward(gv, fx, oracle.forward)
+
+
+def test_hand_worked_two_layer_sage_forward():
+    gv, fx = _sage_fixture()
+    assert _check_sage_forward(gv, fx, oracle.sage_forward)
+
+
+def _gcn_chain(mistake):
+    """A copy of the oracle's layer chain with one planted mistake, built from
+    the oracle's single-layer function (the chain is what is under test)."""
+    def forward(rowptr, colidx, norm, x, weights_t, biases, acts=None, mu=None, rstd=None):
+        L = len(weights_t)
+        acts = acts or ["none"] * L
+        h, res = x, []
+        for l, wt in enumerate(weights_t):
+            std = (l == 0) != (mistake == "no_standardisation") or mistake == "std_every_layer"
+            b = biases[(l + 1) % L] if mistake == "bias_shift" else biases[l]
+            a = acts[(l + 1) % L] if mistake == "act_shift" else acts[l]
+            if mistake == "act_ignored":
+                a = "none"
+            z, m, out, _ = oracle.layer(rowptr, colidx, norm, h, wt, b, a,
+                                        mu if std else None, rstd if std else None)
+            res.append((z, m, out))
+            h = out if mistake != "feed_z_down" else np.nextafter(z, -np.inf)
+        return res
+    return forward
+
+
+def _sage_chain(mistake):
+    def forward(rowptr, colidx, x, ws_t, wn_t, biases, acts=None, mu=None, rstd=None):
+        L = len(ws_t)
+        acts = acts or ["none"] * L
+        h, res = x, []
+        for l in range(L):
+            std = (l == 0) != (mistake == "no_standardisation") or mistake == "std_every_layer"
+            b = biases[(l + 1) % L] if mistake == "bias_shift" else biases[l]
+            a = acts[(l + 1) % L] if mistake == "act_shift" else acts[l]
+            if mistake == "act_ignored":
+                a = "none"
+            ws, wn = (wn_t[l], ws_t[l]) if mistake == "weights_swapped" else (ws_t[l], wn_t[l])
+            z, m, out, _, _ = oracle.sage_layer(rowptr, colidx, h, ws, wn, b, a,
+                                                mu if std else None, rstd if std else None)
+            res.append((z, m, out))
+            h = out if mistake != "feed_z_down" else np.nextafter(z, -np.inf)
+        return res
+    return forward
+
+
+_CHAIN_MISTAKES = ["std_every_layer", "no_standardisation", "bias_shift", "act_shift",
+                   "act_ignored", "feed_z_down"]
+
+
+@pytest.mark.parametrize("mistake", _CHAIN_MISTAKES)
+def test_forward_fixture_rejects_planted_chain_mistakes(mistake):
+    """Each plausible chaining mistake fails the hand-worked fixture.  The
+    fp64-z-fed-forward mistake is planted as the layer input rounded away
+    from fl32(z) (the oracle's layer takes fp32 input); the fixture's row 1
+    would give beta = 1/2 exactly from 7/12 and 5/12, against
+    33554431/2^26 from their fp32 roundings."""
+    gv, fx = _forward_fixture()
+    assert not _check_forward(gv, fx, _gcn_chain(mistake))
+
+
+@pytest.mark.parametrize("mistake", _CHAIN_MISTAKES + ["weights_swapped"])
+def test_sage_forward_fixture_rejects_planted_chain_mistakes(mistake):
+    gv, fx = _sage_fixture()
+    assert not _check_sage_forward(gv, fx, _sage_chain(mistake))
