@@ -1,6 +1,6 @@
 """Benchmark of the binarized-GCN inference path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 5]
 
 A step is one whole forward pass (every layer: sign pack, binary GEMM, CSR
 aggregation) over a seeded synthetic workload whose inputs, packed weights
@@ -9,9 +9,10 @@ twice, as eager calls and as a HIP-graph replay (checked bit-equal to the
 eager pass first); the faster loop gives the reported value (--mode).  A
 third timing ("cold_ms_per_step") runs each pass after a 512 MiB write that
 evicts the last-level cache and the L2s, so the inputs come from HBM; it is
-reported beside the value, not as it.  The default workload
-is the PubMed-shaped citation graph (19,717 nodes, 500 -> 64 -> 3); the other
-five (the sixth a two-weight GraphSAGE model) are selectable with --workload.
+reported beside the value, not as it.  The default workload is the largest
+one: the products-shaped graph (2,449,029 nodes, 126,149,029 CSR entries of
+A + I, 100 -> 256 -> 256 -> 47, mean aggregation); the other five (the
+sixth a two-weight GraphSAGE model) are selectable with --workload.
 
 Prints one JSON line.  Besides the forward-pass throughput it carries
  - "kernels":  each layer's steps timed alone through their entry points
@@ -33,9 +34,10 @@ Prints one JSON line.  Besides the forward-pass throughput it carries
  - "paper_theoretical": the paper's analytic cycle-operation and size
    ratios for this workload (theory, quoted as such), beside the ratio of
    the fp32 features to the packed sign words this library stores;
- - "cpu_baseline": the plain CPU oracle timed on this host on a bounded
-   sample of the same workload: whole forward passes up to 200 K nodes,
-   else each layer's two steps on row samples scaled to all rows.
+ - "cpu_baseline": the plain CPU oracle timed on this host: whole forward
+   passes of the same workload, repeated for --cpu-budget seconds (a
+   single pass when one takes longer), with the thread count and the host
+   CPU model.
 
     python bench.py --bgemm-ab
 
@@ -77,17 +79,25 @@ def words(k):
 
 
 def kernel_specs(w, ldF, ldc):
-    """Algorithmic work of each kernel of one forward pass."""
+    """Algorithmic work of each kernel of one forward pass, in the units of
+    the hot-path scope: every array read or written once, the products as
+    16-bit integers in rows of d rounded up to 8 (the library stores most of
+    them as 8-bit half-codes, so these are the bytes the method needs, not
+    the bytes this implementation moves):
+      pack   N*K*4 + N*Kw*8 + N*4 (+ 2*K*4 for mu, rstd on layer 0)
+      bGEMM  N*K*d sign products; N*Kw*8 + d*Kw*8 + N*ldc*2 bytes
+      SpMM   8(N+1) + 4 nnz + 4N + 2 N ldc + 4 N d bytes (row pointers,
+             column indices, scales, products, output); 2 nnz d flops."""
     n, nnz = w.graph.n, w.graph.nnz
     specs = []
     for l, wt in enumerate(w.weights_t):
         d, K = wt.shape
         kw = words(K)
-        pack_bytes = n * K * 4 + n * kw * 8 + n * 4 + (n + 1) * 8 + (2 * K * 4 if l == 0 else 0)
-        es = 1 if (d <= 256 and K <= 2048) else 2   # stored bytes per product
+        ldc_l = (d + 7) // 8 * 8
+        pack_bytes = n * K * 4 + n * kw * 8 + n * 4 + (2 * K * 4 if l == 0 else 0)
         gemm_ops = n * K * d
-        gemm_bytes = n * kw * 8 + d * kw * 8 + n * d * es
-        spmm_bytes = 8 * (n + 1) + 4 * nnz + 4 * n + n * d * es + n * d * 4 + 8 * d
+        gemm_bytes = n * kw * 8 + d * kw * 8 + n * ldc_l * 2
+        spmm_bytes = 8 * (n + 1) + 4 * nnz + 4 * n + 2 * n * ldc_l + 4 * n * d
         specs.append(dict(layer=l, K=K, d=d, pack_bytes=pack_bytes, gemm_ops=gemm_ops,
                           gemm_bytes=gemm_bytes, spmm_bytes=spmm_bytes,
                           spmm_flops=2 * nnz * d))
@@ -293,86 +303,48 @@ def traffic_probe(w, model, x, rowptr, colidx, torch, bg, dev):
     print(json.dumps({"traffic_probe": w.name, "copy_bytes": COPY_BYTES}), flush=True)
 
 
+def host_cpu_model():
+    """The host CPU's model name (first 'model name' of /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(w, budget_s=10.0):
-    """The oracle on this host: the whole forward pass for small graphs, else
-    per-layer row samples of its two steps, scaled to all rows."""
-    import numpy as np
+    """The oracle on this host, whole forward passes of the same workload:
+    passes are repeated until budget_s has elapsed (one pass when a single
+    pass takes longer).  Each layer's double-precision arrays are dropped as
+    soon as the next layer has its input, as a caller of the per-layer chain
+    may.  Returns nodes per second over the timed passes."""
     import oracle
 
     g = w.graph
-    L = len(w.weights_t)
     cores = oracle.threads()
     sage = w.weights_self_t is not None
-    if g.n <= 200_000 or sage:
-        t0 = time.time()
-        reps = 0
-        while True:
-            if sage:
-                oracle.sage_forward(g.rowptr, g.colidx, w.x, w.weights_self_t, w.weights_t,
-                                    w.biases, mu=w.mu, rstd=w.rstd)
-            else:
-                oracle.forward(g.rowptr, g.colidx, w.norm, w.x, w.weights_t, w.biases,
-                               mu=w.mu, rstd=w.rstd)
-            reps += 1
-            if time.time() - t0 >= budget_s or reps >= 10_000:
-                break
-        dt = time.time() - t0
-        return dict(value=g.n * reps / dt, unit="nodes/s", cores=cores, kind="oracle",
-                    sample="whole %d-node forward pass x %d in %.1f s" % (g.n, reps, dt))
-    # Larger graphs: every layer's two steps timed on row samples and scaled
-    # to all n rows (rows are independent in both): the transform (sign pack
-    # of the layer input and the ±1 products with the packed weights) on a
-    # block of rows, and the aggregation on random output rows (its inputs
-    # beta and dot are whole arrays the sampled rows gather from; their values
-    # do not change the work).  Layer inputs past layer 0 are seeded N(0,1)
-    # stand-ins, as in the tests.
-    rng = np.random.default_rng(7)
-    part = budget_s / (2 * L)
-    total = 0.0
-    desc = []
-
-    def grow(run, n_max):
-        k = 64
-        while True:
-            t0 = time.time()
-            run(k)
-            dt = time.time() - t0
-            if dt >= part or k >= n_max:
-                return k, dt
-            k = min(n_max, k * (2 if dt * 4 > part else 8))
-
-    for l, wt in enumerate(w.weights_t):
-        d_out, K = wt.shape
-        B, _ = oracle.binarize(wt)
-
-        def transform(k, l=l, K=K, B=B):
-            r0 = int(rng.integers(0, max(1, g.n - k)))
-            if l == 0:
-                xs = w.x[r0:r0 + k]
-                F, _ = oracle.binarize(xs, mu=w.mu, rstd=w.rstd)
-            else:
-                xs = rng.standard_normal((k, K)).astype(np.float32)
-                F, _ = oracle.binarize(xs)
-            oracle.sign_dot(F, B, K)
-
-        beta = np.zeros(g.n, dtype=np.float64)
-        alpha = np.ones(d_out, dtype=np.float64)
-        dot = np.zeros((g.n, d_out), dtype=np.int64)
-
-        def aggregate(k, d_out=d_out):
-            ids = np.sort(rng.choice(g.n, size=k, replace=False)).astype(np.int64)
-            oracle.aggregate(g.rowptr, g.colidx, w.norm, beta, alpha, dot,
-                             w.biases[l], ids=ids)
-
-        kt, tt = grow(transform, g.n)
-        ka, ta = grow(aggregate, g.n)
-        del dot
-        total += tt * g.n / kt + ta * g.n / ka
-        desc.append("layer %d: transform %d rows %.1f s, aggregation %d rows %.1f s" % (
-            l, kt, tt, ka, ta))
-    return dict(value=g.n / total, unit="nodes/s", cores=cores, kind="oracle",
-                sample="per layer, each step on a row sample scaled to all %d rows (%s); "
-                       "estimated whole forward %.1f s" % (g.n, "; ".join(desc), total))
+    t0 = time.time()
+    reps = 0
+    while True:
+        if sage:
+            chain = oracle.sage_forward_layers(g.rowptr, g.colidx, w.x, w.weights_self_t,
+                                               w.weights_t, w.biases, mu=w.mu, rstd=w.rstd)
+        else:
+            chain = oracle.forward_layers(g.rowptr, g.colidx, w.norm, w.x, w.weights_t,
+                                          w.biases, mu=w.mu, rstd=w.rstd)
+        for _ in chain:
+            pass
+        reps += 1
+        if time.time() - t0 >= budget_s or reps >= 10_000:
+            break
+    dt = time.time() - t0
+    return dict(value=g.n * reps / dt, unit="nodes/s", cores=cores, kind="oracle",
+                cpu_model=host_cpu_model(),
+                sample="whole %d-node forward pass x %d in %.1f s (plain oracle, not a "
+                       "tuned CPU library; %d OpenMP threads)" % (g.n, reps, dt, cores))
 
 
 def main():
@@ -380,7 +352,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6])
+    ap.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5, 6])
     ap.add_argument("--kernel-reps", type=int, default=20)
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")

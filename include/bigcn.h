@@ -330,7 +330,6 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
                            int32_t n_layers, float* out, int64_t ldo,
                            void* workspace, size_t ws_bytes, void* stream);
 
-/* Human-readable text of a status code (static storage). */
 /* ---------------------------------------------------------------------------
  * bigcn_check_csr -- validates the contents of a CSR graph on the device
  * (the entry points above take them on trust: a bad row pointer or column
@@ -353,6 +352,7 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
 bigcn_status bigcn_check_csr(int64_t n, int64_t nnz, const int64_t* rowptr,
                              const int32_t* colidx, int32_t* flags, void* stream);
 
+/* Human-readable text of a status code (static storage, never NULL). */
 const char* bigcn_status_string(bigcn_status s);
 
 #ifdef __cplusplus

@@ -204,18 +204,26 @@ def sage_layer(rowptr, colidx, h, wt_self, wt_neigh, bias=None, act="none",
     return z, mass, out, a_s, a_n
 
 
-def sage_forward(rowptr, colidx, x, weights_self_t, weights_neigh_t, biases,
-                 acts=None, mu=None, rstd=None):
-    """Free-running two-weight GraphSAGE forward; list of (z, mass, out)."""
+def sage_forward_layers(rowptr, colidx, x, weights_self_t, weights_neigh_t, biases,
+                        acts=None, mu=None, rstd=None):
+    """Free-running two-weight GraphSAGE forward, one layer at a time: yields
+    (z, mass, out) per layer.  Layer 0 reads x, standardised by mu/rstd if
+    given; layer l reads the fp32 output of layer l-1 and nothing else, so a
+    caller may drop each layer's fp64 arrays before asking for the next."""
     acts = acts or ["none"] * len(weights_self_t)
     h = x
-    res = []
     for l, (ws, wn) in enumerate(zip(weights_self_t, weights_neigh_t)):
         z, m, out, _, _ = sage_layer(rowptr, colidx, h, ws, wn, biases[l], acts[l],
                                      mu if l == 0 else None, rstd if l == 0 else None)
-        res.append((z, m, out))
+        yield z, m, out
         h = out
-    return res
+
+
+def sage_forward(rowptr, colidx, x, weights_self_t, weights_neigh_t, biases,
+                 acts=None, mu=None, rstd=None):
+    """Free-running two-weight GraphSAGE forward; list of (z, mass, out)."""
+    return list(sage_forward_layers(rowptr, colidx, x, weights_self_t, weights_neigh_t,
+                                    biases, acts, mu, rstd))
 
 
 def layer_backward(rowptr, colidx, norm, h, wt, gout, out=None, act="none"):
@@ -249,17 +257,23 @@ def layer_backward(rowptr, colidx, norm, h, wt, gout, out=None, act="none"):
     return r
 
 
-def forward(rowptr, colidx, norm, x, weights_t, biases, acts=None, mu=None,
-            rstd=None):
-    """Free-running multi-layer forward: layer l's input is the fp32 output of
-    layer l-1 (layer 0 reads x, standardised by mu/rstd if given).  Returns a
-    list of (z, mass, out) per layer."""
+def forward_layers(rowptr, colidx, norm, x, weights_t, biases, acts=None, mu=None,
+                   rstd=None):
+    """Free-running multi-layer forward (Sec. 4.1: H(0) = X), one layer at a
+    time: yields (z, mass, out) per layer.  Layer 0 reads x, standardised by
+    mu/rstd if given (Sec. 6.2); layer l reads the fp32 output of layer l-1
+    and nothing else, so a caller may drop each layer's fp64 arrays before
+    asking for the next."""
     acts = acts or ["none"] * len(weights_t)
     h = x
-    res = []
     for l, wt in enumerate(weights_t):
         z, m, out, _ = layer(rowptr, colidx, norm, h, wt, biases[l], acts[l],
                              mu if l == 0 else None, rstd if l == 0 else None)
-        res.append((z, m, out))
+        yield z, m, out
         h = out
-    return res
+
+
+def forward(rowptr, colidx, norm, x, weights_t, biases, acts=None, mu=None,
+            rstd=None):
+    """Free-running multi-layer forward: list of (z, mass, out) per layer."""
+    return list(forward_layers(rowptr, colidx, norm, x, weights_t, biases, acts, mu, rstd))

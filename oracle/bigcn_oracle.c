@@ -144,7 +144,10 @@ static double atilde(int norm, int64_t deg_i, int64_t deg_j) {
 }
 
 /* Eq. (13) for listed output rows.  Source node j's β and dot row sit at
- * position slot[j] of beta / dot (slot == NULL: position j). */
+ * position slot[j] of beta / dot (slot == NULL: position j).  Row i of
+ * the result is the sum over the neighbours j of row i of Â, taken in CSR
+ * order, of Ã_ij times the row ζ_j: each element z_ik is a sequential sum
+ * 0 + t_1k + t_2k + ... (+ b_k), the neighbours visited in CSR order. */
 static void aggregate_rows(const int64_t* rowptr, const int32_t* colidx,
                            int norm, const int64_t* slot, const double* beta,
                            const double* alpha, const int64_t* dot,
@@ -155,24 +158,29 @@ static void aggregate_rows(const int64_t* rowptr, const int32_t* colidx,
   for (int64_t r = 0; r < n_out; ++r) {
     int64_t i = ids ? ids[r] : r;
     int64_t deg_i = rowptr[i + 1] - rowptr[i];
+    double* zr = z + r * d;
+    double* mr = mass + r * d;
     for (int32_t k = 0; k < d; ++k) {
-      double s = 0.0, m = 0.0;
-      for (int64_t e = rowptr[i]; e < rowptr[i + 1]; ++e) {
-        int64_t j = colidx[e];
-        int64_t c = slot ? slot[j] : j;
-        int64_t deg_j = rowptr[j + 1] - rowptr[j];
+      zr[k] = 0.0;
+      mr[k] = 0.0;
+    }
+    for (int64_t e = rowptr[i]; e < rowptr[i + 1]; ++e) {
+      int64_t j = colidx[e];
+      int64_t c = slot ? slot[j] : j;
+      int64_t deg_j = rowptr[j + 1] - rowptr[j];
+      for (int32_t k = 0; k < d; ++k) {
         double zeta = beta[c] * alpha[k] * (double)dot[c * ldd + k]; /* (11) */
         double t = atilde(norm, deg_i, deg_j) * zeta;                /* (13) */
-        s += t;
-        m += fabs(t);
+        zr[k] += t;
+        mr[k] += fabs(t);
       }
+    }
+    for (int32_t k = 0; k < d; ++k) {
       if (bias != NULL) {
-        s += (double)bias[k];
-        m += fabs((double)bias[k]);
+        zr[k] += (double)bias[k];
+        mr[k] += fabs((double)bias[k]);
       }
-      double v = (act == ORACLE_ACT_RELU && s < 0.0) ? 0.0 : s;
-      z[r * d + k] = s;
-      mass[r * d + k] = m;
+      double v = (act == ORACLE_ACT_RELU && zr[k] < 0.0) ? 0.0 : zr[k];
       out[r * d + k] = (float)v;
     }
   }
@@ -362,27 +370,34 @@ int oracle_sage_layer(int64_t n, const int64_t* rowptr, const int32_t* colidx,
   oracle_sign_dot(fbits, n_src, ldw, bs, d_out, ldw, d_in, dots, d_out);
   oracle_sign_dot(fbits, n_src, ldw, bn, d_out, ldw, d_in, dotn, d_out);
 
+  /* Row i: the self term, then the neighbours in CSR order, then the
+   * bias, each element a sequential sum in that order. */
 #pragma omp parallel for schedule(dynamic, 16)
   for (int64_t r = 0; r < n_out; ++r) {
     int64_t i = ids ? ids[r] : r;
     int64_t deg = rowptr[i + 1] - rowptr[i];
     int64_t ci = slot[i];
+    double* zr = z + r * d_out;
+    double* mr = mass + r * d_out;
     for (int32_t k = 0; k < d_out; ++k) {
       double self = beta[ci] * as[k] * (double)dots[ci * d_out + k];
-      double s = self, m = fabs(self);
-      for (int64_t e = rowptr[i]; e < rowptr[i + 1]; ++e) {
-        int64_t c = slot[colidx[e]];
+      zr[k] = self;
+      mr[k] = fabs(self);
+    }
+    for (int64_t e = rowptr[i]; e < rowptr[i + 1]; ++e) {
+      int64_t c = slot[colidx[e]];
+      for (int32_t k = 0; k < d_out; ++k) {
         double t = beta[c] * an[k] * (double)dotn[c * d_out + k] / (double)deg;
-        s += t;
-        m += fabs(t);
+        zr[k] += t;
+        mr[k] += fabs(t);
       }
+    }
+    for (int32_t k = 0; k < d_out; ++k) {
       if (bias != NULL) {
-        s += (double)bias[k];
-        m += fabs((double)bias[k]);
+        zr[k] += (double)bias[k];
+        mr[k] += fabs((double)bias[k]);
       }
-      double v = (act == ORACLE_ACT_RELU && s < 0.0) ? 0.0 : s;
-      z[r * d_out + k] = s;
-      mass[r * d_out + k] = m;
+      double v = (act == ORACLE_ACT_RELU && zr[k] < 0.0) ? 0.0 : zr[k];
       out[r * d_out + k] = (float)v;
     }
   }
