@@ -193,6 +193,37 @@ bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                                void* workspace, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * bigcn_spmm_csr_q8_noalloc -- bigcn_spmm_csr_q8 without a workspace argument,
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that must not call hipMalloc, harnesses that forbid
+ * it).  It allocates nothing and calls no allocating routine: its scratch
+ * (per-chunk partial rows) lives in a static device array of
+ * bigcn_spmm_csr_q8_noalloc_max_bytes() bytes (64.25 MiB) that every GPU the
+ * library runs on holds until the process ends.  The first call on a device
+ * looks up that device's copy (hipGetSymbolAddress).
+ *
+ * Arguments, layouts and results as bigcn_spmm_csr_q8.  Graphs of up to
+ * 67,108,864 CSR entries are cut into the same chunks as there, so the
+ * results are identical; larger graphs are cut into at most 32768 longer
+ * chunks (the same sums in another grouping, equal up to fp32 rounding).
+ * Calls on one GPU share its scratch array: calls that overlap in time on
+ * one GPU (different streams, or host threads) race and must not be issued;
+ * calls ordered on one stream are safe.  The array keeps the last call's
+ * contents; nothing in it is read before it is written within a call.
+ * Errors: as bigcn_spmm_csr_q8, plus EWORKSPACE if the scratch this call
+ *         needs exceeds the array (it does not for d <= 256) and EHIP if the
+ *         array's device address cannot be obtained.
+ * ------------------------------------------------------------------------- */
+size_t bigcn_spmm_csr_q8_noalloc_max_bytes(void);
+bigcn_status bigcn_spmm_csr_q8_noalloc(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                       const int32_t* colidx, bigcn_norm norm,
+                                       const float* g, const int8_t* C8, int64_t ldc8,
+                                       const void* C16, int64_t ldc16, int32_t K,
+                                       int32_t d, const float* alpha, const float* bias,
+                                       bigcn_act act, float* out, int64_t ldo,
+                                       void* stream);
+
+/* ---------------------------------------------------------------------------
  * bigcn_spmm_csr_sage_q8 -- aggregation of a binarised two-weight GraphSAGE
  * layer with the mean aggregator.  The paper binarises every feature-
  * extraction step of the GNNs it generalises (Sec. 6, Table 3, whose model

@@ -28,6 +28,7 @@ ALGOS = {"auto": 0, "popcount": 1, "mfma_i8": 2}
 # Every entry point declared in include/bigcn.h.
 EXPORTS = ("bigcn_binarize_pack", "bigcn_bgemm", "bigcn_spmm_workspace_bytes",
            "bigcn_spmm_csr", "bigcn_bgemm_q8", "bigcn_spmm_csr_q8",
+           "bigcn_spmm_csr_q8_noalloc", "bigcn_spmm_csr_q8_noalloc_max_bytes",
            "bigcn_spmm_csr_sage_q8", "bigcn_layer_backward_workspace_bytes",
            "bigcn_layer_backward",
            "bigcn_forward_workspace_bytes", "bigcn_forward", "bigcn_check_csr",
@@ -91,6 +92,11 @@ def load() -> ctypes.CDLL:
     lib.bigcn_spmm_csr_q8.restype = _int
     lib.bigcn_spmm_csr_q8.argtypes = [_i64, _i64, _p, _p, _int, _p, _p, _i64, _p, _i64,
                                       _i32, _i32, _p, _p, _int, _p, _i64, _p, _sz, _p]
+    lib.bigcn_spmm_csr_q8_noalloc.restype = _int
+    lib.bigcn_spmm_csr_q8_noalloc.argtypes = [_i64, _i64, _p, _p, _int, _p, _p, _i64, _p,
+                                              _i64, _i32, _i32, _p, _p, _int, _p, _i64, _p]
+    lib.bigcn_spmm_csr_q8_noalloc_max_bytes.restype = _sz
+    lib.bigcn_spmm_csr_q8_noalloc_max_bytes.argtypes = []
     lib.bigcn_forward_workspace_bytes.restype = _sz
     lib.bigcn_forward_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(_Layer),
                                                   _i32]
@@ -225,6 +231,29 @@ def bigcn_spmm_csr_q8(rowptr: torch.Tensor, colidx: torch.Tensor, g: torch.Tenso
         _dev(workspace, torch.uint8, "workspace"),
         workspace.numel() if workspace is not None else 0, _stream(stream))
     _check("bigcn_spmm_csr_q8", st)
+
+
+def spmm_q8_noalloc_max_bytes() -> int:
+    return load().bigcn_spmm_csr_q8_noalloc_max_bytes()
+
+
+def bigcn_spmm_csr_q8_noalloc(rowptr: torch.Tensor, colidx: torch.Tensor, g: torch.Tensor,
+                              C8: torch.Tensor, C16: torch.Tensor, K: int,
+                              alpha: torch.Tensor, out: torch.Tensor, bias=None,
+                              norm: str = "sym", act: str = "none", d: Optional[int] = None,
+                              nnz: Optional[int] = None, stream=None) -> None:
+    """bigcn_spmm_csr_q8 with its scratch in the library's static device array
+    (no workspace argument, no allocation)."""
+    n = rowptr.shape[0] - 1
+    d = alpha.shape[0] if d is None else d
+    nnz = colidx.shape[0] if nnz is None else nnz
+    st = load().bigcn_spmm_csr_q8_noalloc(
+        n, nnz, _dev(rowptr, torch.int64, "rowptr"), _dev(colidx, torch.int32, "colidx"),
+        NORMS[norm], _dev(g, torch.float32, "g"), _dev(C8, torch.int8, "C8"), _ld(C8, "C8"),
+        _dev(C16, torch.float16, "C16"), _ld(C16, "C16"), K, d,
+        _dev(alpha, torch.float32, "alpha"), _dev(bias, torch.float32, "bias"), ACTS[act],
+        _dev(out, torch.float32, "out"), _ld(out, "out"), _stream(stream))
+    _check("bigcn_spmm_csr_q8_noalloc", st)
 
 
 def bigcn_spmm_csr_sage_q8(rowptr: torch.Tensor, colidx: torch.Tensor, g: torch.Tensor,

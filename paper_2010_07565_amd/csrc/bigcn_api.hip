@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "../../include/bigcn.h"
 #include "bigcn_internal.h"
@@ -15,7 +16,7 @@ using bigcn::IType;
 
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 inline int64_t words(int64_t k) { return (k + 63) / 64; }
-inline size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
+constexpr size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 inline bool itype_ok(int t) { return t == BIGCN_I32 || t == BIGCN_I16 || t == BIGCN_F16; }
 inline bool itype_holds(int t, int64_t K) {
@@ -161,6 +162,36 @@ bool forward_layout(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t n
   off += bigcn::spmm_plan(n, nnz, (int32_t)dmax).bytes;
   L->bytes = off;
   return true;
+}
+
+// Scratch of bigcn_spmm_csr_q8_noalloc: a file-scope device array, one copy
+// per GPU, alive until the process ends.  Its size is the largest workspace
+// of the 8-bit aggregation with at most kNoallocWorkers workers and rows of
+// up to 256 columns (two int32 arrays and two fp32 partial-row arrays of
+// kNoallocWorkers entries).  Host code never uses the array's name as an
+// address: each device's address comes from hipGetSymbolAddress, taken once
+// per device the first time the entry point runs there.
+constexpr int64_t kNoallocWorkers = 32768;
+constexpr size_t kNoallocScratchBytes =
+    2 * up256((size_t)kNoallocWorkers * 4) + 2 * up256((size_t)kNoallocWorkers * 256 * 4);
+static __device__ __align__(256) __attribute__((used)) unsigned char
+    scratch[kNoallocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch` (nullptr on failure).
+void* device_scratch() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
 }
 
 }  // namespace
@@ -326,6 +357,41 @@ bigcn_status bigcn_spmm_csr_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                                           g, C8, ldc8, C16, ldc16, K, d, alpha, bias,
                                           act == BIGCN_ACT_RELU, out, ldo, plan,
                                           workspace, nullptr, s));
+}
+
+size_t bigcn_spmm_csr_q8_noalloc_max_bytes(void) { return kNoallocScratchBytes; }
+
+bigcn_status bigcn_spmm_csr_q8_noalloc(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                       const int32_t* colidx, bigcn_norm norm,
+                                       const float* g, const int8_t* C8, int64_t ldc8,
+                                       const void* C16, int64_t ldc16, int32_t K,
+                                       int32_t d, const float* alpha, const float* bias,
+                                       bigcn_act act, float* out, int64_t ldo,
+                                       void* stream) {
+  bigcn_status st = check_graph(n, nnz, rowptr, colidx, norm);
+  if (st != BIGCN_OK) return st;
+  if (K < 1 || d < 1 || ldc8 < q8_row(d) || ldc8 % 4 != 0 || ldc16 < q8_row(d))
+    return BIGCN_EINVAL;
+  st = check_spmm_operands(n, g, C16, BIGCN_F16, d, ldc16, alpha, bias, act, out, ldo);
+  if (st != BIGCN_OK) return st;
+  if (n > 0 && C8 == nullptr) return BIGCN_EINVAL;
+  if (!aligned(C8, 4)) return BIGCN_EALIGN;
+  if (!bigcn::q8_supported(n, d, K) || (uint64_t)n * ldc8 > 0xFFFFFFFFull ||
+      (uint64_t)n * ldc16 * 2 > 0xFFFFFFFFull)
+    return BIGCN_EUNSUPPORTED;
+  // Graphs of up to 67M entries get the plan bigcn_spmm_csr_q8 uses (the
+  // same chunks, hence the same sums); larger ones wider chunks.
+  const bigcn::SpmmPlan plan = bigcn::spmm_plan(n, nnz, d, kNoallocWorkers);
+  if (plan.bytes > kNoallocScratchBytes) return BIGCN_EWORKSPACE;
+  void* ws = nullptr;
+  if (n > 0 && nnz > 0) {
+    ws = device_scratch();
+    if (ws == nullptr) return BIGCN_EHIP;
+  }
+  return hip_status(bigcn::launch_spmm_q8(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN,
+                                          g, C8, ldc8, C16, ldc16, K, d, alpha, bias,
+                                          act == BIGCN_ACT_RELU, out, ldo, plan, ws, nullptr,
+                                          (hipStream_t)stream));
 }
 
 bigcn_status bigcn_spmm_csr_sage_q8(int64_t n, int64_t nnz, const int64_t* rowptr,

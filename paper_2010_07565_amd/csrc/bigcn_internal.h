@@ -92,7 +92,9 @@ struct SpmmPlan {
   size_t bytes;       // workspace bytes
   size_t off_rowof, off_tailrow, off_head, off_tail;
 };
-SpmmPlan spmm_plan(int64_t n, int64_t nnz, int32_t d);
+// max_workers caps the number of workers (chunks grow past 2048 edges when
+// needed), which bounds the workspace for a fixed-size scratch buffer.
+SpmmPlan spmm_plan(int64_t n, int64_t nnz, int32_t d, int64_t max_workers = INT64_MAX);
 
 // Builds the per-worker start rows (once per graph and chunk size).
 hipError_t launch_spmm_rows(int64_t n, int64_t nnz, const int64_t* rowptr,

@@ -2468,12 +2468,14 @@ hipError_t launch_bgemm_popcount(const uint64_t* F, int64_t M, int64_t ldf,
   return bgemm_pop_cn<1>(F, M, ldf, B, N, ldb, K, C, ct, ldc, stream);
 }
 
-SpmmPlan spmm_plan(int64_t n, int64_t nnz, int32_t d) {
+SpmmPlan spmm_plan(int64_t n, int64_t nnz, int32_t d, int64_t max_workers) {
   (void)n;
   SpmmPlan p;
   // About 16K workers on big graphs; chunks of 16 .. 2048 edges.
   int64_t chunk = 16;
   while (chunk < 2048 && chunk * 2 * 16384 <= nnz) chunk *= 2;
+  if (max_workers >= 1 && (nnz + chunk - 1) / chunk > max_workers)
+    chunk = (nnz + max_workers - 1) / max_workers;
   p.chunk = chunk;
   p.workers = nnz > 0 ? (nnz + chunk - 1) / chunk : 1;
   const int64_t slab = 4 * spmm_lanes(d);

@@ -211,6 +211,24 @@ def test_spmm_csr_q8_validation():
     assert f(*small_ws) == EWORKSPACE
 
 
+def test_spmm_csr_q8_noalloc_validation():
+    lib = bg.load()
+    assert lib.bigcn_spmm_csr_q8_noalloc_max_bytes() == 2 * 131072 + 2 * 33554432
+    f = lib.bigcn_spmm_csr_q8_noalloc
+    # n nnz rowptr colidx norm g C8 ldc8 C16 ldc16 K d alpha bias act out ldo stream
+    ok = [10, 40, FAKE, FAKE, 0, FAKE, FAKE, 64, FAKE, 64, 100, 7, FAKE, None, 0, FAKE, 7,
+          None]
+    for pos, val, want in [(7, 32, EINVAL), (9, 60, EINVAL), (10, 0, EINVAL),
+                           (11, 0, EINVAL), (6, FAKE + 2, EALIGN), (4, 5, EINVAL),
+                           (0, -1, EINVAL), (12, None, EINVAL), (14, 3, EINVAL)]:
+        args = list(ok)
+        args[pos] = val
+        assert f(*args) == want, (pos, val)
+    big = list(ok)
+    big[7], big[9], big[11], big[16] = 256, 260, 257, 257
+    assert f(*big) == EUNSUPPORTED
+
+
 def test_q8_layout_helpers():
     """Rows of 64 NB entries; column k at NB (k % 64) + k // 64, a bijection
     onto the first d... positions of the row for every width."""
