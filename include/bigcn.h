@@ -301,6 +301,27 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
                                   size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * bigcn_source_slots -- the source order bigcn_forward can store its
+ * per-node products and scales in (built once per graph, like the CSR).
+ * The aggregation of Eq. (13) reads one source row per edge; in a power-law
+ * graph most edges lead to a few high-degree nodes.  Listing nodes by
+ * descending degree class (class 0 for degree <= 1, else floor(log2
+ * degree)), by node id within a class, puts those nodes' rows and scales
+ * together in memory, so more of the gathers hit cache.
+ *   rowptr, colidx  the graph (as for bigcn_spmm_csr; degree = row count).
+ *   slot     int32[n] output: node i's position in that order.
+ *   colslot  int32[nnz] output: slot[colidx[e]].
+ *   workspace  bigcn_source_slots_workspace_bytes(n) bytes, 256-byte
+ *            aligned; contents on entry are ignored.
+ * Errors: EINVAL (n < 0, nnz < 0, n > INT32_MAX, NULL rowptr / slot with
+ *         n > 0, NULL colidx / colslot with nnz > 0), EALIGN, EWORKSPACE.
+ * ------------------------------------------------------------------------- */
+size_t bigcn_source_slots_workspace_bytes(int64_t n);
+bigcn_status bigcn_source_slots(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                const int32_t* colidx, int32_t* slot, int32_t* colslot,
+                                void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * bigcn_forward -- the whole multi-layer forward pass (Sec. 4.1):
  *     H^(0) = X,  H^(l+1) = act_l( Ã ζ^(l) + b_l ),  l = 0 .. n_layers-1,
  * every layer binarised (features and weights).  Layer 0 standardises X with
@@ -314,6 +335,13 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
  *   bias   fp32[d_out] or NULL;  act  output activation of the layer.
  *
  *   n, nnz, rowptr, colidx, norm   the graph, as for bigcn_spmm_csr.
+ *   slot, colslot  both NULL, or the source order of bigcn_source_slots
+ *        (device int32[n] and int32[nnz]): slot a permutation of [0, n),
+ *        colslot[e] = slot[colidx[e]].  Each layer then stores node i's
+ *        products and scale at row slot[i] of its internal buffers and the
+ *        aggregations gather by colslot; inputs and outputs keep the node
+ *        order, every sum keeps its terms and their order, and the result
+ *        is bit-identical to the call without them.  Ignored when nnz = 0.
  *   x    [n][ldx] fp32 node features, ldx >= layers[0].d_in.
  *   out  [n][ldo] fp32 result of the last layer, ldo >= last d_out.
  *   workspace  at least bigcn_forward_workspace_bytes(...) bytes, 256-byte
@@ -331,7 +359,9 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
  * norm must be MEAN; its products stay unfused (8-bit neighbour codes, exact
  * half self products, then bigcn_spmm_csr_sage_q8's aggregation).
  * Errors: as the per-step calls, plus EINVAL for inconsistent layer widths
- *         or n_layers < 1, or a GraphSAGE layer with norm SYM, EUNSUPPORTED
+ *         or n_layers < 1, only one of slot / colslot, or a GraphSAGE layer
+ *         with norm SYM, EALIGN for slot / colslot not 4-byte aligned,
+ *         EUNSUPPORTED
  *         for d_in > 8192 on a layer or a GraphSAGE layer outside the 8-bit
  *         shapes (d_out <= 256, d_in <= 2048).
  * ------------------------------------------------------------------------- */
@@ -355,7 +385,8 @@ size_t bigcn_forward_workspace_bytes(int64_t n, int64_t nnz,
                                      const bigcn_layer* layers,
                                      int32_t n_layers);
 bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
-                           const int32_t* colidx, bigcn_norm norm,
+                           const int32_t* colidx, const int32_t* slot,
+                           const int32_t* colslot, bigcn_norm norm,
                            const float* x, int64_t ldx, const float* mu,
                            const float* rstd, const bigcn_layer* layers,
                            int32_t n_layers, float* out, int64_t ldo,

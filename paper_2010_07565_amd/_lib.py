@@ -32,6 +32,7 @@ EXPORTS = ("bigcn_binarize_pack", "bigcn_bgemm", "bigcn_spmm_workspace_bytes",
            "bigcn_spmm_csr_sage_q8", "bigcn_layer_backward_workspace_bytes",
            "bigcn_layer_backward",
            "bigcn_forward_workspace_bytes", "bigcn_forward", "bigcn_check_csr",
+           "bigcn_source_slots_workspace_bytes", "bigcn_source_slots",
            "bigcn_status_string")
 
 
@@ -103,8 +104,12 @@ def load() -> ctypes.CDLL:
     lib.bigcn_check_csr.restype = _int
     lib.bigcn_check_csr.argtypes = [_i64, _i64, _p, _p, _p, _p]
     lib.bigcn_forward.restype = _int
-    lib.bigcn_forward.argtypes = [_i64, _i64, _p, _p, _int, _p, _i64, _p, _p,
+    lib.bigcn_forward.argtypes = [_i64, _i64, _p, _p, _p, _p, _int, _p, _i64, _p, _p,
                                   ctypes.POINTER(_Layer), _i32, _p, _i64, _p, _sz, _p]
+    lib.bigcn_source_slots_workspace_bytes.restype = _sz
+    lib.bigcn_source_slots_workspace_bytes.argtypes = [_i64]
+    lib.bigcn_source_slots.restype = _int
+    lib.bigcn_source_slots.argtypes = [_i64, _i64, _p, _p, _p, _p, _p, _sz, _p]
     _lib = lib
     return lib
 
@@ -368,16 +373,36 @@ def forward_workspace_bytes(n: int, nnz: int, layers: Sequence[Layer]) -> int:
     return load().bigcn_forward_workspace_bytes(n, nnz, _layers(layers), len(layers))
 
 
+def source_slots_workspace_bytes(n: int) -> int:
+    return load().bigcn_source_slots_workspace_bytes(n)
+
+
+def bigcn_source_slots(rowptr: torch.Tensor, colidx: torch.Tensor, slot: torch.Tensor,
+                       colslot: torch.Tensor, workspace: torch.Tensor,
+                       nnz: Optional[int] = None, stream=None) -> None:
+    """The source order of the forward pass: slot [n], colslot [nnz] (int32)."""
+    n = rowptr.shape[0] - 1
+    nnz = colidx.shape[0] if nnz is None else nnz
+    st = load().bigcn_source_slots(
+        n, nnz, _dev(rowptr, torch.int64, "rowptr"), _dev(colidx, torch.int32, "colidx"),
+        _dev(slot, torch.int32, "slot"), _dev(colslot, torch.int32, "colslot"),
+        _dev(workspace, torch.uint8, "workspace"),
+        workspace.numel() if workspace is not None else 0, _stream(stream))
+    _check("bigcn_source_slots", st)
+
+
 def bigcn_forward(rowptr: torch.Tensor, colidx: torch.Tensor, x: torch.Tensor,
                   layers: Sequence[Layer], out: torch.Tensor, workspace: torch.Tensor,
                   mu=None, rstd=None, norm: str = "sym", nnz: Optional[int] = None,
-                  stream=None) -> None:
-    """The whole forward pass into ``out`` [n, last d_out]."""
+                  stream=None, slot=None, colslot=None) -> None:
+    """The whole forward pass into ``out`` [n, last d_out]; slot / colslot
+    from bigcn_source_slots, or None for the node order."""
     n = rowptr.shape[0] - 1
     nnz = colidx.shape[0] if nnz is None else nnz
     arr = _layers(layers)
     st = load().bigcn_forward(
         n, nnz, _dev(rowptr, torch.int64, "rowptr"), _dev(colidx, torch.int32, "colidx"),
+        _dev(slot, torch.int32, "slot"), _dev(colslot, torch.int32, "colslot"),
         NORMS[norm], _dev(x, torch.float32, "x"), _ld(x, "x"),
         _dev(mu, torch.float32, "mu"), _dev(rstd, torch.float32, "rstd"),
         arr, len(layers), _dev(out, torch.float32, "out"), _ld(out, "out"),
@@ -427,11 +452,14 @@ class BiGCN:
     into a preallocated output with a preallocated workspace.  With
     ``weights_self_t`` (one W^T per layer, or None) the layers given are
     two-weight GraphSAGE layers: ``weights_t`` holds their neighbour
-    weights, the graph is A and ``norm`` must be "mean"."""
+    weights, the graph is A and ``norm`` must be "mean".  With
+    ``source_order`` (the default) the graph's source order is built once
+    (bigcn_source_slots) and every pass stores its per-node products in it;
+    the results are the same bit for bit."""
 
     def __init__(self, rowptr, colidx, weights_t, biases=None, acts=None,
                  norm: str = "sym", mu=None, rstd=None, device="cuda",
-                 weights_self_t=None):
+                 weights_self_t=None, source_order: bool = True):
         self.device = torch.device(device)
         self.rowptr = torch.as_tensor(rowptr, dtype=torch.int64, device=self.device)
         self.colidx = torch.as_tensor(colidx, dtype=torch.int32, device=self.device)
@@ -462,12 +490,23 @@ class BiGCN:
             self.layers.append(Layer(wt.shape[1], wt.shape[0], wbits, alpha, bt, a, wbs, als))
         self.ws = torch.empty(forward_workspace_bytes(self.n, self.nnz, self.layers),
                               dtype=torch.uint8, device=self.device)
+        self.slot = self.colslot = None
+        if source_order and self.n > 0 and self.nnz > 0:
+            self.slot = torch.empty(self.n, dtype=torch.int32, device=self.device)
+            self.colslot = torch.empty(self.nnz, dtype=torch.int32, device=self.device)
+            sws = torch.empty(max(1, source_slots_workspace_bytes(self.n)), dtype=torch.uint8,
+                              device=self.device)
+            bigcn_source_slots(self.rowptr, self.colidx, self.slot, self.colslot, sws,
+                               self.nnz)
+            torch.cuda.synchronize(self.device)
+            del sws
         self.out = torch.empty((self.n, self.layers[-1].d_out), dtype=torch.float32,
                                device=self.device)
 
     def forward(self, x: torch.Tensor, stream=None) -> torch.Tensor:
         bigcn_forward(self.rowptr, self.colidx, x, self.layers, self.out, self.ws,
-                      self.mu, self.rstd, self.norm, stream=stream)
+                      self.mu, self.rstd, self.norm, stream=stream, slot=self.slot,
+                      colslot=self.colslot)
         return self.out
 
     def capture(self, x: torch.Tensor):
@@ -480,7 +519,8 @@ class BiGCN:
         torch.cuda.synchronize()
         with torch.cuda.graph(graph):
             bigcn_forward(self.rowptr, self.colidx, x, self.layers, self.out, self.ws,
-                          self.mu, self.rstd, self.norm)
+                          self.mu, self.rstd, self.norm, slot=self.slot,
+                          colslot=self.colslot)
         torch.cuda.synchronize()
         self._graph = graph                     # keep the graph alive
 

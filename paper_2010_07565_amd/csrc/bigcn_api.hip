@@ -432,6 +432,27 @@ bigcn_status bigcn_spmm_csr_sage_q8(int64_t n, int64_t nnz, const int64_t* rowpt
                                           (hipStream_t)stream));
 }
 
+size_t bigcn_source_slots_workspace_bytes(int64_t n) {
+  if (n < 0) return 0;
+  return bigcn::source_slots_plan(n).bytes;
+}
+
+bigcn_status bigcn_source_slots(int64_t n, int64_t nnz, const int64_t* rowptr,
+                                const int32_t* colidx, int32_t* slot, int32_t* colslot,
+                                void* workspace, size_t ws_bytes, void* stream) {
+  if (n < 0 || nnz < 0 || n > INT32_MAX) return BIGCN_EINVAL;
+  if (n > 0 && (rowptr == nullptr || slot == nullptr)) return BIGCN_EINVAL;
+  if (nnz > 0 && (colidx == nullptr || colslot == nullptr)) return BIGCN_EINVAL;
+  if (!aligned(rowptr, 8) || !aligned(colidx, 4) || !aligned(slot, 4) || !aligned(colslot, 4))
+    return BIGCN_EALIGN;
+  if (n == 0) return BIGCN_OK;
+  if (workspace == nullptr || ws_bytes < bigcn::source_slots_plan(n).bytes)
+    return BIGCN_EWORKSPACE;
+  if (!aligned(workspace, 256)) return BIGCN_EALIGN;
+  return hip_status(bigcn::launch_source_slots(n, nnz, rowptr, colidx, slot, colslot,
+                                               workspace, (hipStream_t)stream));
+}
+
 size_t bigcn_forward_workspace_bytes(int64_t n, int64_t nnz,
                                      const bigcn_layer* layers, int32_t n_layers) {
   if (n < 0 || nnz < 0 || layers == nullptr || n_layers < 1) return 0;
@@ -443,7 +464,8 @@ size_t bigcn_forward_workspace_bytes(int64_t n, int64_t nnz,
 }
 
 bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
-                           const int32_t* colidx, bigcn_norm norm,
+                           const int32_t* colidx, const int32_t* slot,
+                           const int32_t* colslot, bigcn_norm norm,
                            const float* x, int64_t ldx, const float* mu,
                            const float* rstd, const bigcn_layer* layers,
                            int32_t n_layers, float* out, int64_t ldo,
@@ -451,6 +473,14 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
   if (layers == nullptr || n_layers < 1) return BIGCN_EINVAL;
   bigcn_status st = check_graph(n, nnz, rowptr, colidx, norm);
   if (st != BIGCN_OK) return st;
+  if ((slot == nullptr) != (colslot == nullptr)) return BIGCN_EINVAL;
+  if (!aligned(slot, 4) || !aligned(colslot, 4)) return BIGCN_EALIGN;
+  if (nnz == 0) {  // nothing is gathered: any order is the same
+    slot = nullptr;
+    colslot = nullptr;
+  }
+  // the aggregations gather sources by slot when a source order is given
+  const int32_t* gcol = colslot != nullptr ? colslot : colidx;
   for (int32_t l = 0; l < n_layers; ++l) {
     const bigcn_layer& ly = layers[l];
     if (ly.d_in < 1 || ly.d_out < 1 || ly.ldw < words(ly.d_in)) return BIGCN_EINVAL;
@@ -514,12 +544,13 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
       e = bigcn::launch_pack_bgemm_q8(hin, n, ly.d_in, ldin, l == 0 ? mu : nullptr,
                                       l == 0 ? rstd : nullptr, rowptr,
                                       norm == BIGCN_NORM_SYM, ly.wbits, ly.d_out, ly.ldw,
-                                      C8, q8_row(ly.d_out), C16, q8_row(ly.d_out), g, s);
+                                      C8, q8_row(ly.d_out), C16, q8_row(ly.d_out), g, s,
+                                      slot);
       if (e != hipSuccess) return BIGCN_EHIP;
     } else if (!have_products) {
       e = bigcn::launch_pack(hin, n, ly.d_in, ldin, l == 0 ? mu : nullptr,
                              l == 0 ? rstd : nullptr, rowptr, norm == BIGCN_NORM_SYM,
-                             F, L.ldF, g, s);
+                             F, L.ldF, g, s, slot);
       if (e != hipSuccess) return BIGCN_EHIP;
       if (q8)
         e = bigcn::launch_bgemm_q8(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C8,
@@ -541,6 +572,7 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
     if (q8) {
       bigcn::FusedNext fn = {};
       fn.kind = kind;
+      fn.slot = slot;
       if (ly.wbits_self != nullptr) {
         fn.kind = 2;
         fn.Cself = ws + L.off_S;
@@ -558,12 +590,12 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
         fn.ldc16 = q8_row(nxt.d_out);
         fn.g = (float*)(ws + L.off_g[nset]);
       }
-      e = bigcn::launch_spmm_q8(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN, g, C8,
+      e = bigcn::launch_spmm_q8(n, nnz, rowptr, gcol, norm == BIGCN_NORM_MEAN, g, C8,
                                 q8_row(ly.d_out), C16, q8_row(ly.d_out), ly.d_in, ly.d_out,
                                 ly.alpha, ly.bias,
                                 ly.act == BIGCN_ACT_RELU, hout, ldout, plan, wsp, &fn, s);
     } else {
-      e = bigcn::launch_spmm(n, nnz, rowptr, colidx, norm == BIGCN_NORM_MEAN, g, C16, ct,
+      e = bigcn::launch_spmm(n, nnz, rowptr, gcol, norm == BIGCN_NORM_MEAN, g, C16, ct,
                              ly.d_out, L.ldc16, ly.alpha, ly.bias, ly.act == BIGCN_ACT_RELU,
                              hout, ldout, plan, wsp, s);
     }

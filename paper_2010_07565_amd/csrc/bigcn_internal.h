@@ -16,11 +16,14 @@ enum class IType : int { I32 = 0, I16 = 1, F16 = 2, F32 = 3 };
 inline size_t itype_size(IType t) { return (t == IType::I32 || t == IType::F32) ? 4 : 2; }
 
 // Sign-pack rows of x; see bigcn_binarize_pack.  sym != 0 folds D̂^-1/2 into
-// the scale when rowptr is given.
+// the scale when rowptr is given.  With slot (a permutation of [0, rows))
+// row r's bits and scale are written to row slot[r] (the source order of
+// the forward pass); the degree for D̂ is still row r's.
 hipError_t launch_pack(const float* x, int64_t rows, int32_t cols, int64_t ldx,
                        const float* mu, const float* rstd,
                        const int64_t* rowptr, int sym, uint64_t* bits,
-                       int64_t ldw, float* scale, hipStream_t stream);
+                       int64_t ldw, float* scale, hipStream_t stream,
+                       const int32_t* slot = nullptr);
 
 // C[i][j] = K - 2 popcount(F_i ^ B_j) on the vector ALUs.
 hipError_t launch_bgemm_popcount(const uint64_t* F, int64_t M, int64_t ldf,
@@ -52,7 +55,8 @@ hipError_t launch_pack_bgemm_q8(const float* x, int64_t rows, int32_t cols, int6
                                 const float* mu, const float* rstd, const int64_t* rowptr,
                                 int sym, const uint64_t* B, int32_t N, int64_t ldb,
                                 int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
-                                float* g, hipStream_t stream);
+                                float* g, hipStream_t stream,
+                                const int32_t* slot = nullptr);
 hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
                            const uint64_t* B, int32_t N, int64_t ldb, int32_t K,
                            int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
@@ -80,6 +84,9 @@ struct FusedNext {
   const void* Cself;      // kind 2
   int64_t ldself;
   const float* alpha_self;
+  // Source order (nullable): row r's next-layer products (kind 1) or self
+  // products and scale (kind 2) sit at row slot[r].
+  const int32_t* slot;
 };
 
 // Aggregation over the CSR of Â with the fused rescale / bias / activation
@@ -120,5 +127,19 @@ hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                           const float* bias, int relu, float* out, int64_t ldo,
                           const SpmmPlan& plan, void* workspace,
                           const FusedNext* next, hipStream_t stream);
+
+// Source order of the forward pass (see bigcn_source_slots): slot[i] for
+// every node, colslot[e] = slot[colidx[e]]; workspace of SlotPlan::bytes.
+struct SlotPlan {
+  int64_t groups;   // groups of 64 nodes
+  int64_t total;    // class counts, 32 per group
+  int64_t blocks;   // scan blocks of 1024 counts
+  size_t off_sums;  // byte offset of the block sums
+  size_t bytes;
+};
+SlotPlan source_slots_plan(int64_t n);
+hipError_t launch_source_slots(int64_t n, int64_t nnz, const int64_t* rowptr,
+                               const int32_t* colidx, int32_t* slot, int32_t* colslot,
+                               void* workspace, hipStream_t stream);
 
 }  // namespace bigcn

@@ -79,14 +79,15 @@ __global__ __launch_bounds__(kBlock) void k_pack(
     const float* __restrict__ x, int64_t rows, int32_t cols, int64_t ldx,
     const float* __restrict__ mu, const float* __restrict__ rstd,
     const int64_t* __restrict__ rowptr, int sym, uint64_t* __restrict__ bits,
-    int64_t ldw, float* __restrict__ scale) {
+    int64_t ldw, float* __restrict__ scale, const int32_t* __restrict__ slot) {
   const int lane = threadIdx.x & 63;
   const int64_t nwaves = (int64_t)gridDim.x * kWavesPerBlock;
   const int kw = (cols + 63) >> 6;
   for (int64_t r = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
        r < rows; r += nwaves) {
     const float* xr = x + r * ldx;
-    uint64_t* br = bits + r * ldw;
+    const int64_t dst = slot != nullptr ? (int64_t)slot[r] : r;
+    uint64_t* br = bits + dst * ldw;
     float l1 = 0.f;
     for (int64_t wb = 0; wb < ldw; wb += 64) {
       // Lane q keeps word wb + q of this batch of 64 words.
@@ -135,7 +136,7 @@ __global__ __launch_bounds__(kBlock) void k_pack(
         const int64_t dg = rowptr[r + 1] - rowptr[r];
         s = s * (dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f);
       }
-      scale[r] = s;
+      scale[dst] = s;
     }
   }
 }
@@ -153,6 +154,8 @@ constexpr int64_t kPackRowsMaxLd = (int64_t)1 << 24;
 // in place (lane j: output j, its weight words in registers, the row's words
 // being the ballots): the 8-bit half-codes, exact rows and flags of
 // k_bgemm_pop_q8 (one byte per column) are written instead of the bits.
+// With slot != nullptr row r's results go to row slot[r] of bits / scale /
+// codes (the source order of the aggregation); else to row r.
 
 template <bool STD, int RW, int KWT, bool FQ>
 __global__ __launch_bounds__(kBlock) void k_pack_rows(
@@ -161,7 +164,7 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
     const int64_t* __restrict__ rowptr, int sym, uint64_t* __restrict__ bits,
     int64_t ldw, float* __restrict__ scale, const uint64_t* __restrict__ B, int32_t N,
     int64_t ldb, int8_t* __restrict__ C8, int64_t ldc8, _Float16* __restrict__ C16,
-    int64_t ldc16) {
+    int64_t ldc16, const int32_t* __restrict__ slot) {
   // Column statistics: in registers (lane l keeps columns 64 w + l) up to
   // 16 words, so the first row loads need not wait for a block barrier;
   // in LDS (mu[0..cols), rstd[cols..2 cols)) for wider rows.
@@ -224,6 +227,9 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
       const int64_t rq = r0 + (lane < nq ? lane : 0);
       dg = rowptr[rq + 1] - rowptr[rq];
     }
+    // lane q < nq: the output row of row r0 + q
+    int32_t dq = 0;
+    if (slot != nullptr) dq = slot[r0 + (lane < nq ? lane : 0)];
     float l1[RW];
     uint64_t mine = 0;  // lane ldw q + w: word w of row q (pad words stay zero)
     int pc[RW];  // FQ: lane j's popcount of row XOR weights
@@ -271,20 +277,29 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
       if (r >= rows) break;  // wave-uniform
       if (lane == q) myl1 = l1[q];
       if constexpr (FQ) {
+        const int64_t dr = slot != nullptr ? (int64_t)__builtin_amdgcn_readlane(dq, q) : r;
         const int dot = cols - 2 * pc[q];
         const int code = (dot - (cols & 1)) >> 1;
-        C8[r * ldc8 + lane] = (int8_t)code;
+        C8[dr * ldc8 + lane] = (int8_t)code;
         const bool flag =
             __builtin_amdgcn_ballot_w64(lane < N && (code < -128 || code > 127)) != 0;
-        if (flag) C16[r * ldc16 + lane] = (_Float16)dot;
+        if (flag) C16[dr * ldc16 + lane] = (_Float16)dot;
         if (lane == q) myflag = flag;
       }
     }
-    if (!FQ && lane < nq * ldw) bits[r0 * ldw + lane] = mine;
+    if constexpr (!FQ) {
+      if (slot == nullptr) {
+        if (lane < nq * ldw) bits[r0 * ldw + lane] = mine;
+      } else {  // word lane % ldw of row lane / ldw, at that row's slot
+        const int q = lane / (int)ldw;
+        const int dr = __builtin_amdgcn_ds_bpermute((q < RW ? q : 0) * 4, dq);  // all lanes
+        if (lane < nq * ldw) bits[(int64_t)dr * ldw + (lane - q * (int)ldw)] = mine;
+      }
+    }
     if (lane < nq) {
       float sc = myl1 / (float)cols;
       if (rowptr != nullptr && sym) sc = sc * (dg > 0 ? 1.0f / sqrtf((float)dg) : 0.f);
-      scale[r0 + lane] = myflag ? -fabsf(sc) : sc;
+      scale[slot != nullptr ? (int64_t)dq : r0 + lane] = myflag ? -fabsf(sc) : sc;
     }
   }
 }
@@ -1094,6 +1109,8 @@ struct NextLayer {
   const _Float16* Cself;  // NX == 2: self products [n][ldself], natural order
   int64_t ldself;
   const float* gself;     // NX == 2: per-node scale (its magnitude is β_i)
+  const int32_t* slot;    // nullable: row r's next products / self products
+                          // sit at row slot[r] (the source order), else at r
 };
 
 struct EpiIL {
@@ -1109,12 +1126,14 @@ __device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4
                                   const EpiIL& ep, float* __restrict__ out, int64_t ldo,
                                   const NextLayer& nx, int lane) {
   const float rowfac = deg > 0 ? row_factor_deg(deg, mean) : 0.f;
+  int64_t dst = r;  // row of the next products / self products
+  if (NX != 0 && nx.slot != nullptr) dst = nx.slot[r];
   float self[NB];
   if (NX == 2) {
-    const float gi = fabsf(nx.gself[r]);
+    const float gi = fabsf(nx.gself[dst]);
 #pragma unroll
     for (int c = 0; c < NB; ++c)
-      self[c] = ep.valid[c] ? gi * ep.alpha_s[c] * (float)nx.Cself[r * nx.ldself + lane + 64 * c]
+      self[c] = ep.valid[c] ? gi * ep.alpha_s[c] * (float)nx.Cself[dst * nx.ldself + lane + 64 * c]
                             : 0.f;
   }
   float v[NB];
@@ -1165,10 +1184,10 @@ __device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4
     big |= (lane + 64 * c < nx.dn) && (code < -128 || code > 127);
     packed |= (uint32_t)(uint8_t)(int8_t)code << (8 * c);
   }
-  store_codes<NBN>(nx.C8 + r * nx.ldc8 + NBN * lane, packed);
+  store_codes<NBN>(nx.C8 + dst * nx.ldc8 + NBN * lane, packed);
   const bool flag = __builtin_amdgcn_ballot_w64(big) != 0;
-  if (flag) store_exact<NBN>(nx.C16 + r * nx.ldc16 + NBN * lane, dot);
-  if (lane == 0) nx.g[r] = flag ? -sc : sc;
+  if (flag) store_exact<NBN>(nx.C16 + dst * nx.ldc16 + NBN * lane, dot);
+  if (lane == 0) nx.g[dst] = flag ? -sc : sc;
 }
 
 template <int NB>
@@ -1668,8 +1687,10 @@ __device__ inline void finish_slot(int64_t r, int64_t deg, int mean, const float
                                    const uint64_t* s_bn) {
   static_assert(CPL * G <= 64 && CPL <= 16 && CPL % 4 == 0, "narrow layout");
   const float rowfac = deg > 0 ? row_factor_deg(deg, mean) : 0.f;
+  int64_t dst = r;  // row of the next products / self products
+  if (NX != 0 && nx.slot != nullptr) dst = nx.slot[r];
   float gi = 0.f;
-  if (NX == 2) gi = fabsf(nx.gself[r]);
+  if (NX == 2) gi = fabsf(nx.gself[dst]);
   // this lane's constants in 16-byte LDS reads, all issued before any use
   const float* al = ep.s_alpha + CPL * c;
   float av[CPL], bv[CPL], sv[NX == 2 ? CPL : 1];
@@ -1694,7 +1715,7 @@ __device__ inline void finish_slot(int64_t r, int64_t deg, int mean, const float
     const bool ok = (ep.valid >> k) & 1;
     float t = deg > 0 ? fmaf(sum[k], rowfac * av[k], bv[k]) : bv[k];
     if (NX == 2)
-      t += ok ? gi * sv[k] * (float)nx.Cself[r * nx.ldself + CPL * c + k] : 0.f;
+      t += ok ? gi * sv[k] * (float)nx.Cself[dst * nx.ldself + CPL * c + k] : 0.f;
     v[k] = act(t, ep.relu);
   }
   if (NX != 1 || out != nullptr) {
@@ -1747,9 +1768,9 @@ __device__ inline void finish_slot(int64_t r, int64_t deg, int mean, const float
     const uint64_t z = word ^ s_bn[kq];
     const int pc = __builtin_popcount((uint32_t)z) + __builtin_popcount((uint32_t)(z >> 32));
     const int code = ((Kn - 2 * pc) - par) >> 1;
-    nx.C8[r * nx.ldc8 + nbn * (kq & 63) + (kq >> 6)] = (int8_t)code;
+    nx.C8[dst * nx.ldc8 + nbn * (kq & 63) + (kq >> 6)] = (int8_t)code;
   }
-  if (c == 0) nx.g[r] = sc;
+  if (c == 0) nx.g[dst] = sc;
 }
 
 template <int G, int CPL, int NX>
@@ -2349,6 +2370,7 @@ hipError_t spmm_dispatch_l(int64_t n, int64_t nnz, const int64_t* rowptr,
 
 // Fused binary GEMM of the FQ variant (unused otherwise).
 struct PackQ8 {
+  const int32_t* slot = nullptr;  // output row order (nullable)
   const uint64_t* B = nullptr;
   int32_t N = 0;
   int64_t ldb = 0;
@@ -2371,7 +2393,7 @@ hipError_t pack_rows_launch(const float* x, int64_t rows, int32_t cols, int64_t 
   const size_t lds = (STD && KWT > 16) ? (size_t)2 * cols * sizeof(float) : 0;
   hipLaunchKernelGGL((k_pack_rows<STD, RW, KWT, FQ>), grid, dim3(kBlock), lds, stream, x,
                      rows, cols, ldx, mu, rstd, rowptr, sym, bits, ldw, scale, pq.B, pq.N,
-                     pq.ldb, pq.C8, pq.ldc8, pq.C16, pq.ldc16);
+                     pq.ldb, pq.C8, pq.ldc8, pq.C16, pq.ldc16, pq.slot);
   return hipGetLastError();
 }
 
@@ -2401,26 +2423,28 @@ hipError_t pack_rows_dispatch(const float* x, int64_t rows, int32_t cols, int64_
 hipError_t launch_pack(const float* x, int64_t rows, int32_t cols, int64_t ldx,
                        const float* mu, const float* rstd,
                        const int64_t* rowptr, int sym, uint64_t* bits,
-                       int64_t ldw, float* scale, hipStream_t stream) {
+                       int64_t ldw, float* scale, hipStream_t stream, const int32_t* slot) {
   if (rows == 0) return hipSuccess;
   const int kw = (cols + 63) >> 6;
   // k_pack_rows writes a group's words with one lane per word (RW * ldw <=
   // 64 for the RW its dispatch picks from kw)
   const int rw = kw <= 2 ? 8 : kw <= 4 ? 4 : kw <= 8 ? 2 : 1;
   if (kw <= 32 && ldx <= kPackRowsMaxLd && rw * ldw <= 64) {
+    PackQ8 pq;
+    pq.slot = slot;
     if (mu != nullptr)
       return pack_rows_dispatch<true>(x, rows, cols, ldx, mu, rstd, rowptr, sym, bits,
-                                      ldw, scale, stream);
+                                      ldw, scale, stream, pq);
     return pack_rows_dispatch<false>(x, rows, cols, ldx, mu, rstd, rowptr, sym, bits,
-                                     ldw, scale, stream);
+                                     ldw, scale, stream, pq);
   }
   dim3 grid(grid_cap((rows + kWavesPerBlock - 1) / kWavesPerBlock, 8192));
   if (mu != nullptr)
     hipLaunchKernelGGL(k_pack<true>, grid, dim3(kBlock), 0, stream, x, rows, cols,
-                       ldx, mu, rstd, rowptr, sym, bits, ldw, scale);
+                       ldx, mu, rstd, rowptr, sym, bits, ldw, scale, slot);
   else
     hipLaunchKernelGGL(k_pack<false>, grid, dim3(kBlock), 0, stream, x, rows,
-                       cols, ldx, mu, rstd, rowptr, sym, bits, ldw, scale);
+                       cols, ldx, mu, rstd, rowptr, sym, bits, ldw, scale, slot);
   return hipGetLastError();
 }
 
@@ -2436,9 +2460,10 @@ hipError_t launch_pack_bgemm_q8(const float* x, int64_t rows, int32_t cols, int6
                                 const float* mu, const float* rstd, const int64_t* rowptr,
                                 int sym, const uint64_t* B, int32_t N, int64_t ldb,
                                 int8_t* C8, int64_t ldc8, void* C16, int64_t ldc16,
-                                float* g, hipStream_t stream) {
+                                float* g, hipStream_t stream, const int32_t* slot) {
   if (rows == 0) return hipSuccess;
   PackQ8 pq;
+  pq.slot = slot;
   pq.B = B;
   pq.N = N;
   pq.ldb = ldb;
@@ -2589,6 +2614,7 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   nx.ldc16 = fn.ldc16;
   nx.g = fn.g;
   nx.sym = !mean;
+  nx.slot = fn.slot;
   nx.Cself = (const _Float16*)fn.Cself;
   nx.ldself = fn.ldself;
   nx.gself = g;
@@ -2658,6 +2684,7 @@ hipError_t spmm_narrow_gc(int64_t n, const int64_t* rowptr, const int32_t* colid
   nx.ldc16 = fn.ldc16;
   nx.g = fn.g;
   nx.sym = !mean;
+  nx.slot = fn.slot;
   nx.Cself = (const _Float16*)fn.Cself;
   nx.ldself = fn.ldself;
   nx.gself = g;
@@ -2740,6 +2767,180 @@ hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
       return spmm_q8_nb<4>(n, nnz, rowptr, colidx, mean, g, C8, ldc8, C16, ldc16, K, d,
                            alpha, bias, relu, out, ldo, p, ws, fn, stream);
   }
+}
+
+// ------------------------------------------------------ source order ----
+//
+// The forward pass stores each node's products and scale at a slot: nodes
+// listed by descending degree class (class 0 for degree <= 1, else
+// floor(log2 degree)), by node id within a class.  The aggregation gathers
+// a source row per edge; in a power-law graph most gathers hit a small set
+// of high-degree nodes, and with them first their rows and scales share
+// cache lines, so a gather hits the XCD's L2 more often.  Destination rows
+// keep their order, so no input or output moves and every sum keeps its
+// terms and their order.
+//
+// One wave per group of 64 consecutive nodes counts its nodes per class;
+// an exclusive scan over (class descending, group ascending) gives each
+// (class, group) its first slot; each node then takes that slot plus the
+// number of lower lanes of its group in its class.
+
+constexpr int kSlotClasses = 32;
+
+__device__ inline int degree_class(int64_t deg) {
+  return deg <= 1 ? 0 : 63 - __builtin_clzll((uint64_t)deg);
+}
+
+// counts[(31 - c) * groups + w] = nodes of group w in class c.
+__global__ __launch_bounds__(kBlock) void k_slot_count(int64_t n,
+                                                       const int64_t* __restrict__ rowptr,
+                                                       int64_t groups,
+                                                       int32_t* __restrict__ counts) {
+  const int lane = threadIdx.x & 63;
+  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
+  if (w >= groups) return;
+  const int64_t i = w * 64 + lane;
+  const int cls = i < n ? degree_class(rowptr[i + 1] - rowptr[i]) : -1;
+  int mine = 0;
+#pragma unroll 4
+  for (int c = 0; c < kSlotClasses; ++c) {
+    const int cnt = (int)__builtin_popcountll(__builtin_amdgcn_ballot_w64(cls == c));
+    if (lane == c) mine = cnt;
+  }
+  if (lane < kSlotClasses) counts[(int64_t)(kSlotClasses - 1 - lane) * groups + w] = mine;
+}
+
+// Exclusive scan of v[0, total), in place, in three passes: block sums of
+// 1024 entries, a scan of those sums by one block, then each block's scan
+// plus its offset.  Entries and sums stay below 2^31 (at most n nodes).
+constexpr int kScanPer = 4;
+constexpr int kScanTile = kBlock * kScanPer;
+
+__device__ inline int32_t block_exclusive_scan(int32_t v, int32_t* s_tmp, int32_t& total) {
+  const int t = threadIdx.x;
+  s_tmp[t] = v;
+  __syncthreads();
+  for (int off = 1; off < kBlock; off <<= 1) {
+    const int32_t add = t >= off ? s_tmp[t - off] : 0;
+    __syncthreads();
+    s_tmp[t] += add;
+    __syncthreads();
+  }
+  total = s_tmp[kBlock - 1];
+  const int32_t incl = s_tmp[t];
+  __syncthreads();
+  return incl - v;
+}
+
+__global__ __launch_bounds__(kBlock) void k_scan_sums(const int32_t* __restrict__ v,
+                                                      int64_t total,
+                                                      int32_t* __restrict__ sums) {
+  __shared__ int32_t s_tmp[kBlock];
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanPer;
+  int32_t acc = 0;
+#pragma unroll
+  for (int u = 0; u < kScanPer; ++u) acc += base + u < total ? v[base + u] : 0;
+  int32_t sum;
+  block_exclusive_scan(acc, s_tmp, sum);
+  if (threadIdx.x == 0) sums[blockIdx.x] = sum;
+}
+
+__global__ __launch_bounds__(kBlock) void k_scan_top(int32_t* __restrict__ sums, int64_t nb) {
+  __shared__ int32_t s_tmp[kBlock];
+  const int64_t per = (nb + kBlock - 1) / kBlock;
+  const int64_t b0 = (int64_t)threadIdx.x * per;
+  int32_t acc = 0;
+  for (int64_t b = b0; b < b0 + per && b < nb; ++b) acc += sums[b];
+  int32_t total;
+  int32_t run = block_exclusive_scan(acc, s_tmp, total);
+  for (int64_t b = b0; b < b0 + per && b < nb; ++b) {
+    const int32_t x = sums[b];
+    sums[b] = run;
+    run += x;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_scan_apply(int32_t* __restrict__ v, int64_t total,
+                                                       const int32_t* __restrict__ sums) {
+  __shared__ int32_t s_tmp[kBlock];
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanPer;
+  int32_t x[kScanPer];
+  int32_t acc = 0;
+#pragma unroll
+  for (int u = 0; u < kScanPer; ++u) {
+    x[u] = base + u < total ? v[base + u] : 0;
+    acc += x[u];
+  }
+  int32_t unused;
+  int32_t run = sums[blockIdx.x] + block_exclusive_scan(acc, s_tmp, unused);
+#pragma unroll
+  for (int u = 0; u < kScanPer; ++u) {
+    if (base + u < total) v[base + u] = run;
+    run += x[u];
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_slot_scatter(int64_t n,
+                                                         const int64_t* __restrict__ rowptr,
+                                                         int64_t groups,
+                                                         const int32_t* __restrict__ first,
+                                                         int32_t* __restrict__ slot) {
+  const int lane = threadIdx.x & 63;
+  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block();
+  if (w >= groups) return;
+  const int64_t i = w * 64 + lane;
+  const int cls = i < n ? degree_class(rowptr[i + 1] - rowptr[i]) : -1;
+  const uint64_t below = (1ull << lane) - 1;
+  int rank = 0;
+#pragma unroll 4
+  for (int c = 0; c < kSlotClasses; ++c) {
+    const uint64_t m = __builtin_amdgcn_ballot_w64(cls == c);
+    if (cls == c) rank = (int)__builtin_popcountll(m & below);
+  }
+  if (i < n) slot[i] = first[(int64_t)(kSlotClasses - 1 - cls) * groups + w] + rank;
+}
+
+__global__ __launch_bounds__(kBlock) void k_colslot(int64_t nnz,
+                                                    const int32_t* __restrict__ colidx,
+                                                    const int32_t* __restrict__ slot,
+                                                    int32_t* __restrict__ colslot) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < nnz; e += stride)
+    colslot[e] = slot[colidx[e]];
+}
+
+SlotPlan source_slots_plan(int64_t n) {
+  SlotPlan p;
+  p.groups = (n + 63) / 64;
+  p.total = p.groups * kSlotClasses;
+  p.blocks = (p.total + kScanTile - 1) / kScanTile;
+  auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
+  p.off_sums = up((size_t)p.total * 4);
+  p.bytes = p.off_sums + up((size_t)(p.blocks > 0 ? p.blocks : 1) * 4);
+  return p;
+}
+
+hipError_t launch_source_slots(int64_t n, int64_t nnz, const int64_t* rowptr,
+                               const int32_t* colidx, int32_t* slot, int32_t* colslot,
+                               void* ws, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  const SlotPlan p = source_slots_plan(n);
+  int32_t* counts = (int32_t*)ws;
+  int32_t* sums = (int32_t*)((char*)ws + p.off_sums);
+  const dim3 wgrid((unsigned)((p.groups + kWavesPerBlock - 1) / kWavesPerBlock));
+  hipLaunchKernelGGL(k_slot_count, wgrid, dim3(kBlock), 0, stream, n, rowptr, p.groups,
+                     counts);
+  hipLaunchKernelGGL(k_scan_sums, dim3((unsigned)p.blocks), dim3(kBlock), 0, stream, counts,
+                     p.total, sums);
+  hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, stream, sums, p.blocks);
+  hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)p.blocks), dim3(kBlock), 0, stream, counts,
+                     p.total, sums);
+  hipLaunchKernelGGL(k_slot_scatter, wgrid, dim3(kBlock), 0, stream, n, rowptr, p.groups,
+                     counts, slot);
+  if (nnz > 0)
+    hipLaunchKernelGGL(k_colslot, dim3(grid_cap((nnz + kBlock - 1) / kBlock, 8192)),
+                       dim3(kBlock), 0, stream, nnz, colidx, slot, colslot);
+  return hipGetLastError();
 }
 
 bool bgemm_mfma_supported(int32_t N, int32_t K) { return N >= 1 && N <= 256 && K >= 1; }

@@ -110,28 +110,54 @@ def test_forward_validation():
     n, nnz = 50, 200
     need = lib.bigcn_forward_workspace_bytes(n, nnz, layers, 2)
     assert need > 0
-    args = [n, nnz, FAKE, FAKE, 0, FAKE, 100, None, None, layers, 2, FAKE, 4, FAKE,
-            need, None]
+    # n nnz rowptr colidx slot colslot norm x ldx mu rstd layers nl out ldo ws bytes stream
+    args = [n, nnz, FAKE, FAKE, None, None, 0, FAKE, 100, None, None, layers, 2, FAKE, 4,
+            FAKE, need, None]
     a = list(args)
-    a[14] = need - 1
+    a[16] = need - 1
     assert lib.bigcn_forward(*a) == EWORKSPACE
     a = list(args)
-    a[10] = 0
+    a[12] = 0
     assert lib.bigcn_forward(*a) == EINVAL
     bad = (L * 2)(L(100, 16, FAKE, 2, FAKE, None, 0), L(15, 4, FAKE, 1, FAKE, None, 0))
     a = list(args)
-    a[9] = bad
+    a[11] = bad
     assert lib.bigcn_forward(*a) == EINVAL        # widths do not chain
     short = (L * 2)(L(100, 16, FAKE, 1, FAKE, None, 0), L(16, 4, FAKE, 1, FAKE, None, 0))
     a = list(args)
-    a[9] = short
+    a[11] = short
     assert lib.bigcn_forward(*a) == EINVAL        # ldw < ceil(100/64)
     a = list(args)
-    a[6] = 99
+    a[8] = 99
     assert lib.bigcn_forward(*a) == EINVAL        # ldx < d_in
     a = list(args)
-    a[13] = FAKE + 128
+    a[15] = FAKE + 128
     assert lib.bigcn_forward(*a) == EALIGN        # workspace alignment
+    a = list(args)
+    a[4] = FAKE
+    assert lib.bigcn_forward(*a) == EINVAL        # slot without colslot
+    a[5] = FAKE + 2
+    assert lib.bigcn_forward(*a) == EALIGN        # colslot alignment
+
+
+def test_source_slots_validation():
+    lib = bg.load()
+    f = lib.bigcn_source_slots
+    n, nnz = 1000, 5000
+    need = lib.bigcn_source_slots_workspace_bytes(n)
+    # 16 groups of 64 nodes x 32 classes of int32, then one block sum
+    assert need == 2048 + 256
+    assert lib.bigcn_source_slots_workspace_bytes(0) > 0
+    ok = [n, nnz, FAKE, FAKE, FAKE, FAKE, FAKE, need, None]
+    for pos, val, want in [(0, -1, EINVAL), (1, -1, EINVAL), (2, None, EINVAL),
+                           (4, None, EINVAL), (5, None, EINVAL), (3, None, EINVAL),
+                           (7, need - 1, EWORKSPACE), (6, None, EWORKSPACE),
+                           (6, FAKE + 64, EALIGN), (4, FAKE + 2, EALIGN),
+                           (0, 1 << 31, EINVAL)]:
+        args = list(ok)
+        args[pos] = val
+        assert f(*args) == want, (pos, val)
+    assert f(0, 0, None, None, None, None, None, 0, None) == 0     # empty graph
 
 
 def test_workspace_queries_grow_with_size():
@@ -267,11 +293,11 @@ def test_forward_rejects_sage_layer_with_symmetric_norm():
     L = _lib._Layer
     layers = (L * 1)(L(100, 16, FAKE, 2, FAKE, None, 0, FAKE, 2, FAKE))
     need = lib.bigcn_forward_workspace_bytes(50, 200, layers, 1)
-    args = [50, 200, FAKE, FAKE, 0, FAKE, 100, None, None, layers, 1, FAKE, 16, FAKE,
-            need, None]
+    args = [50, 200, FAKE, FAKE, None, None, 0, FAKE, 100, None, None, layers, 1, FAKE, 16,
+            FAKE, need, None]
     assert lib.bigcn_forward(*args) == EINVAL        # GraphSAGE needs norm MEAN
     short = (L * 1)(L(100, 16, FAKE, 2, FAKE, None, 0, FAKE, 1, FAKE))
-    args[4], args[9] = 1, short
+    args[6], args[11] = 1, short
     assert lib.bigcn_forward(*args) == EINVAL        # ldw_self < ceil(100/64)
 
 

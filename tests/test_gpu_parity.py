@@ -676,3 +676,76 @@ def test_sage_forward_equals_chained_and_oracle(dev):
         fc = flips & clean[:, None]
         assert np.all(np.abs(z[fc]) <= TOL * m[fc] + 1e-30), "sign flip away from zero"
         flipped = flipped | flips.any(axis=1)
+
+
+# ------------------------------------------------------------ source order --
+
+def _expected_slots(g):
+    """Stable order by descending degree class (0 for degree <= 1, else
+    floor(log2 degree)), written with numpy: slot[i] = position of node i."""
+    deg = np.diff(g.rowptr)
+    cls = np.where(deg <= 1, 0, np.floor(np.log2(np.maximum(deg, 1))).astype(np.int64))
+    order = np.argsort(-cls, kind="stable")
+    slot = np.empty(g.n, dtype=np.int64)
+    slot[order] = np.arange(g.n)
+    return slot
+
+
+def _graph_kinds(rng):
+    yield workloads.random_small_graph(1, 0, rng)
+    yield workloads.random_small_graph(63, 100, rng, isolated=5)
+    yield workloads.random_small_graph(200, 900, rng, isolated=7)
+    yield _star_plus_random(3001, rng)
+    yield _with_empty_rows(rng)
+    yield workloads.rmat_graph(50_000, 400_000, 99)
+
+
+def test_source_slots_match_stable_degree_order(dev):
+    rng = np.random.default_rng(314)
+    for g in _graph_kinds(rng):
+        slot = torch.empty(g.n, dtype=torch.int32, device=dev)
+        colslot = torch.empty(max(g.nnz, 1), dtype=torch.int32, device=dev)
+        ws = torch.empty(bg.source_slots_workspace_bytes(g.n), dtype=torch.uint8, device=dev)
+        bg.bigcn_source_slots(_t(g.rowptr, dev), _t(g.colidx, dev), slot, colslot, ws,
+                              nnz=g.nnz)
+        torch.cuda.synchronize()
+        want = _expected_slots(g)
+        got = slot.cpu().numpy().astype(np.int64)
+        assert np.array_equal(got, want), g.n
+        assert np.array_equal(colslot[:g.nnz].cpu().numpy(), want[g.colidx]), g.n
+
+
+@pytest.mark.parametrize("case", ["gcn_q8", "gcn_exact", "gcn_relu_mean", "sage"])
+def test_forward_in_source_order_is_bit_identical(dev, case):
+    """bigcn_forward with the source order equals the node order bit for
+    bit: every sum keeps its terms and their order."""
+    rng = np.random.default_rng({"gcn_q8": 1, "gcn_exact": 2, "gcn_relu_mean": 3,
+                                 "sage": 4}[case])
+    if case == "sage":
+        g = _sage_graph(1500, rng)
+    else:
+        g = _star_plus_random(2500, rng)
+    dims, acts, norm = {"gcn_q8": ([130, 256, 256, 40], None, "sym"),
+                        "gcn_exact": ([2100, 300, 47], ["relu", "none"], "sym"),
+                        "gcn_relu_mean": ([64, 128, 64, 7], ["relu", "relu", "none"], "mean"),
+                        "sage": ([100, 256, 64, 9], None, "mean")}[case]
+    L = len(dims) - 1
+    x = rng.standard_normal((g.n, dims[0])).astype(np.float32)
+    mu, rstd = workloads.bn_stats(x)
+    wts = [workloads.glorot_t(dims[i], dims[i + 1], rng) for i in range(L)]
+    wsf = [workloads.glorot_t(dims[i], dims[i + 1], rng) for i in range(L)] \
+        if case == "sage" else None
+    bs = [rng.uniform(-0.1, 0.1, dims[i + 1]).astype(np.float32) for i in range(L)]
+    xt = _t(x, dev)
+    outs = []
+    for so in (False, True):
+        model = bg.BiGCN(g.rowptr, g.colidx, wts, bs, acts=acts, norm=norm, mu=mu, rstd=rstd,
+                         device=dev, weights_self_t=wsf, source_order=so)
+        assert (model.slot is not None) == so
+        outs.append(model.forward(xt).clone())
+        if so:   # and its graph replay
+            replay = model.capture(xt)
+            outs.append(replay().clone())
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1]) and torch.equal(outs[1], outs[2])
+    assert bool(torch.isfinite(outs[0]).all())
