@@ -453,13 +453,18 @@ class BiGCN:
     ``weights_self_t`` (one W^T per layer, or None) the layers given are
     two-weight GraphSAGE layers: ``weights_t`` holds their neighbour
     weights, the graph is A and ``norm`` must be "mean".  With
-    ``source_order`` (the default) the graph's source order is built once
+    ``source_order`` the graph's source order is built once
     (bigcn_source_slots) and every pass stores its per-node products in it;
-    the results are the same bit for bit."""
+    the results are the same bit for bit.  "auto" (the default) takes it
+    for graphs of at least SOURCE_ORDER_MIN_NNZ entries, where it measured
+    faster (reddit-shaped: 4.39 -> 4.07 ms, products-shaped: 14.6 -> 11.5 ms
+    per pass); on graphs of a few million entries it measured 1-3 % slower."""
+
+    SOURCE_ORDER_MIN_NNZ = 1 << 23
 
     def __init__(self, rowptr, colidx, weights_t, biases=None, acts=None,
                  norm: str = "sym", mu=None, rstd=None, device="cuda",
-                 weights_self_t=None, source_order: bool = True):
+                 weights_self_t=None, source_order="auto"):
         self.device = torch.device(device)
         self.rowptr = torch.as_tensor(rowptr, dtype=torch.int64, device=self.device)
         self.colidx = torch.as_tensor(colidx, dtype=torch.int32, device=self.device)
@@ -491,6 +496,8 @@ class BiGCN:
         self.ws = torch.empty(forward_workspace_bytes(self.n, self.nnz, self.layers),
                               dtype=torch.uint8, device=self.device)
         self.slot = self.colslot = None
+        if source_order == "auto":
+            source_order = self.nnz >= self.SOURCE_ORDER_MIN_NNZ
         if source_order and self.n > 0 and self.nnz > 0:
             self.slot = torch.empty(self.n, dtype=torch.int32, device=self.device)
             self.colslot = torch.empty(self.nnz, dtype=torch.int32, device=self.device)

@@ -46,10 +46,11 @@ hipError_t launch_bgemm_mfma(const uint64_t* F, int64_t M, int64_t ldf,
 constexpr int q8_lane_bytes(int32_t N) { return N <= 64 ? 1 : N <= 128 ? 2 : 4; }
 bool q8_supported(int64_t n, int32_t N, int32_t K);
 // The pack of a layer's input followed, in the same kernel, by its binary
-// GEMM into 8-bit half-codes (layers of N <= 64 outputs and at most 1024
-// inputs, row stride at most 2^24 elements): the codes, exact rows and
-// flagged scale of launch_pack + launch_bgemm_q8, bit for bit, without
-// writing the packed bits.
+// GEMM into 8-bit half-codes (layers of N <= 256 outputs with
+// ceil(K / 64) * q8_lane_bytes(N) <= 16: up to 1024 inputs for 64 outputs,
+// 512 for 128, 256 for 256; row stride at most 2^24 elements): the codes,
+// exact rows and flagged scale of launch_pack + launch_bgemm_q8, bit for
+// bit, without writing the packed bits.
 bool pack_bgemm_q8_supported(int32_t cols, int32_t N, int64_t ldx);
 hipError_t launch_pack_bgemm_q8(const float* x, int64_t rows, int32_t cols, int64_t ldx,
                                 const float* mu, const float* rstd, const int64_t* rowptr,

@@ -30,6 +30,7 @@ constexpr int kBlock = 256;  // 4 waves
 constexpr int kWavesPerBlock = kBlock / 64;
 
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef int int4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
@@ -70,6 +71,35 @@ __device__ inline float wave_sum(float v) {
   const float c = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
   const float d = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
   return (a + b) + (c + d);
+}
+
+// 8-bit half-codes of one row, NB per lane (lane l: columns l + 64 c), and a
+// flagged row's exact products in the same order.
+template <int NB>
+__device__ inline void store_codes(int8_t* p, uint32_t packed) {
+  if constexpr (NB == 4)
+    *reinterpret_cast<uint32_t*>(p) = packed;
+  else if constexpr (NB == 2)
+    *reinterpret_cast<uint16_t*>(p) = (uint16_t)packed;
+  else
+    *reinterpret_cast<uint8_t*>(p) = (uint8_t)packed;
+}
+
+template <int NB>
+__device__ inline void store_exact(_Float16* p, const int* v) {
+  if constexpr (NB == 4) {
+    half4_t h;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) h[c] = (_Float16)v[c];
+    *reinterpret_cast<half4_t*>(p) = h;
+  } else if constexpr (NB == 2) {
+    half2_t h;
+    h[0] = (_Float16)v[0];
+    h[1] = (_Float16)v[1];
+    *reinterpret_cast<half2_t*>(p) = h;
+  } else {
+    *p = (_Float16)v[0];
+  }
 }
 
 // ---------------------------------------------------------------- pack ----
@@ -150,14 +180,15 @@ constexpr int64_t kPackRowsMaxLd = (int64_t)1 << 24;
 // reduced together.  kw <= KWT <= 32 and RW * ldw <= 64: lane RW q + w
 // collects word w of row q, so the group's words (rows r0.. contiguous at
 // stride ldw) and scales leave in one store each.
-// With FQ (KWT <= 16) the binary GEMM of a layer of N <= 64 outputs follows
-// in place (lane j: output j, its weight words in registers, the row's words
-// being the ballots): the 8-bit half-codes, exact rows and flags of
-// k_bgemm_pop_q8 (one byte per column) are written instead of the bits.
+// With NBQ > 0 the binary GEMM of a layer of N <= 64 NBQ outputs follows in
+// place (lane l: outputs l + 64 c for c < NBQ, their weight words in
+// registers, KWT NBQ <= 16; the row's words are the ballots): the 8-bit
+// half-codes, exact rows and flags of k_bgemm_pop_q8 (NBQ bytes per lane, the
+// interleaved row layout) are written instead of the bits.
 // With slot != nullptr row r's results go to row slot[r] of bits / scale /
 // codes (the source order of the aggregation); else to row r.
 
-template <bool STD, int RW, int KWT, bool FQ>
+template <bool STD, int RW, int KWT, int NBQ>
 __global__ __launch_bounds__(kBlock) void k_pack_rows(
     const float* __restrict__ x, int64_t rows, int32_t cols, int64_t ldx,
     const float* __restrict__ mu, const float* __restrict__ rstd,
@@ -169,6 +200,8 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
   // 16 words, so the first row loads need not wait for a block barrier;
   // in LDS (mu[0..cols), rstd[cols..2 cols)) for wider rows.
   extern __shared__ float s_norm[];
+  constexpr bool FQ = NBQ > 0;
+  constexpr int NQ = FQ ? NBQ : 1;
   constexpr bool kNLds = STD && KWT > 16;
   const int lane = threadIdx.x & 63;
   const int kw = (cols + 63) >> 6;
@@ -192,14 +225,20 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
     __syncthreads();
   }
   const int64_t step = (int64_t)gridDim.x * kWavesPerBlock * RW;
-  static_assert(!FQ || KWT <= 16, "fused GEMM keeps its weight words in registers");
-  uint64_t wr[FQ ? KWT : 1];  // FQ: lane j's weight words
+  static_assert(!FQ || KWT * NBQ <= 16, "fused GEMM keeps its weight words in registers");
+  uint64_t wr[NQ][FQ ? KWT : 1];  // FQ: the words of lane l's columns l + 64 c
   if constexpr (FQ) {
     const __amdgpu_buffer_rsrc_t rsb = raw_rsrc(B, (uint32_t)(N * ldb * 8));
 #pragma unroll
-    for (int w = 0; w < KWT; ++w) {
-      const uint32_t off = (lane < N && w < kw) ? (uint32_t)(lane * ldb + w) * 8u : kPastEnd;
-      wr[w] = __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(rsb, (int)off, 0, 0));
+    for (int c = 0; c < NQ; ++c) {
+      const int col = lane + 64 * c;
+#pragma unroll
+      for (int w = 0; w < KWT; ++w) {
+        const uint32_t off =
+            (col < N && w < kw) ? (uint32_t)(col * ldb + w) * 8u : kPastEnd;
+        wr[c][w] = __builtin_bit_cast(
+            uint64_t, __builtin_amdgcn_raw_buffer_load_b64(rsb, (int)off, 0, 0));
+      }
     }
   }
   for (int64_t r0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * RW;
@@ -232,11 +271,12 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
     if (slot != nullptr) dq = slot[r0 + (lane < nq ? lane : 0)];
     float l1[RW];
     uint64_t mine = 0;  // lane ldw q + w: word w of row q (pad words stay zero)
-    int pc[RW];  // FQ: lane j's popcount of row XOR weights
+    int pc[RW][NQ];  // FQ: popcount of row XOR the weights of column lane + 64 c
 #pragma unroll
     for (int q = 0; q < RW; ++q) {
       l1[q] = 0.f;
-      pc[q] = 0;
+#pragma unroll
+      for (int c = 0; c < NQ; ++c) pc[q][c] = 0;
 #pragma unroll
       for (int w = 0; w < KWT; ++w) {
         if (w >= kw) break;  // wave-uniform
@@ -260,9 +300,12 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
         }
         if (!FQ && lane == q * ldw + w) mine = b;
         if constexpr (FQ) {
-          const uint64_t z = b ^ wr[w];
-          pc[q] = __builtin_popcount((uint32_t)(z >> 32)) +
-                  (__builtin_popcount((uint32_t)z) + pc[q]);
+#pragma unroll
+          for (int c = 0; c < NQ; ++c) {
+            const uint64_t z = b ^ wr[c][w];
+            pc[q][c] = __builtin_popcount((uint32_t)(z >> 32)) +
+                       (__builtin_popcount((uint32_t)z) + pc[q][c]);
+          }
         }
       }
     }
@@ -278,12 +321,19 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
       if (lane == q) myl1 = l1[q];
       if constexpr (FQ) {
         const int64_t dr = slot != nullptr ? (int64_t)__builtin_amdgcn_readlane(dq, q) : r;
-        const int dot = cols - 2 * pc[q];
-        const int code = (dot - (cols & 1)) >> 1;
-        C8[dr * ldc8 + lane] = (int8_t)code;
-        const bool flag =
-            __builtin_amdgcn_ballot_w64(lane < N && (code < -128 || code > 127)) != 0;
-        if (flag) C16[dr * ldc16 + lane] = (_Float16)dot;
+        int dot[NQ];
+        uint32_t packed = 0;
+        bool big = false;
+#pragma unroll
+        for (int c = 0; c < NQ; ++c) {
+          dot[c] = cols - 2 * pc[q][c];
+          const int code = (dot[c] - (cols & 1)) >> 1;
+          big |= lane + 64 * c < N && (code < -128 || code > 127);
+          packed |= (uint32_t)(uint8_t)(int8_t)code << (8 * c);
+        }
+        store_codes<NQ>(C8 + dr * ldc8 + NQ * lane, packed);
+        const bool flag = __builtin_amdgcn_ballot_w64(big) != 0;
+        if (flag) store_exact<NQ>(C16 + dr * ldc16 + NQ * lane, dot);
         if (lane == q) myflag = flag;
       }
     }
@@ -429,36 +479,8 @@ __global__ __launch_bounds__(kBlock) void k_bgemm_pop(
 // g[i] (g >= 0 otherwise).  One wave covers all N columns, so the flag is
 // decided per row with a ballot.
 
-typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float2_t __attribute__((ext_vector_type(2)));
-
-template <int NB>
-__device__ inline void store_codes(int8_t* p, uint32_t packed) {
-  if constexpr (NB == 4)
-    *reinterpret_cast<uint32_t*>(p) = packed;
-  else if constexpr (NB == 2)
-    *reinterpret_cast<uint16_t*>(p) = (uint16_t)packed;
-  else
-    *reinterpret_cast<uint8_t*>(p) = (uint8_t)packed;
-}
-
-template <int NB>
-__device__ inline void store_exact(_Float16* p, const int* v) {
-  if constexpr (NB == 4) {
-    half4_t h;
-#pragma unroll
-    for (int c = 0; c < 4; ++c) h[c] = (_Float16)v[c];
-    *reinterpret_cast<half4_t*>(p) = h;
-  } else if constexpr (NB == 2) {
-    half2_t h;
-    h[0] = (_Float16)v[0];
-    h[1] = (_Float16)v[1];
-    *reinterpret_cast<half2_t*>(p) = h;
-  } else {
-    *p = (_Float16)v[0];
-  }
-}
 
 template <int RM, int NB>
 __global__ __launch_bounds__(kBlock) void k_bgemm_pop_q8(
@@ -2380,39 +2402,47 @@ struct PackQ8 {
   int64_t ldc16 = 0;
 };
 
-template <bool STD, int RW, int KWT, bool FQ>
+template <bool STD, int RW, int KWT, int NBQ>
 hipError_t pack_rows_launch(const float* x, int64_t rows, int32_t cols, int64_t ldx,
                             const float* mu, const float* rstd, const int64_t* rowptr,
                             int sym, uint64_t* bits, int64_t ldw, float* scale,
                             const PackQ8& pq, hipStream_t stream) {
   const int64_t groups = (rows + RW - 1) / RW;
   // The fused GEMM's waves each load their weight words (and the column
-  // statistics): fewer waves, taking several row groups each, measured
-  // faster (500 inputs, 64 outputs: 10.3 us at 1024 blocks, 12.4 us at 2465).
-  dim3 grid(grid_cap((groups + kWavesPerBlock - 1) / kWavesPerBlock, FQ ? 1024 : 8192));
+  // statistics): with one column per lane fewer waves, taking several row
+  // groups each, measured faster (500 inputs, 64 outputs: 10.3 us at 1024
+  // blocks, 12.4 us at 2465); with 2 or 4 columns per lane a row costs more
+  // ALU work and the full 8192 blocks measured faster (products-shaped
+  // layer 0, 100 inputs and 256 outputs: about 0.08 ms less than at 1024).
+  dim3 grid(grid_cap((groups + kWavesPerBlock - 1) / kWavesPerBlock, NBQ == 1 ? 1024 : 8192));
   const size_t lds = (STD && KWT > 16) ? (size_t)2 * cols * sizeof(float) : 0;
-  hipLaunchKernelGGL((k_pack_rows<STD, RW, KWT, FQ>), grid, dim3(kBlock), lds, stream, x,
+  hipLaunchKernelGGL((k_pack_rows<STD, RW, KWT, NBQ>), grid, dim3(kBlock), lds, stream, x,
                      rows, cols, ldx, mu, rstd, rowptr, sym, bits, ldw, scale, pq.B, pq.N,
                      pq.ldb, pq.C8, pq.ldc8, pq.C16, pq.ldc16, pq.slot);
   return hipGetLastError();
 }
 
-template <bool STD, bool FQ = false>
+template <bool STD, int NBQ = 0>
 hipError_t pack_rows_dispatch(const float* x, int64_t rows, int32_t cols, int64_t ldx,
                               const float* mu, const float* rstd, const int64_t* rowptr,
                               int sym, uint64_t* bits, int64_t ldw, float* scale,
                               hipStream_t stream, const PackQ8& pq = PackQ8()) {
   const int kw = (cols + 63) >> 6;
-#define BIGCN_PACK(RWV, KWV)                                                              \
-  return pack_rows_launch<STD, RWV, KWV, FQ>(x, rows, cols, ldx, mu, rstd, rowptr, sym, \
-                                             bits, ldw, scale, pq, stream)
+#define BIGCN_PACK(RWV, KWV)                                                               \
+  return pack_rows_launch<STD, RWV, KWV, NBQ>(x, rows, cols, ldx, mu, rstd, rowptr, sym, \
+                                              bits, ldw, scale, pq, stream)
   if (kw <= 1) BIGCN_PACK(8, 1);
   if (kw <= 2) BIGCN_PACK(8, 2);
   if (kw <= 4) BIGCN_PACK(4, 4);
-  if (kw <= 8) BIGCN_PACK(2, 8);
-  if (kw <= 16) BIGCN_PACK(1, 16);
-  if constexpr (!FQ) BIGCN_PACK(1, 32);
-  return hipErrorInvalidValue;  // the fused GEMM takes at most 16 words
+  if constexpr (NBQ <= 2) {
+    if (kw <= 8) BIGCN_PACK(2, 8);
+  }
+  if constexpr (NBQ <= 1) {
+    if (kw <= 16) BIGCN_PACK(1, 16);
+  }
+  if constexpr (NBQ == 0) BIGCN_PACK(1, 32);
+  // the fused GEMM keeps at most 16 weight words per lane
+  return hipErrorInvalidValue;
 #undef BIGCN_PACK
 }
 
@@ -2448,12 +2478,13 @@ hipError_t launch_pack(const float* x, int64_t rows, int32_t cols, int64_t ldx,
   return hipGetLastError();
 }
 
-// Inputs of more than 16 words keep the weights in LDS inside a loop the
-// compiler does not unroll; there the separate pack and GEMM are faster
-// (1433 inputs: 15.1 us fused against 8.0 + 5.2 us).
+// A lane keeps the weight words of its NB columns in registers, at most 16:
+// inputs of more words would keep them in LDS inside a loop the compiler
+// does not unroll; there the separate pack and GEMM are faster (1433 inputs,
+// 64 outputs: 15.1 us fused against 8.0 + 5.2 us).
 bool pack_bgemm_q8_supported(int32_t cols, int32_t N, int64_t ldx) {
-  return cols >= 1 && (cols + 63) / 64 <= 16 && N >= 1 && N <= 64 && ldx >= cols &&
-         ldx <= kPackRowsMaxLd;
+  if (cols < 1 || N < 1 || N > 256 || ldx < cols || ldx > kPackRowsMaxLd) return false;
+  return (int64_t)((cols + 63) / 64) * q8_lane_bytes(N) <= 16;
 }
 
 hipError_t launch_pack_bgemm_q8(const float* x, int64_t rows, int32_t cols, int64_t ldx,
@@ -2471,11 +2502,17 @@ hipError_t launch_pack_bgemm_q8(const float* x, int64_t rows, int32_t cols, int6
   pq.ldc8 = ldc8;
   pq.C16 = (_Float16*)C16;
   pq.ldc16 = ldc16;
-  if (mu != nullptr)
-    return pack_rows_dispatch<true, true>(x, rows, cols, ldx, mu, rstd, rowptr, sym, nullptr,
-                                          0, g, stream, pq);
-  return pack_rows_dispatch<false, true>(x, rows, cols, ldx, mu, rstd, rowptr, sym, nullptr, 0,
-                                         g, stream, pq);
+#define BIGCN_PQ(NBV)                                                                    \
+  return mu != nullptr ? pack_rows_dispatch<true, NBV>(x, rows, cols, ldx, mu, rstd, rowptr, \
+                                                       sym, nullptr, 0, g, stream, pq)       \
+                       : pack_rows_dispatch<false, NBV>(x, rows, cols, ldx, mu, rstd, rowptr, \
+                                                        sym, nullptr, 0, g, stream, pq)
+  switch (q8_lane_bytes(N)) {
+    case 1: BIGCN_PQ(1);
+    case 2: BIGCN_PQ(2);
+    default: BIGCN_PQ(4);
+  }
+#undef BIGCN_PQ
 }
 
 hipError_t launch_bgemm_popcount(const uint64_t* F, int64_t M, int64_t ldf,

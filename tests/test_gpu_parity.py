@@ -749,3 +749,43 @@ def test_forward_in_source_order_is_bit_identical(dev, case):
     torch.cuda.synchronize()
     assert torch.equal(outs[0], outs[1]) and torch.equal(outs[1], outs[2])
     assert bool(torch.isfinite(outs[0]).all())
+
+
+@pytest.mark.parametrize("dims", [[300, 100, 7], [256, 256, 40], [100, 256, 47], [700, 64, 5]])
+def test_fused_pack_gemm_matches_chained(dev, dims):
+    """Layer 0 of the forward packs its input and multiplies it with the
+    weights in one kernel for up to 256 outputs (1, 2 or 4 columns per
+    lane); the result equals the chained entry points bit for bit, also for
+    rows whose products overflow the 8-bit code (their signs equal a weight
+    column's: dot = K, the exact fallback)."""
+    rng = np.random.default_rng(sum(dims))
+    g = _star_plus_random(1200, rng)
+    L = len(dims) - 1
+    x = rng.standard_normal((g.n, dims[0])).astype(np.float32)
+    wts = [workloads.glorot_t(dims[i], dims[i + 1], rng) for i in range(L)]
+    for r in (3, 500, 1199):                 # sign(x_r) = sign(W[:, j])
+        x[r] = wts[0][r % dims[1]] * rng.uniform(0.5, 2.0, dims[0]).astype(np.float32)
+    bs = [rng.uniform(-0.1, 0.1, dims[i + 1]).astype(np.float32) for i in range(L)]
+    rowptr_t, colidx_t = _t(g.rowptr, dev), _t(g.colidx, dev)
+    xt = _t(x, dev)
+    outs = []
+    for so in (False, True):
+        model = bg.BiGCN(rowptr_t, colidx_t, wts, bs, norm="sym", device=dev, source_order=so)
+        outs.append(model.forward(xt).clone())
+    h = xt
+    for l in range(L):
+        h, *_ = gpu_layer(dev, g, "sym", None, wts[l], bs[l], rowptr_t=rowptr_t,
+                          colidx_t=colidx_t, ht=h)
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], h) and torch.equal(outs[1], h)
+    if dims[0] > 255:                        # the planted rows were flagged
+        F = torch.empty((g.n, (dims[0] + 63) // 64), dtype=torch.int64, device=dev)
+        gs = torch.empty(g.n, dtype=torch.float32, device=dev)
+        bg.bigcn_binarize_pack(xt, F, gs, None, None, rowptr_t, "sym")
+        wb, _ = bg.pack_weights(_t(wts[0], dev))
+        W = bg.q8_row(dims[1])
+        C8 = torch.empty((g.n, W), dtype=torch.int8, device=dev)
+        C16 = torch.empty((g.n, W), dtype=torch.float16, device=dev)
+        bg.bigcn_bgemm_q8(F, wb, dims[0], C8, C16, gs)
+        torch.cuda.synchronize()
+        assert bool((gs[[3, 500, 1199]] < 0).all())

@@ -142,15 +142,23 @@ def test_forward_equals_chained_layers(dev, cfg):
     g = w.graph
     rowptr_t, colidx_t = _t(g.rowptr, dev), _t(g.colidx, dev)
     xt = _t(w.x, dev)
-    model = bg.BiGCN(rowptr_t, colidx_t, w.weights_t, w.biases, norm=w.norm,
-                     mu=w.mu, rstd=w.rstd, device=dev, weights_self_t=w.weights_self_t)
-    out = model.forward(xt).clone()
-    out2 = model.forward(xt).clone()
+    outs = []
+    for so in (True, False, "auto"):   # source order, node order, the model's default
+        model = bg.BiGCN(rowptr_t, colidx_t, w.weights_t, w.biases, norm=w.norm,
+                         mu=w.mu, rstd=w.rstd, device=dev, weights_self_t=w.weights_self_t,
+                         source_order=so)
+        outs.append(model.forward(xt).clone())
+        if so is True:
+            outs.append(model.forward(xt).clone())
+        del model
+    out = outs[0]
     ref = chained(dev, w, rowptr_t, colidx_t, xt)
     torch.cuda.synchronize()
     log("cfg %d forward vs chained: max |diff| %.3g" % (cfg, (out - ref).abs().max().item()))
-    assert torch.equal(out, out2), "forward pass not reproducible"
+    assert torch.equal(out, outs[1]), "forward pass not reproducible"
     assert torch.equal(out, ref), "forward pass differs from the chained entry points"
+    assert torch.equal(outs[2], ref) and torch.equal(outs[3], ref), \
+        "node-order forward differs"
     assert bool(torch.isfinite(out).all())
 
 
