@@ -10,7 +10,12 @@ LIB = os.path.join(HERE, "libbigcn.so")
 SOURCES = [os.path.join(HERE, "csrc", f)
            for f in ("bigcn_kernels.hip", "bigcn_api.hip", "bigcn_backward.hip")]
 
-# -packed-fp32-ops keeps the compiler from emitting packed fp32 VALU ops.
+# -packed-fp32-ops keeps the compiler from emitting packed fp32 VALU ops in
+# the device code.  hipcc hands -Xclang options to the host pass as well,
+# where the x86 back end prints that it does not know the feature and
+# ignores it; the driver cannot forward a -Xclang pair to the device pass
+# alone (-Xarch_device takes options without arguments), and a per-function
+# target attribute would keep header device functions from inlining.
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
                "-Wall", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                "-I", os.path.join(ROOT, "include")]

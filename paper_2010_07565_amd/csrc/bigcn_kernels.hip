@@ -279,7 +279,7 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
       for (int c = 0; c < NQ; ++c) pc[q][c] = 0;
 #pragma unroll
       for (int w = 0; w < KWT; ++w) {
-        if (w >= kw) break;  // wave-uniform
+        if (w >= kw) continue;  // wave-uniform (every later word too)
         // Lanes past cols hold junk (the next row or zero): the last word's
         // lane mask drops their bits and its sum skips them.
         const bool full = (w + 1) * 64 <= cols;  // wave-uniform
@@ -317,7 +317,7 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
 #pragma unroll
     for (int q = 0; q < RW; ++q) {
       const int64_t r = r0 + q;
-      if (r >= rows) break;  // wave-uniform
+      if (r >= rows) continue;  // wave-uniform (every later row too)
       if (lane == q) myl1 = l1[q];
       if constexpr (FQ) {
         const int64_t dr = slot != nullptr ? (int64_t)__builtin_amdgcn_readlane(dq, q) : r;
