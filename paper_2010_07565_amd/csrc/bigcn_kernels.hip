@@ -73,6 +73,62 @@ __device__ inline float wave_sum(float v) {
   return (a + b) + (c + d);
 }
 
+// One level of the row-group sum below: of the partial sums a and b (two
+// rows, one register each) a lane keeps one, sends the other to its DPP
+// partner and adds what the partner sent, so one register carries both
+// rows from here on.
+template <int CTRL>
+__device__ inline float merge_rows(float a, float b, bool take_b) {
+  const float keep = take_b ? b : a;
+  const float send = take_b ? a : b;
+  return keep + dpp<CTRL>(send);
+}
+
+// The wave sums of RW rows (RW in {1, 2, 4, 8}), each formed by exactly the
+// additions of wave_sum (same operands, same tree), for about three
+// instructions per row instead of thirteen: the first log2(RW) levels of the
+// tree merge the rows' registers pairwise.  Lane u of every 16 lanes plays
+// place p(u) of its 8-lane half row (the upper half row of 16 mirrored, and
+// the upper quad of each half row mirrored), so that the partners of the
+// quad_perm, half-mirror and mirror exchanges always carry the same row.
+// Lane q < RW returns the sum of row q.
+template <int RW>
+__device__ inline float rows_sum(const float (&v)[RW], int lane) {
+  int u = lane & 15;
+  if (u >= 8) u = 15 - u;
+  const bool s3 = u >= 4;
+  const int c = s3 ? 7 - u : u;
+  const bool s1 = (c & 1) != 0, s2 = (c & 2) != 0;
+  float t;
+  if constexpr (RW == 8) {
+    const float p0 = merge_rows<0xB1>(v[0], v[1], s1), p1 = merge_rows<0xB1>(v[2], v[3], s1);
+    const float p2 = merge_rows<0xB1>(v[4], v[5], s1), p3 = merge_rows<0xB1>(v[6], v[7], s1);
+    const float q0 = merge_rows<0x4E>(p0, p1, s2), q1 = merge_rows<0x4E>(p2, p3, s2);
+    t = merge_rows<0x141>(q0, q1, s3);  // lane: row 4 s3 + c
+  } else if constexpr (RW == 4) {
+    const float p0 = merge_rows<0xB1>(v[0], v[1], s1), p1 = merge_rows<0xB1>(v[2], v[3], s1);
+    t = merge_rows<0x4E>(p0, p1, s2);  // lane: row c
+    t += dpp<0x141>(t);
+  } else if constexpr (RW == 2) {
+    t = merge_rows<0xB1>(v[0], v[1], s1);  // lane: row c & 1
+    t += dpp<0x4E>(t);
+    t += dpp<0x141>(t);
+  } else {
+    static_assert(RW == 1, "row groups of 1, 2, 4 or 8");
+    t = v[0];
+    t += dpp<0xB1>(t);
+    t += dpp<0x4E>(t);
+    t += dpp<0x141>(t);
+  }
+  t += dpp<0x140>(t);  // rows of 16 lanes
+  // the four rows of 16: (r0 + r1) + (r2 + r3)
+  t += __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((lane ^ 16) * 4, __builtin_bit_cast(int, t)));
+  t += __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((lane ^ 32) * 4, __builtin_bit_cast(int, t)));
+  // a lane carrying row `lane`: place `lane` for rows 0-3, 11 - lane for 4-7
+  const int src = lane < RW ? (RW == 8 && lane >= 4 ? 11 - lane : lane) : 0;
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src * 4, __builtin_bit_cast(int, t)));
+}
+
 // 8-bit half-codes of one row, NB per lane (lane l: columns l + 64 c), and a
 // flagged row's exact products in the same order.
 template <int NB>
@@ -83,6 +139,34 @@ __device__ inline void store_codes(int8_t* p, uint32_t packed) {
     *reinterpret_cast<uint16_t*>(p) = (uint16_t)packed;
   else
     *reinterpret_cast<uint8_t*>(p) = (uint8_t)packed;
+}
+
+// The low bytes of NB ints as one word (byte c from v[c]), by byte permutes.
+template <int NB>
+__device__ inline uint32_t pack_low_bytes(const int* v) {
+  if constexpr (NB == 4) {
+    // v_perm: selector bytes 0-3 take the second operand's bytes, 4-7 the
+    // first's, 0x0C gives zero
+    const uint32_t lo = __builtin_amdgcn_perm((uint32_t)v[1], (uint32_t)v[0], 0x0C0C0400u);
+    return __builtin_amdgcn_perm((uint32_t)v[3], (uint32_t)v[2], 0x04000C0Cu) | lo;
+  } else if constexpr (NB == 2) {
+    return __builtin_amdgcn_perm((uint32_t)v[1], (uint32_t)v[0], 0x0C0C0400u);
+  } else {
+    return (uint32_t)v[0] & 0xFFu;
+  }
+}
+
+// store_codes for a row address the whole wave shares: a buffer resource
+// built on the scalar unit and a lane offset, no per-lane address math.
+template <int NB>
+__device__ inline void store_codes_row(int8_t* row, int lane, uint32_t packed) {
+  const __amdgpu_buffer_rsrc_t rs = raw_rsrc(row, 64u * NB);
+  if constexpr (NB == 4)
+    __builtin_amdgcn_raw_buffer_store_b32(packed, rs, lane * 4, 0, 0);
+  else if constexpr (NB == 2)
+    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)packed, rs, lane * 2, 0, 0);
+  else
+    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)packed, rs, lane, 0, 0);
 }
 
 template <int NB>
@@ -224,6 +308,13 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
     }
     __syncthreads();
   }
+  // With the statistics in registers, lanes past cols load zero (their
+  // statistics are zero too), so their |y| adds zero without a mask.
+  constexpr bool kZeroPad = !kNLds;
+  // 8-bit codes (cols - cols % 2) / 2 - popcount leave [-128, 127] only
+  // for rows of more than 255 inputs.
+  const int half = (cols - (cols & 1)) >> 1;
+  const bool may_big = cols > 255;
   const int64_t step = (int64_t)gridDim.x * kWavesPerBlock * RW;
   static_assert(!FQ || KWT * NBQ <= 16, "fused GEMM keeps its weight words in registers");
   uint64_t wr[NQ][FQ ? KWT : 1];  // FQ: the words of lane l's columns l + 64 c
@@ -241,23 +332,36 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
       }
     }
   }
+  // Lane offset of word w within a row (the row's own offset q ldx is the
+  // scalar offset of its loads); lanes past cols read past the range: zero.
+  uint32_t voff[KWT];
+#pragma unroll
+  for (int w = 0; w < KWT; ++w)
+    voff[w] = !kZeroPad || w * 64 + lane < cols ? (uint32_t)(w * 64 + lane) * 4u : kPastEnd;
   for (int64_t r0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * RW;
        r0 < rows; r0 += step) {
     // The group's nq rows as one raw buffer ending with the last row's
-    // element cols - 1 (element (q, k) at byte 4 (q ldx + k)), so rows past
-    // the matrix read as zero; elements past cols in a row are loaded but
-    // masked below.  Every load is issued before any result is used.
+    // element cols - 1 (element (q, k) at byte 4 (q ldx + k)); without
+    // kZeroPad elements past cols in a row are loaded but masked below.
+    // Every load is issued before any result is used.
     const int nq = (int)(rows - r0 < RW ? rows - r0 : RW);
     const __amdgpu_buffer_rsrc_t rsx =
         raw_rsrc(x + r0 * ldx, (uint32_t)(((nq - 1) * ldx + cols) * 4));
+    // lane q < nq: the output row of row r0 + q (the fused GEMM stores each
+    // row's codes as soon as they are formed, so it is loaded first)
+    int32_t dq = 0;
+    if (FQ && slot != nullptr) dq = slot[r0 + (lane < nq ? lane : 0)];
+    // Rows past the matrix (q >= nq, last group only) load row nq - 1
+    // again, so no scalar offset leaves the range; nothing of theirs is
+    // stored.
     float v[RW][KWT];
 #pragma unroll
     for (int q = 0; q < RW; ++q) {
-      const uint32_t vo = (uint32_t)(q * ldx + lane) * 4u;
+      const int qo = (q < nq ? q : nq - 1) * (int)ldx * 4;
 #pragma unroll
       for (int w = 0; w < KWT; ++w)
         v[q][w] = __builtin_bit_cast(
-            float, __builtin_amdgcn_raw_buffer_load_b32(rsx, (int)(vo + 256u * w), 0, 0));
+            float, __builtin_amdgcn_raw_buffer_load_b32(rsx, (int)voff[w], qo, 0));
     }
     // lane q < nq: the degree of row r0 + q (for the normalisation factor),
     // loaded after the rows so that waiting for it does not hold them back
@@ -266,22 +370,22 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
       const int64_t rq = r0 + (lane < nq ? lane : 0);
       dg = rowptr[rq + 1] - rowptr[rq];
     }
-    // lane q < nq: the output row of row r0 + q
-    int32_t dq = 0;
-    if (slot != nullptr) dq = slot[r0 + (lane < nq ? lane : 0)];
+    if (!FQ && slot != nullptr) dq = slot[r0 + (lane < nq ? lane : 0)];
     float l1[RW];
     uint64_t mine = 0;  // lane ldw q + w: word w of row q (pad words stay zero)
-    int pc[RW][NQ];  // FQ: popcount of row XOR the weights of column lane + 64 c
+    bool myflag = false;  // FQ, lane q < nq: row r0 + q has exact products
 #pragma unroll
     for (int q = 0; q < RW; ++q) {
       l1[q] = 0.f;
+      int pc[NQ];  // FQ: popcount of row XOR the weights of column lane + 64 c
 #pragma unroll
-      for (int c = 0; c < NQ; ++c) pc[q][c] = 0;
+      for (int c = 0; c < NQ; ++c) pc[c] = 0;
 #pragma unroll
       for (int w = 0; w < KWT; ++w) {
         if (w >= kw) continue;  // wave-uniform (every later word too)
-        // Lanes past cols hold junk (the next row or zero): the last word's
-        // lane mask drops their bits and its sum skips them.
+        // Lanes past cols hold zero (kZeroPad) or junk (the next row or
+        // zero): the last word's lane mask drops their bits and its sum
+        // skips them.
         const bool full = (w + 1) * 64 <= cols;  // wave-uniform
         float y = v[q][w];
         if constexpr (STD) {
@@ -292,51 +396,49 @@ __global__ __launch_bounds__(kBlock) void k_pack_rows(
           y = t * (kNLds ? s_norm[cols + kk] : rr[w]);
         }
         uint64_t b = __builtin_amdgcn_fcmpf(y, 0.f, 3 /* ordered >= */);
-        if (full) {
+        if (!full) b &= (1ull << (cols & 63)) - 1;
+        if (kZeroPad || full)
           l1[q] += fabsf(y);
-        } else {
-          b &= (1ull << (cols & 63)) - 1;
+        else
           l1[q] += lane < (cols & 63) ? fabsf(y) : 0.f;
-        }
         if (!FQ && lane == q * ldw + w) mine = b;
         if constexpr (FQ) {
 #pragma unroll
           for (int c = 0; c < NQ; ++c) {
             const uint64_t z = b ^ wr[c][w];
-            pc[q][c] = __builtin_popcount((uint32_t)(z >> 32)) +
-                       (__builtin_popcount((uint32_t)z) + pc[q][c]);
+            pc[c] = __builtin_popcount((uint32_t)(z >> 32)) +
+                    (__builtin_popcount((uint32_t)z) + pc[c]);
+          }
+        }
+      }
+      if constexpr (FQ) {
+        if (q < nq) {  // wave-uniform
+          const int64_t dr =
+              slot != nullptr ? (int64_t)__builtin_amdgcn_readlane(dq, q) : r0 + q;
+          int code[NQ];
+#pragma unroll
+          for (int c = 0; c < NQ; ++c)
+            code[c] = half - pc[c];  // (dot - cols % 2) / 2, dot = cols - 2 popcount
+          store_codes_row<NQ>(C8 + dr * ldc8, lane, pack_low_bytes<NQ>(code));
+          if (may_big) {
+            bool big = false;
+#pragma unroll
+            for (int c = 0; c < NQ; ++c)
+              big |= lane + 64 * c < N && (code[c] < -128 || code[c] > 127);
+            const bool flag = __builtin_amdgcn_ballot_w64(big) != 0;
+            if (flag) {
+              int dot[NQ];
+#pragma unroll
+              for (int c = 0; c < NQ; ++c) dot[c] = cols - 2 * pc[c];
+              store_exact<NQ>(C16 + dr * ldc16 + NQ * lane, dot);
+            }
+            if (lane == q) myflag = flag;
           }
         }
       }
     }
-#pragma unroll
-    for (int q = 0; q < RW; ++q) l1[q] = wave_sum(l1[q]);
-    // lane q < nq: row r0 + q's sum and (FQ) overflow flag
-    float myl1 = 0.f;
-    bool myflag = false;
-#pragma unroll
-    for (int q = 0; q < RW; ++q) {
-      const int64_t r = r0 + q;
-      if (r >= rows) continue;  // wave-uniform (every later row too)
-      if (lane == q) myl1 = l1[q];
-      if constexpr (FQ) {
-        const int64_t dr = slot != nullptr ? (int64_t)__builtin_amdgcn_readlane(dq, q) : r;
-        int dot[NQ];
-        uint32_t packed = 0;
-        bool big = false;
-#pragma unroll
-        for (int c = 0; c < NQ; ++c) {
-          dot[c] = cols - 2 * pc[q][c];
-          const int code = (dot[c] - (cols & 1)) >> 1;
-          big |= lane + 64 * c < N && (code < -128 || code > 127);
-          packed |= (uint32_t)(uint8_t)(int8_t)code << (8 * c);
-        }
-        store_codes<NQ>(C8 + dr * ldc8 + NQ * lane, packed);
-        const bool flag = __builtin_amdgcn_ballot_w64(big) != 0;
-        if (flag) store_exact<NQ>(C16 + dr * ldc16 + NQ * lane, dot);
-        if (lane == q) myflag = flag;
-      }
-    }
+    // lane q < nq: row r0 + q's sum
+    const float myl1 = rows_sum<RW>(l1, lane);
     if constexpr (!FQ) {
       if (slot == nullptr) {
         if (lane < nq * ldw) bits[r0 * ldw + lane] = mine;
