@@ -1220,9 +1220,6 @@ __device__ inline float4_t load_partial(const float* p) {
 //            half-codes with the exact fallback, as k_bgemm_pop_q8 does.
 // With NX == 1 the output row is also written to out if out != nullptr.
 struct NextLayer {
-  const uint64_t* sB;  // LDS: next weights, [kw'][NBN][64] interleaved columns
-  uint64_t wr[4];      // or, when NB * NBN <= 4, this lane's words in registers:
-                       // wr[w * NBN + c] = word w of column lane + 64c
   int32_t dn;          // next layer's output width d'
   int8_t* C8;          // codes [n][ldc8]
   int64_t ldc8;
@@ -1237,6 +1234,30 @@ struct NextLayer {
                           // sit at row slot[r] (the source order), else at r
 };
 
+// The next layer's weights as finish_row reads them.
+struct NextRegs {
+  const uint64_t* sB;  // LDS: next weights, [kw'][NBN][64] interleaved columns
+  uint64_t wr[4];      // or, when NB * NBN <= 4, this lane's words in registers:
+                       // wr[w * NBN + c] = word w of column lane + 64c
+};
+
+// The NextLayer argument of the kernel that finishes rows, read afresh
+// where a row is finished: kernels calling finish_row take it as their first
+// argument, so it starts the kernel-argument segment, and its fields are
+// scalar loads from there at each use (the opaque pointer keeps the compiler
+// from hoisting them), not values held in scalar registers through the edge
+// loop, where they only crowd out the loop's own.
+typedef const __attribute__((address_space(4))) NextLayer* KernargNext;
+__device__ inline NextLayer fresh_next() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  KernargNext p = (KernargNext)__builtin_amdgcn_kernarg_segment_ptr();
+  __asm__ volatile("" : "+s"(p));
+  return *p;
+#else
+  return NextLayer{};  // (the host pass only parses device functions)
+#endif
+}
+
 struct EpiIL {
   float alpha[4], bias[4];
   float alpha_s[4];    // self weights' α (NX == 2)
@@ -1248,7 +1269,8 @@ struct EpiIL {
 template <int NX, int NB, int NBN>
 __device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4_t acc,
                                   const EpiIL& ep, float* __restrict__ out, int64_t ldo,
-                                  const NextLayer& nx, int lane) {
+                                  const NextRegs& nr, int lane) {
+  const NextLayer nx = fresh_next();  // the calling kernel's first argument
   const float rowfac = deg > 0 ? row_factor_deg(deg, mean) : 0.f;
   int64_t dst = r;  // row of the next products / self products
   if (NX != 0 && nx.slot != nullptr) dst = nx.slot[r];
@@ -1297,8 +1319,8 @@ __device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4
 #pragma unroll
     for (int w = 0; w < NB; ++w) {
       if (w >= kwn) break;
-      const uint64_t bw = NB * NBN <= 4 ? nx.wr[(w * NBN + c) & 3]
-                                        : nx.sB[(w * NBN + c) * 64 + lane];
+      const uint64_t bw = NB * NBN <= 4 ? nr.wr[(w * NBN + c) & 3]
+                                        : nr.sB[(w * NBN + c) * 64 + lane];
       const uint64_t z = word[w] ^ bw;
       pc += __builtin_popcount((uint32_t)z);
       pc += __builtin_popcount((uint32_t)(z >> 32));
@@ -1335,7 +1357,7 @@ __device__ inline void make_epi_il(EpiIL& ep, int lane, int32_t d,
 // at most four words (NB * NBN <= 4; no LDS, no block barrier), else staged
 // in LDS by the whole block (stage_weights, which ends in a barrier).
 template <int NB, int NBN>
-__device__ inline void load_next_weights(NextLayer& nx, uint64_t* sBn,
+__device__ inline void load_next_weights(NextRegs& nx, int32_t dn, uint64_t* sBn,
                                          const uint64_t* __restrict__ Bn, int64_t ldbn,
                                          int32_t d, int lane) {
   const int kwn = (d + 63) >> 6;
@@ -1346,11 +1368,11 @@ __device__ inline void load_next_weights(NextLayer& nx, uint64_t* sBn,
       for (int c = 0; c < NBN; ++c) {
         const int col = lane + 64 * c;
         nx.wr[(w * NBN + c) & 3] =
-            (w < kwn && col < nx.dn) ? Bn[(int64_t)col * ldbn + w] : 0ull;
+            (w < kwn && col < dn) ? Bn[(int64_t)col * ldbn + w] : 0ull;
       }
     nx.sB = nullptr;
   } else {
-    stage_weights<NBN, true>(sBn, Bn, nx.dn, ldbn, kwn, 0);
+    stage_weights<NBN, true>(sBn, Bn, dn, ldbn, kwn, 0);
     nx.sB = sBn;
   }
 }
@@ -1400,14 +1422,14 @@ __device__ inline int64_t readlane64(int64_t v, int l) {
 // p * sum g term is zero and its running sum is not kept.
 template <int U, int NX, int NB, int NBN, int P>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) void k_spmm_wave_q8(
-    int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
+    NextLayer nx, int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, int mean, const float* __restrict__ g,
     const int8_t* __restrict__ C8, int64_t ldc8, const _Float16* __restrict__ C16,
     int64_t ldc16, int par, int32_t d, const float* __restrict__ alpha,
     const float* __restrict__ bias, int relu, float* __restrict__ out,
     int64_t ldo, int64_t chunk, int64_t workers, int32_t dpad,
     int32_t* __restrict__ tail_row, float* __restrict__ head,
-    float* __restrict__ tail, NextLayer nx, const uint64_t* __restrict__ Bn,
+    float* __restrict__ tail, const uint64_t* __restrict__ Bn,
     int64_t ldbn, const float* __restrict__ alpha_s) {
   static_assert(64 % U == 0, "group size");
   extern __shared__ uint64_t sBn[];
@@ -1426,7 +1448,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
   };
   int32_t jA = ld_idx(0);  // issued first: independent of everything else
   int32_t jB = ld_idx(64);
-  if (NX == 1) load_next_weights<NB, NBN>(nx, sBn, Bn, ldbn, d, lane);
+  NextRegs nr = {};
+  if (NX == 1) load_next_weights<NB, NBN>(nr, nx.dn, sBn, Bn, ldbn, d, lane);
   if (!live) return;
   EpiIL ep;
   make_epi_il<NB>(ep, lane, d, alpha, bias, relu, alpha_s);
@@ -1454,7 +1477,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
   const float4_t zero4 = {0.f, 0.f, 0.f, 0.f};
   if (!before) {
     for (int64_t q = r - 1; q >= 0 && rowptr[q] == s; --q)
-      finish_row<NX, NB, NBN>(q, 0, mean, zero4, ep, out, ldo, nx, lane);
+      finish_row<NX, NB, NBN>(q, 0, mean, zero4, ep, out, ldo, nr, lane);
   }
   float4_t a0 = zero4, a1 = zero4;
   float gsum = 0.f;  // sum of g_j over the current row (for the parity term)
@@ -1503,7 +1526,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
           if (before) {
             store_partial<NB>(head + w * dpad + NB * lane, sum);
           } else {
-            finish_row<NX, NB, NBN>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nx, lane);
+            finish_row<NX, NB, NBN>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nr, lane);
           }
           a0 = zero4;
           a1 = zero4;
@@ -1519,7 +1542,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
             }
             cur_end = __builtin_amdgcn_readlane(win, (int)(r - rbase));
             if (cur_end == eu)
-              finish_row<NX, NB, NBN>(r, 0, mean, zero4, ep, out, ldo, nx, lane);
+              finish_row<NX, NB, NBN>(r, 0, mean, zero4, ep, out, ldo, nr, lane);
           } while (cur_end == eu);
         }
         float gj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
@@ -1551,11 +1574,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
     if (before) {
       store_partial<NB>(head + w * dpad + NB * lane, sum);
     } else {
-      finish_row<NX, NB, NBN>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nx, lane);
+      finish_row<NX, NB, NBN>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nr, lane);
     }
     if (t == nnz)
       for (int64_t q = r + 1; q < n; ++q)
-        finish_row<NX, NB, NBN>(q, 0, mean, zero4, ep, out, ldo, nx, lane);
+        finish_row<NX, NB, NBN>(q, 0, mean, zero4, ep, out, ldo, nr, lane);
     if (lane == 0) tail_row[w] = -1;
   } else if (before) {
     store_partial<NB>(head + w * dpad + NB * lane, sum);
@@ -1573,15 +1596,16 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
 // are finished in worker order.
 template <int NX, int NB, int NBN>
 __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
-    const int64_t* __restrict__ rowptr, int mean, int32_t d,
+    NextLayer nx, const int64_t* __restrict__ rowptr, int mean, int32_t d,
     const float* __restrict__ alpha, const float* __restrict__ bias, int relu,
     float* __restrict__ out, int64_t ldo, int64_t chunk, int64_t workers,
     int32_t dpad, const int32_t* __restrict__ tail_row,
-    const float* __restrict__ head, const float* __restrict__ tail, NextLayer nx,
+    const float* __restrict__ head, const float* __restrict__ tail,
     const uint64_t* __restrict__ Bn, int64_t ldbn, const float* __restrict__ alpha_s) {
   extern __shared__ uint64_t sBn[];
   const int lane = threadIdx.x & 63;
-  if (NX == 1) load_next_weights<NB, NBN>(nx, sBn, Bn, ldbn, d, lane);
+  NextRegs nr = {};
+  if (NX == 1) load_next_weights<NB, NBN>(nr, nx.dn, sBn, Bn, ldbn, d, lane);
   const int64_t w0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * 4;
   if (w0 >= workers) return;
   EpiIL ep;
@@ -1618,7 +1642,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
       for (int u = 0; u < 8; ++u) a += h[u];
     }
     for (; v <= wend; ++v) a += load_partial<NB>(head + v * dpad + NB * lane);
-    finish_row<NX, NB, NBN>(r, e - readlane64(bq, q), mean, a, ep, out, ldo, nx, lane);
+    finish_row<NX, NB, NBN>(r, e - readlane64(bq, q), mean, a, ep, out, ldo, nr, lane);
   }
 }
 
@@ -2745,7 +2769,6 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   float* head = (float*)(base + p.off_head);
   float* tail = (float*)(base + p.off_tail);
   NextLayer nx;
-  nx.sB = nullptr;
   nx.dn = fn.d_out;
   nx.C8 = fn.C8;
   nx.ldc8 = fn.ldc8;
@@ -2762,21 +2785,21 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   dim3 grid((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock));
   if (K & 1)
     hipLaunchKernelGGL((k_spmm_wave_q8<8, NX, NB, NBN, 1>), grid, dim3(kBlock), lds, stream,
-                       n, nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16,
+                       nx, n, nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16,
                        ldc16, 1, d, alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,
-                       tail_row, head, tail, nx, fn.wbits, fn.ldw, fn.alpha_self);
+                       tail_row, head, tail, fn.wbits, fn.ldw, fn.alpha_self);
   else
     hipLaunchKernelGGL((k_spmm_wave_q8<8, NX, NB, NBN, 0>), grid, dim3(kBlock), lds, stream,
-                       n, nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16,
+                       nx, n, nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16,
                        ldc16, 0, d, alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,
-                       tail_row, head, tail, nx, fn.wbits, fn.ldw, fn.alpha_self);
+                       tail_row, head, tail, fn.wbits, fn.ldw, fn.alpha_self);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t fix_waves = (p.workers + 3) / 4;
   hipLaunchKernelGGL((k_spmm_fix_q8<NX, NB, NBN>),
                      dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
-                     dim3(kBlock), lds, stream, rowptr, mean, d, alpha, bias, relu, out,
-                     ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail, nx, fn.wbits,
+                     dim3(kBlock), lds, stream, nx, rowptr, mean, d, alpha, bias, relu, out,
+                     ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail, fn.wbits,
                      fn.ldw, fn.alpha_self);
   return hipGetLastError();
 }
