@@ -1241,37 +1241,58 @@ struct NextRegs {
                        // wr[w * NBN + c] = word w of column lane + 64c
 };
 
-// The NextLayer argument of the kernel that finishes rows, read afresh
-// where a row is finished: kernels calling finish_row take it as their first
-// argument, so it starts the kernel-argument segment, and its fields are
-// scalar loads from there at each use (the opaque pointer keeps the compiler
-// from hoisting them), not values held in scalar registers through the edge
-// loop, where they only crowd out the loop's own.
-typedef const __attribute__((address_space(4))) NextLayer* KernargNext;
-__device__ inline NextLayer fresh_next() {
+// Everything finish_row reads besides a row's sums and the next weights:
+// the first argument of the kernels that finish rows, so that it starts the
+// kernel-argument segment.  finish_row reads it afresh at each call (scalar
+// loads from that segment behind an opaque pointer, which the compiler
+// cannot hoist) instead of the kernel holding its fields in scalar
+// registers through the edge loop, where they would crowd out the loop's
+// own values.  The per-column alpha, bias and alpha_self sit in LDS
+// (stage_epi).
+struct FinishArgs {
+  NextLayer nx;
+  float* out;            // [n][ldo]; nullable when a next layer is formed
+  int64_t ldo;
+  const float* alpha;    // this layer's alpha [d]
+  const float* bias;     // [d] or null
+  const float* alpha_s;  // two-weight layer: the self weights' alpha [d]
+  int mean;              // destination factor, see row_factor_deg
+  int relu;
+  int32_t d;             // output width, at most 256
+};
+
+typedef const __attribute__((address_space(4))) FinishArgs* KernargFinish;
+__device__ inline FinishArgs fresh_finish() {
 #if defined(__HIP_DEVICE_COMPILE__)
-  KernargNext p = (KernargNext)__builtin_amdgcn_kernarg_segment_ptr();
+  KernargFinish p = (KernargFinish)__builtin_amdgcn_kernarg_segment_ptr();
   __asm__ volatile("" : "+s"(p));
   return *p;
 #else
-  return NextLayer{};  // (the host pass only parses device functions)
+  return FinishArgs{};  // (the host pass only parses device functions)
 #endif
 }
 
-struct EpiIL {
-  float alpha[4], bias[4];
-  float alpha_s[4];    // self weights' α (NX == 2)
-  bool valid[4];       // column lane + 64c < d
-  int relu;
-  int32_t d;
-};
+// LDS copy of alpha, bias and alpha_self (zero past d) for finish_row, one
+// column per thread of the block; ends in a barrier.
+__device__ inline void stage_epi(float (*s_epi)[256], const FinishArgs& fa) {
+  static_assert(kBlock == 256, "one column per thread");
+  const int t = threadIdx.x;
+  const bool ok = t < fa.d;
+  s_epi[0][t] = ok ? fa.alpha[t] : 0.f;
+  s_epi[1][t] = ok && fa.bias != nullptr ? fa.bias[t] : 0.f;
+  s_epi[2][t] = ok && fa.alpha_s != nullptr ? fa.alpha_s[t] : 0.f;
+  __syncthreads();
+}
 
 template <int NX, int NB, int NBN>
-__device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4_t acc,
-                                  const EpiIL& ep, float* __restrict__ out, int64_t ldo,
-                                  const NextRegs& nr, int lane) {
-  const NextLayer nx = fresh_next();  // the calling kernel's first argument
-  const float rowfac = deg > 0 ? row_factor_deg(deg, mean) : 0.f;
+__device__ inline void finish_row(int64_t r, int64_t deg, const float4_t acc,
+                                  const float (*s_epi)[256], const NextRegs& nr, int lane) {
+  const FinishArgs fa = fresh_finish();  // the calling kernel's first argument
+  const NextLayer& nx = fa.nx;
+  bool valid[NB];  // column lane + 64c < d
+#pragma unroll
+  for (int c = 0; c < NB; ++c) valid[c] = lane + 64 * c < fa.d;
+  const float rowfac = deg > 0 ? row_factor_deg(deg, fa.mean) : 0.f;
   int64_t dst = r;  // row of the next products / self products
   if (NX != 0 && nx.slot != nullptr) dst = nx.slot[r];
   float self[NB];
@@ -1279,20 +1300,22 @@ __device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4
     const float gi = fabsf(nx.gself[dst]);
 #pragma unroll
     for (int c = 0; c < NB; ++c)
-      self[c] = ep.valid[c] ? gi * ep.alpha_s[c] * (float)nx.Cself[dst * nx.ldself + lane + 64 * c]
-                            : 0.f;
+      self[c] = valid[c] ? gi * s_epi[2][lane + 64 * c] *
+                               (float)nx.Cself[dst * nx.ldself + lane + 64 * c]
+                         : 0.f;
   }
   float v[NB];
 #pragma unroll
   for (int c = 0; c < NB; ++c) {
-    float t = deg > 0 ? fmaf(acc[c], rowfac * ep.alpha[c], ep.bias[c]) : ep.bias[c];
+    const float al = s_epi[0][lane + 64 * c], bi = s_epi[1][lane + 64 * c];
+    float t = deg > 0 ? fmaf(acc[c], rowfac * al, bi) : bi;
     if (NX == 2) t += self[c];
-    v[c] = act(t, ep.relu);
+    v[c] = act(t, fa.relu);
   }
-  if (NX != 1 || out != nullptr) {
+  if (NX != 1 || fa.out != nullptr) {
 #pragma unroll
     for (int c = 0; c < NB; ++c)
-      if (ep.valid[c]) out[r * ldo + lane + 64 * c] = v[c];
+      if (valid[c]) fa.out[r * fa.ldo + lane + 64 * c] = v[c];
   }
   if (NX != 1) return;
   // Next layer: signs (one ballot per 64 elements = one packed word) and
@@ -1301,14 +1324,14 @@ __device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4
   float l1 = 0.f;
 #pragma unroll
   for (int c = 0; c < NB; ++c) {
-    word[c] = __builtin_amdgcn_ballot_w64(ep.valid[c] && v[c] >= 0.f);
-    l1 += ep.valid[c] ? fabsf(v[c]) : 0.f;
+    word[c] = __builtin_amdgcn_ballot_w64(valid[c] && v[c] >= 0.f);
+    l1 += valid[c] ? fabsf(v[c]) : 0.f;
   }
   l1 = wave_sum(l1);
-  float sc = l1 / (float)ep.d;
+  float sc = l1 / (float)fa.d;
   if (nx.sym) sc = sc * (deg > 0 ? 1.0f / sqrtf((float)deg) : 0.f);
-  const int kwn = (ep.d + 63) >> 6;  // <= NB
-  const int Kn = ep.d;
+  const int kwn = (fa.d + 63) >> 6;  // <= NB
+  const int Kn = fa.d;
   const int par = Kn & 1;
   bool big = false;
   uint32_t packed = 0;
@@ -1334,23 +1357,6 @@ __device__ inline void finish_row(int64_t r, int64_t deg, int mean, const float4
   const bool flag = __builtin_amdgcn_ballot_w64(big) != 0;
   if (flag) store_exact<NBN>(nx.C16 + dst * nx.ldc16 + NBN * lane, dot);
   if (lane == 0) nx.g[dst] = flag ? -sc : sc;
-}
-
-template <int NB>
-__device__ inline void make_epi_il(EpiIL& ep, int lane, int32_t d,
-                                   const float* __restrict__ alpha,
-                                   const float* __restrict__ bias, int relu,
-                                   const float* __restrict__ alpha_s = nullptr) {
-  ep.relu = relu;
-  ep.d = d;
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const int k = lane + 64 * c;
-    ep.valid[c] = c < NB && k < d;
-    ep.alpha[c] = ep.valid[c] ? alpha[k] : 0.f;
-    ep.bias[c] = (ep.valid[c] && bias != nullptr) ? bias[k] : 0.f;
-    ep.alpha_s[c] = (ep.valid[c] && alpha_s != nullptr) ? alpha_s[k] : 0.f;
-  }
 }
 
 // The next layer's weights for finish_row: in registers when a lane needs
@@ -1422,17 +1428,15 @@ __device__ inline int64_t readlane64(int64_t v, int l) {
 // p * sum g term is zero and its running sum is not kept.
 template <int U, int NX, int NB, int NBN, int P>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) void k_spmm_wave_q8(
-    NextLayer nx, int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
-    const int32_t* __restrict__ colidx, int mean, const float* __restrict__ g,
+    FinishArgs fa, int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
+    const int32_t* __restrict__ colidx, const float* __restrict__ g,
     const int8_t* __restrict__ C8, int64_t ldc8, const _Float16* __restrict__ C16,
-    int64_t ldc16, int par, int32_t d, const float* __restrict__ alpha,
-    const float* __restrict__ bias, int relu, float* __restrict__ out,
-    int64_t ldo, int64_t chunk, int64_t workers, int32_t dpad,
+    int64_t ldc16, int par, int64_t chunk, int64_t workers, int32_t dpad,
     int32_t* __restrict__ tail_row, float* __restrict__ head,
-    float* __restrict__ tail, const uint64_t* __restrict__ Bn,
-    int64_t ldbn, const float* __restrict__ alpha_s) {
+    float* __restrict__ tail, const uint64_t* __restrict__ Bn, int64_t ldbn) {
   static_assert(64 % U == 0, "group size");
   extern __shared__ uint64_t sBn[];
+  __shared__ float s_epi[3][256];
   // the scales of the window's 64 edges, read back as 16-byte broadcasts
   __shared__ __attribute__((aligned(16))) float s_gw[kWavesPerBlock][64];
   const int lane = threadIdx.x & 63;
@@ -1449,10 +1453,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
   int32_t jA = ld_idx(0);  // issued first: independent of everything else
   int32_t jB = ld_idx(64);
   NextRegs nr = {};
-  if (NX == 1) load_next_weights<NB, NBN>(nr, nx.dn, sBn, Bn, ldbn, d, lane);
+  if (NX == 1) load_next_weights<NB, NBN>(nr, fa.nx.dn, sBn, Bn, ldbn, fa.d, lane);
+  stage_epi(s_epi, fa);
   if (!live) return;
-  EpiIL ep;
-  make_epi_il<NB>(ep, lane, d, alpha, bias, relu, alpha_s);
   const int rb8 = (int)ldc8;
   const int rb16 = (int)(ldc16 * 2);
   const __amdgpu_buffer_rsrc_t rs8 = raw_rsrc(C8, (uint32_t)(n * rb8));
@@ -1477,7 +1480,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
   const float4_t zero4 = {0.f, 0.f, 0.f, 0.f};
   if (!before) {
     for (int64_t q = r - 1; q >= 0 && rowptr[q] == s; --q)
-      finish_row<NX, NB, NBN>(q, 0, mean, zero4, ep, out, ldo, nr, lane);
+      finish_row<NX, NB, NBN>(q, 0, zero4, s_epi, nr, lane);
   }
   float4_t a0 = zero4, a1 = zero4;
   float gsum = 0.f;  // sum of g_j over the current row (for the parity term)
@@ -1526,7 +1529,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
           if (before) {
             store_partial<NB>(head + w * dpad + NB * lane, sum);
           } else {
-            finish_row<NX, NB, NBN>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nr, lane);
+            finish_row<NX, NB, NBN>(r, cur_end - cur_beg, sum, s_epi, nr, lane);
           }
           a0 = zero4;
           a1 = zero4;
@@ -1542,7 +1545,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
             }
             cur_end = __builtin_amdgcn_readlane(win, (int)(r - rbase));
             if (cur_end == eu)
-              finish_row<NX, NB, NBN>(r, 0, mean, zero4, ep, out, ldo, nr, lane);
+              finish_row<NX, NB, NBN>(r, 0, zero4, s_epi, nr, lane);
           } while (cur_end == eu);
         }
         float gj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
@@ -1574,11 +1577,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
     if (before) {
       store_partial<NB>(head + w * dpad + NB * lane, sum);
     } else {
-      finish_row<NX, NB, NBN>(r, cur_end - cur_beg, mean, sum, ep, out, ldo, nr, lane);
+      finish_row<NX, NB, NBN>(r, cur_end - cur_beg, sum, s_epi, nr, lane);
     }
     if (t == nnz)
       for (int64_t q = r + 1; q < n; ++q)
-        finish_row<NX, NB, NBN>(q, 0, mean, zero4, ep, out, ldo, nr, lane);
+        finish_row<NX, NB, NBN>(q, 0, zero4, s_epi, nr, lane);
     if (lane == 0) tail_row[w] = -1;
   } else if (before) {
     store_partial<NB>(head + w * dpad + NB * lane, sum);
@@ -1596,20 +1599,18 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
 // are finished in worker order.
 template <int NX, int NB, int NBN>
 __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
-    NextLayer nx, const int64_t* __restrict__ rowptr, int mean, int32_t d,
-    const float* __restrict__ alpha, const float* __restrict__ bias, int relu,
-    float* __restrict__ out, int64_t ldo, int64_t chunk, int64_t workers,
+    FinishArgs fa, const int64_t* __restrict__ rowptr, int64_t chunk, int64_t workers,
     int32_t dpad, const int32_t* __restrict__ tail_row,
     const float* __restrict__ head, const float* __restrict__ tail,
-    const uint64_t* __restrict__ Bn, int64_t ldbn, const float* __restrict__ alpha_s) {
+    const uint64_t* __restrict__ Bn, int64_t ldbn) {
   extern __shared__ uint64_t sBn[];
+  __shared__ float s_epi[3][256];
   const int lane = threadIdx.x & 63;
   NextRegs nr = {};
-  if (NX == 1) load_next_weights<NB, NBN>(nr, nx.dn, sBn, Bn, ldbn, d, lane);
+  if (NX == 1) load_next_weights<NB, NBN>(nr, fa.nx.dn, sBn, Bn, ldbn, fa.d, lane);
+  stage_epi(s_epi, fa);
   const int64_t w0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * 4;
   if (w0 >= workers) return;
-  EpiIL ep;
-  make_epi_il<NB>(ep, lane, d, alpha, bias, relu, alpha_s);
   // lane q < 4: worker w0 + q's cut row and that row's bounds
   const int64_t wq = w0 + (lane & 3);
   const int32_t rq = wq < workers ? tail_row[wq] : -1;
@@ -1642,7 +1643,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
       for (int u = 0; u < 8; ++u) a += h[u];
     }
     for (; v <= wend; ++v) a += load_partial<NB>(head + v * dpad + NB * lane);
-    finish_row<NX, NB, NBN>(r, e - readlane64(bq, q), mean, a, ep, out, ldo, nr, lane);
+    finish_row<NX, NB, NBN>(r, e - readlane64(bq, q), a, s_epi, nr, lane);
   }
 }
 
@@ -2768,7 +2769,8 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   int32_t* tail_row = (int32_t*)(base + p.off_tailrow);
   float* head = (float*)(base + p.off_head);
   float* tail = (float*)(base + p.off_tail);
-  NextLayer nx;
+  FinishArgs fa;
+  NextLayer& nx = fa.nx;
   nx.dn = fn.d_out;
   nx.C8 = fn.C8;
   nx.ldc8 = fn.ldc8;
@@ -2780,27 +2782,32 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   nx.Cself = (const _Float16*)fn.Cself;
   nx.ldself = fn.ldself;
   nx.gself = g;
+  fa.out = out;
+  fa.ldo = ldo;
+  fa.alpha = alpha;
+  fa.bias = bias;
+  fa.alpha_s = fn.alpha_self;
+  fa.mean = mean;
+  fa.relu = relu;
+  fa.d = d;
   const size_t lds = (NX > 0 && NB * NBN > 4)
                          ? (size_t)((d + 63) >> 6) * NBN * 64 * sizeof(uint64_t) : 0;
   dim3 grid((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock));
   if (K & 1)
     hipLaunchKernelGGL((k_spmm_wave_q8<8, NX, NB, NBN, 1>), grid, dim3(kBlock), lds, stream,
-                       nx, n, nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16,
-                       ldc16, 1, d, alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,
-                       tail_row, head, tail, fn.wbits, fn.ldw, fn.alpha_self);
+                       fa, n, nnz, rowptr, colidx, g, C8, ldc8, (const _Float16*)C16, ldc16,
+                       1, p.chunk, p.workers, p.dpad, tail_row, head, tail, fn.wbits, fn.ldw);
   else
     hipLaunchKernelGGL((k_spmm_wave_q8<8, NX, NB, NBN, 0>), grid, dim3(kBlock), lds, stream,
-                       nx, n, nnz, rowptr, colidx, mean, g, C8, ldc8, (const _Float16*)C16,
-                       ldc16, 0, d, alpha, bias, relu, out, ldo, p.chunk, p.workers, p.dpad,
-                       tail_row, head, tail, fn.wbits, fn.ldw, fn.alpha_self);
+                       fa, n, nnz, rowptr, colidx, g, C8, ldc8, (const _Float16*)C16, ldc16,
+                       0, p.chunk, p.workers, p.dpad, tail_row, head, tail, fn.wbits, fn.ldw);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t fix_waves = (p.workers + 3) / 4;
   hipLaunchKernelGGL((k_spmm_fix_q8<NX, NB, NBN>),
                      dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
-                     dim3(kBlock), lds, stream, nx, rowptr, mean, d, alpha, bias, relu, out,
-                     ldo, p.chunk, p.workers, p.dpad, tail_row, head, tail, fn.wbits,
-                     fn.ldw, fn.alpha_self);
+                     dim3(kBlock), lds, stream, fa, rowptr, p.chunk, p.workers, p.dpad,
+                     tail_row, head, tail, fn.wbits, fn.ldw);
   return hipGetLastError();
 }
 
