@@ -349,7 +349,34 @@ def test_bgemm_q8_matches_oracle(dev, M, N, K):
                                           (65, 301, "sym", "relu"), (128, 256, "sym", "none")])
 def test_spmm_q8_matches_oracle(dev, d, K, norm, act):
     rng = np.random.default_rng(d + K)
-    g = _star_plus_random(900, rng)
+    _check_spmm_q8(dev, _star_plus_random(900, rng), rng, d, K, norm, act)
+
+
+def _long_rows(rng):
+    """Rows averaging well over 64 entries (the wide aggregation then walks
+    edges in groups of 16), with a hub and six rows holding only their
+    self-loop."""
+    n = 700
+    edges = set()
+    for i in range(n - 6):
+        for j in rng.choice(n - 6, size=60, replace=False):
+            if i != j:
+                edges.add((min(i, int(j)), max(i, int(j))))
+    for j in range(1, n - 6):                  # hub: node 0 reaches every node
+        edges.add((0, j))
+    g = workloads.graph_from_edges(n, sorted(edges))
+    assert g.nnz >= 64 * g.n
+    return g
+
+
+@pytest.mark.parametrize("d,K,norm,act", [(256, 256, "sym", "none"), (256, 301, "mean", "relu"),
+                                          (129, 602, "sym", "relu"), (65, 255, "mean", "none")])
+def test_spmm_q8_long_rows_matches_oracle(dev, d, K, norm, act):
+    rng = np.random.default_rng(7 * d + K)
+    _check_spmm_q8(dev, _long_rows(rng), rng, d, K, norm, act)
+
+
+def _check_spmm_q8(dev, g, rng, d, K, norm, act):
     par = K & 1
     dot = 2 * rng.integers(-60, 61, size=(g.n, d)) + par
     big_rows = rng.choice(g.n, size=30, replace=False)
