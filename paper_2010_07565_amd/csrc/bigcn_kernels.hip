@@ -1520,10 +1520,13 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
         }
         continue;
       }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
+      // A group with a row end or a flagged source, edge by edge (false once
+      // past the chunk's end): unrolled for groups of 8, a loop for groups of
+      // 16 (the body holds two row epilogues; their graphs have long rows and
+      // few such groups, and 16 copies do not unroll).
+      auto slow_edge = [&](int u) -> bool {
         const int eu = e0 + u;
-        if (eu >= nE) break;
+        if (eu >= nE) return false;
         if (eu == cur_end) {
           const float4_t sum = P != 0 ? 2.f * (a0 + a1) + fpar * gsum : 2.f * (a0 + a1);
           if (before) {
@@ -1564,6 +1567,17 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
         else
           fma_n<NB>(a0, gj, v);
         if constexpr (P != 0) gsum += gj;
+        return true;
+      };
+      static_assert(U == 8 || U == 16, "group sizes");
+      if constexpr (U == 8) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (!slow_edge(u)) break;
+      } else {
+#pragma unroll 1
+        for (int u = 0; u < U; ++u)
+          if (!slow_edge(u)) break;
       }
     }
     jA = jB;
