@@ -25,7 +25,9 @@ Prints one JSON line.  Besides the forward-pass throughput it carries
    the aggregation entries also carry the gather model, every edge reading
    its source's whole product row), bit operations on the vector ALUs for
    the binary GEMM; "traffic" is the counter-measured HBM bytes of that call
-   (profiles/hbm_traffic_<workload>.md) while the kernel sources match;
+   (profiles/hbm_traffic_<workload>.md) while the kernel sources match, and
+   "traffic_gbs" / "traffic_frac" those bytes over the call's average time
+   (against 8 TB/s);
    "cold" is the same entry point timed after cache-evicting writes;
  - "bgemm_ab": the binary GEMM of every layer shape run with both
    algorithms (XOR + bit count on the vector ALUs, +-1 int8 on the matrix
@@ -618,6 +620,12 @@ def main():
                     achieved=round(dom["achieved"], 2), peak=dom["peak"], unit=dom["unit"],
                     frac=round(dom["frac"], 4), traffic=traffic,
                     traffic_unit="bytes per call (HBM read + written)",
+                    # the counted bytes over the same average duration: the
+                    # rate the memory system actually delivered for this call
+                    traffic_gbs=(round(traffic / (dom["us"] * 1e-6) / 1e9, 1)
+                                 if traffic is not None else None),
+                    traffic_frac=(round(traffic / (dom["us"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+                                  if traffic is not None else None),
                     algorithmic_bytes=dom["work"] if dom["bound"] == "hbm" else dom.get("bytes"),
                     avg_us=round(dom["us"], 3),
                     timing="warm: back-to-back calls (a HIP graph between two HIP events on "
