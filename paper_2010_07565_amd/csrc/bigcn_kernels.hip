@@ -1284,10 +1284,37 @@ __device__ inline void stage_epi(float (*s_epi)[256], const FinishArgs& fa) {
   __syncthreads();
 }
 
-template <int NX, int NB, int NBN>
+// Without a fused next layer and with groups of 8 edges (short epilogues,
+// frequent on graphs of short rows) the epilogue's arguments stay in the
+// kernel's scalar registers and alpha, bias and alpha_self of a lane's
+// columns in its registers: a kernel-argument read and LDS reads at every
+// finished row measured slower there (arxiv-shaped, 123 -> 139-144 us), and
+// these variants have the registers to spare.  finish_row's EPI_LDS says
+// which form it takes.
+template <int NB>
+struct EpiRegs {
+  float alpha[NB], bias[NB], alpha_s[NB];
+};
+template <int NB>
+__device__ inline void make_epi_regs(EpiRegs<NB>& er, const FinishArgs& fa, int lane) {
+#pragma unroll
+  for (int c = 0; c < NB; ++c) {
+    const int k = lane + 64 * c;
+    const bool ok = k < fa.d;
+    er.alpha[c] = ok ? fa.alpha[k] : 0.f;
+    er.bias[c] = ok && fa.bias != nullptr ? fa.bias[k] : 0.f;
+    er.alpha_s[c] = ok && fa.alpha_s != nullptr ? fa.alpha_s[k] : 0.f;
+  }
+}
+
+template <int NX, int NB, int NBN, bool EPI_LDS>
 __device__ inline void finish_row(int64_t r, int64_t deg, const float4_t acc,
-                                  const float (*s_epi)[256], const NextRegs& nr, int lane) {
-  const FinishArgs fa = fresh_finish();  // the calling kernel's first argument
+                                  const float (*s_epi)[256], const EpiRegs<NB>& er,
+                                  const NextRegs& nr, const FinishArgs& fa_arg, int lane) {
+  // EPI_LDS: the arguments are read afresh (see FinishArgs) and alpha /
+  // bias come from LDS; else from the kernel argument's scalar registers
+  // and the lane's registers (EpiRegs).
+  const FinishArgs fa = EPI_LDS ? fresh_finish() : fa_arg;
   const NextLayer& nx = fa.nx;
   bool valid[NB];  // column lane + 64c < d
 #pragma unroll
@@ -1300,14 +1327,15 @@ __device__ inline void finish_row(int64_t r, int64_t deg, const float4_t acc,
     const float gi = fabsf(nx.gself[dst]);
 #pragma unroll
     for (int c = 0; c < NB; ++c)
-      self[c] = valid[c] ? gi * s_epi[2][lane + 64 * c] *
+      self[c] = valid[c] ? gi * (EPI_LDS ? s_epi[2][lane + 64 * c] : er.alpha_s[c]) *
                                (float)nx.Cself[dst * nx.ldself + lane + 64 * c]
                          : 0.f;
   }
   float v[NB];
 #pragma unroll
   for (int c = 0; c < NB; ++c) {
-    const float al = s_epi[0][lane + 64 * c], bi = s_epi[1][lane + 64 * c];
+    const float al = EPI_LDS ? s_epi[0][lane + 64 * c] : er.alpha[c];
+    const float bi = EPI_LDS ? s_epi[1][lane + 64 * c] : er.bias[c];
     float t = deg > 0 ? fmaf(acc[c], rowfac * al, bi) : bi;
     if (NX == 2) t += self[c];
     v[c] = act(t, fa.relu);
@@ -1454,7 +1482,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
   int32_t jB = ld_idx(64);
   NextRegs nr = {};
   if (NX == 1) load_next_weights<NB, NBN>(nr, fa.nx.dn, sBn, Bn, ldbn, fa.d, lane);
-  stage_epi(s_epi, fa);
+  constexpr bool kEpiLds = NX == 1 || U == 16;  // where finish_row reads alpha / bias
+  if constexpr (kEpiLds) stage_epi(s_epi, fa);
+  EpiRegs<NB> er = {};
+  if constexpr (!kEpiLds) make_epi_regs<NB>(er, fa, lane);
   if (!live) return;
   const int rb8 = (int)ldc8;
   const int rb16 = (int)(ldc16 * 2);
@@ -1480,7 +1511,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
   const float4_t zero4 = {0.f, 0.f, 0.f, 0.f};
   if (!before) {
     for (int64_t q = r - 1; q >= 0 && rowptr[q] == s; --q)
-      finish_row<NX, NB, NBN>(q, 0, zero4, s_epi, nr, lane);
+      finish_row<NX, NB, NBN, kEpiLds>(q, 0, zero4, s_epi, er, nr, fa, lane);
   }
   float4_t a0 = zero4, a1 = zero4;
   float gsum = 0.f;  // sum of g_j over the current row (for the parity term)
@@ -1532,7 +1563,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
           if (before) {
             store_partial<NB>(head + w * dpad + NB * lane, sum);
           } else {
-            finish_row<NX, NB, NBN>(r, cur_end - cur_beg, sum, s_epi, nr, lane);
+            finish_row<NX, NB, NBN, kEpiLds>(r, cur_end - cur_beg, sum, s_epi, er, nr, fa, lane);
           }
           a0 = zero4;
           a1 = zero4;
@@ -1548,7 +1579,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
             }
             cur_end = __builtin_amdgcn_readlane(win, (int)(r - rbase));
             if (cur_end == eu)
-              finish_row<NX, NB, NBN>(r, 0, zero4, s_epi, nr, lane);
+              finish_row<NX, NB, NBN, kEpiLds>(r, 0, zero4, s_epi, er, nr, fa, lane);
           } while (cur_end == eu);
         }
         float gj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
@@ -1591,11 +1622,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
     if (before) {
       store_partial<NB>(head + w * dpad + NB * lane, sum);
     } else {
-      finish_row<NX, NB, NBN>(r, cur_end - cur_beg, sum, s_epi, nr, lane);
+      finish_row<NX, NB, NBN, kEpiLds>(r, cur_end - cur_beg, sum, s_epi, er, nr, fa, lane);
     }
     if (t == nnz)
       for (int64_t q = r + 1; q < n; ++q)
-        finish_row<NX, NB, NBN>(q, 0, zero4, s_epi, nr, lane);
+        finish_row<NX, NB, NBN, kEpiLds>(q, 0, zero4, s_epi, er, nr, fa, lane);
     if (lane == 0) tail_row[w] = -1;
   } else if (before) {
     store_partial<NB>(head + w * dpad + NB * lane, sum);
@@ -1622,7 +1653,10 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
   const int lane = threadIdx.x & 63;
   NextRegs nr = {};
   if (NX == 1) load_next_weights<NB, NBN>(nr, fa.nx.dn, sBn, Bn, ldbn, fa.d, lane);
-  stage_epi(s_epi, fa);
+  constexpr bool kEpiLds = NX == 1;  // where finish_row reads alpha / bias
+  if constexpr (kEpiLds) stage_epi(s_epi, fa);
+  EpiRegs<NB> er = {};
+  if constexpr (!kEpiLds) make_epi_regs<NB>(er, fa, lane);
   const int64_t w0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_index_in_block()) * 4;
   if (w0 >= workers) return;
   // lane q < 4: worker w0 + q's cut row and that row's bounds
@@ -1657,7 +1691,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
       for (int u = 0; u < 8; ++u) a += h[u];
     }
     for (; v <= wend; ++v) a += load_partial<NB>(head + v * dpad + NB * lane);
-    finish_row<NX, NB, NBN>(r, e - readlane64(bq, q), a, s_epi, nr, lane);
+    finish_row<NX, NB, NBN, kEpiLds>(r, e - readlane64(bq, q), a, s_epi, er, nr, fa, lane);
   }
 }
 
