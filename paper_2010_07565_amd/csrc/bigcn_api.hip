@@ -559,7 +559,10 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
         e = run_bgemm(F, n, L.ldF, ly.wbits, ly.d_out, ly.ldw, ly.d_in, C16, ct, L.ldc16,
                       BIGCN_BGEMM_AUTO, s);
       if (e != hipSuccess) return BIGCN_EHIP;
-      if (ly.wbits_self != nullptr) {  // the node's own products, exact in half
+      // the node's own products, exact in half, unless the aggregation forms
+      // them in its epilogue from F
+      if (ly.wbits_self != nullptr &&
+          !bigcn::self_in_epilogue_supported(nnz, ly.d_out, ly.d_in)) {
         e = run_bgemm(F, n, L.ldF, ly.wbits_self, ly.d_out, ly.ldw_self, ly.d_in,
                       ws + L.off_S, IType::F16, L.ldS, BIGCN_BGEMM_AUTO, s);
         if (e != hipSuccess) return BIGCN_EHIP;
@@ -574,10 +577,19 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
       fn.kind = kind;
       fn.slot = slot;
       if (ly.wbits_self != nullptr) {
-        fn.kind = 2;
-        fn.Cself = ws + L.off_S;
-        fn.ldself = L.ldS;
         fn.alpha_self = ly.alpha_self;
+        if (bigcn::self_in_epilogue_supported(nnz, ly.d_out, ly.d_in)) {
+          fn.kind = 3;
+          fn.F = F;
+          fn.ldF = L.ldF;
+          fn.wself = ly.wbits_self;
+          fn.ldw_self = ly.ldw_self;
+          fn.kin = ly.d_in;
+        } else {
+          fn.kind = 2;
+          fn.Cself = ws + L.off_S;
+          fn.ldself = L.ldS;
+        }
       } else if (kind != 0) {
         const bigcn_layer& nxt = layers[l + 1];
         const int nset = (l + 1) & 1;

@@ -71,6 +71,11 @@ hipError_t launch_bgemm_q8(const uint64_t* F, int64_t M, int64_t ldf,
 //   kind 2: no next layer; the rows get the self term of a two-weight
 //           GraphSAGE layer, |g_i| alpha_self[k] Cself[i][k], before bias and
 //           activation (Cself: exact half products with the self weights).
+//   kind 3: as kind 2, the self products formed in the epilogue from the
+//           layer's own packed signs F (row i at F + i ldF, the rows the
+//           aggregation's g and products use) and the self weights' packed
+//           W^T (wself [d][ldw_self], kin inputs) instead of read from Cself;
+//           see self_in_epilogue_supported.
 // g receives the next layer's per-node scale.
 struct FusedNext {
   int kind;
@@ -86,9 +91,19 @@ struct FusedNext {
   int64_t ldself;
   const float* alpha_self;
   // Source order (nullable): row r's next-layer products (kind 1) or self
-  // products and scale (kind 2) sit at row slot[r].
+  // products and scale (kinds 2, 3) sit at row slot[r].
   const int32_t* slot;
+  const uint64_t* F;      // kind 3
+  int64_t ldF;
+  const uint64_t* wself;
+  int64_t ldw_self;
+  int32_t kin;
 };
+// Layers whose self term kind 3 can form: the wide 8-bit aggregation (65-256
+// outputs) with the self weights' words per lane, ceil(kin / 64) times
+// q8_lane_bytes(d), at most 16 (kin <= 256 for 129-256 outputs, <= 512 for
+// 65-128), staged in LDS.
+bool self_in_epilogue_supported(int64_t nnz, int32_t d, int32_t kin);
 
 // Aggregation over the CSR of Â with the fused rescale / bias / activation
 // epilogue.  The edge range [0, nnz) is cut into fixed chunks of `chunk`

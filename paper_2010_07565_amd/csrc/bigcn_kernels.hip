@@ -1232,6 +1232,9 @@ struct NextLayer {
   const float* gself;     // NX == 2: per-node scale (its magnitude is β_i)
   const int32_t* slot;    // nullable: row r's next products / self products
                           // sit at row slot[r] (the source order), else at r
+  const uint64_t* F;      // NX == 3: the layer's packed signs, row r at F + r ldF
+  int64_t ldF;            // (r = slot[r] when slot is given)
+  int32_t kin;            // NX == 3: the layer's input width
 };
 
 // The next layer's weights as finish_row reads them.
@@ -1307,6 +1310,15 @@ __device__ inline void make_epi_regs(EpiRegs<NB>& er, const FinishArgs& fa, int 
   }
 }
 
+// The first kw of a row's NW packed words (zero past kw), the row address
+// the same in every lane: read-only, so they come through scalar loads.
+template <int NW>
+__device__ inline void load_row_words(uint64_t (&fw)[NW], const uint64_t* __restrict__ row,
+                                      int kw) {
+#pragma unroll
+  for (int w = 0; w < NW; ++w) fw[w] = w < kw ? row[w] : 0ull;
+}
+
 template <int NX, int NB, int NBN, bool EPI_LDS>
 __device__ inline void finish_row(int64_t r, int64_t deg, const float4_t acc,
                                   const float (*s_epi)[256], const EpiRegs<NB>& er,
@@ -1323,6 +1335,30 @@ __device__ inline void finish_row(int64_t r, int64_t deg, const float4_t acc,
   int64_t dst = r;  // row of the next products / self products
   if (NX != 0 && nx.slot != nullptr) dst = nx.slot[r];
   float self[NB];
+  if constexpr (NX == 3) {
+    // The two-weight layer's self products, formed here: the row's own
+    // packed signs (wave-uniform, scalar loads) against the self weights
+    // staged in LDS (NBN words per lane and column) -- the products Cself
+    // holds for NX == 2, exactly.
+    const int kws = (nx.kin + 63) >> 6;  // <= NBN
+    uint64_t fw[NBN];
+    load_row_words<NBN>(fw, nx.F + dst * nx.ldF, kws);
+    const float gi = fabsf(nx.gself[dst]);
+#pragma unroll
+    for (int c = 0; c < NB; ++c) {
+      uint32_t pc = 0;
+#pragma unroll
+      for (int w = 0; w < NBN; ++w) {
+        if (w >= kws) continue;  // wave-uniform
+        const uint64_t z = fw[w] ^ nr.sB[(w * NB + c) * 64 + lane];
+        pc += __builtin_popcount((uint32_t)z);
+        pc += __builtin_popcount((uint32_t)(z >> 32));
+      }
+      const int dot = nx.kin - 2 * (int)pc;
+      self[c] = valid[c] ? gi * (EPI_LDS ? s_epi[2][lane + 64 * c] : er.alpha_s[c]) * (float)dot
+                         : 0.f;
+    }
+  }
   if (NX == 2) {
     const float gi = fabsf(nx.gself[dst]);
 #pragma unroll
@@ -1337,7 +1373,7 @@ __device__ inline void finish_row(int64_t r, int64_t deg, const float4_t acc,
     const float al = EPI_LDS ? s_epi[0][lane + 64 * c] : er.alpha[c];
     const float bi = EPI_LDS ? s_epi[1][lane + 64 * c] : er.bias[c];
     float t = deg > 0 ? fmaf(acc[c], rowfac * al, bi) : bi;
-    if (NX == 2) t += self[c];
+    if (NX == 2 || NX == 3) t += self[c];
     v[c] = act(t, fa.relu);
   }
   if (NX != 1 || fa.out != nullptr) {
@@ -1482,7 +1518,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
   int32_t jB = ld_idx(64);
   NextRegs nr = {};
   if (NX == 1) load_next_weights<NB, NBN>(nr, fa.nx.dn, sBn, Bn, ldbn, fa.d, lane);
-  constexpr bool kEpiLds = NX == 1 || U == 16;  // where finish_row reads alpha / bias
+  // NX == 3: the self weights, NBN words by NB columns per lane, in LDS
+  if (NX == 3) load_next_weights<NBN, NB>(nr, fa.d, sBn, Bn, ldbn, fa.nx.kin, lane);
+  // where finish_row reads its arguments and alpha / bias (see EpiRegs)
+  constexpr bool kEpiLds = NX == 1 || NX == 3 || U == 16;
   if constexpr (kEpiLds) stage_epi(s_epi, fa);
   EpiRegs<NB> er = {};
   if constexpr (!kEpiLds) make_epi_regs<NB>(er, fa, lane);
@@ -1653,7 +1692,9 @@ __global__ __launch_bounds__(kBlock) void k_spmm_fix_q8(
   const int lane = threadIdx.x & 63;
   NextRegs nr = {};
   if (NX == 1) load_next_weights<NB, NBN>(nr, fa.nx.dn, sBn, Bn, ldbn, fa.d, lane);
-  constexpr bool kEpiLds = NX == 1;  // where finish_row reads alpha / bias
+  // NX == 3: the self weights, NBN words by NB columns per lane, in LDS
+  if (NX == 3) load_next_weights<NBN, NB>(nr, fa.d, sBn, Bn, ldbn, fa.nx.kin, lane);
+  constexpr bool kEpiLds = NX == 1 || NX == 3;  // where finish_row reads alpha / bias
   if constexpr (kEpiLds) stage_epi(s_epi, fa);
   EpiRegs<NB> er = {};
   if constexpr (!kEpiLds) make_epi_regs<NB>(er, fa, lane);
@@ -2830,6 +2871,9 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   nx.Cself = (const _Float16*)fn.Cself;
   nx.ldself = fn.ldself;
   nx.gself = g;
+  nx.F = fn.F;
+  nx.ldF = fn.ldF;
+  nx.kin = fn.kin;
   fa.out = out;
   fa.ldo = ldo;
   fa.alpha = alpha;
@@ -2838,8 +2882,13 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   fa.mean = mean;
   fa.relu = relu;
   fa.d = d;
-  const size_t lds = (NX > 0 && NB * NBN > 4)
+  // LDS for the weights finish_row multiplies with: the next layer's (NX 1,
+  // when a lane needs more than four words) or the self weights (NX 3)
+  const size_t lds = NX == 3 ? (size_t)((fn.kin + 63) >> 6) * NB * 64 * sizeof(uint64_t)
+                     : (NX > 0 && NB * NBN > 4)
                          ? (size_t)((d + 63) >> 6) * NBN * 64 * sizeof(uint64_t) : 0;
+  const uint64_t* wB = NX == 3 ? fn.wself : fn.wbits;
+  const int64_t ldB = NX == 3 ? fn.ldw_self : fn.ldw;
   dim3 grid((unsigned)((p.workers + kWavesPerBlock - 1) / kWavesPerBlock));
   // Gathers in flight per wave: groups of 16 edges where rows average at
   // least 64 entries (a group then almost always lies inside one row, and
@@ -2851,7 +2900,7 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
     constexpr int UV = decltype(u)::value, PV = decltype(par)::value;
     hipLaunchKernelGGL((k_spmm_wave_q8<UV, NX, NB, NBN, PV>), grid, dim3(kBlock), lds, stream,
                        fa, n, nnz, rowptr, colidx, g, C8, ldc8, (const _Float16*)C16, ldc16,
-                       PV, p.chunk, p.workers, p.dpad, tail_row, head, tail, fn.wbits, fn.ldw);
+                       PV, p.chunk, p.workers, p.dpad, tail_row, head, tail, wB, ldB);
   };
   using I8 = std::integral_constant<int, 8>;
   using I16 = std::integral_constant<int, 16>;
@@ -2869,7 +2918,7 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   hipLaunchKernelGGL((k_spmm_fix_q8<NX, NB, NBN>),
                      dim3((unsigned)((fix_waves + kWavesPerBlock - 1) / kWavesPerBlock)),
                      dim3(kBlock), lds, stream, fa, rowptr, p.chunk, p.workers, p.dpad,
-                     tail_row, head, tail, fn.wbits, fn.ldw);
+                     tail_row, head, tail, wB, ldB);
   return hipGetLastError();
 }
 
@@ -2885,6 +2934,9 @@ hipError_t spmm_q8_nb(int64_t n, int64_t nnz, const int64_t* rowptr,
                                  K, d, alpha, bias, relu, out, ldo, p, ws, fn, stream)
   if (fn.kind == 0) BIGCN_Q8S(0, 1);
   if (fn.kind == 2) BIGCN_Q8S(2, 1);
+  if constexpr (NB >= 2) {
+    if (fn.kind == 3) BIGCN_Q8S(3, 16 / NB);  // NBN: the self weights' words per lane
+  }
   switch (q8_lane_bytes(fn.d_out)) {
     case 1: BIGCN_Q8S(1, 1);
     case 2: BIGCN_Q8S(1, 2);
@@ -2961,6 +3013,11 @@ hipError_t spmm_narrow(int64_t n, const int64_t* rowptr, const int32_t* colidx, 
                                alpha, bias, relu, out, ldo, fn, stream);
 }
 
+bool self_in_epilogue_supported(int64_t nnz, int32_t d, int32_t kin) {
+  const int nb = q8_lane_bytes(d);
+  return nnz > 0 && d <= 256 && nb >= 2 && ((kin + 63) >> 6) * nb <= 16;
+}
+
 hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
                           const int32_t* colidx, int mean, const float* g,
                           const int8_t* C8, int64_t ldc8, const void* C16,
@@ -2971,6 +3028,7 @@ hipError_t launch_spmm_q8(int64_t n, int64_t nnz, const int64_t* rowptr,
   if (n == 0) return hipSuccess;
   FusedNext none = {};
   const FusedNext& fn = next != nullptr ? *next : none;
+  if (fn.kind == 3 && !self_in_epilogue_supported(nnz, d, fn.kin)) return hipErrorInvalidValue;
   if (nnz == 0 && fn.kind == 2) {
     const int64_t total = n * (int64_t)d;
     hipLaunchKernelGGL(k_sage_self_only, dim3((unsigned)((total + kBlock - 1) / kBlock)),
