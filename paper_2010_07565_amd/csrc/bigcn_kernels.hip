@@ -2906,10 +2906,17 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   using I16 = std::integral_constant<int, 16>;
   using P0 = std::integral_constant<int, 0>;
   using P1 = std::integral_constant<int, 1>;
-  const bool long_rows = nnz >= 64 * n;
-  if (long_rows) {
-    if (K & 1) launch(I16{}, P1{}); else launch(I16{}, P0{});
+  // (the self term formed in the epilogue keeps groups of 8: at 16 it would
+  // not fit the register budget)
+  bool long_rows = nnz >= 64 * n;
+  if constexpr (NX != 3) {
+    if (long_rows) {
+      if (K & 1) launch(I16{}, P1{}); else launch(I16{}, P0{});
+    }
   } else {
+    long_rows = false;
+  }
+  if (!long_rows) {
     if (K & 1) launch(I8{}, P1{}); else launch(I8{}, P0{});
   }
   hipError_t e = hipGetLastError();

@@ -659,13 +659,16 @@ def test_sage_layer_without_edges(dev):
     assert mass_error(out.cpu().numpy(), z, m) <= TOL
 
 
-def test_sage_forward_equals_chained_and_oracle(dev):
+@pytest.mark.parametrize("dims", [[200, 128, 64, 9], [201, 256, 129, 7]])
+def test_sage_forward_equals_chained_and_oracle(dev, dims):
     """A 3-layer two-weight GraphSAGE model through bigcn_forward equals the
     chained entry points bit for bit, and matches the oracle's free-running
-    forward (hidden sign flips only at legitimate near-zeros)."""
-    rng = np.random.default_rng(66)
+    forward (hidden sign flips only at legitimate near-zeros).  The forward
+    forms the self products of its 65-256-output layers in the aggregation
+    epilogue from the packed signs (odd K in the second shape), the chained
+    entry points read them from the half self products."""
+    rng = np.random.default_rng(66 + dims[0])
     g = _sage_graph(900, rng)
-    dims = [200, 128, 64, 9]
     x = rng.standard_normal((g.n, dims[0])).astype(np.float32)
     mu, rstd = workloads.bn_stats(x)
     wn = [workloads.glorot_t(dims[i], dims[i + 1], rng) for i in range(3)]
