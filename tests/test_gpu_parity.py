@@ -68,6 +68,47 @@ def test_pack_matches_oracle(dev, rows, cols, mode):
     assert np.all(np.abs(got - want) <= 1e-5 * np.abs(want) + 1e-30)
 
 
+def _fixed_tree_mean_abs(x):
+    """Mean |x| of each row formed in float32 in the kernels' fixed order
+    (test-side restatement of that order, not of the method: the oracle's
+    beta is fp64): lane l of a 64-lane wave adds |x[64 w + l]| over words w
+    in order; then lanes pair by xor 1, xor 2, their 8-lane halves, their 16-
+    lane rows, and the four rows add as (r0 + r1) + (r2 + r3)."""
+    rows, cols = x.shape
+    kw = (cols + 63) // 64
+    pad = np.zeros((rows, kw * 64), dtype=np.float32)
+    pad[:, :cols] = np.abs(x)
+    lanes = np.zeros((rows, 64), dtype=np.float32)
+    for w in range(kw):
+        lanes = (lanes + pad[:, 64 * w:64 * w + 64]).astype(np.float32)
+    v = lanes.reshape(rows, 4, 16)             # four rows of 16 lanes
+    q = (v[..., 0::2] + v[..., 1::2]).astype(np.float32)            # xor 1
+    q = (q[..., 0::2] + q[..., 1::2]).astype(np.float32)            # xor 2: quads
+    q = (q[..., 0::2] + q[..., 1::2]).astype(np.float32)            # 8-lane halves
+    r = (q[..., 0] + q[..., 1]).astype(np.float32)                  # 16-lane rows
+    tot = ((r[:, 0] + r[:, 1]).astype(np.float32) + (r[:, 2] + r[:, 3]).astype(np.float32))
+    return (tot.astype(np.float32) / np.float32(cols)).astype(np.float32)
+
+
+@pytest.mark.parametrize("cols", [100, 200, 256, 500, 700])
+def test_pack_scale_follows_fixed_order(dev, cols):
+    """The pack's row scale, bit for bit, is the float32 mean |x| summed in the
+    fixed order every kernel that forms a scale uses (so that a layer packed
+    on its own and one formed in an aggregation epilogue agree bit for bit);
+    the widths cover row groups of 8, 4, 2 and 1 rows per wave."""
+    rng = np.random.default_rng(cols)
+    rows = 301                                  # a ragged last row group
+    x = (rng.standard_normal((rows, cols)) * rng.uniform(0.01, 100.0, (rows, 1))).astype(
+        np.float32)
+    kw = (cols + 63) // 64
+    bits = torch.zeros((rows, kw), dtype=torch.int64, device=dev)
+    scale = torch.zeros(rows, dtype=torch.float32, device=dev)
+    bg.bigcn_binarize_pack(_t(x, dev), bits, scale)
+    torch.cuda.synchronize()
+    assert np.array_equal(scale.cpu().numpy().view(np.uint32),
+                          _fixed_tree_mean_abs(x).view(np.uint32))
+
+
 def test_pack_strided_input(dev):
     rng = np.random.default_rng(5)
     big = rng.standard_normal((50, 300)).astype(np.float32)
