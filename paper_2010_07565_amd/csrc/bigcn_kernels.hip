@@ -1781,6 +1781,89 @@ __device__ inline uint64_t dpp_u64(uint64_t v) {
   return ((uint64_t)hi << 32) | lo;
 }
 
+// Lane swaps between two registers: swap32 exchanges lanes 32..63 of a with
+// lanes 0..31 of b; swap16 exchanges the odd 16-lane rows of a with the even
+// rows of b.  (The results are read into scalars before the bit casts.)
+__device__ inline void swap32(float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, a),
+                                                  __builtin_bit_cast(uint32_t, b), false, false);
+  const uint32_t x = r[0], y = r[1];
+  a = __builtin_bit_cast(float, x);
+  b = __builtin_bit_cast(float, y);
+}
+__device__ inline void swap16(float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(uint32_t, a),
+                                                  __builtin_bit_cast(uint32_t, b), false, false);
+  const uint32_t x = r[0], y = r[1];
+  a = __builtin_bit_cast(float, x);
+  b = __builtin_bit_cast(float, y);
+}
+
+// v[k] summed over the 64 / G lanes that share lane % G, the result in every
+// lane, for CPL values per lane (CPL a multiple of 4; the whole wave active).
+// A reduce-scatter first halves the values per lane twice (wave halves, then
+// pairs of 16-lane rows: after it lane l holds value i + (CPL/4)(row & 1) +
+// (CPL/2)(row >> 1) for i < CPL/4), the rows are then summed by rotations
+// within the row, and the same two swaps bring every value back to every
+// lane.  One swap or add per value and step instead of a lane exchange and
+// an add per value for each of the six slot bits.
+template <int G, int CPL>
+__device__ inline void slot_allreduce(float (&v)[CPL]) {
+  static_assert(CPL % 4 == 0, "values per lane");
+  constexpr int H = CPL / 2, Q = CPL / 4;
+  float h[H];
+#pragma unroll
+  for (int i = 0; i < H; ++i) {
+    float a = v[i], b = v[i + H];
+    swap32(a, b);
+    h[i] = a + b;  // lanes 0..31: value i, lanes 32..63: value i + H
+  }
+  float p[Q];
+#pragma unroll
+  for (int i = 0; i < Q; ++i) {
+    float a = h[i], b = h[i + Q];
+    swap16(a, b);
+    p[i] = a + b;
+  }
+#pragma unroll
+  for (int i = 0; i < Q; ++i) {
+    if constexpr (G <= 1) p[i] += dpp<0x121>(p[i]);  // row_ror:1
+    if constexpr (G <= 2) p[i] += dpp<0x122>(p[i]);  // row_ror:2
+    if constexpr (G <= 4) p[i] += dpp<0x124>(p[i]);  // row_ror:4
+    p[i] += dpp<0x128>(p[i]);                        // row_ror:8
+  }
+#pragma unroll
+  for (int i = 0; i < Q; ++i) {
+    float a = p[i], b = p[i];
+    swap16(a, b);
+    h[i] = a;
+    h[i + Q] = b;
+  }
+#pragma unroll
+  for (int i = 0; i < H; ++i) {
+    float a = h[i], b = h[i];
+    swap32(a, b);
+    v[i] = a;
+    v[i + H] = b;
+  }
+}
+
+// One value per lane summed over the lanes that share lane % G, in every lane.
+template <int G>
+__device__ inline float slot_allreduce1(float t) {
+  float a = t, b = t;
+  swap32(a, b);
+  t = a + b;
+  a = t;
+  b = t;
+  swap16(a, b);
+  t = a + b;
+  if constexpr (G <= 1) t += dpp<0x121>(t);
+  if constexpr (G <= 2) t += dpp<0x122>(t);
+  if constexpr (G <= 4) t += dpp<0x124>(t);
+  return t + dpp<0x128>(t);
+}
+
 // Gathered code rows land in LDS (buffer loads with the lds modifier: lane
 // l's bytes go to base + size * l, a range past the buffer gives zeros), so
 // a wave keeps NB rows per lane in flight without holding them in
@@ -2327,12 +2410,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
           add_edges4(tmp, tg, k, ok, ip);
         }
         if (__builtin_amdgcn_readlane(ce, ld) <= cbase + nk) {  // the row ends here
-#pragma unroll
-          for (int m = G; m < 64; m <<= 1) {
-#pragma unroll
-            for (int k = 0; k < CPL; ++k) tmp[k] += __shfl_xor(tmp[k], m);
-            tg += __shfl_xor(tg, m);
-          }
+          slot_allreduce<G, CPL>(tmp);
+          // the sum of g is used for odd K only (fpar = 0 otherwise)
+          if (par != 0) tg = slot_allreduce1<G>(tg);
           if (q == ld / G) {
 #pragma unroll
             for (int k = 0; k < CPL; ++k) acc[k] = tmp[k];

@@ -411,7 +411,12 @@ def _long_rows(rng):
 
 
 @pytest.mark.parametrize("d,K,norm,act", [(256, 256, "sym", "none"), (256, 301, "mean", "relu"),
-                                          (129, 602, "sym", "relu"), (65, 255, "mean", "none")])
+                                          (129, 602, "sym", "relu"), (65, 255, "mean", "none"),
+                                          # at most 64 columns: long rows summed by all
+                                          # slots of a wave, for each slot width
+                                          (47, 256, "mean", "none"), (41, 255, "sym", "relu"),
+                                          (20, 301, "mean", "relu"), (13, 64, "sym", "none"),
+                                          (6, 5, "mean", "none"), (3, 1433, "sym", "relu")])
 def test_spmm_q8_long_rows_matches_oracle(dev, d, K, norm, act):
     rng = np.random.default_rng(7 * d + K)
     _check_spmm_q8(dev, _long_rows(rng), rng, d, K, norm, act)
