@@ -1490,8 +1490,12 @@ __device__ inline int64_t readlane64(int64_t v, int l) {
 // (find_row: no row plan is needed); finished rows go through
 // finish_row<NX, NB, NBN>.  P = K mod 2 (the parity p): for even K the
 // p * sum g term is zero and its running sum is not kept.
+// Occupancy: 8 waves per SIMD for groups of 8 edges fusing the next layer's
+// pack and GEMM (their SGPRs then fit 8 waves; on the arxiv-shaped graph the
+// forward pass measured 0.520 -> 0.500 ms, the products-shaped one within
+// noise), else 6 (groups of 16 at 8 waves spill in the edge loop).
 template <int U, int NX, int NB, int NBN, int P>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) void k_spmm_wave_q8(
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(U == 8 && NX == 1 ? 8 : 6))) void k_spmm_wave_q8(
     FinishArgs fa, int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, const float* __restrict__ g,
     const int8_t* __restrict__ C8, int64_t ldc8, const _Float16* __restrict__ C16,
@@ -2987,9 +2991,11 @@ hipError_t spmm_q8_nx(int64_t n, int64_t nnz, const int64_t* rowptr,
   using P0 = std::integral_constant<int, 0>;
   using P1 = std::integral_constant<int, 1>;
   // (the self term formed in the epilogue keeps groups of 8: at 16 it would
-  // not fit the register budget)
+  // not fit the register budget; so do layers of at most 64 columns, which
+  // come here only for graphs of 2^31 entries or more: their 16-edge loop
+  // indexed its codes through scratch memory)
   bool long_rows = nnz >= 64 * n;
-  if constexpr (NX != 3) {
+  if constexpr (NX != 3 && NB >= 2) {
     if (long_rows) {
       if (K & 1) launch(I16{}, P1{}); else launch(I16{}, P0{});
     }
