@@ -1491,11 +1491,14 @@ __device__ inline int64_t readlane64(int64_t v, int l) {
 // finish_row<NX, NB, NBN>.  P = K mod 2 (the parity p): for even K the
 // p * sum g term is zero and its running sum is not kept.
 // Occupancy: 8 waves per SIMD for groups of 8 edges fusing the next layer's
-// pack and GEMM (their SGPRs then fit 8 waves; on the arxiv-shaped graph the
-// forward pass measured 0.520 -> 0.500 ms, the products-shaped one within
-// noise), else 6 (groups of 16 at 8 waves spill in the edge loop).
+// pack and GEMM, or the GraphSAGE self term for even K (their SGPRs then fit
+// 8 waves; on the arxiv-shaped graph the forward pass measured 0.520 ->
+// 0.500 ms, the GraphSAGE one 0.736 -> 0.712 ms, the products-shaped one
+// within noise), else 6 (groups of 16, and the odd-K self term, spill in the
+// edge loop at 8 waves).
 template <int U, int NX, int NB, int NBN, int P>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(U == 8 && NX == 1 ? 8 : 6))) void k_spmm_wave_q8(
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
+    U == 8 && (NX == 1 || (NX == 3 && P == 0)) ? 8 : 6))) void k_spmm_wave_q8(
     FinishArgs fa, int64_t n, int64_t nnz, const int64_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, const float* __restrict__ g,
     const int8_t* __restrict__ C8, int64_t ldc8, const _Float16* __restrict__ C16,
