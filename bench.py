@@ -39,7 +39,8 @@ Prints one JSON line.  Besides the forward-pass throughput it carries
  - "cpu_baseline": the plain CPU oracle timed on this host: whole forward
    passes of the same workload, repeated for --cpu-budget seconds (a
    single pass when one takes longer), with the thread count and the host
-   CPU model.
+   CPU model; for graphs of at most 200 K nodes also on one thread
+   ("single_thread").
 
     python bench.py --bgemm-ab
 
@@ -348,16 +349,14 @@ def host_cpu_model():
     return None
 
 
-def cpu_baseline(w, budget_s=10.0):
-    """The oracle on this host, whole forward passes of the same workload:
-    passes are repeated until budget_s has elapsed (one pass when a single
-    pass takes longer).  Each layer's double-precision arrays are dropped as
-    soon as the next layer has its input, as a caller of the per-layer chain
-    may.  Returns nodes per second over the timed passes."""
+def _time_oracle_passes(w, budget_s):
+    """Whole oracle forward passes of workload w, repeated until budget_s has
+    elapsed (one pass when a single pass takes longer).  Each layer's
+    double-precision arrays are dropped as soon as the next layer has its
+    input, as a caller of the per-layer chain may.  Returns (passes, s)."""
     import oracle
 
     g = w.graph
-    cores = oracle.threads()
     sage = w.weights_self_t is not None
     t0 = time.time()
     reps = 0
@@ -373,11 +372,32 @@ def cpu_baseline(w, budget_s=10.0):
         reps += 1
         if time.time() - t0 >= budget_s or reps >= 10_000:
             break
-    dt = time.time() - t0
-    return dict(value=g.n * reps / dt, unit="nodes/s", cores=cores, kind="oracle",
-                cpu_model=host_cpu_model(),
-                sample="whole %d-node forward pass x %d in %.1f s (plain oracle, not a "
-                       "tuned CPU library; %d OpenMP threads)" % (g.n, reps, dt, cores))
+    return reps, time.time() - t0
+
+
+def cpu_baseline(w, budget_s=10.0, single_thread_max_nodes=200_000):
+    """The oracle on this host, whole forward passes of the same workload on
+    every OpenMP thread (nodes per second over the timed passes).  Graphs of
+    at most single_thread_max_nodes nodes are also timed on one thread."""
+    import oracle
+
+    g = w.graph
+    cores = oracle.threads()
+    reps, dt = _time_oracle_passes(w, budget_s)
+    out = dict(value=g.n * reps / dt, unit="nodes/s", cores=cores, kind="oracle",
+               cpu_model=host_cpu_model(),
+               sample="whole %d-node forward pass x %d in %.1f s (plain oracle, not a "
+                      "tuned CPU library; %d OpenMP threads)" % (g.n, reps, dt, cores))
+    if g.n <= single_thread_max_nodes:
+        oracle.set_threads(1)
+        try:
+            reps1, dt1 = _time_oracle_passes(w, budget_s)
+        finally:
+            oracle.set_threads(cores)
+        out["single_thread"] = dict(
+            value=g.n * reps1 / dt1, unit="nodes/s", cores=1,
+            sample="whole %d-node forward pass x %d in %.1f s on one thread" % (g.n, reps1, dt1))
+    return out
 
 
 def main():

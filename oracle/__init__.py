@@ -67,6 +67,8 @@ def _load():
                                               _i32, _p, _p, _int] + [_p] * 9
         lib.oracle_threads.restype = _int
         lib.oracle_threads.argtypes = []
+        lib.oracle_set_threads.restype = None
+        lib.oracle_set_threads.argtypes = [_int]
         _lib = lib
     return _lib
 
@@ -74,6 +76,11 @@ def _load():
 def threads() -> int:
     """Threads the oracle's OpenMP loops use."""
     return _load().oracle_threads()
+
+
+def set_threads(n: int) -> None:
+    """Sets the threads the oracle's OpenMP loops use from now on (n >= 1)."""
+    _load().oracle_set_threads(int(n))
 
 
 def _ptr(a):

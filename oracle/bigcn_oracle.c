@@ -544,3 +544,6 @@ done:
 
 /* Number of threads the oracle's parallel loops use. */
 int oracle_threads(void) { return omp_get_max_threads(); }
+
+/* Sets that number (n >= 1) for the calls that follow on this thread. */
+void oracle_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }

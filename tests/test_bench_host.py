@@ -67,3 +67,19 @@ def test_committed_traffic_summaries_parse():
         for e in rec["entries"]:
             assert e["fetch_bytes"] > 0 and e["write_bytes"] > 0
             assert e["entry"] in ("pack", "bgemm", "spmm")
+
+
+def test_cpu_baseline_times_small_graphs_on_one_thread_too():
+    # the oracle's thread count is restored after the one-thread passes
+    import oracle
+    import workloads
+    w = workloads.make_workload(1)
+    before = oracle.threads()
+    r = bench.cpu_baseline(w, budget_s=0.0)
+    assert oracle.threads() == before
+    assert r["kind"] == "oracle" and r["cores"] == before and r["value"] > 0
+    one = r["single_thread"]
+    assert one["cores"] == 1 and one["value"] > 0 and one["unit"] == "nodes/s"
+    # above the size limit only the all-threads figure is taken
+    r = bench.cpu_baseline(w, budget_s=0.0, single_thread_max_nodes=w.n - 1)
+    assert "single_thread" not in r
