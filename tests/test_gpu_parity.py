@@ -422,6 +422,63 @@ def test_spmm_q8_long_rows_matches_oracle(dev, d, K, norm, act):
     _check_spmm_q8(dev, _long_rows(rng), rng, d, K, norm, act)
 
 
+def test_spmm_q8_beyond_int32_edges(dev):
+    """More than 2^31 CSR entries, the largest edge offsets the aggregation
+    meets: a layer of at most 64 columns then leaves the narrow kernel (its
+    edge offsets are 32-bit) for the wave-per-edge one.  2^21 rows of 1024
+    entries, an empty row and a row of 3; 47 columns, odd K with rows that
+    need their exact products; checked against the oracle on sampled rows."""
+    n = (1 << 21) + 2
+    deg = np.full(n, 1024, dtype=np.int64)
+    deg[0] = 0
+    deg[-1] = 3
+    rowptr = np.zeros(n + 1, dtype=np.int64)
+    np.cumsum(deg, out=rowptr[1:])
+    nnz = int(rowptr[-1])
+    assert nnz > (1 << 31)
+    rng = np.random.default_rng(2031)
+    # 2^31 uniform sources, drawn on the GPU by a seeded generator (a host
+    # draw takes over a minute) and copied back once for the oracle
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2031)
+    cols = torch.randint(0, n, (nnz,), dtype=torch.int32, device=dev, generator=gen)
+    colidx = cols.cpu().numpy()
+    d, K, norm, act = 47, 301, "mean", "relu"
+    par = K & 1
+    dot = 2 * rng.integers(-60, 61, size=(n, d)) + par
+    # exact products needed: random sources and some of rows 1, 2 and n - 1
+    big_rows = np.concatenate([rng.choice(n, size=64, replace=False),
+                               colidx[[rowptr[1], rowptr[2] + 7, rowptr[n - 1]]]])
+    dot[big_rows, 0] = K
+    beta = rng.uniform(0.1, 2.0, n).astype(np.float32).astype(np.float64)
+    alpha = rng.uniform(0.1, 2.0, d).astype(np.float32)
+    bias = rng.uniform(-0.1, 0.1, d).astype(np.float32)
+    ids = np.unique(np.concatenate([[0, 1, 2, n - 2, n - 1],
+                                    rng.choice(n, size=250, replace=False)]))
+    z, m, _ = oracle.aggregate(rowptr, colidx, norm, beta, alpha.astype(np.float64), dot,
+                               bias, act, ids=ids)
+    gg = beta.astype(np.float32)
+    flag = (np.abs(dot) > 255).any(axis=1)
+    gg[flag] = -np.abs(gg[flag])
+    W = bg.q8_row(d)
+    pos = il_pos(d)
+    c8 = np.zeros((n, W), dtype=np.int8)
+    c8[:, pos] = np.clip((dot - par) // 2, -128, 127).astype(np.int8)
+    c16 = np.zeros((n, W), dtype=np.float16)
+    c16[:, pos] = np.where(flag[:, None], dot, 0).astype(np.float16)
+    del dot
+    out = torch.full((n, d), float("nan"), dtype=torch.float32, device=dev)
+    ws = torch.empty(bg.spmm_workspace_bytes(n, nnz, d), dtype=torch.uint8, device=dev)
+    bg.bigcn_spmm_csr_q8(_t(rowptr, dev), cols, _t(gg, dev), _t(c8, dev), _t(c16, dev), K,
+                         _t(alpha, dev), out, ws, _t(bias, dev), norm, act)
+    torch.cuda.synchronize()
+    got = out[torch.from_numpy(ids).to(dev)].cpu().numpy()
+    del out, ws, cols
+    torch.cuda.empty_cache()
+    err = mass_error(got, z, m, relu=True)
+    assert err <= TOL, err
+
+
 def _check_spmm_q8(dev, g, rng, d, K, norm, act):
     par = K & 1
     dot = 2 * rng.integers(-60, 61, size=(g.n, d)) + par
