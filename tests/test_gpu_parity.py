@@ -35,7 +35,7 @@ def _colnorm(rowptr):
 # ------------------------------------------------------------------- pack --
 
 PACK_SHAPES = [(1, 1), (3, 63), (5, 64), (7, 65), (130, 127), (257, 128),
-               (100, 500), (33, 1433), (20, 4200)]
+               (100, 500), (33, 1433), (20, 4200), (9, 8192)]
 
 
 @pytest.mark.parametrize("rows,cols", PACK_SHAPES)
