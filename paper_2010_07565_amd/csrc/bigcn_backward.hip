@@ -8,11 +8,13 @@
 //   dζ    = Ã^T G                                (the edge-chunked aggregation
 //                                                 of bigcn_kernels.hip on fp32
 //                                                 rows; Â structurally symmetric)
-//   dW~^T = (H~^T dζ)^T,  H~ = diag(β) F         (fp32 MFMA, 64-row runs added
-//                                                 to fp64 partial sums per chunk
-//                                                 of rows, summed in order)
+//   dW~^T = (H~^T dζ)^T,  H~ = diag(β) F         (bf16 MFMA on the exact
+//                                                 three-piece split of the fp32
+//                                                 operand; 64-row runs added to
+//                                                 fp64 partial sums per chunk of
+//                                                 rows, summed in order)
 //   dH~   = dζ W~^T,      W~ = B diag(α);  dH = dH~ 1[|dH~| < 1]   (Eq. (14);
-//                                                 fp32 MFMA)
+//                                                 bf16 MFMA, the same split)
 //   dW    = Eq. (15) with 1[|W| < 1] for the derivative of sign.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -98,27 +100,65 @@ __global__ __launch_bounds__(kB) void k_bwd_colsum_final(
 
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
-// ±1 in fp32 from bit sh of dw: a set bit (sign +1) gives +1.0f, a clear bit
-// -1.0f (the bit moved to the sign position, then flipped with the pattern
-// of -1.0f).
-__device__ inline float pm1(uint32_t dw, int sh) {
-  return __builtin_bit_cast(float, ((dw >> sh) << 31) ^ 0xBF800000u);
+// bf16 operands of the 16x16x32 matrix-core product: lane (m, q) holds eight
+// consecutive K entries 8q .. 8q+7 of its A row m / B column m.
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16v2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 values rounded to nearest bf16 and packed, and those two bf16
+// values back in fp32 (the packed halves moved into place).
+__device__ inline uint32_t pk_bf16(float a, float b, float& fa, float& fb) {
+  const f32x2_t v = {a, b};
+  const uint32_t p = __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16v2_t));
+  fa = __builtin_bit_cast(float, p << 16);
+  fb = __builtin_bit_cast(float, p & 0xFFFF0000u);
+  return p;
 }
 
-// Bit k of a packed row, ±1: word k/64 of the row, already loaded in w[].
-__device__ inline float pm1_word(uint64_t w, int sh) {
-  return pm1(sh < 32 ? (uint32_t)w : (uint32_t)(w >> 32), sh & 31);
+// x = h + md + lo exactly for normal fp32 x: each piece is the remainder of
+// the previous ones rounded to bf16 (8 significant bits each; the
+// remainders are exact in fp32).  With a ±1 operand every piece's product
+// is exact, so three bf16 products accumulate the fp32 product.
+__device__ inline void split_bf16x3(const float (&x)[8], bf16x8_t& h, bf16x8_t& md,
+                                    bf16x8_t& lo) {
+  uint32_t ph[4], pm[4], pl[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float a0, a1, b0, b1, c0, c1;
+    ph[i] = pk_bf16(x[2 * i], x[2 * i + 1], a0, a1);
+    const float r0 = x[2 * i] - a0, r1 = x[2 * i + 1] - a1;
+    pm[i] = pk_bf16(r0, r1, b0, b1);
+    pl[i] = pk_bf16(r0 - b0, r1 - b1, c0, c1);
+  }
+  h = __builtin_bit_cast(bf16x8_t, ph);
+  md = __builtin_bit_cast(bf16x8_t, pm);
+  lo = __builtin_bit_cast(bf16x8_t, pl);
+}
+
+// ±1 in bf16 from bit sh of eight 32-bit words (a set bit gives +1: the bit
+// flips the sign of the pattern of -1).
+__device__ inline bf16x8_t pm1_bf16x8(const uint32_t (&w)[8], int sh) {
+  uint32_t p[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t b0 = (w[2 * i] >> sh) & 1u;
+    const uint32_t b1 = (w[2 * i + 1] >> sh) << 31;
+    p[i] = ((b0 << 15) | b1) ^ 0xBF80BF80u;
+  }
+  return __builtin_bit_cast(bf16x8_t, p);
 }
 
 // Partial sums of dW~^T over a chunk of R rows, on the matrix cores:
 //   part[c][j][k] = sum_{i in chunk c} s(F_i, k) * β_i dζ_ij.
-// One wave per (chunk c, 16 columns j, 16*NT bits k): fp32 MFMA 16x16x4 with
-// A[j][q] = β_i dζ_ij and B[q][k] = s(F_i, k) for the four rows i = r0+4s+q
-// of step s (lane group q); the products are exact (one operand is ±1).
-// Each run of 64 rows is summed in fp32 (64 terms per output) and added to
-// fp64 accumulators, runs in row order.  Lane (n, q) ends holding outputs
-// (4q + r, n) of each 16x16 tile.
-constexpr int kWtBatch = 16;  // row steps (4 rows each) whose loads are issued together
+// One wave per (chunk c, 16 columns j, 16*NT bits k): bf16 MFMA 16x16x32
+// with A[j][i] = β_i dζ_ij as three bf16 pieces (its exact split) and
+// B[i][k] = s(F_i, k) = ±1 over the 32 rows i = r0 + 32 t + 8q + u (u < 8)
+// of step t (lane group q), so every product is exact.  Each run of 64 rows
+// (two steps, all of its loads issued together) is summed in fp32 and added
+// to fp64 accumulators, runs in row order.  Lane (n, q) ends holding
+// outputs (4q + r, n) of each 16x16 tile.
+constexpr int kWtRun = 64;  // rows per fp32 run
 
 template <int NT>
 __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
@@ -146,33 +186,45 @@ __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
   for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc64[nt][r] = 0.0;
-  for (int64_t r0 = i0; r0 < i1; r0 += 64) {
+  for (int64_t r0 = i0; r0 < i1; r0 += kWtRun) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[nt] = float4_t{0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < 16; s0 += kWtBatch) {  // kWtBatch steps of loads in flight
-      // Loads at clamped (in-range) addresses with no branch, so all of the
-      // batch's loads are in flight together; rows past the chunk and
-      // columns past d_out are then zeroed by a 0/1 factor (a select would
-      // let the compiler move the loads into a branch and wait on each).
-      float a[kWtBatch];
-      uint64_t wd[kWtBatch][NW];
+    // Loads at clamped (in-range) addresses with no branch, so all of the
+    // run's loads are in flight together; rows past the chunk and columns
+    // past d_out are then zeroed by a 0/1 factor (a select would let the
+    // compiler move the loads into a branch and wait on each).
+    float a[kWtRun / 4];
+    uint64_t wd[kWtRun / 4][NW];
 #pragma unroll
-      for (int u = 0; u < kWtBatch; ++u) {
-        const int64_t row = r0 + 4 * (s0 + u) + q;
-        const int64_t rc = row < i1 ? row : i1 - 1;
-        a[u] = beta[rc] * dz[rc * lddz + jc] * (row < i1 && j < d_out ? 1.f : 0.f);
+    for (int u = 0; u < kWtRun / 4; ++u) {
+      const int64_t row = r0 + 32 * (u >> 3) + 8 * q + (u & 7);
+      const int64_t rc = row < i1 ? row : i1 - 1;
+      a[u] = beta[rc] * dz[rc * lddz + jc] * (row < i1 && j < d_out ? 1.f : 0.f);
 #pragma unroll
-        for (int w = 0; w < NW; ++w) wd[u][w] = F[rc * ldf + (w0 + w < kw ? w0 + w : kw - 1)];
-      }
-      __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any MFMA
+      for (int w = 0; w < NW; ++w) wd[u][w] = F[rc * ldf + (w0 + w < kw ? w0 + w : kw - 1)];
+    }
+    __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any MFMA
 #pragma unroll
-      for (int u = 0; u < kWtBatch; ++u)
+    for (int t = 0; t < kWtRun / 32; ++t) {
+      float x8[8];
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int sh = (k0 & 63) + 16 * (nt & 3) + m;
-          const float b = pm1_word(wd[u][nt >> 2], sh);
-          acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u], b, acc[nt], 0, 0, 0);
+      for (int u = 0; u < 8; ++u) x8[u] = a[8 * t + u];
+      bf16x8_t ah, am, alo;
+      split_bf16x3(x8, ah, am, alo);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int sh = (k0 & 63) + 16 * (nt & 3) + m;
+        uint32_t h32[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const uint64_t x = wd[8 * t + u][nt >> 2];
+          h32[u] = sh < 32 ? (uint32_t)x : (uint32_t)(x >> 32);
         }
+        const bf16x8_t b = pm1_bf16x8(h32, sh & 31);
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b, acc[nt], 0, 0, 0);
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, b, acc[nt], 0, 0, 0);
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, b, acc[nt], 0, 0, 0);
+      }
     }
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
@@ -243,13 +295,14 @@ __global__ __launch_bounds__(kB) void k_bwd_weights(
 }
 
 // dH~[i][k] = sum_j α_j dζ_ij s(B_j, k) and Eq. (14), on the matrix cores.
-// One wave per (16*RT rows, 16*NT columns k): fp32 MFMA 16x16x4 with
-// A[i][q] = α_j dζ_ij and B[q][k] = s(B_j, k) (exact products); each ±1
-// operand is built once and used by the RT row tiles.  Step s of a 32-wide
-// chunk of j gives lane group q the index j = j0 + 8q + s, so a lane's eight
-// A values of a row tile are two 16-byte loads of its row.  The packed
-// weight words and α sit in LDS (rows padded to a multiple of 32 with
-// zeros).  The sum over j runs in fp32, as a sequential sum would.
+// One wave per (16*RT rows, 16*NT columns k): bf16 MFMA 16x16x32 over each
+// 32-wide chunk of j with A[i][j] = α_j dζ_ij as three bf16 pieces (its
+// exact split) and B[j][k] = s(B_j, k) = ±1, so every product is exact and
+// the sum runs in fp32, as a sequential sum would; each ±1 operand is built
+// once and used by the RT row tiles and the three pieces.  Lane group q
+// takes j = j0 + 8q + s (s < 8), so a lane's eight A values of a row tile
+// are two 16-byte loads of its row.  The packed weight words and α sit in
+// LDS (rows padded to a multiple of 32 with zeros).
 template <int NT, int RT>
 __global__ __launch_bounds__(kB) void k_bwd_htilde_mfma(
     int64_t n, int32_t d_in, int32_t d_out, const float* __restrict__ dz, int64_t lddz,
@@ -314,27 +367,38 @@ __global__ __launch_bounds__(kB) void k_bwd_htilde_mfma(
       __builtin_amdgcn_sched_barrier(0);
       const float4_t al0 = *reinterpret_cast<const float4_t*>(sA + jb);
       const float4_t al1 = *reinterpret_cast<const float4_t*>(sA + jb + 4);
-      float a[RT][8];
+      bf16x8_t ah[RT], am[RT], alo[RT];
 #pragma unroll
-      for (int r = 0; r < RT; ++r)
+      for (int r = 0; r < RT; ++r) {
+        float a[8];
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
           const float v = s < 4 ? v0[r][s] : v1[r][s - 4];
           const float al = s < 4 ? al0[s] : al1[s - 4];
-          a[r][s] = jb + s < d_out ? al * v : 0.f;
+          a[s] = jb + s < d_out ? al * v : 0.f;
         }
+        split_bf16x3(a, ah[r], am[r], alo[r]);
+      }
+      uint64_t wd[8][NW];
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        uint64_t wd[NW];
+      for (int s = 0; s < 8; ++s)
 #pragma unroll
-        for (int w = 0; w < NW; ++w) wd[w] = w0 + w < kw ? sB[(jb + s) * kw + w0 + w] : 0ull;
+        for (int w = 0; w < NW; ++w) wd[s][w] = w0 + w < kw ? sB[(jb + s) * kw + w0 + w] : 0ull;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int sh = (k0 & 63) + 16 * (nt & 3) + m;
-          const float b = pm1_word(wd[nt >> 2], sh);
+      for (int nt = 0; nt < NT; ++nt) {
+        const int sh = (k0 & 63) + 16 * (nt & 3) + m;
+        uint32_t h32[8];
 #pragma unroll
-          for (int r = 0; r < RT; ++r)
-            acc[r][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[r][s], b, acc[r][nt], 0, 0, 0);
+        for (int s = 0; s < 8; ++s) {
+          const uint64_t x = wd[s][nt >> 2];
+          h32[s] = sh < 32 ? (uint32_t)x : (uint32_t)(x >> 32);
+        }
+        const bf16x8_t b = pm1_bf16x8(h32, sh & 31);
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+          acc[r][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[r], b, acc[r][nt], 0, 0, 0);
+          acc[r][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am[r], b, acc[r][nt], 0, 0, 0);
+          acc[r][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo[r], b, acc[r][nt], 0, 0, 0);
         }
       }
     }
