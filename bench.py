@@ -212,8 +212,9 @@ def backward_bench(w, model, x, rowptr, colidx, args, torch, bg, dev):
     """Every layer's bigcn_layer_backward on the workload's shapes: layer 0
     reads the features, deeper layers a seeded N(0,1) stand-in input, the
     incoming gradient is seeded N(0, 0.05^2).  All outputs are requested
-    (dH, dH~, dW, dW~, db, dzeta).  Per-layer durations from time_calls; a
-    step is the whole backward pass (the sum)."""
+    (dH, dH~, dW, dW~, db, dzeta), in the model's source order when it has
+    one.  Per-layer durations from time_calls; a step is the whole backward
+    pass (the sum)."""
     import numpy as np
     import workloads
     g = w.graph
@@ -239,7 +240,9 @@ def backward_bench(w, model, x, rowptr, colidx, args, torch, bg, dev):
         ws = torch.empty(bg.layer_backward_workspace_bytes(g.n, g.nnz, d_in, d_out),
                          dtype=torch.uint8, device=dev)
         t = time_calls(lambda: bg.bigcn_layer_backward(rowptr, colidx, h, wt_t, ly.wbits,
-                                                       ly.alpha, G, dwt, ws, w.norm, **outs),
+                                                       ly.alpha, G, dwt, ws, w.norm,
+                                                       slot=model.slot,
+                                                       colslot=model.colslot, **outs),
                        args.kernel_reps, torch)
         total += t
         flops = 2.0 * 2.0 * g.n * d_in * d_out          # dW~ and dH~ products

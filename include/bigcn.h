@@ -268,6 +268,10 @@ bigcn_status bigcn_spmm_csr_sage_q8(int64_t n, int64_t nnz, const int64_t* rowpt
  * The CSR of Â must be structurally symmetric (an undirected graph with its
  * self-loops, as for the forward); Ã and its normalisation as for
  * bigcn_spmm_csr.
+ *   slot, colslot  the source order of bigcn_source_slots, or both NULL:
+ *          G and the source factors are then staged in that order and dζ
+ *          gathers them through colslot (the same terms in the same order:
+ *          every result is identical either way).
  *   h      [n][ldh] fp32 layer input (before binarisation), ldh >= d_in
  *   wt     [d_out][ldwt] fp32 W^T; wbits [d_out][ldw], alpha fp32[d_out]:
  *          W^T packed by bigcn_binarize_pack
@@ -282,14 +286,16 @@ bigcn_status bigcn_spmm_csr_sage_q8(int64_t n, int64_t nnz, const int64_t* rowpt
  * Sums over nodes (db, dW~) are formed in fp64 over fixed chunks of rows
  * and added in order; every result is reproducible bit for bit.
  * Errors: EINVAL (bad sizes, NULL required pointers, short leading
- *         dimensions, bad norm / act), EALIGN (pointers not aligned to their
- *         element size, workspace not 256-byte aligned), EWORKSPACE,
- *         EUNSUPPORTED (d_in > 2048 or d_out > 256).
+ *         dimensions, bad norm / act, only one of slot / colslot), EALIGN
+ *         (pointers not aligned to their element size, workspace not
+ *         256-byte aligned), EWORKSPACE, EUNSUPPORTED (d_in > 2048 or
+ *         d_out > 256).
  * ------------------------------------------------------------------------- */
 size_t bigcn_layer_backward_workspace_bytes(int64_t n, int64_t nnz, int32_t d_in,
                                             int32_t d_out);
 bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
-                                  const int32_t* colidx, bigcn_norm norm, const float* h,
+                                  const int32_t* colidx, const int32_t* slot,
+                                  const int32_t* colslot, bigcn_norm norm, const float* h,
                                   int64_t ldh, int32_t d_in, const float* wt, int64_t ldwt,
                                   const uint64_t* wbits, int64_t ldw, const float* alpha,
                                   int32_t d_out, const float* gout, int64_t ldg,

@@ -87,7 +87,7 @@ def load() -> ctypes.CDLL:
     lib.bigcn_layer_backward_workspace_bytes.restype = _sz
     lib.bigcn_layer_backward_workspace_bytes.argtypes = [_i64, _i64, _i32, _i32]
     lib.bigcn_layer_backward.restype = _int
-    lib.bigcn_layer_backward.argtypes = ([_i64, _i64, _p, _p, _int, _p, _i64, _i32, _p, _i64,
+    lib.bigcn_layer_backward.argtypes = ([_i64, _i64, _p, _p, _p, _p, _int, _p, _i64, _i32, _p, _i64,
                                           _p, _i64, _p, _i32, _p, _i64, _p, _i64, _int]
                                          + [_p, _i64] * 4 + [_p, _p, _i64, _p, _sz, _p])
     lib.bigcn_spmm_csr_q8.restype = _int
@@ -298,14 +298,17 @@ def bigcn_layer_backward(rowptr: torch.Tensor, colidx: torch.Tensor, h: torch.Te
                          gout: torch.Tensor, dwt: torch.Tensor, workspace: torch.Tensor,
                          norm: str = "sym", act: str = "none", out=None, dh=None,
                          dh_tilde=None, dwt_tilde=None, db=None, dzeta=None,
-                         nnz: Optional[int] = None, stream=None) -> None:
-    """Back propagation of one binarised layer (Alg. 1, Eqs. (14)-(15))."""
+                         nnz: Optional[int] = None, stream=None, slot=None,
+                         colslot=None) -> None:
+    """Back propagation of one binarised layer (Alg. 1, Eqs. (14)-(15));
+    slot / colslot from bigcn_source_slots, or None for the node order."""
     n, d_in = h.shape
     d_out = wt.shape[0]
     nnz = colidx.shape[0] if nnz is None else nnz
     o = _ldn(out, "out")
     st = load().bigcn_layer_backward(
         n, nnz, _dev(rowptr, torch.int64, "rowptr"), _dev(colidx, torch.int32, "colidx"),
+        _dev(slot, torch.int32, "slot"), _dev(colslot, torch.int32, "colslot"),
         NORMS[norm], _dev(h, torch.float32, "h"), _ld(h, "h"), d_in,
         _dev(wt, torch.float32, "wt"), _ld(wt, "wt"), _dev(wbits, torch.int64, "wbits"),
         _ld(wbits, "wbits"), _dev(alpha, torch.float32, "alpha"), d_out,

@@ -34,12 +34,14 @@ inline int64_t words(int64_t k) { return (k + 63) / 64; }
 // Gm = G (zero where the ReLU output is not positive, and in the pad columns
 // up to ldm), unless Gm is null (G is then aggregated in place); s_i = the
 // source-side factor of Ã^T (D̂_ii^-1/2 symmetric, D̂_ii^-1 mean); ones = 1
-// (the per-column scale of the aggregation).
+// (the per-column scale of the aggregation).  With slot, node i's row of Gm
+// and its factor go to position slot[i] (the source order of the forward
+// pass), where the aggregation reads them through the column slots.
 __global__ __launch_bounds__(kB) void k_bwd_prep(
     int64_t n, int32_t d, const float* __restrict__ G, int64_t ldg,
     const float* __restrict__ out, int64_t ldo, int relu, float* __restrict__ Gm,
     int64_t ldm, const int64_t* __restrict__ rowptr, int mean, float* __restrict__ s,
-    float* __restrict__ ones) {
+    float* __restrict__ ones, const int32_t* __restrict__ slot) {
   const int64_t idx = (int64_t)blockIdx.x * kB + threadIdx.x;
   if (Gm != nullptr && idx < n * ldm) {
     const int64_t i = idx / ldm;
@@ -49,34 +51,37 @@ __global__ __launch_bounds__(kB) void k_bwd_prep(
       v = G[i * ldg + k];
       if (relu && !(out[i * ldo + k] > 0.f)) v = 0.f;
     }
-    Gm[idx] = v;
+    Gm[(slot != nullptr ? (int64_t)slot[i] : i) * ldm + k] = v;
   }
   if (idx < n) {
     const int64_t deg = rowptr[idx + 1] - rowptr[idx];
     const float dg = (float)deg;
-    s[idx] = deg > 0 ? (mean ? 1.0f / dg : 1.0f / sqrtf(dg)) : 0.f;
+    s[slot != nullptr ? (int64_t)slot[idx] : idx] =
+        deg > 0 ? (mean ? 1.0f / dg : 1.0f / sqrtf(dg)) : 0.f;
   }
   if (idx < d) ones[idx] = 1.f;
 }
 
 // Column sums of Gm over a chunk of R rows (block = chunk), fp64, rows in
-// order (eight loads in flight); then the chunks in order.
+// node order (row i at slot[i] when given; eight loads in flight); then the
+// chunks in order.
 __global__ __launch_bounds__(kB) void k_bwd_colsum_part(
     int64_t n, int32_t d, const float* __restrict__ Gm, int64_t ldm, int64_t R,
-    double* __restrict__ part) {
+    double* __restrict__ part, const int32_t* __restrict__ slot) {
   const int64_t c = blockIdx.x;
   const int64_t i0 = c * R, i1 = std::min<int64_t>(n, i0 + R);
+  auto row = [&](int64_t i) -> int64_t { return slot != nullptr ? (int64_t)slot[i] : i; };
   for (int k = threadIdx.x; k < d; k += kB) {
     double acc = 0.0;
     int64_t i = i0;
     for (; i + 8 <= i1; i += 8) {
       float v[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = Gm[(i + u) * ldm + k];
+      for (int u = 0; u < 8; ++u) v[u] = Gm[row(i + u) * ldm + k];
 #pragma unroll
       for (int u = 0; u < 8; ++u) acc += (double)v[u];
     }
-    for (; i < i1; ++i) acc += (double)Gm[i * ldm + k];
+    for (; i < i1; ++i) acc += (double)Gm[row(i) * ldm + k];
     part[c * d + k] = acc;
   }
 }
@@ -540,7 +545,8 @@ size_t bigcn_layer_backward_workspace_bytes(int64_t n, int64_t nnz, int32_t d_in
 }
 
 bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
-                                  const int32_t* colidx, bigcn_norm norm, const float* h,
+                                  const int32_t* colidx, const int32_t* slot,
+                                  const int32_t* colslot, bigcn_norm norm, const float* h,
                                   int64_t ldh, int32_t d_in, const float* wt, int64_t ldwt,
                                   const uint64_t* wbits, int64_t ldw, const float* alpha,
                                   int32_t d_out, const float* gout, int64_t ldg,
@@ -561,6 +567,8 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
     return BIGCN_EINVAL;
   if (n > 0 && (rowptr == nullptr || h == nullptr || gout == nullptr)) return BIGCN_EINVAL;
   if (nnz > 0 && colidx == nullptr) return BIGCN_EINVAL;
+  // the source order: both arrays or neither
+  if ((slot == nullptr) != (colslot == nullptr)) return BIGCN_EINVAL;
   if (act == BIGCN_ACT_RELU && n > 0 && (out == nullptr || ldo < d_out)) return BIGCN_EINVAL;
   if ((dh != nullptr && lddh < d_in) || (dh_tilde != nullptr && lddht < d_in) ||
       (dwt_tilde != nullptr && lddwt < d_in) || (dzeta != nullptr && lddz < d_out))
@@ -568,7 +576,8 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
   if (!aligned(rowptr, 8) || !aligned(colidx, 4) || !aligned(h, 4) || !aligned(wt, 4) ||
       !aligned(wbits, 8) || !aligned(alpha, 4) || !aligned(gout, 4) || !aligned(out, 4) ||
       !aligned(dh, 4) || !aligned(dh_tilde, 4) || !aligned(dwt, 4) ||
-      !aligned(dwt_tilde, 4) || !aligned(db, 4) || !aligned(dzeta, 4))
+      !aligned(dwt_tilde, 4) || !aligned(db, 4) || !aligned(dzeta, 4) ||
+      !aligned(slot, 4) || !aligned(colslot, 4))
     return BIGCN_EALIGN;
   const BwdLayout L = bwd_layout(n, nnz, d_in, d_out);
   if (workspace == nullptr || ws_bytes < L.bytes) return BIGCN_EWORKSPACE;
@@ -592,8 +601,9 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
                          {wt, d_out, d_in, ldwt}};
   bool z_alone = true;
   for (const Span& o : others) z_alone = z_alone && !sz.overlaps(o);
-  const bool g_direct = act != BIGCN_ACT_RELU && ldg % 4 == 0 && aligned(gout, 16) &&
-                        !sg.overlaps(Span{db, 1, d_out, d_out});
+  // (in the source order G is always staged: its rows move to their slots)
+  const bool g_direct = slot == nullptr && act != BIGCN_ACT_RELU && ldg % 4 == 0 &&
+                        aligned(gout, 16) && !sg.overlaps(Span{db, 1, d_out, d_out});
   const bool z_direct =
       dzeta != nullptr && lddz % 4 == 0 && aligned(dzeta, 16) && z_alone;
   float* Gm = g_direct ? nullptr : (float*)(ws + L.off_Gm);
@@ -620,21 +630,24 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
   hipLaunchKernelGGL(k_bwd_prep,
                      dim3(grid_of(std::max<int64_t>(g_direct ? n : n * L.ldm, L.ldm))),
                      dim3(kB), 0, s, n, d_out, gout, ldg, out, ldo,
-                     act == BIGCN_ACT_RELU ? 1 : 0, Gm, L.ldm, rowptr, mean, sc, ones);
+                     act == BIGCN_ACT_RELU ? 1 : 0, Gm, L.ldm, rowptr, mean, sc, ones, slot);
   BIGCN_CHECK(hipGetLastError());
   if (db != nullptr) {
     hipLaunchKernelGGL(k_bwd_colsum_part, dim3((unsigned)L.chunks_db), dim3(kB), 0, s, n,
-                       d_out, Gsrc, ldsrc, L.Rdb, pdb);
+                       d_out, Gsrc, ldsrc, L.Rdb, pdb, slot);
     hipLaunchKernelGGL(k_bwd_colsum_final, dim3(grid_of(d_out)), dim3(kB), 0, s, d_out,
                        L.chunks_db, pdb, db);
     BIGCN_CHECK(hipGetLastError());
   }
   // dζ = Ã^T G: sources scaled by s_i, destinations by D̂^-1/2 (symmetric)
-  // or not at all (mean, normalisation mode 2).
+  // or not at all (mean, normalisation mode 2); in the source order the
+  // sources are read through the column slots (the same terms in the same
+  // order: the results do not change).
   if (n > 0) {
     const bigcn::SpmmPlan plan = bigcn::spmm_plan(n, nnz, d_out);
     BIGCN_CHECK(bigcn::launch_spmm_rows(n, nnz, rowptr, plan, wsp, s));
-    BIGCN_CHECK(bigcn::launch_spmm(n, nnz, rowptr, colidx, mean ? 2 : 0, sc, Gsrc,
+    BIGCN_CHECK(bigcn::launch_spmm(n, nnz, rowptr, slot != nullptr ? colslot : colidx,
+                                   mean ? 2 : 0, sc, Gsrc,
                                    bigcn::IType::F32, d_out, ldsrc, ones, nullptr, 0, dz,
                                    ldz, plan, wsp, s));
     if (dzeta != nullptr && !z_direct)

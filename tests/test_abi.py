@@ -308,23 +308,27 @@ def test_layer_backward_validation():
     need = lib.bigcn_layer_backward_workspace_bytes(n, nnz, d_in, d_out)
     assert need > 0
     assert lib.bigcn_layer_backward_workspace_bytes(n, nnz, 0, d_out) == 0
-    # n nnz rowptr colidx norm h ldh d_in wt ldwt wbits ldw alpha d_out gout ldg out ldo act
-    # dh lddh dht lddht dwt lddw dwtt lddwt db dzeta lddz ws bytes stream
-    ok = [n, nnz, FAKE, FAKE, 0, FAKE, d_in, d_in, FAKE, d_in, FAKE, 2, FAKE, d_out, FAKE,
-          d_out, None, 0, 0, FAKE, d_in, None, 0, FAKE, d_in, None, 0, None, None, 0, FAKE,
-          need, None]
-    for pos, val, want in [(6, 99, EINVAL), (11, 1, EINVAL), (15, 6, EINVAL),
-                           (18, 1, EINVAL),            # ReLU without the forward output
-                           (23, None, EINVAL), (24, 99, EINVAL), (4, 7, EINVAL),
-                           (31, need - 1, EWORKSPACE), (30, FAKE + 64, EALIGN),
-                           (5, FAKE + 2, EALIGN), (10, FAKE + 4, EALIGN)]:
+    # n nnz rowptr colidx slot colslot norm h ldh d_in wt ldwt wbits ldw alpha d_out gout
+    # ldg out ldo act dh lddh dht lddht dwt lddw dwtt lddwt db dzeta lddz ws bytes stream
+    ok = [n, nnz, FAKE, FAKE, None, None, 0, FAKE, d_in, d_in, FAKE, d_in, FAKE, 2, FAKE,
+          d_out, FAKE, d_out, None, 0, 0, FAKE, d_in, None, 0, FAKE, d_in, None, 0, None,
+          None, 0, FAKE, need, None]
+    for pos, val, want in [(8, 99, EINVAL), (13, 1, EINVAL), (17, 6, EINVAL),
+                           (20, 1, EINVAL),            # ReLU without the forward output
+                           (25, None, EINVAL), (26, 99, EINVAL), (6, 7, EINVAL),
+                           (4, FAKE, EINVAL), (5, FAKE, EINVAL),   # one of slot / colslot
+                           (33, need - 1, EWORKSPACE), (32, FAKE + 64, EALIGN),
+                           (7, FAKE + 2, EALIGN), (12, FAKE + 4, EALIGN)]:
         args = list(ok)
         args[pos] = val
         assert f(*args) == want, (pos, val)
+    odd = list(ok)
+    odd[4], odd[5] = FAKE + 2, FAKE                    # slot not 4-byte aligned
+    assert f(*odd) == EALIGN
     big = list(ok)
-    big[7], big[6], big[9], big[20], big[24] = 3000, 3000, 3000, 3000, 3000
-    big[11] = 47
+    big[9], big[8], big[11], big[22], big[26] = 3000, 3000, 3000, 3000, 3000
+    big[13] = 47
     assert f(*big) == EUNSUPPORTED
     wide = list(ok)
-    wide[13], wide[15] = 300, 300
+    wide[15], wide[17] = 300, 300
     assert f(*wide) == EUNSUPPORTED

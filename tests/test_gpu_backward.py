@@ -30,7 +30,7 @@ def _t(a, dev):
     return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
 
-def gpu_backward(dev, g, norm, h, wt, G, out=None, act="none"):
+def gpu_backward(dev, g, norm, h, wt, G, out=None, act="none", source_order=False):
     n, d_in = h.shape
     d_out = wt.shape[0]
     wt_t = _t(wt, dev)
@@ -44,11 +44,18 @@ def gpu_backward(dev, g, norm, h, wt, G, out=None, act="none"):
     ws = torch.empty(bg.layer_backward_workspace_bytes(n, g.nnz, d_in, d_out),
                      dtype=torch.uint8, device=dev)
     colidx = _t(g.colidx, dev) if g.nnz else torch.zeros(1, dtype=torch.int32, device=dev)
-    bg.bigcn_layer_backward(_t(g.rowptr, dev), colidx, _t(h, dev), wt_t, wbits, alpha,
+    rowptr = _t(g.rowptr, dev)
+    slot = colslot = None
+    if source_order:
+        slot = torch.empty(n, dtype=torch.int32, device=dev)
+        colslot = torch.empty(max(g.nnz, 1), dtype=torch.int32, device=dev)
+        sws = torch.empty(bg.source_slots_workspace_bytes(n), dtype=torch.uint8, device=dev)
+        bg.bigcn_source_slots(rowptr, colidx, slot, colslot, sws, nnz=g.nnz)
+    bg.bigcn_layer_backward(rowptr, colidx, _t(h, dev), wt_t, wbits, alpha,
                             _t(G, dev), r["dwt"], ws, norm, act,
                             out=None if out is None else _t(out, dev), dh=r["dh"],
                             dh_tilde=r["dh_tilde"], dwt_tilde=r["dwt_tilde"], db=r["db"],
-                            dzeta=r["dzeta"], nnz=g.nnz)
+                            dzeta=r["dzeta"], nnz=g.nnz, slot=slot, colslot=colslot)
     torch.cuda.synchronize()
     return {k: v.cpu().numpy().astype(np.float64) for k, v in r.items()}
 
@@ -99,6 +106,24 @@ def test_layer_backward_matches_oracle(dev, norm, act, d_in, d_out, scale):
     check_backward(got, ref, np.where(out > 0, G, 0) if act == "relu" else G, wt, d_in)
     if scale >= 1:
         assert (np.abs(ref["dh_tilde"]) >= 1).any()    # Eq. (14) kills some entries
+
+
+@pytest.mark.parametrize("norm,act", [("sym", "none"), ("mean", "relu"), ("sym", "relu")])
+def test_layer_backward_in_source_order_is_bit_identical(dev, norm, act):
+    """With the source order of the forward pass (G and the source factors
+    staged at their slots, dζ gathered through the column slots) every
+    result equals the node-order call bit for bit."""
+    rng = np.random.default_rng(77 + (norm == "mean") + 2 * (act == "relu"))
+    g = _star(700, rng)
+    d_in, d_out = 200, 47
+    h = rng.standard_normal((g.n, d_in)).astype(np.float32)
+    wt = (rng.standard_normal((d_out, d_in)) * 0.8).astype(np.float32)
+    G = (rng.standard_normal((g.n, d_out)) * 0.1).astype(np.float32)
+    out = rng.standard_normal((g.n, d_out)).astype(np.float32) if act == "relu" else None
+    a = gpu_backward(dev, g, norm, h, wt, G, out, act)
+    b = gpu_backward(dev, g, norm, h, wt, G, out, act, source_order=True)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
 
 
 def test_layer_backward_without_edges(dev):
