@@ -27,6 +27,7 @@
 namespace {
 
 constexpr int kB = 256;  // threads per block (4 waves)
+typedef float float4_t __attribute__((ext_vector_type(4)));
 
 inline size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
 inline int64_t words(int64_t k) { return (k + 63) / 64; }
@@ -37,29 +38,50 @@ inline int64_t words(int64_t k) { return (k + 63) / 64; }
 // (the per-column scale of the aggregation).  With slot, node i's row of Gm
 // and its factor go to position slot[i] (the source order of the forward
 // pass), where the aggregation reads them through the column slots.
+// A row takes 2^lpr_log2 lanes (the power of two covering ldm / 4 quads,
+// ldm <= 256 a multiple of 4), so a wave stages 64 >> lpr_log2 rows; lane
+// quad c covers columns 4c .. 4c+3 with one 16-byte store (Gm 16-byte
+// aligned), reading G (and out) as one 16-byte load each when vec (d and
+// their row strides multiples of 4, both 16-byte aligned).
 __global__ __launch_bounds__(kB) void k_bwd_prep(
     int64_t n, int32_t d, const float* __restrict__ G, int64_t ldg,
     const float* __restrict__ out, int64_t ldo, int relu, float* __restrict__ Gm,
     int64_t ldm, const int64_t* __restrict__ rowptr, int mean, float* __restrict__ s,
-    float* __restrict__ ones, const int32_t* __restrict__ slot) {
-  const int64_t idx = (int64_t)blockIdx.x * kB + threadIdx.x;
-  if (Gm != nullptr && idx < n * ldm) {
-    const int64_t i = idx / ldm;
-    const int64_t k = idx - i * ldm;
-    float v = 0.f;
-    if (k < d) {
-      v = G[i * ldg + k];
-      if (relu && !(out[i * ldo + k] > 0.f)) v = 0.f;
+    float* __restrict__ ones, const int32_t* __restrict__ slot, int lpr_log2, int vec) {
+  const int lane = threadIdx.x & 63;
+  const int64_t i = ((int64_t)blockIdx.x * (kB / 64) + (threadIdx.x >> 6)) * (64 >> lpr_log2) +
+                    (lane >> lpr_log2);
+  const int c = lane & ((1 << lpr_log2) - 1);
+  if (i < n) {
+    const int64_t dst = slot != nullptr ? (int64_t)slot[i] : i;
+    if (Gm != nullptr && 4 * c < ldm) {
+      float4_t v = {0.f, 0.f, 0.f, 0.f};
+      if (vec) {
+        v = *reinterpret_cast<const float4_t*>(G + i * ldg + 4 * c);
+        float4_t o = {1.f, 1.f, 1.f, 1.f};
+        if (relu) o = *reinterpret_cast<const float4_t*>(out + i * ldo + 4 * c);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (relu && !(o[u] > 0.f)) v[u] = 0.f;
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int k = 4 * c + u;
+          if (k < d) {
+            const float x = G[i * ldg + k];
+            v[u] = relu && !(out[i * ldo + k] > 0.f) ? 0.f : x;
+          }
+        }
+      }
+      *reinterpret_cast<float4_t*>(Gm + dst * ldm + 4 * c) = v;
     }
-    Gm[(slot != nullptr ? (int64_t)slot[i] : i) * ldm + k] = v;
+    if (c == 0) {
+      const int64_t deg = rowptr[i + 1] - rowptr[i];
+      const float dg = (float)deg;
+      s[dst] = deg > 0 ? (mean ? 1.0f / dg : 1.0f / sqrtf(dg)) : 0.f;
+    }
   }
-  if (idx < n) {
-    const int64_t deg = rowptr[idx + 1] - rowptr[idx];
-    const float dg = (float)deg;
-    s[slot != nullptr ? (int64_t)slot[idx] : idx] =
-        deg > 0 ? (mean ? 1.0f / dg : 1.0f / sqrtf(dg)) : 0.f;
-  }
-  if (idx < d) ones[idx] = 1.f;
+  if (blockIdx.x == 0 && threadIdx.x < d) ones[threadIdx.x] = 1.f;
 }
 
 // Column sums of Gm over a chunk of R rows (block = chunk), fp64, rows in
@@ -102,8 +124,6 @@ __global__ __launch_bounds__(kB) void k_bwd_colsum_final(
   for (; c < chunks; ++c) acc += part[c * d + k];
   db[k] = (float)acc;
 }
-
-typedef float float4_t __attribute__((ext_vector_type(4)));
 
 // bf16 operands of the 16x16x32 matrix-core product: lane (m, q) holds eight
 // consecutive K entries 8q .. 8q+7 of its A row m / B column m.
@@ -627,10 +647,20 @@ bigcn_status bigcn_layer_backward(int64_t n, int64_t nnz, const int64_t* rowptr,
   if (n > 0)
     BIGCN_CHECK(bigcn::launch_pack(h, n, d_in, ldh, nullptr, nullptr, nullptr, 0, F, L.kw,
                                    beta, s));
-  hipLaunchKernelGGL(k_bwd_prep,
-                     dim3(grid_of(std::max<int64_t>(g_direct ? n : n * L.ldm, L.ldm))),
-                     dim3(kB), 0, s, n, d_out, gout, ldg, out, ldo,
-                     act == BIGCN_ACT_RELU ? 1 : 0, Gm, L.ldm, rowptr, mean, sc, ones, slot);
+  {
+    int lpr_log2 = 0;
+    while ((1 << lpr_log2) * 4 < L.ldm) ++lpr_log2;  // lanes per staged row
+    const int64_t rows_per_block = (kB / 64) * (64 >> lpr_log2);
+    const bool relu = act == BIGCN_ACT_RELU;
+    // (d a multiple of 4 as well: no load reaches past a row's d entries)
+    const bool vec = d_out % 4 == 0 && ldg % 4 == 0 && aligned(gout, 16) &&
+                     (!relu || (ldo % 4 == 0 && aligned(out, 16)));
+    hipLaunchKernelGGL(k_bwd_prep,
+                       dim3((unsigned)std::max<int64_t>(1, (n + rows_per_block - 1) /
+                                                               rows_per_block)),
+                       dim3(kB), 0, s, n, d_out, gout, ldg, out, ldo, relu ? 1 : 0, Gm, L.ldm,
+                       rowptr, mean, sc, ones, slot, lpr_log2, vec ? 1 : 0);
+  }
   BIGCN_CHECK(hipGetLastError());
   if (db != nullptr) {
     hipLaunchKernelGGL(k_bwd_colsum_part, dim3((unsigned)L.chunks_db), dim3(kB), 0, s, n,
