@@ -385,6 +385,13 @@ typedef struct {
   const uint64_t* wbits_self;
   int64_t ldw_self;
   const float* alpha_self;
+  /* NULL, or where this hidden layer's fp32 output H^(l+1) [n][ldo] is
+   * written as well (ldo >= d_out, 4-byte aligned, overlapping no other
+   * argument); ignored for the last layer, whose output is bigcn_forward's
+   * out.  Without it a layer whose aggregation forms the next layer's
+   * products in its epilogue writes no fp32 output at all. */
+  float* out;
+  int64_t ldo;
 } bigcn_layer;
 
 size_t bigcn_forward_workspace_bytes(int64_t n, int64_t nnz,

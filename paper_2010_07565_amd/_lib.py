@@ -8,6 +8,7 @@ the library's HIP kernels; there is no fallback path.
 from __future__ import annotations
 
 import ctypes
+import dataclasses
 import os
 from dataclasses import dataclass
 from typing import Optional, Sequence
@@ -47,7 +48,8 @@ class _Layer(ctypes.Structure):
                 ("wbits", ctypes.c_void_p), ("ldw", ctypes.c_int64),
                 ("alpha", ctypes.c_void_p), ("bias", ctypes.c_void_p),
                 ("act", ctypes.c_int), ("wbits_self", ctypes.c_void_p),
-                ("ldw_self", ctypes.c_int64), ("alpha_self", ctypes.c_void_p)]
+                ("ldw_self", ctypes.c_int64), ("alpha_self", ctypes.c_void_p),
+                ("out", ctypes.c_void_p), ("ldo", ctypes.c_int64)]
 
 
 _lib = None
@@ -354,6 +356,7 @@ class Layer:
     act: str = "none"
     wbits_self: Optional[torch.Tensor] = None
     alpha_self: Optional[torch.Tensor] = None
+    out: Optional[torch.Tensor] = None   # fp32 [n, d_out]: a hidden output, written if given
 
     def _c(self) -> _Layer:
         sage = self.wbits_self is not None
@@ -362,7 +365,9 @@ class Layer:
                       _dev(self.bias, torch.float32, "bias"), ACTS[self.act],
                       _dev(self.wbits_self, torch.int64, "wbits_self") if sage else None,
                       _ld(self.wbits_self, "wbits_self") if sage else 0,
-                      _dev(self.alpha_self, torch.float32, "alpha_self") if sage else None)
+                      _dev(self.alpha_self, torch.float32, "alpha_self") if sage else None,
+                      _dev(self.out, torch.float32, "out"),
+                      _ld(self.out, "out") if self.out is not None else 0)
 
 
 def _layers(layers: Sequence[Layer]):
@@ -513,8 +518,18 @@ class BiGCN:
         self.out = torch.empty((self.n, self.layers[-1].d_out), dtype=torch.float32,
                                device=self.device)
 
-    def forward(self, x: torch.Tensor, stream=None) -> torch.Tensor:
-        bigcn_forward(self.rowptr, self.colidx, x, self.layers, self.out, self.ws,
+    def forward(self, x: torch.Tensor, stream=None, hidden=None) -> torch.Tensor:
+        """The forward pass on ``x``; ``hidden`` (optional, one entry per
+        layer but the last, each None or an fp32 [n, d_out] tensor) receives
+        those layers' outputs as well."""
+        layers = self.layers
+        if hidden is not None:
+            hidden = list(hidden)
+            if len(hidden) != len(self.layers) - 1:
+                raise ValueError("hidden: one entry per layer but the last")
+            layers = [dataclasses.replace(ly, out=h)
+                      for ly, h in zip(self.layers, hidden + [None])]
+        bigcn_forward(self.rowptr, self.colidx, x, layers, self.out, self.ws,
                       self.mu, self.rstd, self.norm, stream=stream, slot=self.slot,
                       colslot=self.colslot)
         return self.out

@@ -490,6 +490,10 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
     if (!aligned(ly.wbits, 8) || !aligned(ly.alpha, 4) || !aligned(ly.bias, 4))
       return BIGCN_EALIGN;
     if (ly.d_in > kMaxBgemmK) return BIGCN_EUNSUPPORTED;
+    if (l + 1 < n_layers && ly.out != nullptr) {  // a requested hidden output
+      if (ly.ldo < ly.d_out) return BIGCN_EINVAL;
+      if (!aligned(ly.out, 4)) return BIGCN_EALIGN;
+    }
     if (ly.wbits_self != nullptr) {  // two-weight GraphSAGE layer
       if (ly.alpha_self == nullptr || ly.ldw_self < words(ly.d_in)) return BIGCN_EINVAL;
       if (!aligned(ly.wbits_self, 8) || !aligned(ly.alpha_self, 4)) return BIGCN_EALIGN;
@@ -569,8 +573,12 @@ bigcn_status bigcn_forward(int64_t n, int64_t nnz, const int64_t* rowptr,
       }
     }
     const int kind = fuse_kind(n, nnz, layers, n_layers, l);
-    float* hout = last ? out : (kind != 0 ? nullptr : H[l & 1]);
-    const int64_t ldout = last ? ldo : L.ldh;
+    // the layer's fp32 output: the caller's for the last layer or when asked
+    // for, else the workspace (none when the epilogue forms the next layer's
+    // products)
+    float* hout = last ? out
+                       : (ly.out != nullptr ? ly.out : (kind != 0 ? nullptr : H[l & 1]));
+    const int64_t ldout = last ? ldo : (ly.out != nullptr ? ly.ldo : L.ldh);
     const bigcn::SpmmPlan plan = bigcn::spmm_plan(n, nnz, ly.d_out);
     if (q8) {
       bigcn::FusedNext fn = {};

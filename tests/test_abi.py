@@ -130,6 +130,14 @@ def test_forward_validation():
     a = list(args)
     a[8] = 99
     assert lib.bigcn_forward(*a) == EINVAL        # ldx < d_in
+    # a requested hidden output: ld >= d_out, 4-byte aligned (the last
+    # layer's fields are ignored)
+    for h_out, h_ld, want in [(FAKE, 15, EINVAL), (FAKE + 2, 16, EALIGN)]:
+        hid = (L * 2)(L(100, 16, FAKE, 2, FAKE, None, 0, None, 0, None, h_out, h_ld),
+                      L(16, 4, FAKE, 1, FAKE, None, 0, None, 0, None, FAKE + 2, 0))
+        a = list(args)
+        a[11] = hid
+        assert lib.bigcn_forward(*a) == want
     a = list(args)
     a[15] = FAKE + 128
     assert lib.bigcn_forward(*a) == EALIGN        # workspace alignment

@@ -118,8 +118,9 @@ def check_sage_layer(dev, w, l, h, mu, rstd, ids, rowptr_t, colidx_t):
     assert err <= TOL
 
 
-def chained(dev, w, rowptr_t, colidx_t, xt):
+def chained(dev, w, rowptr_t, colidx_t, xt, every_layer=False):
     h = xt
+    outs = []
     for l, wt in enumerate(w.weights_t):
         if w.weights_self_t is not None:
             out, *_ = gpu_sage_layer(dev, w.graph, None, w.weights_self_t[l], wt,
@@ -132,7 +133,8 @@ def chained(dev, w, rowptr_t, colidx_t, xt):
                                      rstd=w.rstd if l == 0 else None,
                                      rowptr_t=rowptr_t, colidx_t=colidx_t, ht=h)
         h = out
-    return h
+        outs.append(out)
+    return outs if every_layer else h
 
 
 @pytest.mark.timeout(1200)
@@ -143,22 +145,28 @@ def test_forward_equals_chained_layers(dev, cfg):
     rowptr_t, colidx_t = _t(g.rowptr, dev), _t(g.colidx, dev)
     xt = _t(w.x, dev)
     outs = []
+    hidden = [torch.full((g.n, wt.shape[0]), float("nan"), device=dev)
+              for wt in w.weights_t[:-1]]
     for so in (True, False, "auto"):   # source order, node order, the model's default
         model = bg.BiGCN(rowptr_t, colidx_t, w.weights_t, w.biases, norm=w.norm,
                          mu=w.mu, rstd=w.rstd, device=dev, weights_self_t=w.weights_self_t,
                          source_order=so)
         outs.append(model.forward(xt).clone())
         if so is True:
-            outs.append(model.forward(xt).clone())
+            # again, the hidden layers' outputs requested as well
+            outs.append(model.forward(xt, hidden=hidden).clone())
         del model
     out = outs[0]
-    ref = chained(dev, w, rowptr_t, colidx_t, xt)
+    refs = chained(dev, w, rowptr_t, colidx_t, xt, every_layer=True)
+    ref = refs[-1]
     torch.cuda.synchronize()
     log("cfg %d forward vs chained: max |diff| %.3g" % (cfg, (out - ref).abs().max().item()))
     assert torch.equal(out, outs[1]), "forward pass not reproducible"
     assert torch.equal(out, ref), "forward pass differs from the chained entry points"
     assert torch.equal(outs[2], ref) and torch.equal(outs[3], ref), \
         "node-order forward differs"
+    for l, h in enumerate(hidden):      # requested hidden outputs, bit for bit
+        assert torch.equal(h, refs[l]), "hidden output of layer %d differs" % l
     assert bool(torch.isfinite(out).all())
 
 
