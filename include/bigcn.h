@@ -350,20 +350,24 @@ bigcn_status bigcn_source_slots(int64_t n, int64_t nnz, const int64_t* rowptr,
  *        is bit-identical to the call without them.  Ignored when nnz = 0.
  *   x    [n][ldx] fp32 node features, ldx >= layers[0].d_in.
  *   out  [n][ldo] fp32 result of the last layer, ldo >= last d_out.
- *   workspace  at least bigcn_forward_workspace_bytes(...) bytes, 256-byte
- *          aligned; contents on entry are ignored.
+ *   workspace  at least bigcn_forward_workspace_bytes(...) bytes for the
+ *          same layers (a hidden output the caller gives needs no workspace
+ *          copy), 256-byte aligned; contents on entry are ignored.
  * Internally each layer's products are kept exactly: as 8-bit half-codes
  * (see bigcn_bgemm_q8) for layers of up to 256 output columns with
  * d_in <= 2048, otherwise in IEEE half (d_in <= 2048) or int16.  When two
  * consecutive layers both use 8-bit codes, the second layer's sign pack and
  * binary GEMM run inside the aggregation that produces its input: the
- * hidden activations are never written to memory.  The result is
+ * hidden activations are not written to memory unless the layer gives an
+ * output (bigcn_layer.out).  The result is
  * bit-identical to chaining the per-step entry points (bigcn_binarize_pack,
  * bigcn_bgemm_q8, bigcn_spmm_csr_q8 for 8-bit layers).
  * A layer with wbits_self set is a two-weight GraphSAGE layer: the graph
  * given is then A (the neighbour sets, normally without self-loops) and
- * norm must be MEAN; its products stay unfused (8-bit neighbour codes, exact
- * half self products, then bigcn_spmm_csr_sage_q8's aggregation).
+ * norm must be MEAN; its products stay unfused (8-bit neighbour codes, then
+ * bigcn_spmm_csr_sage_q8's aggregation; the self products are formed in the
+ * aggregation's epilogue from the packed signs for 65-256 output columns,
+ * else read as exact half products).
  * Errors: as the per-step calls, plus EINVAL for inconsistent layer widths
  *         or n_layers < 1, only one of slot / colslot, or a GraphSAGE layer
  *         with norm SYM, EALIGN for slot / colslot not 4-byte aligned,

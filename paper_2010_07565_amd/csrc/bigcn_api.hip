@@ -129,10 +129,16 @@ inline int64_t q8_row(int32_t d) { return 64 * bigcn::q8_lane_bytes(d); }
 bool forward_layout(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t nl,
                     ForwardLayout* L) {
   int64_t kwmax = 1, dmax = 1, hmax = 1, smax = 0;
+  bool need_h[2] = {false, false};  // a hidden output in workspace set l & 1
   for (int32_t l = 0; l < nl; ++l) {
     kwmax = std::max<int64_t>(kwmax, words(layers[l].d_in));
     dmax = std::max<int64_t>(dmax, layers[l].d_out);
-    if (l + 1 < nl) hmax = std::max<int64_t>(hmax, layers[l].d_out);
+    // a hidden layer writes its fp32 output to the workspace unless its
+    // aggregation forms the next layer's products or the caller gives one
+    if (l + 1 < nl && layers[l].out == nullptr && fuse_kind(n, nnz, layers, nl, l) == 0) {
+      hmax = std::max<int64_t>(hmax, layers[l].d_out);
+      need_h[l & 1] = true;
+    }
     if (layers[l].wbits_self != nullptr) smax = std::max<int64_t>(smax, layers[l].d_out);
   }
   L->ldS = (smax + 7) / 8 * 8;
@@ -153,9 +159,9 @@ bool forward_layout(int64_t n, int64_t nnz, const bigcn_layer* layers, int32_t n
     off += up256((size_t)n * L->ldc16 * 2);
   }
   L->off_H0 = off;
-  if (nl >= 2) off += up256((size_t)n * L->ldh * 4);
+  if (need_h[0]) off += up256((size_t)n * L->ldh * 4);
   L->off_H1 = off;
-  if (nl >= 3) off += up256((size_t)n * L->ldh * 4);
+  if (need_h[1]) off += up256((size_t)n * L->ldh * 4);
   L->off_S = off;
   off += up256((size_t)n * L->ldS * 2);
   L->off_spmm = off;
