@@ -65,6 +65,10 @@ def _load():
         lib.oracle_layer_backward.restype = _int
         lib.oracle_layer_backward.argtypes = [_i64, _p, _p, _int, _p, _i64, _i32, _p,
                                               _i32, _p, _p, _int] + [_p] * 9
+        lib.oracle_layer_backward_at.restype = _int
+        lib.oracle_layer_backward_at.argtypes = [_i64, _p, _p, _int, _p, _i64, _i32, _p,
+                                                 _i32, _p, _p, _int, _i64, _p, _i32,
+                                                 _p] + [_p] * 9
         lib.oracle_threads.restype = _int
         lib.oracle_threads.argtypes = []
         lib.oracle_set_threads.restype = None
@@ -261,6 +265,42 @@ def layer_backward(rowptr, colidx, norm, h, wt, gout, out=None, act="none"):
                                                  "dwt", "db")])
     if rc != 0:
         raise ValueError("oracle_layer_backward failed (%d)" % rc)
+    return r
+
+
+def layer_backward_at(rowptr, colidx, norm, h, wt, gout, rows, cols, out=None,
+                      act="none"):
+    """layer_backward's entries for the listed node rows (dzeta, mass_dzeta
+    [len(rows), d_out]; dh_tilde, mass_dh, dh [len(rows), d_in]) and output
+    columns j (dwt_tilde, mass_dwt, dwt [len(cols), d_in], row c holding
+    column cols[c] of the W^T layout), and all of db [d_out]; each equal, bit
+    for bit, to the whole layer's."""
+    rowptr = _c(rowptr, np.int64)
+    colidx = _c(colidx, np.int32)
+    h = _c(h, np.float32)
+    wt = _c(wt, np.float32)
+    gout = _c(gout, np.float32)
+    rows = _c(rows, np.int64)
+    cols = _c(cols, np.int32)
+    n, d_in = h.shape
+    d_out = wt.shape[0]
+    assert wt.shape[1] == d_in and gout.shape == (n, d_out)
+    if act == "relu":
+        out = _c(out, np.float32)
+        assert out.shape == (n, d_out)
+    nr, nc = len(rows), len(cols)
+    r = {k: np.zeros(shape, dtype=np.float64) for k, shape in (
+        ("dzeta", (nr, d_out)), ("mass_dzeta", (nr, d_out)), ("dh_tilde", (nr, d_in)),
+        ("mass_dh", (nr, d_in)), ("dh", (nr, d_in)), ("dwt_tilde", (nc, d_in)),
+        ("mass_dwt", (nc, d_in)), ("dwt", (nc, d_in)), ("db", (d_out,)))}
+    rc = _load().oracle_layer_backward_at(
+        n, rowptr.ctypes.data, colidx.ctypes.data, NORMS[norm], h.ctypes.data, d_in, d_in,
+        wt.ctypes.data, d_out, gout.ctypes.data, _ptr(out if act == "relu" else None),
+        ACTS[act], nr, rows.ctypes.data, nc, cols.ctypes.data,
+        *[r[k].ctypes.data for k in ("dzeta", "mass_dzeta", "dh_tilde", "mass_dh", "dh",
+                                     "dwt_tilde", "mass_dwt", "dwt", "db")])
+    if rc != 0:
+        raise ValueError("oracle_layer_backward_at failed (%d)" % rc)
     return r
 
 

@@ -542,6 +542,137 @@ done:
   return rc;
 }
 
+/* ---------------------------------------------------------------------
+ * oracle_layer_backward_at: the same back propagation (Alg. 1, Eqs. (14)-
+ * (15)) for a subset of its outputs, for graphs too large for the whole
+ * layer: the rows listed in `rows` of dζ and dH~ / dH, the columns j listed
+ * in `cols` of dW~ and dW (every k of each), and all of db.  Every entry is
+ * the sum oracle_layer_backward forms, over the same terms in the same
+ * order, so the two agree bit for bit; only the entries asked for are
+ * formed (column j of dW~ needs dζ_:j for every node, row i of dH~ needs
+ * dζ_i,: for every column), and the masked gradient is read in place.
+ *   rows [n_rows] node ids;  cols [n_cols] output columns (< d_out)
+ * Outputs (doubles):  dzeta, mass_dzeta [n_rows][d_out]; dh_tilde, mass_dh,
+ *   dh [n_rows][d_in]; dwt_tilde, mass_dwt, dwt [n_cols][d_in]; db [d_out].
+ * Returns 0, -1 on a non-finite input, -2 on allocation failure, -3 on an
+ * id out of range.
+ * ------------------------------------------------------------------- */
+static double g_masked(const float* gout, const float* out, int act, int32_t d_out,
+                       int64_t i, int32_t k) {
+  if (act == ORACLE_ACT_RELU && !(out[i * d_out + k] > 0.0f)) return 0.0;
+  return (double)gout[i * d_out + k];
+}
+
+/* dζ_jk = sum_{i in N(j)} Ã_ij G_ik and the mass of its terms. */
+static double dzeta_at(const int64_t* rowptr, const int32_t* colidx, int norm,
+                       const float* gout, const float* out, int act, int32_t d_out,
+                       int64_t j, int32_t k, double* mass) {
+  int64_t deg_j = rowptr[j + 1] - rowptr[j];
+  double s = 0.0, m = 0.0;
+  for (int64_t e = rowptr[j]; e < rowptr[j + 1]; ++e) {
+    int64_t i = colidx[e];
+    int64_t deg_i = rowptr[i + 1] - rowptr[i];
+    double t = atilde(norm, deg_i, deg_j) * g_masked(gout, out, act, d_out, i, k);
+    s += t;
+    m += fabs(t);
+  }
+  *mass = m;
+  return s;
+}
+
+int oracle_layer_backward_at(int64_t n, const int64_t* rowptr, const int32_t* colidx,
+                             int norm, const float* h, int64_t ldh, int32_t d_in,
+                             const float* wt, int32_t d_out, const float* gout,
+                             const float* out, int act, int64_t n_rows,
+                             const int64_t* rows, int32_t n_cols, const int32_t* cols,
+                             double* dzeta, double* mass_dzeta, double* dh_tilde,
+                             double* mass_dh, double* dh, double* dwt_tilde,
+                             double* mass_dwt, double* dwt, double* db) {
+  const int64_t ldw = (d_in + 63) / 64;
+  int rc = 0;
+  for (int64_t r = 0; r < n_rows; ++r)
+    if (rows[r] < 0 || rows[r] >= n) return -3;
+  for (int32_t c = 0; c < n_cols; ++c)
+    if (cols[c] < 0 || cols[c] >= d_out) return -3;
+  uint64_t* fbits = calloc((size_t)(n ? n : 1) * ldw, sizeof(uint64_t));
+  double* beta = calloc((size_t)(n ? n : 1), sizeof(double));
+  uint64_t* wbits = calloc((size_t)d_out * ldw, sizeof(uint64_t));
+  double* alpha = calloc((size_t)d_out, sizeof(double));
+  double* zcol = calloc((size_t)(n ? n : 1), sizeof(double));
+  if (!fbits || !beta || !wbits || !alpha || !zcol) {
+    rc = -2;
+    goto done;
+  }
+  if (oracle_binarize(h, n, d_in, ldh, NULL, NULL, NULL, 0, fbits, ldw, beta) != 0 ||
+      oracle_binarize(wt, d_out, d_in, d_in, NULL, NULL, NULL, 0, wbits, ldw, alpha) != 0) {
+    rc = -1;
+    goto done;
+  }
+  /* Bias: dL/db_k = sum_i G_ik. */
+  for (int32_t k = 0; k < d_out; ++k) {
+    double s = 0.0;
+    for (int64_t i = 0; i < n; ++i) s += g_masked(gout, out, act, d_out, i, k);
+    db[k] = s;
+  }
+  /* Listed columns j: dζ_:j, then dW~_kj = sum_i H~_ik dζ_ij and Eq. (15). */
+  for (int32_t c = 0; c < n_cols; ++c) {
+    const int32_t j = cols[c];
+#pragma omp parallel for schedule(dynamic, 1024)
+    for (int64_t i = 0; i < n; ++i) {
+      double m;
+      zcol[i] = dzeta_at(rowptr, colidx, norm, gout, out, act, d_out, i, j, &m);
+    }
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int32_t k = 0; k < d_in; ++k) {
+      double s = 0.0, m = 0.0;
+      for (int64_t i = 0; i < n; ++i) {
+        double ht = beta[i] * (double)sign_at(fbits + i * ldw, k);  /* H~_ik */
+        double t = ht * zcol[i];
+        s += t;
+        m += fabs(t);
+      }
+      dwt_tilde[(int64_t)c * d_in + k] = s;
+      mass_dwt[(int64_t)c * d_in + k] = m;
+    }
+    double colsum = 0.0;  /* sum_k dW~_kj B_kj */
+    for (int32_t k = 0; k < d_in; ++k)
+      colsum += dwt_tilde[(int64_t)c * d_in + k] * (double)sign_at(wbits + (int64_t)j * ldw, k);
+    for (int32_t i = 0; i < d_in; ++i) {
+      double bij = (double)sign_at(wbits + (int64_t)j * ldw, i);
+      double ste = fabs((double)wt[(int64_t)j * d_in + i]) < 1.0 ? 1.0 : 0.0;
+      dwt[(int64_t)c * d_in + i] = bij * colsum / (double)d_in +
+                                   alpha[j] * dwt_tilde[(int64_t)c * d_in + i] * ste;
+    }
+  }
+  /* Listed rows i: dζ_i,:, then dH~_ik = sum_j dζ_ij W~_kj and Eq. (14). */
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t r = 0; r < n_rows; ++r) {
+    const int64_t i = rows[r];
+    for (int32_t j = 0; j < d_out; ++j)
+      dzeta[r * d_out + j] = dzeta_at(rowptr, colidx, norm, gout, out, act, d_out, i, j,
+                                      &mass_dzeta[r * d_out + j]);
+    for (int32_t k = 0; k < d_in; ++k) {
+      double s = 0.0, m = 0.0;
+      for (int32_t j = 0; j < d_out; ++j) {
+        double wtl = (double)sign_at(wbits + (int64_t)j * ldw, k) * alpha[j];  /* W~_kj */
+        double t = dzeta[r * d_out + j] * wtl;
+        s += t;
+        m += fabs(t);
+      }
+      dh_tilde[r * d_in + k] = s;
+      mass_dh[r * d_in + k] = m;
+      dh[r * d_in + k] = fabs(s) < 1.0 ? s : 0.0;
+    }
+  }
+done:
+  free(fbits);
+  free(beta);
+  free(wbits);
+  free(alpha);
+  free(zcol);
+  return rc;
+}
+
 /* Number of threads the oracle's parallel loops use. */
 int oracle_threads(void) { return omp_get_max_threads(); }
 

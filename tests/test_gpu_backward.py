@@ -18,6 +18,8 @@ from helpers import TOL
 
 pytestmark = pytest.mark.gpu
 
+_WORKLOADS = {}
+
 
 @pytest.fixture(scope="module")
 def dev():
@@ -30,7 +32,10 @@ def _t(a, dev):
     return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
 
-def gpu_backward(dev, g, norm, h, wt, G, out=None, act="none", source_order=False):
+def gpu_backward(dev, g, norm, h, wt, G, out=None, act="none", source_order=False,
+                 rows=None):
+    """All gradients of one layer on the GPU, as fp64 host arrays; with
+    `rows`, only those rows of the node-indexed ones (dh, dh_tilde, dzeta)."""
     n, d_in = h.shape
     d_out = wt.shape[0]
     wt_t = _t(wt, dev)
@@ -57,6 +62,11 @@ def gpu_backward(dev, g, norm, h, wt, G, out=None, act="none", source_order=Fals
                             dh_tilde=r["dh_tilde"], dwt_tilde=r["dwt_tilde"], db=r["db"],
                             dzeta=r["dzeta"], nnz=g.nnz, slot=slot, colslot=colslot)
     torch.cuda.synchronize()
+    if rows is not None:
+        ids = torch.from_numpy(np.asarray(rows, dtype=np.int64)).to(dev)
+        for k in ("dh", "dh_tilde", "dzeta"):
+            assert bool(torch.isfinite(r[k]).all()), k    # every entry written
+            r[k] = r[k][ids]
     return {k: v.cpu().numpy().astype(np.float64) for k, v in r.items()}
 
 
@@ -167,6 +177,49 @@ def test_arxiv_like_layer_backward(dev):
     ref = oracle.layer_backward(g.rowptr, g.colidx, w.norm, h, wt, G)
     got = gpu_backward(dev, g, w.norm, h, wt, G)
     check_backward(got, ref, G, wt, d_in)
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(1200)
+@pytest.mark.parametrize("layer,act", [(0, "none"), (1, "relu"), (2, "none")])
+def test_products_like_layer_backward(dev, layer, act):
+    """Full-size products-like layers (2,449,029 nodes, 126 M entries) in the
+    forward pass's source order, as the backward benchmark runs them: dζ, dH~
+    and dH on sampled rows (random, first, last and the highest-degree
+    hubs), dW~ and dW on four whole output columns (each a sum over every
+    node), db whole, against the oracle's listed-entries form."""
+    from helpers import sample_rows
+    if 5 not in _WORKLOADS:
+        _WORKLOADS[5] = workloads.make_workload(5)
+    w = _WORKLOADS[5]
+    g = w.graph
+    wt = w.weights_t[layer]
+    d_out, d_in = wt.shape
+    h = w.x if layer == 0 else workloads.layer_input(g.n, d_in, seed=3000 + layer)
+    rng = np.random.default_rng(60 + layer)
+    G = (rng.standard_normal((g.n, d_out)) * 0.05).astype(np.float32)
+    out = workloads.layer_input(g.n, d_out, seed=4000 + layer) if act == "relu" else None
+    rows = sample_rows(g, 256, seed=70 + layer)
+    cols = np.unique([0, d_out - 1, d_out // 3, (2 * d_out) // 3]).astype(np.int32)
+    got = gpu_backward(dev, g, w.norm, h, wt, G, out, act, source_order=True, rows=rows)
+    ref = oracle.layer_backward_at(g.rowptr, g.colidx, w.norm, h, wt, G, rows, cols,
+                                   out=out, act=act)
+    Gm = np.where(out > 0, G, 0) if act == "relu" else G
+    del G, out
+    assert _err(got["dzeta"], ref["dzeta"], ref["mass_dzeta"]) <= TOL
+    assert _err(got["dh_tilde"], ref["dh_tilde"], ref["mass_dh"]) <= TOL
+    assert _err(got["dwt_tilde"][cols], ref["dwt_tilde"], ref["mass_dwt"]) <= TOL
+    assert _err(got["db"], ref["db"], np.abs(Gm).sum(axis=0, dtype=np.float64)) <= TOL
+    alpha = np.abs(wt[cols].astype(np.float64)).mean(axis=1)
+    mass_w = ref["mass_dwt"].sum(axis=1, keepdims=True) / d_in + alpha[:, None] * ref["mass_dwt"]
+    assert _err(got["dwt"][cols], ref["dwt"], mass_w) <= TOL
+    amb = np.abs(np.abs(ref["dh_tilde"]) - 1.0) <= TOL * ref["mass_dh"]
+    killed_ref = np.abs(ref["dh_tilde"]) >= 1.0
+    killed_got = (got["dh"] == 0.0) & (np.abs(got["dh_tilde"]) >= 1)
+    assert np.array_equal(killed_ref[~amb], killed_got[~amb])
+    keep = ~amb & ~killed_ref
+    assert _err(got["dh"][keep], ref["dh"][keep], ref["mass_dh"][keep]) <= TOL
+    assert np.all(np.isfinite(got["dwt_tilde"])) and np.all(np.isfinite(got["dwt"]))
 
 
 def test_backward_dzeta_in_place_of_gout(dev):

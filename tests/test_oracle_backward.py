@@ -102,3 +102,46 @@ def test_backward_masses_bound_the_sums():
     r = oracle.layer_backward(g.rowptr, g.colidx, "mean", h, wt, G)
     for k, m in (("dzeta", "mass_dzeta"), ("dwt_tilde", "mass_dwt"), ("dh_tilde", "mass_dh")):
         assert np.all(np.abs(r[k]) <= r[m] * (1 + 1e-12))
+
+
+@pytest.mark.parametrize("norm", ["sym", "mean"])
+@pytest.mark.parametrize("act", ["none", "relu"])
+def test_backward_at_listed_entries(norm, act):
+    """The listed-entries form (for graphs too large for the whole layer)
+    against autograd, and bit for bit against the whole layer's entries."""
+    rng = np.random.default_rng(11 + (norm == "mean") + 2 * (act == "relu"))
+    g = workloads.random_small_graph(45, 100, rng, isolated=3)
+    d_in, d_out = 90, 7
+    h = rng.standard_normal((g.n, d_in)).astype(np.float32)
+    wt = (rng.standard_normal((d_out, d_in)) * 0.9).astype(np.float32)
+    G = (rng.standard_normal((g.n, d_out)) * 0.3).astype(np.float32)
+    bias = rng.uniform(-0.2, 0.2, d_out).astype(np.float32)
+    ref = _autograd(g, norm, h, wt, G, bias, act)
+    out = ref["out"].astype(np.float32)
+    rows = np.array([g.n - 1, 0, 17, 17, 3, 30], dtype=np.int64)   # any order, repeats
+    cols = np.array([6, 0, 3], dtype=np.int32)
+    r = oracle.layer_backward_at(g.rowptr, g.colidx, norm, h, wt, G, rows, cols,
+                                 out=out, act=act)
+    full = oracle.layer_backward(g.rowptr, g.colidx, norm, h, wt, G, out=out, act=act)
+    for k in ("dzeta", "mass_dzeta", "dh_tilde", "mass_dh", "dh"):
+        assert np.array_equal(r[k], full[k][rows]), k
+    for k in ("dwt_tilde", "mass_dwt", "dwt"):
+        assert np.array_equal(r[k], full[k][cols]), k
+    assert np.array_equal(r["db"], full["db"])
+    assert np.allclose(r["dzeta"], ref["dzeta"][rows], rtol=1e-11, atol=1e-12)
+    assert np.allclose(r["dh_tilde"], ref["dh_tilde"][rows], rtol=1e-11, atol=1e-12)
+    assert np.allclose(r["dwt_tilde"], ref["dwt_tilde"][cols], rtol=1e-11, atol=1e-12)
+    assert np.allclose(r["dwt"], ref["dwt"][cols], rtol=1e-11, atol=1e-12)
+    assert np.allclose(r["db"], ref["db"], rtol=1e-11, atol=1e-12)
+
+
+def test_backward_at_rejects_ids_out_of_range():
+    rng = np.random.default_rng(5)
+    g = workloads.random_small_graph(10, 20, rng)
+    h = rng.standard_normal((g.n, 8)).astype(np.float32)
+    wt = rng.standard_normal((3, 8)).astype(np.float32)
+    G = rng.standard_normal((g.n, 3)).astype(np.float32)
+    with pytest.raises(ValueError):
+        oracle.layer_backward_at(g.rowptr, g.colidx, "sym", h, wt, G, [g.n], [0])
+    with pytest.raises(ValueError):
+        oracle.layer_backward_at(g.rowptr, g.colidx, "sym", h, wt, G, [0], [3])
