@@ -431,7 +431,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print("bench.py: this build runs on a single GPU; --gpus %d is not supported "
+        print("bench.py: the path runs on a single GPU; --gpus %d is not supported "
               "(the multi-GPU design is described, not built)" % args.gpus,
               file=sys.stderr)
         sys.exit(2)

@@ -42,7 +42,7 @@ typedef enum {
   BIGCN_EINVAL = -1,       /* bad pointer, size or enum value              */
   BIGCN_EALIGN = -2,       /* pointer or leading dimension misaligned      */
   BIGCN_EWORKSPACE = -3,   /* workspace missing or too small               */
-  BIGCN_EUNSUPPORTED = -4, /* valid request this build does not implement  */
+  BIGCN_EUNSUPPORTED = -4, /* valid request the library does not implement */
   BIGCN_EHIP = -5          /* the HIP runtime refused a launch             */
 } bigcn_status;
 

@@ -254,7 +254,7 @@ const char* bigcn_status_string(bigcn_status s) {
     case BIGCN_EINVAL: return "invalid argument";
     case BIGCN_EALIGN: return "misaligned pointer or leading dimension";
     case BIGCN_EWORKSPACE: return "workspace missing or too small";
-    case BIGCN_EUNSUPPORTED: return "unsupported by this build";
+    case BIGCN_EUNSUPPORTED: return "valid request the library does not implement";
     case BIGCN_EHIP: return "HIP runtime error";
   }
   return "unknown status";
