@@ -161,17 +161,52 @@ __device__ inline void split_bf16x3(const float (&x)[8], bf16x8_t& h, bf16x8_t& 
   lo = __builtin_bit_cast(bf16x8_t, pl);
 }
 
-// ±1 in bf16 from bit sh of eight 32-bit words (a set bit gives +1: the bit
-// flips the sign of the pattern of -1).
-__device__ inline bf16x8_t pm1_bf16x8(const uint32_t (&w)[8], int sh) {
+// A pointer that is the same on every lane, kept in scalar registers (so
+// that a lane offset added to it costs one vector add, and the per-row
+// bases are not hoisted into vector registers).
+template <typename T>
+__device__ inline const T* uniform_ptr(const T* p) {
+  const uint64_t x = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+  return reinterpret_cast<const T*>(((uint64_t)hi << 32) | lo);
+}
+
+// A lane's packed sign word, shifted so that the lane's column m of each
+// 16-column group g of the word (after dropping the first `skip` bits) sits
+// at bit 16g + 15: the top bit of byte 2g + 1.
+__device__ inline uint64_t lane_signs(uint64_t w, int skip, int m) {
+  return (w >> skip) << (15 - m);
+}
+
+// ±1 in bf16 for group g of eight rows' lane_signs words (row u is element
+// u): a byte permute moves the group's byte of rows 2i and 2i+1 to bytes 1
+// and 3, and the mask-and-xor gives -1 (0xBF80) where the bit is clear and
+// +1 (0x3F80) where it is set.
+template <int g, typename Row>
+__device__ inline bf16x8_t pm1_group(Row row) {
+  constexpr uint32_t bi = 2 * (g & 1) + 1;  // byte within the group's 32-bit half
+  constexpr uint32_t sel = 0x0Cu | (bi << 8) | (0x0Cu << 16) | ((4u + bi) << 24);
   uint32_t p[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const uint32_t b0 = (w[2 * i] >> sh) & 1u;
-    const uint32_t b1 = (w[2 * i + 1] >> sh) << 31;
-    p[i] = ((b0 << 15) | b1) ^ 0xBF80BF80u;
+    const uint64_t x0 = row(2 * i), x1 = row(2 * i + 1);
+    const uint32_t a = g < 2 ? (uint32_t)x0 : (uint32_t)(x0 >> 32);
+    const uint32_t b = g < 2 ? (uint32_t)x1 : (uint32_t)(x1 >> 32);
+    p[i] = (__builtin_amdgcn_perm(b, a, sel) & 0x80008000u) ^ 0xBF80BF80u;
   }
   return __builtin_bit_cast(bf16x8_t, p);
+}
+
+// pm1_group for a group index known only after unrolling (nt & 3).
+template <typename Row>
+__device__ inline bf16x8_t pm1_group_at(int g, Row row) {
+  switch (g) {
+    case 0: return pm1_group<0>(row);
+    case 1: return pm1_group<1>(row);
+    case 2: return pm1_group<2>(row);
+    default: return pm1_group<3>(row);
+  }
 }
 
 // Partial sums of dW~^T over a chunk of R rows, on the matrix cores:
@@ -205,6 +240,11 @@ __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
   const int w0 = k0 >> 6;
   const int kw = (d_in + 63) >> 6;
   const int64_t i0 = c * R, i1 = std::min<int64_t>(n, i0 + R);
+  const float jm = j < d_out ? 1.f : 0.f;
+  const int64_t zoff = (int64_t)(8 * q) * lddz + jc, foff = (int64_t)(8 * q) * ldf;
+  int wsel[NW];
+#pragma unroll
+  for (int w = 0; w < NW; ++w) wsel[w] = w0 + w < kw ? w0 + w : kw - 1;
   float4_t acc[NT];
   double acc64[NT][4];
 #pragma unroll
@@ -214,21 +254,41 @@ __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
   for (int64_t r0 = i0; r0 < i1; r0 += kWtRun) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[nt] = float4_t{0.f, 0.f, 0.f, 0.f};
-    // Loads at clamped (in-range) addresses with no branch, so all of the
-    // run's loads are in flight together; rows past the chunk and columns
-    // past d_out are then zeroed by a 0/1 factor (a select would let the
-    // compiler move the loads into a branch and wait on each).
+    // All of the run's loads are issued together, with no branch between
+    // them; columns past d_out are zeroed by a 0/1 factor (a select would
+    // let the compiler move the loads into a branch and wait on each).
     float a[kWtRun / 4];
     uint64_t wd[kWtRun / 4][NW];
+    if (r0 + kWtRun <= i1) {
+      // A whole run: row r0 + 32(u/8) + (u%8) (the same on every lane) plus
+      // this lane's 8q, so each address is a uniform row base and a fixed
+      // lane offset.
 #pragma unroll
-    for (int u = 0; u < kWtRun / 4; ++u) {
-      const int64_t row = r0 + 32 * (u >> 3) + 8 * q + (u & 7);
-      const int64_t rc = row < i1 ? row : i1 - 1;
-      a[u] = beta[rc] * dz[rc * lddz + jc] * (row < i1 && j < d_out ? 1.f : 0.f);
+      for (int u = 0; u < kWtRun / 4; ++u) {
+        const int64_t ub = r0 + 32 * (u >> 3) + (u & 7);
+        const float* zb = uniform_ptr(dz + ub * lddz);
+        const uint64_t* fb = uniform_ptr(F + ub * ldf);
+        a[u] = beta[ub + 8 * q] * zb[zoff] * jm;
 #pragma unroll
-      for (int w = 0; w < NW; ++w) wd[u][w] = F[rc * ldf + (w0 + w < kw ? w0 + w : kw - 1)];
+        for (int w = 0; w < NW; ++w) wd[u][w] = fb[foff + wsel[w]];
+      }
+    } else {
+      // The chunk's last run: rows past it read the chunk's last row (an
+      // in-range address) and are zeroed by the 0/1 factor.
+#pragma unroll
+      for (int u = 0; u < kWtRun / 4; ++u) {
+        const int64_t row = r0 + 32 * (u >> 3) + 8 * q + (u & 7);
+        const int64_t rc = row < i1 ? row : i1 - 1;
+        a[u] = beta[rc] * dz[rc * lddz + jc] * (row < i1 ? jm : 0.f);
+#pragma unroll
+        for (int w = 0; w < NW; ++w) wd[u][w] = F[rc * ldf + wsel[w]];
+      }
     }
     __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any MFMA
+#pragma unroll
+    for (int u = 0; u < kWtRun / 4; ++u)
+#pragma unroll
+      for (int w = 0; w < NW; ++w) wd[u][w] = lane_signs(wd[u][w], k0 & 63, m);
 #pragma unroll
     for (int t = 0; t < kWtRun / 32; ++t) {
       float x8[8];
@@ -238,14 +298,8 @@ __global__ __launch_bounds__(kB) void k_bwd_wtilde_mfma(
       split_bf16x3(x8, ah, am, alo);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        const int sh = (k0 & 63) + 16 * (nt & 3) + m;
-        uint32_t h32[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const uint64_t x = wd[8 * t + u][nt >> 2];
-          h32[u] = sh < 32 ? (uint32_t)x : (uint32_t)(x >> 32);
-        }
-        const bf16x8_t b = pm1_bf16x8(h32, sh & 31);
+        const bf16x8_t b =
+            pm1_group_at(nt & 3, [&](int u) { return wd[8 * t + u][nt >> 2]; });
         acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b, acc[nt], 0, 0, 0);
         acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, b, acc[nt], 0, 0, 0);
         acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, b, acc[nt], 0, 0, 0);
@@ -408,17 +462,11 @@ __global__ __launch_bounds__(kB) void k_bwd_htilde_mfma(
 #pragma unroll
       for (int s = 0; s < 8; ++s)
 #pragma unroll
-        for (int w = 0; w < NW; ++w) wd[s][w] = w0 + w < kw ? sB[(jb + s) * kw + w0 + w] : 0ull;
+        for (int w = 0; w < NW; ++w)
+          wd[s][w] = lane_signs(w0 + w < kw ? sB[(jb + s) * kw + w0 + w] : 0ull, k0 & 63, m);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        const int sh = (k0 & 63) + 16 * (nt & 3) + m;
-        uint32_t h32[8];
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          const uint64_t x = wd[s][nt >> 2];
-          h32[s] = sh < 32 ? (uint32_t)x : (uint32_t)(x >> 32);
-        }
-        const bf16x8_t b = pm1_bf16x8(h32, sh & 31);
+        const bf16x8_t b = pm1_group_at(nt & 3, [&](int s) { return wd[s][nt >> 2]; });
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
           acc[r][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[r], b, acc[r][nt], 0, 0, 0);
