@@ -135,8 +135,13 @@ def _dev(t: Optional[torch.Tensor], dtype, name: str):
 
 
 def _ld(t: torch.Tensor, name: str) -> int:
-    """Leading dimension of a row-major 2-D tensor with unit column stride."""
-    if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
+    """Leading dimension of a row-major 2-D tensor with unit column stride
+    (a tensor without rows has no layout to read: its width)."""
+    if t.dim() != 2:
+        raise ValueError("%s must be a 2-D row-major tensor" % name)
+    if t.shape[0] == 0:
+        return max(t.shape[1], 1)
+    if t.shape[1] > 1 and t.stride(1) != 1:
         raise ValueError("%s must be a 2-D row-major tensor" % name)
     return t.stride(0) if t.shape[0] > 1 else max(t.stride(0), t.shape[1])
 

@@ -340,3 +340,17 @@ def test_layer_backward_validation():
     wide = list(ok)
     wide[15], wide[17] = 300, 300
     assert f(*wide) == EUNSUPPORTED
+
+
+def test_leading_dimension_of_binding_tensors():
+    import numpy as np
+    import torch
+    assert _lib._ld(torch.empty((5, 7)), "x") == 7
+    assert _lib._ld(torch.empty((5, 8))[:, :7], "x") == 8
+    assert _lib._ld(torch.empty((1, 7)), "x") == 7
+    # a tensor without rows (numpy gives it zero strides) takes its width
+    assert _lib._ld(torch.from_numpy(np.zeros((0, 7), np.float32)), "x") == 7
+    with pytest.raises(ValueError):
+        _lib._ld(torch.empty((7, 5)).t(), "x")
+    with pytest.raises(ValueError):
+        _lib._ld(torch.empty(5), "x")

@@ -148,6 +148,37 @@ def test_layer_backward_without_edges(dev):
     assert np.allclose(got["db"], G.astype(np.float64).sum(axis=0), rtol=1e-6)
 
 
+def test_layer_backward_of_an_empty_graph(dev):
+    """No nodes: every sum over nodes is empty, so dW~, dW and db are zero."""
+    rng = np.random.default_rng(10)
+    d_in, d_out = 70, 5
+    g = workloads.Graph(0, np.zeros(1, dtype=np.int64), np.zeros(0, dtype=np.int32))
+    wt = rng.standard_normal((d_out, d_in)).astype(np.float32)
+    got = gpu_backward(dev, g, "mean", np.zeros((0, d_in), np.float32), wt,
+                       np.zeros((0, d_out), np.float32))
+    for k in ("dwt", "dwt_tilde", "db"):
+        assert np.all(got[k] == 0), k
+    assert got["dh"].shape == (0, d_in) and got["dzeta"].shape == (0, d_out)
+
+
+@pytest.mark.parametrize("n,d_in,d_out", [(1, 1, 1), (3, 1, 2), (5, 65, 1), (2, 2048, 3)])
+def test_layer_backward_smallest_and_widest_shapes(dev, n, d_in, d_out):
+    """One node with its self-loop, one input or output column, the widest
+    input the entry point takes: every entry against the oracle."""
+    rng = np.random.default_rng(n * 1000 + d_in + d_out)
+    rows = [[i, (i + 1) % n] if n > 1 else [i] for i in range(n)]
+    adj = [sorted(set(r) | {j for j in range(n) if i in rows[j]}) for i, r in enumerate(rows)]
+    rowptr = np.concatenate([[0], np.cumsum([len(a) for a in adj])]).astype(np.int64)
+    g = workloads.Graph(n, rowptr, np.concatenate(adj).astype(np.int32))
+    h = rng.standard_normal((n, d_in)).astype(np.float32)
+    wt = (rng.standard_normal((d_out, d_in)) * 0.8).astype(np.float32)
+    G = (rng.standard_normal((n, d_out)) * 0.05).astype(np.float32)
+    for norm in ("sym", "mean"):
+        ref = oracle.layer_backward(g.rowptr, g.colidx, norm, h, wt, G)
+        got = gpu_backward(dev, g, norm, h, wt, G)
+        check_backward(got, ref, G, wt, d_in)
+
+
 @pytest.mark.parametrize("layer", [0, 1])
 def test_pubmed_like_layer_backward(dev, layer):
     """Full-size pubmed-like workload, both layers, every entry."""
