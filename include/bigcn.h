@@ -268,10 +268,10 @@ bigcn_status bigcn_spmm_csr_sage_q8(int64_t n, int64_t nnz, const int64_t* rowpt
  * The CSR of Â must be structurally symmetric (an undirected graph with its
  * self-loops, as for the forward); Ã and its normalisation as for
  * bigcn_spmm_csr.
- *   slot, colslot  the source order of bigcn_source_slots, or both NULL:
- *          G and the source factors are then staged in that order and dζ
- *          gathers them through colslot (the same terms in the same order:
- *          every result is identical either way).
+ *   slot, colslot  the source order of bigcn_source_slots, or both NULL.
+ *          When given, G and the source factors are staged in that order
+ *          and dζ gathers them through colslot (the same terms in the same
+ *          order: every result is identical either way).
  *   h      [n][ldh] fp32 layer input (before binarisation), ldh >= d_in
  *   wt     [d_out][ldwt] fp32 W^T; wbits [d_out][ldw], alpha fp32[d_out]:
  *          W^T packed by bigcn_binarize_pack
