@@ -95,6 +95,23 @@ def _c(a, dtype):
     return None if a is None else np.ascontiguousarray(a, dtype=dtype)
 
 
+def _vec(a, dtype, n, name):
+    """An optional per-column or per-row vector, checked to hold n entries
+    (the C code reads exactly that many)."""
+    a = _c(a, dtype)
+    if a is not None and a.shape != (n,):
+        raise ValueError("%s must hold %d entries, not %s" % (name, n, a.shape))
+    return a
+
+
+def _ids(ids, n):
+    """Optional output row ids, checked to lie in [0, n)."""
+    ids = _c(ids, np.int64)
+    if ids is not None and ids.size and (ids.min() < 0 or ids.max() >= n):
+        raise ValueError("row ids must lie in [0, %d)" % n)
+    return ids
+
+
 def words(k: int) -> int:
     return (k + 63) // 64
 
@@ -106,12 +123,13 @@ def binarize(x, mu=None, rstd=None, ids=None, ldw=None):
     x = _c(x, np.float32)
     rows, cols = x.shape
     ldw = words(cols) if ldw is None else ldw
-    ids = _c(ids, np.int64)
+    ids = _ids(ids, rows)
     n_out = rows if ids is None else len(ids)
     bits = np.zeros((n_out, ldw), dtype=np.uint64)
     scale = np.zeros(n_out, dtype=np.float64)
-    rc = _load().oracle_binarize(_ptr(x), rows, cols, cols, _ptr(_c(mu, np.float32)),
-                                 _ptr(_c(rstd, np.float32)), _ptr(ids),
+    rc = _load().oracle_binarize(_ptr(x), rows, cols, cols,
+                                 _ptr(_vec(mu, np.float32, cols, "mu")),
+                                 _ptr(_vec(rstd, np.float32, cols, "rstd")), _ptr(ids),
                                  0 if ids is None else len(ids), bits.ctypes.data,
                                  ldw, scale.ctypes.data)
     if rc != 0:
@@ -141,14 +159,15 @@ def aggregate(rowptr, colidx, norm, beta, alpha, dot, bias=None, act="none",
     dot = _c(dot, np.int64)
     n = len(rowptr) - 1
     d = dot.shape[1]
-    ids = _c(ids, np.int64)
+    assert beta.shape == (n,) and alpha.shape == (d,) and dot.shape[0] == n
+    ids = _ids(ids, n)
     n_out = n if ids is None else len(ids)
     z = np.zeros((n_out, d), dtype=np.float64)
     mass = np.zeros((n_out, d), dtype=np.float64)
     out = np.zeros((n_out, d), dtype=np.float32)
     _load().oracle_aggregate(n, rowptr.ctypes.data, colidx.ctypes.data,
                              NORMS[norm], beta.ctypes.data, alpha.ctypes.data,
-                             dot.ctypes.data, d, d, _ptr(_c(bias, np.float32)),
+                             dot.ctypes.data, d, d, _ptr(_vec(bias, np.float32, d, "bias")),
                              ACTS[act], _ptr(ids), 0 if ids is None else len(ids),
                              z.ctypes.data, mass.ctypes.data, out.ctypes.data)
     return z, mass, out
@@ -165,7 +184,7 @@ def layer(rowptr, colidx, norm, h, wt, bias=None, act="none", mu=None,
     n, d_in = h.shape
     d_out = wt.shape[0]
     assert wt.shape[1] == d_in
-    ids = _c(ids, np.int64)
+    ids = _ids(ids, n)
     n_out = n if ids is None else len(ids)
     z = np.zeros((n_out, d_out), dtype=np.float64)
     mass = np.zeros((n_out, d_out), dtype=np.float64)
@@ -173,8 +192,9 @@ def layer(rowptr, colidx, norm, h, wt, bias=None, act="none", mu=None,
     alpha = np.zeros(d_out, dtype=np.float64)
     rc = _load().oracle_layer(n, rowptr.ctypes.data, colidx.ctypes.data,
                               NORMS[norm], h.ctypes.data, d_in, d_in,
-                              _ptr(_c(mu, np.float32)), _ptr(_c(rstd, np.float32)),
-                              wt.ctypes.data, d_out, _ptr(_c(bias, np.float32)),
+                              _ptr(_vec(mu, np.float32, d_in, "mu")),
+                              _ptr(_vec(rstd, np.float32, d_in, "rstd")),
+                              wt.ctypes.data, d_out, _ptr(_vec(bias, np.float32, d_out, "bias")),
                               ACTS[act], _ptr(ids), 0 if ids is None else len(ids),
                               z.ctypes.data, mass.ctypes.data, out.ctypes.data,
                               alpha.ctypes.data)
@@ -196,7 +216,7 @@ def sage_layer(rowptr, colidx, h, wt_self, wt_neigh, bias=None, act="none",
     n, d_in = h.shape
     d_out = ws.shape[0]
     assert ws.shape == wn.shape == (d_out, d_in)
-    ids = _c(ids, np.int64)
+    ids = _ids(ids, n)
     n_out = n if ids is None else len(ids)
     z = np.zeros((n_out, d_out), dtype=np.float64)
     mass = np.zeros((n_out, d_out), dtype=np.float64)
@@ -204,9 +224,11 @@ def sage_layer(rowptr, colidx, h, wt_self, wt_neigh, bias=None, act="none",
     a_s = np.zeros(d_out, dtype=np.float64)
     a_n = np.zeros(d_out, dtype=np.float64)
     rc = _load().oracle_sage_layer(n, rowptr.ctypes.data, colidx.ctypes.data,
-                                   h.ctypes.data, d_in, d_in, _ptr(_c(mu, np.float32)),
-                                   _ptr(_c(rstd, np.float32)), ws.ctypes.data,
-                                   wn.ctypes.data, d_out, _ptr(_c(bias, np.float32)),
+                                   h.ctypes.data, d_in, d_in,
+                                   _ptr(_vec(mu, np.float32, d_in, "mu")),
+                                   _ptr(_vec(rstd, np.float32, d_in, "rstd")), ws.ctypes.data,
+                                   wn.ctypes.data, d_out,
+                                   _ptr(_vec(bias, np.float32, d_out, "bias")),
                                    ACTS[act], _ptr(ids), 0 if ids is None else len(ids),
                                    z.ctypes.data, mass.ctypes.data, out.ctypes.data,
                                    a_s.ctypes.data, a_n.ctypes.data)

@@ -460,7 +460,9 @@ def _gcn_chain(mistake):
         h, res = x, []
         for l, wt in enumerate(weights_t):
             std = (l == 0) != (mistake == "no_standardisation") or mistake == "std_every_layer"
-            b = biases[(l + 1) % L] if mistake == "bias_shift" else biases[l]
+            # (the shifted bias repeated or cut to this layer's width)
+            b = (np.resize(biases[(l + 1) % L], len(biases[l])) if mistake == "bias_shift"
+                 else biases[l])
             a = acts[(l + 1) % L] if mistake == "act_shift" else acts[l]
             if mistake == "act_ignored":
                 a = "none"
@@ -479,7 +481,9 @@ def _sage_chain(mistake):
         h, res = x, []
         for l in range(L):
             std = (l == 0) != (mistake == "no_standardisation") or mistake == "std_every_layer"
-            b = biases[(l + 1) % L] if mistake == "bias_shift" else biases[l]
+            # (the shifted bias repeated or cut to this layer's width)
+            b = (np.resize(biases[(l + 1) % L], len(biases[l])) if mistake == "bias_shift"
+                 else biases[l])
             a = acts[(l + 1) % L] if mistake == "act_shift" else acts[l]
             if mistake == "act_ignored":
                 a = "none"
